@@ -1,0 +1,137 @@
+"""One pre-norm decoder block on one sequence, float64, forward and backward.
+
+Test infrastructure (see the package docstring).
+
+The block is f^l of the transformer form of the layer-dropout training
+equation (Preliminary section, "Layer Dropout for a Transformer"):
+    Z  = X + r * f_attn(X)        f_attn(X) = MHA(RMSNorm(X; g_attn)) W_o^T
+    X' = Z + r * f_ffn(Z)         f_ffn(Z)  = SwiGLU(RMSNorm(Z; g_mlp)) W_down^T
+with the sub-block choices of this hot path: RMSNorm, causal multi-head
+attention without positional bias, SwiGLU.  The paper's footnote on that
+equation states the formulation holds for any pre-norm attention/FFN variant
+with a residual connection.
+
+Readings (the paper is silent on these):
+  * RMSNorm(x; g) = x / sqrt(mean_d(x^2) + eps) * g, eps from the config;
+  * attention scale 1/sqrt(d_head), causal with the diagonal kept (j <= i);
+  * no biases anywhere;
+  * w_qkv rows are [q | k | v], each d rows, head h owning rows h*dh..h*dh+dh
+    of each part; w_gate_up rows [0, f) are the gate, [f, 2f) the up
+    projection; SwiGLU(u, v) = silu(u) * v, silu(u) = u * sigmoid(u);
+  * weights are stored [out, in] and applied as x @ W^T.
+
+The backward is the chain rule of the forward written out by hand; it is
+pinned against finite differences and against torch float64 autograd.
+"""
+
+import numpy as np
+
+
+def rmsnorm(x, g, eps):
+    rstd = 1.0 / np.sqrt(np.mean(x * x, axis=-1) + eps)
+    return x * rstd[:, None] * g[None, :], rstd
+
+
+def rmsnorm_bwd(x, g, rstd, gy):
+    """Gradient of y = x * rstd * g: returns (dx, dg)."""
+    dg = np.sum(gy * x * rstd[:, None], axis=0)
+    mean_term = np.mean(x * g[None, :] * gy, axis=-1)
+    dx = rstd[:, None] * (g[None, :] * gy) - x * (rstd ** 3 * mean_term)[:, None]
+    return dx, dg
+
+
+def causal_attention(q, k, v, n_heads):
+    """softmax(q k^T / sqrt(dh), causal j <= i) v per head.
+    q, k, v: [S, d].  Returns (out [S, d], probs [H, S, S])."""
+    S, d = q.shape
+    dh = d // n_heads
+    out = np.zeros((S, d))
+    probs = np.zeros((n_heads, S, S))
+    future = np.triu(np.ones((S, S), dtype=bool), k=1)
+    for h in range(n_heads):
+        cols = slice(h * dh, (h + 1) * dh)
+        s = q[:, cols] @ k[:, cols].T / np.sqrt(dh)
+        s[future] = -np.inf
+        s = s - np.max(s, axis=-1, keepdims=True)
+        e = np.exp(s)
+        pr = e / np.sum(e, axis=-1, keepdims=True)
+        probs[h] = pr
+        out[:, cols] = pr @ v[:, cols]
+    return out, probs
+
+
+def causal_attention_bwd(q, k, v, probs, gout, n_heads):
+    """Gradients of causal_attention with respect to q, k, v."""
+    S, d = q.shape
+    dh = d // n_heads
+    gq, gk, gv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    for h in range(n_heads):
+        cols = slice(h * dh, (h + 1) * dh)
+        pr = probs[h]
+        go = gout[:, cols]
+        gv[:, cols] = pr.T @ go
+        dp = go @ v[:, cols].T
+        ds = pr * (dp - np.sum(dp * pr, axis=-1, keepdims=True))
+        gq[:, cols] = ds @ k[:, cols] / np.sqrt(dh)
+        gk[:, cols] = ds.T @ q[:, cols] / np.sqrt(dh)
+    return gq, gk, gv
+
+
+def silu(u):
+    return u / (1.0 + np.exp(-u))
+
+
+def silu_grad(u):
+    sg = 1.0 / (1.0 + np.exp(-u))
+    return sg * (1.0 + u * (1.0 - sg))
+
+
+def forward(x, w, r, n_heads, eps):
+    """Apply the block to one kept sequence x [S, d].
+
+    w: dict with g_attn [d], w_qkv [3d, d], w_o [d, d], g_mlp [d],
+    w_gate_up [2f, d], w_down [d, f].  r is the residual-branch scale.
+    Returns (x_next, cache)."""
+    d = x.shape[1]
+    f = w["w_down"].shape[1]
+    h1, rstd1 = rmsnorm(x, w["g_attn"], eps)
+    qkv = h1 @ w["w_qkv"].T
+    q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+    a, probs = causal_attention(q, k, v, n_heads)
+    z = x + r * (a @ w["w_o"].T)
+    h2, rstd2 = rmsnorm(z, w["g_mlp"], eps)
+    uv = h2 @ w["w_gate_up"].T
+    u, vv = uv[:, :f], uv[:, f:]
+    s = silu(u) * vv
+    x_next = z + r * (s @ w["w_down"].T)
+    cache = dict(x=x, h1=h1, rstd1=rstd1, q=q, k=k, v=v, a=a, probs=probs,
+                 z=z, h2=h2, rstd2=rstd2, u=u, vv=vv, s=s)
+    return x_next, cache
+
+
+def backward(cache, g, w, r, n_heads):
+    """Backward of `forward` for one kept sequence given g = dL/dx_next.
+    Returns (dL/dx, grads dict with the same keys as w)."""
+    c = cache
+    gy = r * g
+    d_down = gy.T @ c["s"]
+    gs = gy @ w["w_down"]
+    gu = gs * c["vv"] * silu_grad(c["u"])
+    gvv = gs * silu(c["u"])
+    guv = np.concatenate([gu, gvv], axis=1)
+    d_gate_up = guv.T @ c["h2"]
+    gh2 = guv @ w["w_gate_up"]
+    gz_norm, d_g_mlp = rmsnorm_bwd(c["z"], w["g_mlp"], c["rstd2"], gh2)
+    gz = g + gz_norm
+    go = r * gz
+    d_o = go.T @ c["a"]
+    ga = go @ w["w_o"]
+    gq, gk, gv = causal_attention_bwd(c["q"], c["k"], c["v"], c["probs"], ga, n_heads)
+    gqkv = np.concatenate([gq, gk, gv], axis=1)
+    d_qkv = gqkv.T @ c["h1"]
+    gh1 = gqkv @ w["w_qkv"]
+    gx_norm, d_g_attn = rmsnorm_bwd(c["x"], w["g_attn"], c["rstd1"], gh1)
+    gx = gz + gx_norm
+    grads = dict(g_attn=d_g_attn, w_qkv=d_qkv, w_o=d_o, g_mlp=d_g_mlp,
+                 w_gate_up=d_gate_up, w_down=d_down)
+    return gx, grads

@@ -1,0 +1,108 @@
+"""Layer and stack forward+backward under per-sequence layer dropout.
+
+Test infrastructure (see the package docstring).
+
+Definition followed (Preliminary section): for layer l at step t,
+    H^{l+1}[b] = H^l[b]                                  if M^{l,t}[b] = 0
+    H^{l+1}[b] = H^l[b] + r f^l(H^l[b])  (both sub-blocks) if M^{l,t}[b] = 1
+with r = res_scale / (1 - p^{l,t}) when rescaling is on (the paper's choice
+r_train = 1/rho, rho = 1 - p, Hyperparameters section "Dropout Scale"), and
+r = res_scale otherwise.  res_scale is a constant residual multiplier (the
+depth multiplier of the parameterisation table; 1 by default).  The same r
+multiplies both sub-blocks (transformer form of the training equation).
+
+Samples are visited in ascending order and each kept sample is processed on
+its own; dropped samples are copied bit for bit and their gradient passes
+through unchanged.  Weight gradients are sums over kept samples (no 1/B);
+they start at zero on every call, so a layer with no kept sample has zero
+gradients.
+"""
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import block
+from .masks import masks as make_masks
+
+WEIGHT_KEYS = ("g_attn", "w_qkv", "w_o", "g_mlp", "w_gate_up", "w_down")
+
+
+@dataclass
+class Config:
+    n_heads: int
+    rms_eps: float = 1e-5
+    rescale: bool = True
+    res_scale: float = 1.0
+
+
+def residual_scale(p, cfg):
+    """r^{l,t}; only evaluated for layers with at least one kept sample."""
+    p = float(np.float32(p))
+    return cfg.res_scale / (1.0 - p) if cfg.rescale else cfg.res_scale
+
+
+def _as64(w):
+    return {k: np.asarray(w[k], dtype=np.float64) for k in WEIGHT_KEYS}
+
+
+def layer_forward(X, w, keep_row, p, cfg):
+    """X [B, S, d] float64 -> (X_next, ctx).  keep_row uint8[B]."""
+    w = _as64(w)
+    X = np.asarray(X, dtype=np.float64)
+    X_next = X.copy()
+    caches = {}
+    r = None
+    for b in range(X.shape[0]):
+        if not keep_row[b]:
+            continue                      # dropped: H^{l+1}[b] = H^l[b]
+        if r is None:
+            r = residual_scale(p, cfg)
+        X_next[b], caches[b] = block.forward(X[b], w, r, cfg.n_heads, cfg.rms_eps)
+    return X_next, dict(caches=caches, r=r, w=w)
+
+
+def layer_backward(ctx, G, cfg):
+    """G = dL/dH^{l+1} [B, S, d] -> (dL/dH^l, grads summed over kept samples)."""
+    G = np.asarray(G, dtype=np.float64)
+    G_prev = G.copy()
+    grads = {k: np.zeros_like(v) for k, v in ctx["w"].items()}
+    for b in sorted(ctx["caches"]):
+        G_prev[b], gb = block.backward(ctx["caches"][b], G[b], ctx["w"], ctx["r"], cfg.n_heads)
+        for k in grads:
+            grads[k] += gb[k]
+    return G_prev, grads
+
+
+def stack_forward(X0, weights, ps, seed, step, cfg, keep=None):
+    """Forward through all layers; returns (X_L, ctxs, keep, idx, count).
+    keep (uint8[L, B]) overrides the Philox masks when given."""
+    B = X0.shape[0]
+    L = len(weights)
+    if keep is None:
+        keep, idx, count = make_masks(ps, seed, step, B)
+    else:
+        keep = np.asarray(keep, dtype=np.uint8)
+        idx = np.full((L, B), -1, dtype=np.int32)
+        count = np.zeros(L, dtype=np.int32)
+        for l in range(L):
+            kept = np.nonzero(keep[l])[0]
+            idx[l, :len(kept)] = kept
+            count[l] = len(kept)
+    X = np.asarray(X0, dtype=np.float64)
+    ctxs = []
+    for l in range(L):
+        X, ctx = layer_forward(X, weights[l], keep[l], ps[l], cfg)
+        ctxs.append(ctx)
+    return X, ctxs, keep, idx, count
+
+
+def stack_step(X0, weights, ps, seed, step, G_L, cfg, keep=None):
+    """One forward+backward step.  Returns dict with X_L, G_0 (dL/dX^0),
+    grads (list per layer), keep, idx, count."""
+    X_L, ctxs, keep, idx, count = stack_forward(X0, weights, ps, seed, step, cfg, keep)
+    G = np.asarray(G_L, dtype=np.float64)
+    grads = [None] * len(weights)
+    for l in reversed(range(len(weights))):
+        G, grads[l] = layer_backward(ctxs[l], G, cfg)
+    return dict(X_L=X_L, G_0=G, grads=grads, keep=keep, idx=idx, count=count)

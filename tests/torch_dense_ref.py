@@ -1,0 +1,50 @@
+"""A second, independent statement of the block for the oracle's pins:
+torch float64 autograd built from library routines (rms_norm,
+scaled_dot_product_attention with is_causal, silu), applied to the whole
+batch and gated by the mask multiply of the layer-dropout training equation
+(H + r M f(H)).  Used only by the CPU pin tests of the oracle."""
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+KEYS = ("g_attn", "w_qkv", "w_o", "g_mlp", "w_gate_up", "w_down")
+
+
+def block_full_batch(X, w, n_heads, eps):
+    B, S, d = X.shape
+    dh = d // n_heads
+    f = w["w_down"].shape[1]
+    h1 = F.rms_norm(X, (d,), w["g_attn"], eps)
+    qkv = h1 @ w["w_qkv"].T
+    q, k, v = (qkv[..., i * d:(i + 1) * d].reshape(B, S, n_heads, dh).transpose(1, 2)
+               for i in range(3))
+    a = F.scaled_dot_product_attention(q, k, v, is_causal=True)
+    a = a.transpose(1, 2).reshape(B, S, d)
+    return h1, a
+
+
+def layer_masked(X, w, keep, r, n_heads, eps):
+    """X + r M f_attn, then + r M f_ffn, over the full batch (mask multiply)."""
+    B, S, d = X.shape
+    f = w["w_down"].shape[1]
+    m = torch.as_tensor(keep, dtype=X.dtype).reshape(B, 1, 1)
+    _, a = block_full_batch(X, w, n_heads, eps)
+    Z = X + r * m * (a @ w["w_o"].T)
+    h2 = F.rms_norm(Z, (d,), w["g_mlp"], eps)
+    uv = h2 @ w["w_gate_up"].T
+    s = F.silu(uv[..., :f]) * uv[..., f:]
+    return Z + r * m * (s @ w["w_down"].T)
+
+
+def stack_step(X0, weights, keep, rs, G, n_heads, eps):
+    """Returns X_L, dL/dX0, grads (numpy float64) with L = sum(G * X_L)."""
+    X = torch.tensor(X0, dtype=torch.float64, requires_grad=True)
+    ws = [{k: torch.tensor(np.asarray(w[k], dtype=np.float64), requires_grad=True) for k in KEYS}
+          for w in weights]
+    H = X
+    for l, w in enumerate(ws):
+        H = layer_masked(H, w, keep[l], rs[l], n_heads, eps)
+    loss = (H * torch.as_tensor(G, dtype=torch.float64)).sum()
+    loss.backward()
+    grads = [{k: w[k].grad.numpy().copy() for k in KEYS} for w in ws]
+    return H.detach().numpy(), X.grad.numpy().copy(), grads
