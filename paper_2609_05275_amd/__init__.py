@@ -1,0 +1,266 @@
+"""Python binding of liblayerdrop (MI355X / gfx950 layer-dropout hot path).
+
+Argument marshalling only: every function here has the name of a C entry
+point in include/layerdrop.h, converts torch tensors to device pointers and
+the current torch stream to a hipStream_t, calls the library, and raises
+LdError on a non-zero status.  All computation happens in the HIP kernels;
+there is no fallback -- importing fails loudly when the library is not built.
+"""
+
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblayerdrop.so")
+
+LD_F32, LD_BF16 = 0, 1
+UNIFORM, ILD, ALD = 0, 1, 2
+CONSTANT, ITS, DTS = 0, 1, 2
+
+WEIGHT_KEYS = ("g_attn", "w_qkv", "w_o", "g_mlp", "w_gate_up", "w_down")
+
+
+class LdError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{status_name(status)}: {msg}")
+        self.status = status
+
+
+class ld_config(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("seq", C.c_int32), ("d_model", C.c_int32),
+                ("n_heads", C.c_int32), ("d_ff", C.c_int32), ("dtype", C.c_int32),
+                ("rms_eps", C.c_float), ("rescale", C.c_int32), ("res_scale", C.c_float)]
+
+
+class ld_weights(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in WEIGHT_KEYS]
+
+
+class ld_grads(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in WEIGHT_KEYS]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_05275_amd.build`")
+_lib = C.CDLL(LIB_PATH)
+
+_vp, _i32, _i64, _u64, _f32, _sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_float, C.c_size_t
+_PCFG = C.POINTER(ld_config)
+_SIGS = {
+    "ld_status_string": (C.c_char_p, [C.c_int]),
+    "ld_last_error": (C.c_char_p, []),
+    "ld_schedule_p": (C.c_int, [_i32, _i32, _f32, _i32, _i32, _i64, _i64, C.POINTER(_f32)]),
+    "ld_masks": (C.c_int, [_i32, _i32, C.POINTER(_f32), _i32, _u64, _u64, _vp, _vp, _vp, _vp]),
+    "ld_gather_rows": (C.c_int, [_PCFG, _vp, _vp, _vp, _vp, _vp]),
+    "ld_scatter_add_rows": (C.c_int, [_PCFG, _vp, _vp, _f32, _vp, _vp, _vp]),
+    "ld_layer_ctx_bytes": (_sz, [_PCFG]),
+    "ld_layer_ws_bytes": (_sz, [_PCFG]),
+    "ld_stack_ws_bytes": (_sz, [_PCFG, _i32]),
+    "ld_layer_fwd": (C.c_int, [_PCFG, C.POINTER(ld_weights), _i32, _f32, _u64, _u64, _vp, _vp,
+                               _vp, _sz, _vp, _vp]),
+    "ld_layer_bwd": (C.c_int, [_PCFG, C.POINTER(ld_weights), _vp, _vp, C.POINTER(ld_grads), _vp,
+                               _sz, _vp]),
+    "ld_stack_step": (C.c_int, [_PCFG, _i32, C.POINTER(ld_weights), C.POINTER(_f32), _u64, _u64,
+                                _vp, _vp, C.POINTER(ld_grads), _vp, _sz, _vp, _vp, _vp, _vp, _vp]),
+    "ld_rmsnorm_fwd": (C.c_int, [_i32, _i32, _i32, _f32, _vp, _vp, _vp, _vp, _vp]),
+    "ld_rmsnorm_bwd_ws_bytes": (_sz, [_i32, _i32]),
+    "ld_rmsnorm_bwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
+                                 _vp]),
+    "ld_swiglu_fwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp]),
+    "ld_swiglu_bwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ld_gemm": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _i32, _vp, _i32, _vp, _i32,
+                          _i32, _f32, _vp, _i32, _vp]),
+    "ld_attn_fwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ld_attn_bwd_ws_bytes": (_sz, [_i32, _i32, _i32]),
+    "ld_attn_bwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
+                              _vp]),
+    "ld_prof_start": (C.c_int, [C.c_char_p]),
+    "ld_prof_stop": (C.c_int, []),
+    "ld_prof_result": (C.c_int, [C.POINTER(_i64), C.POINTER(C.c_double), C.POINTER(C.c_double),
+                                 C.POINTER(C.c_double)]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+def status_name(status):
+    return _lib.ld_status_string(status).decode()
+
+
+def last_error():
+    return _lib.ld_last_error().decode()
+
+
+def _check(status):
+    if status != 0:
+        raise LdError(status, last_error())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return LD_BF16
+    if t.dtype == torch.float32:
+        return LD_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def config(batch, seq, d_model, n_heads, d_ff, dtype=LD_BF16, rms_eps=1e-5, rescale=True,
+           res_scale=1.0):
+    return ld_config(batch, seq, d_model, n_heads, d_ff, dtype, rms_eps, int(bool(rescale)),
+                     res_scale)
+
+
+def weights(w):
+    """ld_weights from a dict of device tensors keyed by WEIGHT_KEYS."""
+    return ld_weights(*[_ptr(w[k]) for k in WEIGHT_KEYS])
+
+
+def grads(g):
+    return ld_grads(*[_ptr(g[k]) for k in WEIGHT_KEYS])
+
+
+# ------------------------------------------------------------------ entry points
+
+def ld_schedule_p(dist, sched, p_max, layer, n_layers, t, n_steps):
+    out = C.c_float()
+    _check(_lib.ld_schedule_p(dist, sched, p_max, layer, n_layers, t, n_steps, C.byref(out)))
+    return out.value
+
+
+def ld_masks(p, seed, step, keep, idx, count, first_layer=0, stream=None):
+    n = len(p)
+    arr = (C.c_float * n)(*[float(v) for v in p])
+    _check(_lib.ld_masks(n, keep.shape[-1], arr, first_layer, seed, step, _ptr(keep), _ptr(idx),
+                         _ptr(count), _stream(stream)))
+
+
+def ld_gather_rows(cfg, idx, count, x, xk, stream=None):
+    _check(_lib.ld_gather_rows(C.byref(cfg), _ptr(idx), _ptr(count), _ptr(x), _ptr(xk),
+                               _stream(stream)))
+
+
+def ld_scatter_add_rows(cfg, idx, count, r, yk, x, stream=None):
+    _check(_lib.ld_scatter_add_rows(C.byref(cfg), _ptr(idx), _ptr(count), r, _ptr(yk), _ptr(x),
+                                    _stream(stream)))
+
+
+def ld_layer_ctx_bytes(cfg):
+    return _lib.ld_layer_ctx_bytes(C.byref(cfg))
+
+
+def ld_layer_ws_bytes(cfg):
+    return _lib.ld_layer_ws_bytes(C.byref(cfg))
+
+
+def ld_stack_ws_bytes(cfg, n_layers):
+    return _lib.ld_stack_ws_bytes(C.byref(cfg), n_layers)
+
+
+def ld_layer_fwd(cfg, w, layer, p, seed, step, x, ctx, ws=None, keep_override=None, stream=None):
+    wb = weights(w)
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(_lib.ld_layer_fwd(C.byref(cfg), C.byref(wb), layer, p, seed, step, _ptr(x), _ptr(ctx),
+                             _ptr(ws), ws_bytes, _ptr(keep_override), _stream(stream)))
+
+
+def ld_layer_bwd(cfg, w, ctx, dx, dw, ws, stream=None):
+    wb, gb = weights(w), grads(dw)
+    _check(_lib.ld_layer_bwd(C.byref(cfg), C.byref(wb), _ptr(ctx), _ptr(dx), C.byref(gb),
+                             _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ld_stack_step(cfg, ws_list, p, seed, step, x, dx, dw_list, ws, keep_override=None,
+                  keep_out=None, idx_out=None, count_out=None, stream=None):
+    L = len(ws_list)
+    wa = (ld_weights * L)(*[weights(w) for w in ws_list])
+    ga = (ld_grads * L)(*[grads(g) for g in dw_list])
+    pa = (C.c_float * L)(*[float(v) for v in p])
+    _check(_lib.ld_stack_step(C.byref(cfg), L, wa, pa, seed, step, _ptr(x), _ptr(dx), ga, _ptr(ws),
+                              ws.numel() * ws.element_size(), _ptr(keep_override), _ptr(keep_out),
+                              _ptr(idx_out), _ptr(count_out), _stream(stream)))
+
+
+def ld_rmsnorm_fwd(x, g, y, rstd, eps=1e-5, stream=None):
+    rows, d = x.shape
+    _check(_lib.ld_rmsnorm_fwd(_dtype_code(x), rows, d, eps, _ptr(x), _ptr(g), _ptr(y), _ptr(rstd),
+                               _stream(stream)))
+
+
+def ld_rmsnorm_bwd_ws_bytes(rows, d):
+    return _lib.ld_rmsnorm_bwd_ws_bytes(rows, d)
+
+
+def ld_rmsnorm_bwd(x, g, rstd, gy, gres, gx, dg, ws, stream=None):
+    rows, d = x.shape
+    _check(_lib.ld_rmsnorm_bwd(_dtype_code(x), rows, d, _ptr(x), _ptr(g), _ptr(rstd), _ptr(gy),
+                               _ptr(gres), _ptr(gx), _ptr(dg), _ptr(ws),
+                               ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ld_swiglu_fwd(uv, s, stream=None):
+    rows, f2 = uv.shape
+    _check(_lib.ld_swiglu_fwd(_dtype_code(uv), rows, f2 // 2, _ptr(uv), _ptr(s), _stream(stream)))
+
+
+def ld_swiglu_bwd(uv, gs, guv, stream=None):
+    rows, f2 = uv.shape
+    _check(_lib.ld_swiglu_bwd(_dtype_code(uv), rows, f2 // 2, _ptr(uv), _ptr(gs), _ptr(guv),
+                              _stream(stream)))
+
+
+def ld_gemm(a_kcontig, b_kcontig, M, N, K, A, lda, B, ldb, Cm, ldc, alpha=1.0, R=None, ldr=0,
+            c_f32=False, dtype=None, stream=None):
+    dt = _dtype_code(A) if dtype is None else dtype
+    _check(_lib.ld_gemm(dt, int(a_kcontig), int(b_kcontig), M, N, K, _ptr(A), lda, _ptr(B), ldb,
+                        _ptr(Cm), ldc, int(c_f32), alpha, _ptr(R), ldr, _stream(stream)))
+
+
+def ld_attn_fwd(n_seq, seq, n_heads, d_head, qkv, o, lse, stream=None):
+    _check(_lib.ld_attn_fwd(_dtype_code(qkv), n_seq, seq, n_heads, d_head, _ptr(qkv), _ptr(o),
+                            _ptr(lse), _stream(stream)))
+
+
+def ld_attn_bwd_ws_bytes(n_seq, seq, n_heads):
+    return _lib.ld_attn_bwd_ws_bytes(n_seq, seq, n_heads)
+
+
+def ld_attn_bwd(n_seq, seq, n_heads, d_head, qkv, o, lse, go, gqkv, ws, stream=None):
+    _check(_lib.ld_attn_bwd(_dtype_code(qkv), n_seq, seq, n_heads, d_head, _ptr(qkv), _ptr(o),
+                            _ptr(lse), _ptr(go), _ptr(gqkv), _ptr(ws),
+                            ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ld_prof_start(kernel_name):
+    _check(_lib.ld_prof_start(kernel_name.encode()))
+
+
+def ld_prof_stop():
+    _check(_lib.ld_prof_stop())
+
+
+def ld_prof_result():
+    n, ms, fl, by = C.c_int64(), C.c_double(), C.c_double(), C.c_double()
+    _check(_lib.ld_prof_result(C.byref(n), C.byref(ms), C.byref(fl), C.byref(by)))
+    return dict(launches=n.value, ms=ms.value, flops=fl.value, bytes=by.value)

@@ -1,0 +1,1127 @@
+// Host side of the C ABI declared in include/layerdrop.h: argument checks,
+// residual scales and integer thresholds, workspace layout, and the order of
+// kernel launches for one layer and for a whole training step.  Nothing here
+// computes activations or gradients; every step runs in the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "ld_internal.h"
+
+using namespace ld;
+
+namespace {
+
+// ------------------------------------------------------------------ errors
+
+thread_local std::string t_err;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return status;
+}
+
+#define LD_HIP(call)                                                                    \
+  do {                                                                                  \
+    hipError_t e_ = (call);                                                             \
+    if (e_ != hipSuccess) return fail(LD_E_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+// --------------------------------------------------------------- profiling
+
+struct ProfRec {
+  hipEvent_t e0, e1;
+  double flops, bytes;
+};
+
+struct Prof {
+  std::mutex mu;
+  bool on = false;
+  std::string name;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+  size_t next = 0;
+} g_prof;
+
+constexpr size_t kMaxProf = 1 << 16;
+
+bool prof_on() { return g_prof.on; }
+
+// Records events around one launch of kernel `name` when profiling it.
+struct ProfScope {
+  bool active = false;
+  size_t slot = 0;
+  hipStream_t s;
+  ProfScope(const char* name, hipStream_t st) : s(st) {
+    if (!g_prof.on || g_prof.name != name) return;
+    if (g_prof.next + 2 > g_prof.pool.size()) {
+      if (g_prof.pool.size() >= 2 * kMaxProf) return;
+      for (int i = 0; i < 64; ++i) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        g_prof.pool.push_back(e);
+      }
+    }
+    slot = g_prof.next;
+    g_prof.next += 2;
+    active = hipEventRecord(g_prof.pool[slot], s) == hipSuccess;
+  }
+  void end(double flops, double bytes) {
+    if (!active) return;
+    if (hipEventRecord(g_prof.pool[slot + 1], s) != hipSuccess) return;
+    g_prof.recs.push_back({g_prof.pool[slot], g_prof.pool[slot + 1], flops, bytes});
+  }
+};
+
+// ------------------------------------------------------------ config checks
+
+struct Dims {
+  int64_t B, S, d, H, dh, f, T, es;
+  int dtype;
+};
+
+int check_cfg(const ld_config* c, Dims* out) {
+  if (!c) return fail(LD_E_INVALID, "cfg is NULL");
+  if (c->batch < 1 || c->seq < 1 || c->d_model < 1 || c->n_heads < 1 || c->d_ff < 1)
+    return fail(LD_E_SHAPE, "batch, seq, d_model, n_heads, d_ff must be >= 1");
+  if (c->dtype != LD_F32 && c->dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype %d", c->dtype);
+  if (c->d_model % c->n_heads) return fail(LD_E_SHAPE, "d_model %% n_heads != 0");
+  if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return fail(LD_E_INVALID, "rms_eps must be > 0");
+  if (!std::isfinite(c->res_scale)) return fail(LD_E_INVALID, "res_scale must be finite");
+  const int dh = c->d_model / c->n_heads;
+  if (c->dtype == LD_BF16) {
+    if (dh != 64 && dh != 128) return fail(LD_E_UNSUPPORTED, "bf16 needs d_head 64 or 128, got %d", dh);
+    if (c->d_model % 8 || c->d_ff % 8) return fail(LD_E_SHAPE, "bf16 needs d_model, d_ff multiples of 8");
+    if (c->seq % 64) return fail(LD_E_SHAPE, "bf16 needs seq %% 64 == 0");
+    if (c->d_model > 8192) return fail(LD_E_UNSUPPORTED, "d_model > 8192");
+  } else {
+    if (dh != 16 && dh != 32 && dh != 64)
+      return fail(LD_E_UNSUPPORTED, "fp32 needs d_head 16, 32 or 64, got %d", dh);
+    if (c->d_model % 4 || c->d_ff % 4) return fail(LD_E_SHAPE, "fp32 needs d_model, d_ff multiples of 4");
+    if (c->d_model > 4096) return fail(LD_E_UNSUPPORTED, "d_model > 4096");
+  }
+  const int64_t T = static_cast<int64_t>(c->batch) * c->seq;
+  if (T * std::max<int64_t>(3ll * c->d_model, 2ll * c->d_ff) >= (1ll << 40) || T >= (1ll << 30))
+    return fail(LD_E_SHAPE, "batch * seq too large");
+  if (out) {
+    out->B = c->batch;
+    out->S = c->seq;
+    out->d = c->d_model;
+    out->H = c->n_heads;
+    out->dh = dh;
+    out->f = c->d_ff;
+    out->T = T;
+    out->es = c->dtype == LD_BF16 ? 2 : 4;
+    out->dtype = c->dtype;
+  }
+  return LD_OK;
+}
+
+int check_p(float p) {
+  if (std::isnan(p) || p < 0.f || p > 1.f) return fail(LD_E_INVALID, "p = %g outside [0, 1]", p);
+  return LD_OK;
+}
+
+// Integer drop threshold: drop iff word < thr; p >= 1 drops all.
+void threshold(float p, uint64_t* thr, uint8_t* drop_all) {
+  *drop_all = 0;
+  *thr = 0;
+  if (p >= 1.f) {
+    *drop_all = 1;
+    return;
+  }
+  if (p <= 0.f) return;
+  *thr = static_cast<uint64_t>(std::floor(std::ldexp(static_cast<double>(p), 64)));
+}
+
+// r for a layer; 0 when nothing can be kept (it is then never applied).
+float residual_scale(const ld_config* c, float p) {
+  if (p >= 1.f) return 0.f;
+  if (!c->rescale) return c->res_scale;
+  return static_cast<float>(static_cast<double>(c->res_scale) / (1.0 - static_cast<double>(p)));
+}
+
+// ------------------------------------------------------------------ layout
+
+constexpr size_t kAlign = 256;
+size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Saved activations of one layer, sized for the whole batch (kept rows are
+// stored compacted from row 0).
+struct ActLayout {
+  size_t xk, rstd1, h1, qkv, att, lse, zk, rstd2, h2, uv, s, total;
+};
+
+ActLayout act_layout(const Dims& D) {
+  ActLayout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += up(bytes);
+    return at;
+  };
+  const size_t es = D.es, T = D.T;
+  L.xk = take(es * T * D.d);
+  L.rstd1 = take(4 * T);
+  L.h1 = take(es * T * D.d);
+  L.qkv = take(es * T * 3 * D.d);
+  L.att = take(es * T * D.d);
+  L.lse = take(4 * T * D.H);
+  L.zk = take(es * T * D.d);
+  L.rstd2 = take(4 * T);
+  L.h2 = take(es * T * D.d);
+  L.uv = take(es * T * 2 * D.f);
+  L.s = take(es * T * D.f);
+  L.total = o;
+  return L;
+}
+
+// Mask block of one layer inside a ld_layer_fwd ctx.
+struct MaskLayout {
+  size_t keep, idx, count, r, total;
+};
+
+MaskLayout mask_layout(int64_t L, int64_t B) {
+  MaskLayout m{};
+  size_t o = 0;
+  m.keep = o;
+  o += up(L * B);
+  m.idx = o;
+  o += up(4 * L * B);
+  m.count = o;
+  o += up(4 * L);
+  m.r = o;
+  o += up(4 * L);
+  m.total = o;
+  return m;
+}
+
+// Backward scratch.
+struct BwdLayout {
+  size_t gk, gs, guv, gh, gz, ga, gqkv, delta, dg_part, total;
+};
+
+BwdLayout bwd_layout(const Dims& D) {
+  BwdLayout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += up(bytes);
+    return at;
+  };
+  const size_t es = D.es, T = D.T;
+  L.gk = take(es * T * D.d);
+  L.gs = take(es * T * D.f);
+  L.guv = take(es * T * 2 * D.f);
+  L.gh = take(es * T * D.d);
+  L.gz = take(es * T * D.d);
+  L.ga = take(es * T * D.d);
+  L.gqkv = take(es * T * 3 * D.d);
+  L.delta = take(4 * T * D.H);
+  L.dg_part = take(4 * rmsnorm_bwd_blocks(T) * D.d);
+  L.total = o;
+  return L;
+}
+
+// Pointers of one layer's mask data on the device.
+struct MaskView {
+  const uint8_t* keep;
+  const int32_t* idx;
+  const int32_t* count;
+  const float* r;
+};
+
+struct ActPtrs {
+  char* base;
+  ActLayout L;
+  template <typename T = void>
+  T* at(size_t off) const {
+    return reinterpret_cast<T*>(base + off);
+  }
+};
+
+int64_t host_count_if_profiling(const int32_t* dev_count, hipStream_t s) {
+  if (!prof_on()) return -1;
+  int32_t c = 0;
+  if (hipMemcpyAsync(&c, dev_count, sizeof(c), hipMemcpyDeviceToHost, s) != hipSuccess) return -1;
+  if (hipStreamSynchronize(s) != hipSuccess) return -1;
+  return c;
+}
+
+// ----------------------------------------------------------- gemm helper
+
+struct GemmCall {
+  int dtype;
+  int a_k, b_k;
+  GemmArgs g;
+  int64_t max_m;
+};
+
+GemmArgs gemm_args() {
+  GemmArgs g;
+  std::memset(&g, 0, sizeof(g));
+  g.alpha = 1.f;
+  return g;
+}
+
+int run_gemm(int dtype, int a_k, int b_k, const GemmArgs& g, int64_t max_m, int64_t host_m,
+             int64_t host_k, hipStream_t s) {
+  const char* name = gemm_kernel_name(dtype, a_k, b_k);
+  ProfScope ps(name, s);
+  hipError_t e = launch_gemm(dtype, a_k, b_k, g, max_m, 0, s);
+  if (e != hipSuccess) return fail(LD_E_HIP, "%s launch: %s", name, hipGetErrorString(e));
+  const double es = dtype == LD_BF16 ? 2.0 : 4.0;
+  const double M = static_cast<double>(host_m), N = g.N, K = static_cast<double>(host_k);
+  const double out_es = g.c_f32 ? 4.0 : es;
+  ps.end(2.0 * M * N * K, es * (M * K + N * K) + out_es * M * N + (g.R ? out_es * M * N : 0.0));
+  return LD_OK;
+}
+
+// ------------------------------------------------------------ one layer
+
+int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
+                  const ActPtrs& act, void* x, hipStream_t s) {
+  const int dt = D.dtype;
+  const int64_t T = D.T;
+  const int64_t hc = host_count_if_profiling(mv.count, s);
+  const int64_t hm = hc * D.S;
+  hipError_t e;
+
+  // gather kept rows of X + RMSNorm (attention input)
+  {
+    RmsFwdArgs a{};
+    a.x = x;
+    a.src = {mv.idx, static_cast<int32_t>(D.S)};
+    a.g = w.g_attn;
+    a.xcopy = act.at(act.L.xk);
+    a.y = act.at(act.L.h1);
+    a.rstd = act.at<float>(act.L.rstd1);
+    a.rc = {mv.count, static_cast<int32_t>(D.S), T};
+    a.d = static_cast<int32_t>(D.d);
+    a.eps = cfg->rms_eps;
+    ProfScope ps("ld_rmsnorm_fwd_k", s);
+    if ((e = launch_rmsnorm_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
+    ps.end(0, D.es * hm * D.d * 3.0 + 4.0 * hm);
+  }
+  // qkv = h1 W_qkv^T
+  {
+    GemmArgs g = gemm_args();
+    g.A = act.at(act.L.h1);
+    g.lda = D.d;
+    g.B = w.w_qkv;
+    g.ldb = D.d;
+    g.C = act.at(act.L.qkv);
+    g.ldc = 3 * D.d;
+    g.N = static_cast<int32_t>(3 * D.d);
+    g.K = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = static_cast<int32_t>(D.S);
+    if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
+  }
+  // causal attention on the kept sequences
+  {
+    AttnArgs a{};
+    a.qkv = act.at(act.L.qkv);
+    a.out = act.at(act.L.att);
+    a.lse = act.at<float>(act.L.lse);
+    a.dev_count = mv.count;
+    a.n_seq = static_cast<int32_t>(D.B);
+    a.S = static_cast<int32_t>(D.S);
+    a.H = static_cast<int32_t>(D.H);
+    a.dh = static_cast<int32_t>(D.dh);
+    a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.dh)));
+    ProfScope ps(attn_fwd_kernel_name(dt), s);
+    if ((e = launch_attn_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "attn_fwd: %s", hipGetErrorString(e));
+    ps.end(2.0 * hc * D.d * D.S * (D.S + 1.0), D.es * hm * D.d * 4.0);
+  }
+  // zk = xk + r * (att W_o^T)
+  {
+    GemmArgs g = gemm_args();
+    g.A = act.at(act.L.att);
+    g.lda = D.d;
+    g.B = w.w_o;
+    g.ldb = D.d;
+    g.C = act.at(act.L.zk);
+    g.ldc = D.d;
+    g.R = act.at(act.L.xk);
+    g.ldr = D.d;
+    g.alpha_dev = mv.r;
+    g.N = static_cast<int32_t>(D.d);
+    g.K = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = static_cast<int32_t>(D.S);
+    if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
+  }
+  // RMSNorm (FFN input)
+  {
+    RmsFwdArgs a{};
+    a.x = act.at(act.L.zk);
+    a.src = {nullptr, 1};
+    a.g = w.g_mlp;
+    a.y = act.at(act.L.h2);
+    a.rstd = act.at<float>(act.L.rstd2);
+    a.rc = {mv.count, static_cast<int32_t>(D.S), T};
+    a.d = static_cast<int32_t>(D.d);
+    a.eps = cfg->rms_eps;
+    ProfScope ps("ld_rmsnorm_fwd_k", s);
+    if ((e = launch_rmsnorm_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
+    ps.end(0, D.es * hm * D.d * 2.0 + 4.0 * hm);
+  }
+  // [u v] = h2 W_gate_up^T
+  {
+    GemmArgs g = gemm_args();
+    g.A = act.at(act.L.h2);
+    g.lda = D.d;
+    g.B = w.w_gate_up;
+    g.ldb = D.d;
+    g.C = act.at(act.L.uv);
+    g.ldc = 2 * D.f;
+    g.N = static_cast<int32_t>(2 * D.f);
+    g.K = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = static_cast<int32_t>(D.S);
+    if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
+  }
+  // s = silu(u) * v
+  {
+    EltArgs a{};
+    a.a = act.at(act.L.uv);
+    a.out = act.at(act.L.s);
+    a.rc = {mv.count, static_cast<int32_t>(D.S), T};
+    a.f = static_cast<int32_t>(D.f);
+    ProfScope ps("ld_swiglu_fwd_k", s);
+    if ((e = launch_swiglu_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "swiglu_fwd: %s", hipGetErrorString(e));
+    ps.end(0, D.es * hm * D.f * 3.0);
+  }
+  // X[kept rows] = zk + r * (s W_down^T)  (scatter into the residual stream)
+  {
+    GemmArgs g = gemm_args();
+    g.A = act.at(act.L.s);
+    g.lda = D.f;
+    g.B = w.w_down;
+    g.ldb = D.f;
+    g.C = x;
+    g.ldc = D.d;
+    g.R = act.at(act.L.zk);
+    g.ldr = D.d;
+    g.r_mapped = 0;
+    g.out_map = {mv.idx, static_cast<int32_t>(D.S)};
+    g.alpha_dev = mv.r;
+    g.N = static_cast<int32_t>(D.d);
+    g.K = static_cast<int32_t>(D.f);
+    g.dev_count = mv.count;
+    g.count_mult = static_cast<int32_t>(D.S);
+    if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.f, s)) return rc;
+  }
+  return LD_OK;
+}
+
+int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const ActPtrs& act,
+                   const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, hipStream_t s) {
+  const int dt = D.dtype;
+  const int64_t T = D.T;
+  const int64_t hc = host_count_if_profiling(mv.count, s);
+  const int64_t hm = hc * D.S;
+  const int32_t S = static_cast<int32_t>(D.S);
+  auto W = [&](size_t off) { return static_cast<void*>(ws + off); };
+  hipError_t e;
+
+  // gk = dL/dX^{l+1} on the kept rows
+  {
+    RowsArgs a{};
+    a.src = dx;
+    a.dst = W(BL.gk);
+    a.src_map = {mv.idx, S};
+    a.dst_map = {nullptr, 1};
+    a.rc = {mv.count, S, T};
+    a.d = static_cast<int32_t>(D.d);
+    ProfScope ps("ld_gather_rows_k", s);
+    if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
+    ps.end(0, 2.0 * D.es * hm * D.d);
+  }
+  // gs = r * gk W_down   [M, f]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.gk);
+    g.lda = D.d;
+    g.B = w.w_down;
+    g.ldb = D.f;
+    g.C = W(BL.gs);
+    g.ldc = D.f;
+    g.alpha_dev = mv.r;
+    g.N = static_cast<int32_t>(D.f);
+    g.K = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    if (int rc = run_gemm(dt, 1, 0, g, T, hm, D.d, s)) return rc;
+  }
+  // dW_down = r * gk^T s   [d, f]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.gk);
+    g.lda = D.d;
+    g.B = act.at(act.L.s);
+    g.ldb = D.f;
+    g.C = dw.w_down;
+    g.ldc = D.f;
+    g.c_f32 = 1;
+    g.alpha_dev = mv.r;
+    g.M = static_cast<int32_t>(D.d);
+    g.N = static_cast<int32_t>(D.f);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    g.count_dim = 1;
+    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s)) return rc;
+  }
+  // guv = SwiGLU backward
+  {
+    EltArgs a{};
+    a.a = act.at(act.L.uv);
+    a.b = W(BL.gs);
+    a.out = W(BL.guv);
+    a.rc = {mv.count, S, T};
+    a.f = static_cast<int32_t>(D.f);
+    ProfScope ps("ld_swiglu_bwd_k", s);
+    if ((e = launch_swiglu_bwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "swiglu_bwd: %s", hipGetErrorString(e));
+    ps.end(0, D.es * hm * D.f * 5.0);
+  }
+  // gh2 = guv W_gate_up   [M, d]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.guv);
+    g.lda = 2 * D.f;
+    g.B = w.w_gate_up;
+    g.ldb = D.d;
+    g.C = W(BL.gh);
+    g.ldc = D.d;
+    g.N = static_cast<int32_t>(D.d);
+    g.K = static_cast<int32_t>(2 * D.f);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    if (int rc = run_gemm(dt, 1, 0, g, T, hm, 2 * D.f, s)) return rc;
+  }
+  // dW_gate_up = guv^T h2   [2f, d]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.guv);
+    g.lda = 2 * D.f;
+    g.B = act.at(act.L.h2);
+    g.ldb = D.d;
+    g.C = dw.w_gate_up;
+    g.ldc = D.d;
+    g.c_f32 = 1;
+    g.M = static_cast<int32_t>(2 * D.f);
+    g.N = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    g.count_dim = 1;
+    if (int rc = run_gemm(dt, 0, 0, g, 2 * D.f, 2 * D.f, hm, s)) return rc;
+  }
+  // gz = gk + RMSNorm_bwd(zk, g_mlp, gh2); dg_mlp
+  {
+    RmsBwdArgs a{};
+    a.x = act.at(act.L.zk);
+    a.g = w.g_mlp;
+    a.rstd = act.at<float>(act.L.rstd2);
+    a.gy = W(BL.gh);
+    a.gres = W(BL.gk);
+    a.gx = W(BL.gz);
+    a.dst = {nullptr, 1};
+    a.dg_part = reinterpret_cast<float*>(ws + BL.dg_part);
+    a.rc = {mv.count, S, T};
+    a.d = static_cast<int32_t>(D.d);
+    ProfScope ps("ld_rmsnorm_bwd_k", s);
+    if ((e = launch_rmsnorm_bwd(dt, a, dw.g_mlp, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_bwd: %s", hipGetErrorString(e));
+    ps.end(0, D.es * hm * D.d * 4.0);
+  }
+  // ga = r * gz W_o   [M, d]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.gz);
+    g.lda = D.d;
+    g.B = w.w_o;
+    g.ldb = D.d;
+    g.C = W(BL.ga);
+    g.ldc = D.d;
+    g.alpha_dev = mv.r;
+    g.N = static_cast<int32_t>(D.d);
+    g.K = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    if (int rc = run_gemm(dt, 1, 0, g, T, hm, D.d, s)) return rc;
+  }
+  // dW_o = r * gz^T att   [d, d]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.gz);
+    g.lda = D.d;
+    g.B = act.at(act.L.att);
+    g.ldb = D.d;
+    g.C = dw.w_o;
+    g.ldc = D.d;
+    g.c_f32 = 1;
+    g.alpha_dev = mv.r;
+    g.M = static_cast<int32_t>(D.d);
+    g.N = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    g.count_dim = 1;
+    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s)) return rc;
+  }
+  // attention backward -> gqkv
+  {
+    AttnArgs a{};
+    a.qkv = act.at(act.L.qkv);
+    a.o = act.at(act.L.att);
+    a.go = W(BL.ga);
+    a.out = W(BL.gqkv);
+    a.lse = act.at<float>(act.L.lse);
+    a.delta = reinterpret_cast<float*>(ws + BL.delta);
+    a.dev_count = mv.count;
+    a.n_seq = static_cast<int32_t>(D.B);
+    a.S = S;
+    a.H = static_cast<int32_t>(D.H);
+    a.dh = static_cast<int32_t>(D.dh);
+    a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.dh)));
+    if ((e = launch_attn_bwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "attn_bwd: %s", hipGetErrorString(e));
+  }
+  // gh1 = gqkv W_qkv   [M, d]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.gqkv);
+    g.lda = 3 * D.d;
+    g.B = w.w_qkv;
+    g.ldb = D.d;
+    g.C = W(BL.gh);
+    g.ldc = D.d;
+    g.N = static_cast<int32_t>(D.d);
+    g.K = static_cast<int32_t>(3 * D.d);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    if (int rc = run_gemm(dt, 1, 0, g, T, hm, 3 * D.d, s)) return rc;
+  }
+  // dW_qkv = gqkv^T h1   [3d, d]
+  {
+    GemmArgs g = gemm_args();
+    g.A = W(BL.gqkv);
+    g.lda = 3 * D.d;
+    g.B = act.at(act.L.h1);
+    g.ldb = D.d;
+    g.C = dw.w_qkv;
+    g.ldc = D.d;
+    g.c_f32 = 1;
+    g.M = static_cast<int32_t>(3 * D.d);
+    g.N = static_cast<int32_t>(D.d);
+    g.dev_count = mv.count;
+    g.count_mult = S;
+    g.count_dim = 1;
+    if (int rc = run_gemm(dt, 0, 0, g, 3 * D.d, 3 * D.d, hm, s)) return rc;
+  }
+  // dL/dX^l[kept rows] = gz + RMSNorm_bwd(xk, g_attn, gh1); dg_attn
+  {
+    RmsBwdArgs a{};
+    a.x = act.at(act.L.xk);
+    a.g = w.g_attn;
+    a.rstd = act.at<float>(act.L.rstd1);
+    a.gy = W(BL.gh);
+    a.gres = W(BL.gz);
+    a.gx = dx;
+    a.dst = {mv.idx, S};
+    a.dg_part = reinterpret_cast<float*>(ws + BL.dg_part);
+    a.rc = {mv.count, S, T};
+    a.d = static_cast<int32_t>(D.d);
+    ProfScope ps("ld_rmsnorm_bwd_k", s);
+    if ((e = launch_rmsnorm_bwd(dt, a, dw.g_attn, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_bwd: %s", hipGetErrorString(e));
+    ps.end(0, D.es * hm * D.d * 4.0);
+  }
+  return LD_OK;
+}
+
+int check_weights(const ld_weights* w) {
+  if (!w || !w->g_attn || !w->w_qkv || !w->w_o || !w->g_mlp || !w->w_gate_up || !w->w_down)
+    return fail(LD_E_INVALID, "weights pointer NULL");
+  return LD_OK;
+}
+int check_grads(const ld_grads* g) {
+  if (!g || !g->g_attn || !g->w_qkv || !g->w_o || !g->g_mlp || !g->w_gate_up || !g->w_down)
+    return fail(LD_E_INVALID, "grads pointer NULL");
+  return LD_OK;
+}
+
+int launch_mask_range(const ld_config* cfg, int32_t n, int32_t batch, const float* p, int32_t first,
+                      uint64_t seed, uint64_t step, const uint8_t* ovr, uint8_t* keep, int32_t* idx,
+                      int32_t* count, float* r_out, hipStream_t s) {
+  for (int32_t l0 = 0; l0 < n; l0 += kMaxMaskLayers) {
+    const int32_t nl = std::min<int32_t>(kMaxMaskLayers, n - l0);
+    MaskArgs a;
+    std::memset(&a, 0, sizeof(a));
+    for (int32_t i = 0; i < nl; ++i) {
+      threshold(p[l0 + i], &a.thr[i], &a.drop_all[i]);
+      a.r[i] = cfg ? residual_scale(cfg, p[l0 + i]) : 0.f;
+    }
+    a.n_layers = nl;
+    a.batch = batch;
+    a.first_layer = first + l0;
+    a.seed = seed;
+    a.step = step;
+    a.keep_override = ovr ? ovr + static_cast<int64_t>(l0) * batch : nullptr;
+    a.keep = keep + static_cast<int64_t>(l0) * batch;
+    a.idx = idx + static_cast<int64_t>(l0) * batch;
+    a.count = count + l0;
+    a.r_out = r_out ? r_out + l0 : nullptr;
+    ProfScope ps("ld_mask_compact", s);
+    hipError_t e = launch_masks(a, s);
+    if (e != hipSuccess) return fail(LD_E_HIP, "mask launch: %s", hipGetErrorString(e));
+    ps.end(0, 13.0 * nl * batch);
+  }
+  return LD_OK;
+}
+
+}  // namespace
+
+// ====================================================================== ABI
+
+extern "C" {
+
+const char* ld_status_string(int status) {
+  switch (status) {
+    case LD_OK: return "LD_OK";
+    case LD_E_INVALID: return "LD_E_INVALID";
+    case LD_E_SHAPE: return "LD_E_SHAPE";
+    case LD_E_UNSUPPORTED: return "LD_E_UNSUPPORTED";
+    case LD_E_WORKSPACE: return "LD_E_WORKSPACE";
+    case LD_E_HIP: return "LD_E_HIP";
+  }
+  return "LD_E_UNKNOWN";
+}
+
+const char* ld_last_error(void) { return t_err.c_str(); }
+
+int ld_schedule_p(int32_t dist, int32_t sched, float p_max, int32_t layer, int32_t n_layers,
+                  int64_t t, int64_t n_steps, float* p_out) {
+  t_err.clear();
+  if (!p_out) return fail(LD_E_INVALID, "p_out is NULL");
+  if (std::isnan(p_max) || p_max < 0.f || p_max > 1.f) return fail(LD_E_INVALID, "p_max outside [0, 1]");
+  if (n_layers < 1 || layer < 0 || layer >= n_layers) return fail(LD_E_INVALID, "layer outside [0, n_layers)");
+  if (n_steps < 1) return fail(LD_E_INVALID, "n_steps < 1");
+  double depth;
+  switch (dist) {
+    case 0: depth = p_max; break;
+    case 1: depth = n_layers == 1 ? 0.0 : static_cast<double>(layer) / (n_layers - 1) * p_max; break;
+    case 2: depth = (layer % 2 == 1) ? static_cast<double>(p_max) : 0.0; break;
+    default: return fail(LD_E_INVALID, "unknown distribution %d", dist);
+  }
+  double tf;
+  const int64_t tc = std::min<int64_t>(std::max<int64_t>(t, 0), n_steps - 1);
+  const double frac = n_steps <= 1 ? 0.0 : static_cast<double>(tc) / static_cast<double>(n_steps - 1);
+  switch (sched) {
+    case 0: tf = 1.0; break;
+    case 1: tf = frac; break;
+    case 2: tf = 1.0 - frac; break;
+    default: return fail(LD_E_INVALID, "unknown schedule %d", sched);
+  }
+  *p_out = static_cast<float>(depth * tf);
+  return LD_OK;
+}
+
+int ld_masks(int32_t n_layers, int32_t batch, const float* p, int32_t first_layer, uint64_t seed,
+             uint64_t step, uint8_t* keep, int32_t* idx, int32_t* count, void* stream) {
+  t_err.clear();
+  if (n_layers < 1 || n_layers > kMaxMaskLayers) return fail(LD_E_INVALID, "n_layers outside [1, %d]", kMaxMaskLayers);
+  if (batch < 1) return fail(LD_E_INVALID, "batch < 1");
+  if (first_layer < 0) return fail(LD_E_INVALID, "first_layer < 0");
+  if (!p || !keep || !idx || !count) return fail(LD_E_INVALID, "NULL pointer");
+  for (int32_t i = 0; i < n_layers; ++i)
+    if (int rc = check_p(p[i])) return rc;
+  return launch_mask_range(nullptr, n_layers, batch, p, first_layer, seed, step, nullptr, keep, idx,
+                           count, nullptr, as_stream(stream));
+}
+
+int ld_gather_rows(const ld_config* cfg, const int32_t* idx, const int32_t* count, const void* x,
+                   void* xk, void* stream) {
+  t_err.clear();
+  Dims D;
+  if (int rc = check_cfg(cfg, &D)) return rc;
+  if (!idx || !count || !x || !xk) return fail(LD_E_INVALID, "NULL pointer");
+  RowsArgs a{};
+  a.src = x;
+  a.dst = xk;
+  a.src_map = {idx, static_cast<int32_t>(D.S)};
+  a.dst_map = {nullptr, 1};
+  a.rc = {count, static_cast<int32_t>(D.S), D.T};
+  a.d = static_cast<int32_t>(D.d);
+  hipError_t e = launch_gather(D.dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+int ld_scatter_add_rows(const ld_config* cfg, const int32_t* idx, const int32_t* count, float r,
+                        const void* yk, void* x, void* stream) {
+  t_err.clear();
+  Dims D;
+  if (int rc = check_cfg(cfg, &D)) return rc;
+  if (!idx || !count || !x || !yk) return fail(LD_E_INVALID, "NULL pointer");
+  if (!std::isfinite(r)) return fail(LD_E_INVALID, "r not finite");
+  RowsArgs a{};
+  a.src = yk;
+  a.dst = x;
+  a.src_map = {nullptr, 1};
+  a.dst_map = {idx, static_cast<int32_t>(D.S)};
+  a.rc = {count, static_cast<int32_t>(D.S), D.T};
+  a.d = static_cast<int32_t>(D.d);
+  a.r = r;
+  hipError_t e = launch_scatter_add(D.dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "scatter_add: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+size_t ld_layer_ctx_bytes(const ld_config* cfg) {
+  Dims D;
+  if (check_cfg(cfg, &D)) return 0;
+  return mask_layout(1, D.B).total + act_layout(D).total;
+}
+
+size_t ld_layer_ws_bytes(const ld_config* cfg) {
+  Dims D;
+  if (check_cfg(cfg, &D)) return 0;
+  return bwd_layout(D).total;
+}
+
+size_t ld_stack_ws_bytes(const ld_config* cfg, int32_t n_layers) {
+  Dims D;
+  if (check_cfg(cfg, &D) || n_layers < 1) return 0;
+  return mask_layout(n_layers, D.B).total + static_cast<size_t>(n_layers) * act_layout(D).total +
+         bwd_layout(D).total;
+}
+
+int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float p, uint64_t seed,
+                 uint64_t step, void* x, void* ctx, void* ws, size_t ws_bytes,
+                 const uint8_t* keep_override, void* stream) {
+  t_err.clear();
+  Dims D;
+  if (int rc = check_cfg(cfg, &D)) return rc;
+  if (int rc = check_weights(w)) return rc;
+  if (int rc = check_p(p)) return rc;
+  if (layer < 0) return fail(LD_E_INVALID, "layer < 0");
+  if (!x || !ctx) return fail(LD_E_INVALID, "NULL pointer");
+  (void)ws;
+  (void)ws_bytes;
+  hipStream_t s = as_stream(stream);
+  const MaskLayout ml = mask_layout(1, D.B);
+  char* c = static_cast<char*>(ctx);
+  uint8_t* keep = reinterpret_cast<uint8_t*>(c + ml.keep);
+  int32_t* idx = reinterpret_cast<int32_t*>(c + ml.idx);
+  int32_t* count = reinterpret_cast<int32_t*>(c + ml.count);
+  float* r = reinterpret_cast<float*>(c + ml.r);
+  if (int rc = launch_mask_range(cfg, 1, static_cast<int32_t>(D.B), &p, layer, seed, step,
+                                 keep_override, keep, idx, count, r, s))
+    return rc;
+  ActPtrs act{c + ml.total, act_layout(D)};
+  return layer_forward(cfg, D, *w, MaskView{keep, idx, count, r}, act, x, s);
+}
+
+int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, void* dx,
+                 const ld_grads* dw, void* ws, size_t ws_bytes, void* stream) {
+  t_err.clear();
+  Dims D;
+  if (int rc = check_cfg(cfg, &D)) return rc;
+  if (int rc = check_weights(w)) return rc;
+  if (int rc = check_grads(dw)) return rc;
+  if (!ctx || !dx || !ws) return fail(LD_E_INVALID, "NULL pointer");
+  const BwdLayout BL = bwd_layout(D);
+  if (ws_bytes < BL.total) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, BL.total);
+  const MaskLayout ml = mask_layout(1, D.B);
+  char* c = const_cast<char*>(static_cast<const char*>(ctx));
+  MaskView mv{reinterpret_cast<uint8_t*>(c + ml.keep), reinterpret_cast<int32_t*>(c + ml.idx),
+              reinterpret_cast<int32_t*>(c + ml.count), reinterpret_cast<float*>(c + ml.r)};
+  ActPtrs act{c + ml.total, act_layout(D)};
+  return layer_backward(D, *w, mv, act, BL, static_cast<char*>(ws), dx, *dw, as_stream(stream));
+}
+
+int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const float* p,
+                  uint64_t seed, uint64_t step, void* x, void* dx, const ld_grads* dw, void* ws,
+                  size_t ws_bytes, const uint8_t* keep_override, uint8_t* keep_out,
+                  int32_t* idx_out, int32_t* count_out, void* stream) {
+  t_err.clear();
+  Dims D;
+  if (int rc = check_cfg(cfg, &D)) return rc;
+  if (n_layers < 1 || n_layers > 1024) return fail(LD_E_INVALID, "n_layers outside [1, 1024]");
+  if (!w || !p || !dw || !x || !dx || !ws) return fail(LD_E_INVALID, "NULL pointer");
+  for (int32_t l = 0; l < n_layers; ++l) {
+    if (int rc = check_weights(&w[l])) return rc;
+    if (int rc = check_grads(&dw[l])) return rc;
+    if (int rc = check_p(p[l])) return rc;
+  }
+  const size_t need = ld_stack_ws_bytes(cfg, n_layers);
+  if (ws_bytes < need) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = as_stream(stream);
+  const int64_t L = n_layers, B = D.B;
+  const MaskLayout ml = mask_layout(L, B);
+  const ActLayout al = act_layout(D);
+  const BwdLayout BL = bwd_layout(D);
+  char* base = static_cast<char*>(ws);
+  uint8_t* keep = reinterpret_cast<uint8_t*>(base + ml.keep);
+  int32_t* idx = reinterpret_cast<int32_t*>(base + ml.idx);
+  int32_t* count = reinterpret_cast<int32_t*>(base + ml.count);
+  float* r = reinterpret_cast<float*>(base + ml.r);
+  char* acts = base + ml.total;
+  char* bws = acts + static_cast<size_t>(L) * al.total;
+
+  if (int rc = launch_mask_range(cfg, n_layers, static_cast<int32_t>(B), p, 0, seed, step,
+                                 keep_override, keep, idx, count, r, s))
+    return rc;
+  auto view = [&](int64_t l) {
+    return MaskView{keep + l * B, idx + l * B, count + l, r + l};
+  };
+  for (int64_t l = 0; l < L; ++l) {
+    ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
+    if (int rc = layer_forward(cfg, D, w[l], view(l), act, x, s)) return rc;
+  }
+  for (int64_t l = L - 1; l >= 0; --l) {
+    ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
+    if (int rc = layer_backward(D, w[l], view(l), act, BL, bws, dx, dw[l], s)) return rc;
+  }
+  if (keep_out) LD_HIP(hipMemcpyAsync(keep_out, keep, L * B, hipMemcpyDeviceToDevice, s));
+  if (idx_out) LD_HIP(hipMemcpyAsync(idx_out, idx, 4 * L * B, hipMemcpyDeviceToDevice, s));
+  if (count_out) LD_HIP(hipMemcpyAsync(count_out, count, 4 * L, hipMemcpyDeviceToDevice, s));
+  return LD_OK;
+}
+
+// ------------------------------------------------------ kernel-level calls
+
+int ld_rmsnorm_fwd(int32_t dtype, int32_t rows, int32_t d, float eps, const void* x, const void* g,
+                   void* y, float* rstd, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (rows < 0 || d < 1) return fail(LD_E_SHAPE, "bad shape");
+  if (d % (dtype == LD_BF16 ? 8 : 4) || d > (dtype == LD_BF16 ? 8192 : 4096)) return fail(LD_E_SHAPE, "unsupported d");
+  if (!(eps > 0.f)) return fail(LD_E_INVALID, "eps must be > 0");
+  if (rows == 0) return LD_OK;
+  if (!x || !g || !y || !rstd) return fail(LD_E_INVALID, "NULL pointer");
+  RmsFwdArgs a{};
+  a.x = x;
+  a.src = {nullptr, 1};
+  a.g = g;
+  a.y = y;
+  a.rstd = rstd;
+  a.rc = {nullptr, 1, rows};
+  a.d = d;
+  a.eps = eps;
+  hipError_t e = launch_rmsnorm_fwd(dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+size_t ld_rmsnorm_bwd_ws_bytes(int32_t rows, int32_t d) {
+  if (rows < 0 || d < 1) return 0;
+  return 4ull * rmsnorm_bwd_blocks(rows) * d;
+}
+
+int ld_rmsnorm_bwd(int32_t dtype, int32_t rows, int32_t d, const void* x, const void* g,
+                   const float* rstd, const void* gy, const void* gres, void* gx, float* dg,
+                   void* ws, size_t ws_bytes, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (rows < 0 || d < 1) return fail(LD_E_SHAPE, "bad shape");
+  if (d % (dtype == LD_BF16 ? 8 : 4) || d > (dtype == LD_BF16 ? 8192 : 4096)) return fail(LD_E_SHAPE, "unsupported d");
+  if (!g || !dg || !ws || (rows > 0 && (!x || !rstd || !gy || !gx))) return fail(LD_E_INVALID, "NULL pointer");
+  if (ws_bytes < ld_rmsnorm_bwd_ws_bytes(rows, d)) return fail(LD_E_WORKSPACE, "workspace too small");
+  RmsBwdArgs a{};
+  a.x = x;
+  a.g = g;
+  a.rstd = rstd;
+  a.gy = gy;
+  a.gres = gres;
+  a.gx = gx;
+  a.dst = {nullptr, 1};
+  a.dg_part = static_cast<float*>(ws);
+  a.rc = {nullptr, 1, rows};
+  a.d = d;
+  hipError_t e = launch_rmsnorm_bwd(dtype, a, dg, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "rmsnorm_bwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+int ld_swiglu_fwd(int32_t dtype, int32_t rows, int32_t f, const void* uv, void* s, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (rows < 0 || f < 1 || f % (dtype == LD_BF16 ? 8 : 4)) return fail(LD_E_SHAPE, "bad shape");
+  if (rows == 0) return LD_OK;
+  if (!uv || !s) return fail(LD_E_INVALID, "NULL pointer");
+  EltArgs a{};
+  a.a = uv;
+  a.out = s;
+  a.rc = {nullptr, 1, rows};
+  a.f = f;
+  hipError_t e = launch_swiglu_fwd(dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "swiglu_fwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+int ld_swiglu_bwd(int32_t dtype, int32_t rows, int32_t f, const void* uv, const void* gs,
+                  void* guv, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (rows < 0 || f < 1 || f % (dtype == LD_BF16 ? 8 : 4)) return fail(LD_E_SHAPE, "bad shape");
+  if (rows == 0) return LD_OK;
+  if (!uv || !gs || !guv) return fail(LD_E_INVALID, "NULL pointer");
+  EltArgs a{};
+  a.a = uv;
+  a.b = gs;
+  a.out = guv;
+  a.rc = {nullptr, 1, rows};
+  a.f = f;
+  hipError_t e = launch_swiglu_bwd(dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "swiglu_bwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+int ld_gemm(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int32_t N, int32_t K,
+            const void* A, int32_t lda, const void* B, int32_t ldb, void* C, int32_t ldc,
+            int32_t c_f32, float alpha, const void* R, int32_t ldr, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (M < 0 || N < 0 || K < 0) return fail(LD_E_SHAPE, "negative extent");
+  if (M == 0 || N == 0) return LD_OK;
+  if (!C || (K > 0 && (!A || !B))) return fail(LD_E_INVALID, "NULL pointer");
+  if (dtype == LD_F32) c_f32 = 1;
+  if (c_f32 && R && dtype == LD_BF16) return fail(LD_E_UNSUPPORTED, "float32 C with a residual needs LD_F32");
+  if (ldc < N || (R && ldr < N)) return fail(LD_E_SHAPE, "ldc/ldr smaller than N");
+  if (K > 0) {
+    if (lda < (a_kcontig ? K : M) || ldb < (b_kcontig ? K : N)) return fail(LD_E_SHAPE, "lda/ldb too small");
+    if (dtype == LD_BF16) {
+      if (lda % 8 || ldb % 8) return fail(LD_E_SHAPE, "bf16 needs lda, ldb multiples of 8");
+      if ((a_kcontig || b_kcontig) && K % 8) return fail(LD_E_SHAPE, "bf16 needs K %% 8 == 0");
+      if ((!a_kcontig && M % 8) || (!b_kcontig && N % 8))
+        return fail(LD_E_SHAPE, "bf16 needs M (N) %% 8 == 0 for a k-strided A (B)");
+    }
+  }
+  GemmArgs g = gemm_args();
+  g.A = A;
+  g.B = B;
+  g.C = C;
+  g.R = R;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.ldr = ldr;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.out_map = {nullptr, 1};
+  g.alpha = alpha;
+  g.c_f32 = c_f32;
+  return run_gemm(dtype, a_kcontig ? 1 : 0, b_kcontig ? 1 : 0, g, M, M, K, as_stream(stream));
+}
+
+int ld_attn_fwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
+                const void* qkv, void* o, float* lse, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (n_seq < 0 || seq < 1 || n_heads < 1) return fail(LD_E_SHAPE, "bad shape");
+  if (dtype == LD_BF16 ? (d_head != 64 && d_head != 128) || seq % 64
+                       : (d_head != 16 && d_head != 32 && d_head != 64))
+    return fail(LD_E_UNSUPPORTED, "unsupported d_head/seq");
+  if (n_seq == 0) return LD_OK;
+  if (!qkv || !o || !lse) return fail(LD_E_INVALID, "NULL pointer");
+  AttnArgs a{};
+  a.qkv = qkv;
+  a.out = o;
+  a.lse = lse;
+  a.n_seq = n_seq;
+  a.S = seq;
+  a.H = n_heads;
+  a.dh = d_head;
+  a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(d_head)));
+  hipError_t e = launch_attn_fwd(dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "attn_fwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+size_t ld_attn_bwd_ws_bytes(int32_t n_seq, int32_t seq, int32_t n_heads) {
+  if (n_seq < 0 || seq < 1 || n_heads < 1) return 0;
+  return 4ull * n_seq * seq * n_heads;
+}
+
+int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
+                const void* qkv, const void* o, const float* lse, const void* go, void* gqkv,
+                void* ws, size_t ws_bytes, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (n_seq < 0 || seq < 1 || n_heads < 1) return fail(LD_E_SHAPE, "bad shape");
+  if (dtype == LD_BF16 ? (d_head != 64 && d_head != 128) || seq % 64
+                       : (d_head != 16 && d_head != 32 && d_head != 64))
+    return fail(LD_E_UNSUPPORTED, "unsupported d_head/seq");
+  if (n_seq == 0) return LD_OK;
+  if (!qkv || !o || !lse || !go || !gqkv || !ws) return fail(LD_E_INVALID, "NULL pointer");
+  if (ws_bytes < ld_attn_bwd_ws_bytes(n_seq, seq, n_heads)) return fail(LD_E_WORKSPACE, "workspace too small");
+  AttnArgs a{};
+  a.qkv = qkv;
+  a.o = o;
+  a.go = go;
+  a.out = gqkv;
+  a.lse = const_cast<float*>(lse);
+  a.delta = static_cast<float*>(ws);
+  a.n_seq = n_seq;
+  a.S = seq;
+  a.H = n_heads;
+  a.dh = d_head;
+  a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(d_head)));
+  hipError_t e = launch_attn_bwd(dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "attn_bwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+// -------------------------------------------------------------- profiling
+
+int ld_prof_start(const char* kernel_name) {
+  t_err.clear();
+  if (!kernel_name) return fail(LD_E_INVALID, "kernel_name is NULL");
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.name = kernel_name;
+  g_prof.recs.clear();
+  g_prof.next = 0;
+  g_prof.on = true;
+  return LD_OK;
+}
+
+int ld_prof_stop(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = false;
+  return LD_OK;
+}
+
+int ld_prof_result(int64_t* launches, double* total_ms, double* flops, double* bytes) {
+  t_err.clear();
+  if (!launches || !total_ms || !flops || !bytes) return fail(LD_E_INVALID, "NULL pointer");
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  double ms = 0, fl = 0, by = 0;
+  for (const ProfRec& r : g_prof.recs) {
+    LD_HIP(hipEventSynchronize(r.e1));
+    float t = 0.f;
+    LD_HIP(hipEventElapsedTime(&t, r.e0, r.e1));
+    ms += t;
+    fl += r.flops;
+    by += r.bytes;
+  }
+  *launches = static_cast<int64_t>(g_prof.recs.size());
+  *total_ms = ms;
+  *flops = fl;
+  *bytes = by;
+  return LD_OK;
+}
+
+}  // extern "C"

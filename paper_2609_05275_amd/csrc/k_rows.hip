@@ -1,0 +1,450 @@
+// Mask + compaction, row gather / scatter-add, RMSNorm and SwiGLU kernels.
+// All of these are HBM-bound: 16-byte vector accesses, one wave per row for
+// the normalisations, fp32 arithmetic on bf16 or fp32 storage.
+#include "ld_internal.h"
+
+namespace ld {
+namespace {
+
+// ------------------------------------------------------------ utilities
+
+template <typename T>
+struct alignas(16) Pack {
+  static constexpr int N = 16 / sizeof(T);
+  T v[N];
+};
+
+template <typename T>
+__device__ __forceinline__ Pack<T> load16(const T* p) {
+  return *reinterpret_cast<const Pack<T>*>(p);
+}
+template <typename T>
+__device__ __forceinline__ void store16(T* p, const Pack<T>& v) {
+  *reinterpret_cast<Pack<T>*>(p) = v;
+}
+
+__device__ __forceinline__ float to_f(float x) { return x; }
+__device__ __forceinline__ float to_f(bf16 x) { return static_cast<float>(x); }
+template <typename T>
+__device__ __forceinline__ T from_f(float x) {
+  return static_cast<T>(x);  // round to nearest even (v_cvt_pk_bf16_f32 for bf16)
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ int64_t row_count(const RowCount& rc) {
+  return rc.dev_count ? static_cast<int64_t>(*rc.dev_count) * rc.mult : rc.rows;
+}
+
+__device__ __forceinline__ int64_t map_row(const RowMap& m, int64_t row) {
+  if (!m.idx) return row;
+  return static_cast<int64_t>(m.idx[row / m.S]) * m.S + row % m.S;
+}
+
+// ------------------------------------------------- Philox4x64-10 + masks
+// Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
+// (SC'11): 10 rounds of two 64x64->128 multiplies, the key bumped by the
+// Weyl constants between rounds.  Only word 0 of the output is used.
+__device__ __forceinline__ uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2,
+                                                 uint64_t c3, uint64_t k0, uint64_t k1) {
+  constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
+  constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    if (round) {
+      k0 += kW0;
+      k1 += kW1;
+    }
+    const uint64_t lo0 = kM0 * c0, hi0 = __umul64hi(kM0, c0);
+    const uint64_t lo1 = kM1 * c2, hi1 = __umul64hi(kM1, c2);
+    const uint64_t n0 = hi1 ^ c1 ^ k0;
+    const uint64_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  return c0;
+}
+
+// One workgroup per layer.  Each chunk of blockDim samples draws its bits,
+// a 64-wide ballot + popcount of the lower lanes gives each kept sample its
+// rank inside the wave, and a serial scan of the per-wave totals in LDS gives
+// the wave offsets, so the kept list comes out ascending.
+__global__ __launch_bounds__(1024) void ld_mask_compact(MaskArgs a) {
+  __shared__ int wave_tot[16];
+  const int layer = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_waves = blockDim.x >> 6;
+  const int64_t row = static_cast<int64_t>(layer) * a.batch;
+  int base = 0;
+  for (int b0 = 0; b0 < a.batch; b0 += blockDim.x) {
+    const int b = b0 + tid;
+    int keep = 0;
+    if (b < a.batch) {
+      if (a.keep_override) {
+        keep = a.keep_override[row + b] != 0;
+      } else if (!a.drop_all[layer]) {
+        const uint64_t w = philox_word0(static_cast<uint64_t>(b),
+                                        static_cast<uint64_t>(a.first_layer + layer), a.step, 0,
+                                        a.seed, 0);
+        keep = !(w < a.thr[layer]);
+      }
+      a.keep[row + b] = static_cast<uint8_t>(keep);
+    }
+    const uint64_t ball = __ballot(keep);
+    const int rank = __popcll(ball & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_tot[wave] = __popcll(ball);
+    __syncthreads();
+    int off = base, tot = 0;
+    for (int w = 0; w < n_waves; ++w) {
+      if (w < wave) off += wave_tot[w];
+      tot += wave_tot[w];
+    }
+    if (keep) a.idx[row + off + rank] = b;
+    __syncthreads();
+    base += tot;
+  }
+  for (int j = base + tid; j < a.batch; j += blockDim.x) a.idx[row + j] = -1;
+  if (tid == 0) {
+    a.count[layer] = base;
+    if (a.r_out) a.r_out[layer] = a.r[layer];
+  }
+}
+
+// ------------------------------------------------------- gather / scatter
+
+template <typename T>
+__global__ __launch_bounds__(256) void ld_gather_rows_k(RowsArgs a) {
+  constexpr int VN = Pack<T>::N;
+  const int64_t chunks = a.d / VN;
+  const int64_t total = row_count(a.rc) * chunks;
+  const T* src = static_cast<const T*>(a.src);
+  T* dst = static_cast<T*>(a.dst);
+  for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < total; id += gridDim.x * 256ll) {
+    const int64_t row = id / chunks, c = (id % chunks) * VN;
+    store16(dst + map_row(a.dst_map, row) * a.d + c, load16(src + map_row(a.src_map, row) * a.d + c));
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void ld_scatter_add_rows_k(RowsArgs a) {
+  constexpr int VN = Pack<T>::N;
+  const int64_t chunks = a.d / VN;
+  const int64_t total = row_count(a.rc) * chunks;
+  const T* y = static_cast<const T*>(a.src);
+  T* x = static_cast<T*>(a.dst);
+  for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < total; id += gridDim.x * 256ll) {
+    const int64_t row = id / chunks, c = (id % chunks) * VN;
+    T* xp = x + map_row(a.dst_map, row) * a.d + c;
+    const Pack<T> yv = load16(y + map_row(a.src_map, row) * a.d + c);
+    Pack<T> xv = load16(xp);
+#pragma unroll
+    for (int i = 0; i < VN; ++i) xv.v[i] = from_f<T>(__builtin_fmaf(a.r, to_f(yv.v[i]), to_f(xv.v[i])));
+    store16(xp, xv);
+  }
+}
+
+// ---------------------------------------------------------------- RMSNorm
+// One wave per row, NCH 16-byte chunks per lane held in registers.
+
+template <typename T, int NCH>
+__global__ __launch_bounds__(256) void ld_rmsnorm_fwd_k(RmsFwdArgs a) {
+  constexpr int VN = Pack<T>::N;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row = blockIdx.x * 4ll + wave;
+  if (row >= row_count(a.rc)) return;
+  const T* x = static_cast<const T*>(a.x) + map_row(a.src, row) * a.d;
+  const T* g = static_cast<const T*>(a.g);
+  Pack<T> v[NCH];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 64 + lane) * VN;
+    if (col < a.d) {
+      v[c] = load16(x + col);
+#pragma unroll
+      for (int i = 0; i < VN; ++i) {
+        const float f = to_f(v[c].v[i]);
+        ss = __builtin_fmaf(f, f, ss);
+      }
+    }
+  }
+  ss = wave_sum(ss);
+  const float rstd = rsqrtf(ss / static_cast<float>(a.d) + a.eps);
+  T* y = static_cast<T*>(a.y) + row * a.d;
+  T* xc = a.xcopy ? static_cast<T*>(a.xcopy) + row * a.d : nullptr;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 64 + lane) * VN;
+    if (col < a.d) {
+      if (xc) store16(xc + col, v[c]);
+      const Pack<T> gv = load16(g + col);
+      Pack<T> o;
+#pragma unroll
+      for (int i = 0; i < VN; ++i) o.v[i] = from_f<T>(to_f(v[c].v[i]) * rstd * to_f(gv.v[i]));
+      store16(y + col, o);
+    }
+  }
+  if (lane == 0) a.rstd[row] = rstd;
+}
+
+constexpr int kBwdRowsPerWave = 16;
+constexpr int kBwdRowsPerBlock = 4 * kBwdRowsPerWave;
+
+// gx = gres + rstd*(g*gy) - x*rstd^3*mean_d(x*g*gy); per-block dg partials
+// summed over the block's rows in a fixed order (rows in sequence inside a
+// wave, then waves 0..3 through LDS).
+template <typename T, int NCH>
+__global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
+  constexpr int VN = Pack<T>::N;
+  extern __shared__ float dg_lds[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t rows = row_count(a.rc);
+  const T* gp = static_cast<const T*>(a.g);
+  float gf[NCH][VN], dga[NCH][VN];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 64 + lane) * VN;
+    Pack<T> gv{};
+    if (col < a.d) gv = load16(gp + col);
+#pragma unroll
+    for (int i = 0; i < VN; ++i) {
+      gf[c][i] = to_f(gv.v[i]);
+      dga[c][i] = 0.f;
+    }
+  }
+  const float inv_d = 1.f / static_cast<float>(a.d);
+  const int64_t r0 = blockIdx.x * static_cast<int64_t>(kBwdRowsPerBlock) + wave * kBwdRowsPerWave;
+  for (int k = 0; k < kBwdRowsPerWave; ++k) {
+    const int64_t row = r0 + k;
+    if (row >= rows) break;
+    const T* x = static_cast<const T*>(a.x) + row * a.d;
+    const T* gy = static_cast<const T*>(a.gy) + row * a.d;
+    const float rstd = a.rstd[row];
+    Pack<T> xv[NCH], gyv[NCH];
+    float dot = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int col = (c * 64 + lane) * VN;
+      if (col < a.d) {
+        xv[c] = load16(x + col);
+        gyv[c] = load16(gy + col);
+#pragma unroll
+        for (int i = 0; i < VN; ++i)
+          dot = __builtin_fmaf(to_f(xv[c].v[i]) * gf[c][i], to_f(gyv[c].v[i]), dot);
+      }
+    }
+    dot = wave_sum(dot);
+    const float coef = rstd * rstd * rstd * dot * inv_d;
+    T* gx = static_cast<T*>(a.gx) + map_row(a.dst, row) * a.d;
+    const T* gres = a.gres ? static_cast<const T*>(a.gres) + row * a.d : nullptr;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int col = (c * 64 + lane) * VN;
+      if (col < a.d) {
+        Pack<T> rv{};
+        if (gres) rv = load16(gres + col);
+        Pack<T> o;
+#pragma unroll
+        for (int i = 0; i < VN; ++i) {
+          const float xf = to_f(xv[c].v[i]), gyf = to_f(gyv[c].v[i]);
+          float val = rstd * gf[c][i] * gyf - xf * coef;
+          if (gres) val += to_f(rv.v[i]);
+          o.v[i] = from_f<T>(val);
+          dga[c][i] = __builtin_fmaf(gyf * xf, rstd, dga[c][i]);
+        }
+        store16(gx + col, o);
+      }
+    }
+  }
+  for (int w = 0; w < 4; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const int col = (c * 64 + lane) * VN;
+        if (col < a.d) {
+#pragma unroll
+          for (int i = 0; i < VN; ++i) dg_lds[col + i] = (w == 0 ? 0.f : dg_lds[col + i]) + dga[c][i];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  float* part = a.dg_part + static_cast<int64_t>(blockIdx.x) * a.d;
+  for (int col = threadIdx.x; col < a.d; col += 256) part[col] = dg_lds[col];
+}
+
+__global__ __launch_bounds__(256) void ld_dg_reduce_k(const float* part, int64_t n_blocks, int d,
+                                                      float* dg) {
+  const int col = blockIdx.x * 256 + threadIdx.x;
+  if (col >= d) return;
+  float s = 0.f;
+  for (int64_t b = 0; b < n_blocks; ++b) s += part[b * d + col];
+  dg[col] = s;
+}
+
+// ----------------------------------------------------------------- SwiGLU
+
+__device__ __forceinline__ float sigmoidf_(float u) { return 1.f / (1.f + expf(-u)); }
+
+template <typename T>
+__global__ __launch_bounds__(256) void ld_swiglu_fwd_k(EltArgs a) {
+  constexpr int VN = Pack<T>::N;
+  const int64_t chunks = a.f / VN;
+  const int64_t total = row_count(a.rc) * chunks;
+  const T* uv = static_cast<const T*>(a.a);
+  T* s = static_cast<T*>(a.out);
+  for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < total; id += gridDim.x * 256ll) {
+    const int64_t row = id / chunks, c = (id % chunks) * VN;
+    const Pack<T> u = load16(uv + row * 2 * a.f + c);
+    const Pack<T> v = load16(uv + row * 2 * a.f + a.f + c);
+    Pack<T> o;
+#pragma unroll
+    for (int i = 0; i < VN; ++i) {
+      const float uf = to_f(u.v[i]);
+      o.v[i] = from_f<T>(uf * sigmoidf_(uf) * to_f(v.v[i]));
+    }
+    store16(s + row * a.f + c, o);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void ld_swiglu_bwd_k(EltArgs a) {
+  constexpr int VN = Pack<T>::N;
+  const int64_t chunks = a.f / VN;
+  const int64_t total = row_count(a.rc) * chunks;
+  const T* uv = static_cast<const T*>(a.a);
+  const T* gs = static_cast<const T*>(a.b);
+  T* guv = static_cast<T*>(a.out);
+  for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < total; id += gridDim.x * 256ll) {
+    const int64_t row = id / chunks, c = (id % chunks) * VN;
+    const Pack<T> u = load16(uv + row * 2 * a.f + c);
+    const Pack<T> v = load16(uv + row * 2 * a.f + a.f + c);
+    const Pack<T> g = load16(gs + row * a.f + c);
+    Pack<T> gu, gv;
+#pragma unroll
+    for (int i = 0; i < VN; ++i) {
+      const float uf = to_f(u.v[i]), vf = to_f(v.v[i]), gf = to_f(g.v[i]);
+      const float sg = sigmoidf_(uf);
+      gu.v[i] = from_f<T>(gf * vf * sg * (1.f + uf * (1.f - sg)));
+      gv.v[i] = from_f<T>(gf * uf * sg);
+    }
+    store16(guv + row * 2 * a.f + c, gu);
+    store16(guv + row * 2 * a.f + a.f + c, gv);
+  }
+}
+
+int elt_grid(int64_t total_chunks) {
+  int64_t g = (total_chunks + 255) / 256;
+  if (g > 8192) g = 8192;
+  if (g < 1) g = 1;
+  return static_cast<int>(g);
+}
+
+template <typename T>
+int nch_for(int d) {
+  const int per = 64 * Pack<T>::N;
+  return (d + per - 1) / per;
+}
+
+template <typename T>
+hipError_t rms_fwd_t(const RmsFwdArgs& a, hipStream_t s) {
+  const int nch = nch_for<T>(a.d);
+  const int64_t max_rows = a.rc.dev_count ? a.rc.rows : a.rc.rows;
+  const dim3 grid(static_cast<unsigned>((max_rows + 3) / 4));
+  if (max_rows == 0) return hipSuccess;
+#define LD_RF(N) \
+  case N: hipLaunchKernelGGL((ld_rmsnorm_fwd_k<T, N>), grid, dim3(256), 0, s, a); break;
+  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : nch <= 8 ? 8 : 16) {
+    LD_RF(1) LD_RF(2) LD_RF(4) LD_RF(8) LD_RF(16)
+  }
+#undef LD_RF
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t rms_bwd_t(const RmsBwdArgs& a, float* dg, hipStream_t s) {
+  const int nch = nch_for<T>(a.d);
+  const int64_t nblk = rmsnorm_bwd_blocks(a.rc.rows);
+  const size_t lds = static_cast<size_t>(a.d) * sizeof(float);
+#define LD_RB(N) \
+  case N: hipLaunchKernelGGL((ld_rmsnorm_bwd_k<T, N>), dim3(nblk), dim3(256), lds, s, a); break;
+  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : nch <= 8 ? 8 : 16) {
+    LD_RB(1) LD_RB(2) LD_RB(4) LD_RB(8) LD_RB(16)
+  }
+#undef LD_RB
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(ld_dg_reduce_k, dim3((a.d + 255) / 256), dim3(256), 0, s, a.dg_part, nblk,
+                     a.d, dg);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t rmsnorm_bwd_blocks(int64_t max_rows) {
+  const int64_t n = (max_rows + kBwdRowsPerBlock - 1) / kBwdRowsPerBlock;
+  return n < 1 ? 1 : n;
+}
+
+hipError_t launch_masks(const MaskArgs& a, hipStream_t s) {
+  int threads = ((a.batch + 63) / 64) * 64;
+  if (threads > 1024) threads = 1024;
+  hipLaunchKernelGGL(ld_mask_compact, dim3(a.n_layers), dim3(threads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(int dtype, const RowsArgs& a, hipStream_t s) {
+  const int vn = dtype == LD_BF16 ? 8 : 4;
+  const int grid = elt_grid(a.rc.rows * (a.d / vn));
+  if (dtype == LD_BF16)
+    hipLaunchKernelGGL(ld_gather_rows_k<bf16>, dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ld_gather_rows_k<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_add(int dtype, const RowsArgs& a, hipStream_t s) {
+  const int vn = dtype == LD_BF16 ? 8 : 4;
+  const int grid = elt_grid(a.rc.rows * (a.d / vn));
+  if (dtype == LD_BF16)
+    hipLaunchKernelGGL(ld_scatter_add_rows_k<bf16>, dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ld_scatter_add_rows_k<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s) {
+  return dtype == LD_BF16 ? rms_fwd_t<bf16>(a, s) : rms_fwd_t<float>(a, s);
+}
+
+hipError_t launch_rmsnorm_bwd(int dtype, const RmsBwdArgs& a, float* dg, hipStream_t s) {
+  return dtype == LD_BF16 ? rms_bwd_t<bf16>(a, dg, s) : rms_bwd_t<float>(a, dg, s);
+}
+
+hipError_t launch_swiglu_fwd(int dtype, const EltArgs& a, hipStream_t s) {
+  const int vn = dtype == LD_BF16 ? 8 : 4;
+  const int grid = elt_grid(a.rc.rows * (a.f / vn));
+  if (dtype == LD_BF16)
+    hipLaunchKernelGGL(ld_swiglu_fwd_k<bf16>, dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ld_swiglu_fwd_k<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_bwd(int dtype, const EltArgs& a, hipStream_t s) {
+  const int vn = dtype == LD_BF16 ? 8 : 4;
+  const int grid = elt_grid(a.rc.rows * (a.f / vn));
+  if (dtype == LD_BF16)
+    hipLaunchKernelGGL(ld_swiglu_bwd_k<bf16>, dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ld_swiglu_bwd_k<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace ld

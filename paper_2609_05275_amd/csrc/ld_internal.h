@@ -1,0 +1,140 @@
+// Internal declarations shared by the HIP kernel translation units and the
+// host-side C ABI.  Not installed; the public surface is include/layerdrop.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "layerdrop.h"
+
+namespace ld {
+
+using bf16 = __bf16;
+
+// ------------------------------------------------------------ kernel args
+
+// Rows of a compacted activation block.  When dev_count is set the row count
+// is (*dev_count) * mult, read on the device, so no host sync is needed on the
+// kept count; otherwise it is `rows`.
+struct RowCount {
+  const int32_t* dev_count;
+  int32_t mult;
+  int64_t rows;
+};
+
+// Mapping from a compacted row m to a row of a [B, S, d] tensor:
+// row(m) = idx[m / S] * S + m % S, or m itself when idx is null.
+struct RowMap {
+  const int32_t* idx;
+  int32_t S;
+};
+
+constexpr int kMaxMaskLayers = 128;
+
+struct MaskArgs {
+  uint64_t thr[kMaxMaskLayers];     // drop iff word < thr (when !drop_all)
+  uint8_t drop_all[kMaxMaskLayers]; // p >= 1
+  float r[kMaxMaskLayers];          // residual scale per layer (0 for p >= 1)
+  int32_t n_layers, batch, first_layer;
+  uint64_t seed, step;
+  const uint8_t* keep_override;     // [n_layers][batch] or null
+  uint8_t* keep;                    // [n_layers][batch]
+  int32_t* idx;                     // [n_layers][batch]
+  int32_t* count;                   // [n_layers]
+  float* r_out;                     // [n_layers] or null: copy of r for the layer
+};
+
+struct RmsFwdArgs {
+  const void* x;      // source rows (through `src` map)
+  RowMap src;
+  const void* g;
+  void* xcopy;        // optional compacted copy of the source rows
+  void* y;            // compacted normalised rows
+  float* rstd;        // compacted
+  RowCount rc;
+  int32_t d;
+  float eps;
+};
+
+struct RmsBwdArgs {
+  const void* x;      // compacted rows
+  const void* g;
+  const float* rstd;
+  const void* gy;
+  const void* gres;   // optional compacted residual gradient
+  void* gx;           // output rows through `dst` map
+  RowMap dst;
+  float* dg_part;     // [n_blocks][d]
+  RowCount rc;
+  int32_t d;
+};
+
+struct EltArgs {
+  const void* a;
+  const void* b;
+  void* out;
+  RowCount rc;
+  int32_t f;
+};
+
+struct RowsArgs {
+  const void* src;
+  void* dst;
+  RowMap src_map, dst_map;
+  RowCount rc;
+  int32_t d;
+  float r;
+};
+
+// C[m, n] = (R ? R[m, n] : 0) + alpha * sum_k A(m, k) B(n, k), see ld_gemm.
+struct GemmArgs {
+  const void* A;
+  const void* B;
+  void* C;
+  const void* R;
+  int64_t lda, ldb, ldc, ldr;
+  int32_t M, N, K;
+  const int32_t* dev_count;  // when set: M (count_dim 0) or K (count_dim 1)
+  int32_t count_mult;        //   = (*dev_count) * count_mult
+  int32_t count_dim;
+  RowMap out_map;            // output (and R) row remap; R uses it too when r_mapped
+  int32_t r_mapped;
+  float alpha;
+  const float* alpha_dev;    // when set, alpha is multiplied by *alpha_dev
+  int32_t c_f32;
+};
+
+struct AttnArgs {
+  const void* qkv;
+  const void* o;
+  const void* go;
+  void* out;          // fwd: o ; bwd: gqkv
+  float* lse;         // fwd out / bwd in  [n, H, S]
+  float* delta;       // bwd: rowsum(dO * O) [n, H, S]
+  const int32_t* dev_count;  // kept sequences on the device, or null
+  int32_t n_seq;             // host count (upper bound when dev_count is set)
+  int32_t S, H, dh;
+  float scale;               // 1/sqrt(dh)
+};
+
+// ------------------------------------------------------------- launchers
+// Each returns the HIP error of its launch(es).  Grids are sized for the
+// host upper bound; work past the device count exits early.
+
+hipError_t launch_masks(const MaskArgs& a, hipStream_t s);
+hipError_t launch_gather(int dtype, const RowsArgs& a, hipStream_t s);
+hipError_t launch_scatter_add(int dtype, const RowsArgs& a, hipStream_t s);
+hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s);
+// Needs rmsnorm_bwd_blocks(max_rows) * d floats of dg_part.
+int64_t rmsnorm_bwd_blocks(int64_t max_rows);
+hipError_t launch_rmsnorm_bwd(int dtype, const RmsBwdArgs& a, float* dg, hipStream_t s);
+hipError_t launch_swiglu_fwd(int dtype, const EltArgs& a, hipStream_t s);
+hipError_t launch_swiglu_bwd(int dtype, const EltArgs& a, hipStream_t s);
+hipError_t launch_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,
+                       int64_t max_k, hipStream_t s);
+const char* gemm_kernel_name(int dtype, int a_kcontig, int b_kcontig);
+hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
+const char* attn_fwd_kernel_name(int dtype);
+
+}  // namespace ld

@@ -1,0 +1,145 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/layerdrop.h declares, its host-only schedule function agrees bit for
+bit with the oracle, and invalid arguments are rejected before anything is
+enqueued (no call here reaches the HIP runtime)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_05275_amd as ld
+from oracle import schedule
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "layerdrop.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return set(re.findall(r"\b(ld_[a-z0-9_]+)\s*\(", src))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert len(names) >= 20
+    lib = C.CDLL(ld.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert names == set(ld.EXPORTED)
+
+
+@pytest.mark.parametrize("dist", [0, 1, 2])
+@pytest.mark.parametrize("sched", [0, 1, 2])
+def test_schedule_matches_oracle_bitwise(dist, sched):
+    for L in (1, 2, 12, 16, 32):
+        for p_max in (0.0, 0.1, 0.2, 0.5, 0.99, 1.0):
+            for (t, T) in ((0, 1001), (500, 1001), (1000, 1001), (7, 1), (2000, 1001), (-3, 10)):
+                for l in range(L):
+                    got = ld.ld_schedule_p(dist, sched, p_max, l, L, t, T)
+                    # the ABI takes p_max as float32; give the oracle that same value
+                    want = schedule.rate(dist, sched, float(np.float32(p_max)), l, L, t, T)
+                    assert np.float32(got) == want, (dist, sched, p_max, l, L, t, T)
+
+
+def test_schedule_rejects_bad_arguments():
+    for args in [(3, 0, 0.2, 0, 4, 0, 1), (0, 3, 0.2, 0, 4, 0, 1), (0, 0, 1.5, 0, 4, 0, 1),
+                 (0, 0, float("nan"), 0, 4, 0, 1), (0, 0, 0.2, 4, 4, 0, 1), (0, 0, 0.2, 0, 0, 0, 1),
+                 (0, 0, 0.2, 0, 4, 0, 0)]:
+        with pytest.raises(ld.LdError) as e:
+            ld.ld_schedule_p(*args)
+        assert e.value.status == 1
+
+
+def test_status_strings():
+    assert ld.status_name(0) == "LD_OK"
+    assert ld.status_name(4) == "LD_E_WORKSPACE"
+    assert ld.status_name(99) == "LD_E_UNKNOWN"
+
+
+def _cfg(**kw):
+    base = dict(batch=8, seq=2048, d_model=2048, n_heads=16, d_ff=5504, dtype=ld.LD_BF16)
+    base.update(kw)
+    return ld.config(**base)
+
+
+def test_workspace_sizes():
+    c = _cfg()
+    ctx = ld.ld_layer_ctx_bytes(c)
+    T, d, f, H = 8 * 2048, 2048, 5504, 16
+    assert ctx >= 2 * T * (8 * d + 3 * f) + 8 * T + 4 * T * H
+    assert ld.ld_layer_ws_bytes(c) >= 2 * T * (7 * d + 3 * f)
+    s16 = ld.ld_stack_ws_bytes(c, 16)
+    assert s16 >= 16 * (ctx - 4096) + ld.ld_layer_ws_bytes(c)
+    assert s16 < 288e9 / 4          # fits the GPU's HBM with room to spare
+    assert ld.ld_stack_ws_bytes(_cfg(batch=4, seq=4096, d_model=4096, n_heads=32, d_ff=11008), 32) < 100e9
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_heads=3), 2),                     # d % H != 0
+    (dict(n_heads=64), 3),                    # d_head 32 unsupported in bf16
+    (dict(seq=100), 2),                       # bf16 needs S % 64 == 0
+    (dict(d_ff=1001), 2),
+    (dict(dtype=7), 1),
+    (dict(rms_eps=0.0), 1),
+    (dict(batch=0), 2),
+])
+def test_invalid_configs_rejected(kw, code):
+    c = _cfg(**kw)
+    assert ld.ld_layer_ctx_bytes(c) == 0
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_gather_rows(c, 8, 8, 8, 8, stream=0)
+    assert e.value.status == code
+
+
+def test_invalid_p_and_pointers_rejected():
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_masks([0.1, float("nan")], 0, 0, _Fake((2, 8)), 8, 8, stream=0)
+    assert e.value.status == 1
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_masks([1.5], 0, 0, _Fake((1, 8)), 8, 8, stream=0)
+    assert e.value.status == 1
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_masks([0.5], 0, 0, _Fake((1, 8)), None, 8, stream=0)
+    assert e.value.status == 1
+    c = _cfg()
+    w = {k: 16 for k in ld.WEIGHT_KEYS}
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_layer_fwd(c, w, 0, -0.1, 0, 0, 16, 16, stream=0)
+    assert e.value.status == 1
+    w["w_o"] = None
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_layer_fwd(c, w, 0, 0.1, 0, 0, 16, 16, stream=0)
+    assert e.value.status == 1
+
+
+def test_gemm_shape_checks():
+    with pytest.raises(ld.LdError) as e:   # lda smaller than K
+        ld.ld_gemm(1, 1, 64, 64, 64, _Fake((64, 64), 2), 32, _Fake((64, 64), 2), 64,
+                   _Fake((64, 64), 2), 64, dtype=ld.LD_BF16, stream=0)
+    assert e.value.status == 2
+    with pytest.raises(ld.LdError) as e:   # bf16 K not a multiple of 8
+        ld.ld_gemm(1, 1, 64, 64, 60, _Fake((64, 64), 2), 64, _Fake((64, 64), 2), 64,
+                   _Fake((64, 64), 2), 64, dtype=ld.LD_BF16, stream=0)
+    assert e.value.status == 2
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_gemm(1, 1, -1, 64, 64, 8, 64, 8, 64, 8, 64, dtype=ld.LD_BF16, stream=0)
+    assert e.value.status == 2
+
+
+class _Fake:
+    """Stands in for a device tensor in calls that must fail validation."""
+
+    def __init__(self, shape, es=1):
+        self.shape = shape
+        self._es = es
+
+    def data_ptr(self):
+        return 4096
+
+    def element_size(self):
+        return self._es
+
+    def numel(self):
+        return int(np.prod(self.shape))
