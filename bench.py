@@ -1,0 +1,236 @@
+"""Benchmark of the layer-dropout training step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-sweep] [--no-cpu]
+
+Workload: the 1B-shape stack (16 pre-norm decoder layers, d_model 2048, 16
+heads of 128, SwiGLU d_ff 5504, seq 2048, batch 8, bf16), one forward +
+backward step per iteration through ld_stack_step, per-sequence layer
+dropout with the increasing-layer (ILD) depth distribution.  The headline
+line is at p_max 0.2 with the increasing time schedule at its end (t = 1000
+of a 0..1000 ramp, i.e. the full p_max); the Philox step counter advances
+every iteration, so each iteration draws fresh masks.  A sweep over p_max in
+{0, 0.1, 0.2, 0.5} and t in {0, 500, 1000} follows unless --no-sweep.
+
+value = effective tokens/s = batch*seq / step time (every token of the
+batch, dropped or not, counts: the step trains the whole batch).
+Executed FLOPs per step = F_sl * sum_l kept_l with
+F_sl = 3 * [2*S*(4 d^2 + 3 d d_ff) + 2 d S (S+1)] per kept (sequence, layer).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import ld_inputs as inp  # noqa: E402
+import paper_2609_05275_amd as ld  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+T_RAMP = 1001               # steps 0..1000 of the p_max ramp
+
+
+def f_sl(sh):
+    S, d, f = sh.seq, sh.d_model, sh.d_ff
+    return 3.0 * (2.0 * S * (4 * d * d + 3 * d * f) + 2.0 * d * S * (S + 1))
+
+
+class Stack:
+    def __init__(self, sh, dev):
+        self.sh, self.dev = sh, dev
+        self.cfg = ld.config(sh.batch, sh.seq, sh.d_model, sh.n_heads, sh.d_ff, ld.LD_BF16)
+        L = sh.n_layers
+        self.W = [inp.device_layer_weights(sh, l, dev) for l in range(L)]
+        self.dW = [{k: torch.empty(s, dtype=torch.float32, device=dev)
+                    for k, s in inp.weight_shapes(sh).items()} for _ in range(L)]
+        self.x0 = inp.device_hidden(sh, dev)
+        self.g0 = inp.device_upstream_grad(sh, dev)
+        self.x = torch.empty_like(self.x0)
+        self.g = torch.empty_like(self.g0)
+        self.ws = torch.empty(ld.ld_stack_ws_bytes(self.cfg, L), dtype=torch.uint8, device=dev)
+        self.count = torch.zeros(L, dtype=torch.int32, device=dev)
+
+    def rates(self, p_max, t):
+        L = self.sh.n_layers
+        return [ld.ld_schedule_p(ld.ILD, ld.ITS, p_max, l, L, t, T_RAMP) for l in range(L)]
+
+    def step(self, ps, step, count_out=None):
+        self.x.copy_(self.x0)
+        self.g.copy_(self.g0)
+        ld.ld_stack_step(self.cfg, self.W, ps, 0, step, self.x, self.g, self.dW, self.ws,
+                         count_out=count_out)
+
+    def kept(self, ps, step):
+        """Sum of kept counts of one step (device mask kernel, outside timing)."""
+        L, B = self.sh.n_layers, self.sh.batch
+        keep = torch.empty(L, B, dtype=torch.uint8, device=self.dev)
+        idx = torch.empty(L, B, dtype=torch.int32, device=self.dev)
+        cnt = torch.empty(L, dtype=torch.int32, device=self.dev)
+        ld.ld_masks(ps, 0, step, keep, idx, cnt)
+        return int(cnt.sum().item())
+
+
+def time_steps(st, ps, first_step, steps, warmup):
+    for i in range(warmup):
+        st.step(ps, first_step - warmup + i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        st.step(ps, first_step + i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    kept = [st.kept(ps, first_step + i) for i in range(steps)]
+    return ms, kept
+
+
+def cpu_baseline(sh, target_s=15.0):
+    """The float64 oracle timed on the host: kept sequences through layer 0
+    forward + backward at the full shape, repeated until ~target_s seconds."""
+    from threadpoolctl import threadpool_info
+    from oracle import block
+    import torch as _t
+    w = {k: v.to("cpu", _t.float64).numpy() for k, v in inp.device_layer_weights(sh, 0, "cuda:0").items()}
+    x = inp.device_hidden(sh, "cuda:0")[0].to("cpu", _t.float64).numpy()
+    g = inp.device_upstream_grad(sh, "cuda:0")[0].to("cpu", _t.float64).numpy()
+    n, t0 = 0, time.perf_counter()
+    while True:
+        _, cache = block.forward(x, w, 1.0 / 0.9, sh.n_heads, 1e-5)
+        block.backward(cache, g, w, 1.0 / 0.9, sh.n_heads)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or n >= 64:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return el / n, n, threads
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--p-max", type=float, default=0.2)
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--prof-kernel", default=None,
+                    help="kernel timed with HIP events for the roofline (default: every GEMM "
+                         "variant is measured in a short pass and the slowest total is used)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU; this build has no multi-GPU path "
+              "(the data-parallel sharding is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    sh = inp.SHAPES["1b"]
+    dev = "cuda:0"
+    st = Stack(sh, dev)
+    fsl = f_sl(sh)
+    tokens = sh.batch * sh.seq
+    ps = st.rates(args.p_max, T_RAMP - 1)
+    first = T_RAMP - 1
+
+    # pick the dominant kernel: one profiled step per candidate (untimed)
+    cands = ["ld_gemm_bf16_nt", "ld_gemm_bf16_nn", "ld_gemm_bf16_tn", "ld_attn_fwd_bf16"]
+    prof_kernel = args.prof_kernel
+    st.step(ps, first - 1)
+    per = {}
+    for k in cands:
+        ld.ld_prof_start(k)
+        st.step(ps, first - 1)
+        torch.cuda.synchronize()
+        ld.ld_prof_stop()
+        per[k] = ld.ld_prof_result()["ms"]
+    if prof_kernel is None:
+        prof_kernel = max(per, key=per.get)
+    print(f"# per-kernel ms in one step: {json.dumps({k: round(v, 3) for k, v in per.items()})}",
+          file=sys.stderr, flush=True)
+
+    # headline: timed steps with the dominant kernel's events recorded live
+    for i in range(args.warmup):
+        st.step(ps, first - args.warmup + i)
+    torch.cuda.synchronize()
+    ld.ld_prof_start(prof_kernel)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        st.step(ps, first + i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ld.ld_prof_stop()
+    pr = ld.ld_prof_result()
+    kept = [st.kept(ps, first + i) for i in range(args.steps)]
+    print(f"# headline: {ms:.2f} ms/step, kept seq-layers mean {np.mean(kept):.1f}", file=sys.stderr,
+          flush=True)
+    exec_tflops = fsl * np.mean(kept) / (ms * 1e-3) / 1e12
+    achieved = pr["flops"] / (pr["ms"] * 1e-3) / 1e12 if pr["ms"] > 0 else 0.0
+
+    sweep = []
+    if not args.no_sweep:
+        for p_max in (0.0, 0.1, 0.2, 0.5):
+            for t in (0, 500, 1000):
+                pp = st.rates(p_max, t)
+                sms, skept = time_steps(st, pp, 10_000 + t, 5, 1)
+                f = 1.0 - np.mean(skept) / (sh.n_layers * sh.batch)
+                sweep.append(dict(p_max=p_max, t=t, ms=round(sms, 3), drop_frac=round(f, 4),
+                                  tokens_per_s=round(tokens / (sms * 1e-3), 1),
+                                  exec_tflops=round(fsl * np.mean(skept) / (sms * 1e-3) / 1e12, 1)))
+                print(f"# sweep {sweep[-1]}", file=sys.stderr, flush=True)
+    fit = None
+    if len(sweep) >= 3:
+        keep_frac = np.array([1 - s["drop_frac"] for s in sweep])
+        tms = np.array([s["ms"] for s in sweep])
+        a, c = np.polyfit(keep_frac, tms, 1)
+        pred = a * keep_frac + c
+        r2 = 1 - np.sum((tms - pred) ** 2) / max(np.sum((tms - tms.mean()) ** 2), 1e-30)
+        fit = dict(ms_per_unit_keep=round(float(a), 3), ms_fixed=round(float(c), 3),
+                   r2=round(float(r2), 4))
+
+    cpu = None
+    if not args.no_cpu:
+        t_unit, n, threads = cpu_baseline(sh)
+        cpu_step_s = t_unit * np.mean(kept)
+        cpu = {"value": round(tokens / cpu_step_s, 3), "unit": "tokens/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"{n} x one sequence through one 1B-shape layer forward+backward "
+                         f"(float64 numpy oracle, {t_unit:.2f} s each), scaled by the mean kept "
+                         f"(sequence, layer) count per step {np.mean(kept):.1f}"}
+
+    out = {
+        "metric": "effective tokens/s per fwd+bwd step (1B-shape stack, ILD p_max 0.2)",
+        "value": round(tokens / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "1B-shape decoder stack: L=16, d_model=2048, heads=16x128, "
+                               "d_ff=5504 SwiGLU, seq=2048, batch=8; ILD p_max=0.2 at the end "
+                               "of a 0..1000 increasing ramp",
+                   "global_batch": sh.batch, "seq_len": sh.seq, "parallelism": "none (1 GPU)"},
+        "executed_tflops": round(exec_tflops, 1),
+        "mfma_frac_executed": round(exec_tflops / PEAK_BF16_TFLOPS, 4),
+        "drop_frac": round(1 - np.mean(kept) / (sh.n_layers * sh.batch), 4),
+        "roofline": {"kernel": prof_kernel, "bound": "mfma", "achieved": round(achieved, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "launches": pr["launches"],
+                     "avg_launch_us": round(pr["ms"] * 1e3 / max(pr["launches"], 1), 2)},
+        "cpu_baseline": cpu,
+        "sweep": sweep,
+        "sweep_fit": fit,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -94,3 +94,36 @@ def upstream_grad(sh, seed=0, batch=None):
 def f64(t):
     """The exact values of a CPU tensor as a float64 numpy array."""
     return t.detach().to(torch.float64).numpy()
+
+
+def _device_seed(seed, tensor_id, layer):
+    return (seed * 1_000_003 + tensor_id * 10_007 + layer) & 0x7FFFFFFFFFFFFFFF
+
+
+def _device_normal(shape, seed, tensor_id, layer, scale, dtype, device):
+    g = torch.Generator(device=device)
+    g.manual_seed(_device_seed(seed, tensor_id, layer))
+    t = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    return (t * scale).to(dtype)
+
+
+def device_layer_weights(sh, layer, device, seed=0):
+    """Same distributions as layer_weights, drawn on the device with torch's
+    seeded generator (used where numpy would take minutes: the benchmark)."""
+    out = {}
+    for k, shp in weight_shapes(sh).items():
+        if k in ("g_attn", "g_mlp"):
+            out[k] = torch.ones(shp, dtype=sh.torch_dtype, device=device)
+        else:
+            out[k] = _device_normal(shp, seed, TENSOR_IDS[k], layer, 0.02, sh.torch_dtype, device)
+    return out
+
+
+def device_hidden(sh, device, seed=0):
+    return _device_normal((sh.batch, sh.seq, sh.d_model), seed, TENSOR_IDS["x"], 0, 1.0,
+                          sh.torch_dtype, device)
+
+
+def device_upstream_grad(sh, device, seed=0):
+    return _device_normal((sh.batch, sh.seq, sh.d_model), seed, TENSOR_IDS["gy"], 0, 1.0,
+                          sh.torch_dtype, device)

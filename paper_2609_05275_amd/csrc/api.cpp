@@ -253,12 +253,16 @@ struct ActPtrs {
   }
 };
 
-int64_t host_count_if_profiling(const int32_t* dev_count, hipStream_t s) {
-  if (!prof_on()) return -1;
-  int32_t c = 0;
-  if (hipMemcpyAsync(&c, dev_count, sizeof(c), hipMemcpyDeviceToHost, s) != hipSuccess) return -1;
-  if (hipStreamSynchronize(s) != hipSuccess) return -1;
-  return c;
+// Kept counts on the host, read back only while profiling (one stream sync).
+std::vector<int64_t> host_counts_if_profiling(const int32_t* dev_count, int64_t n, hipStream_t s) {
+  std::vector<int64_t> out(n, -1);
+  if (!prof_on()) return out;
+  std::vector<int32_t> c(n, 0);
+  if (hipMemcpyAsync(c.data(), dev_count, sizeof(int32_t) * n, hipMemcpyDeviceToHost, s) != hipSuccess)
+    return out;
+  if (hipStreamSynchronize(s) != hipSuccess) return out;
+  for (int64_t i = 0; i < n; ++i) out[i] = c[i];
+  return out;
 }
 
 // ----------------------------------------------------------- gemm helper
@@ -292,11 +296,11 @@ int run_gemm(int dtype, int a_k, int b_k, const GemmArgs& g, int64_t max_m, int6
 
 // ------------------------------------------------------------ one layer
 
+// hc: the layer's kept count when profiling (read back by the caller), else -1.
 int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
-                  const ActPtrs& act, void* x, hipStream_t s) {
+                  const ActPtrs& act, void* x, int64_t hc, hipStream_t s) {
   const int dt = D.dtype;
   const int64_t T = D.T;
-  const int64_t hc = host_count_if_profiling(mv.count, s);
   const int64_t hm = hc * D.S;
   hipError_t e;
 
@@ -430,10 +434,10 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
 }
 
 int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const ActPtrs& act,
-                   const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, hipStream_t s) {
+                   const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, int64_t hc,
+                   hipStream_t s) {
   const int dt = D.dtype;
   const int64_t T = D.T;
-  const int64_t hc = host_count_if_profiling(mv.count, s);
   const int64_t hm = hc * D.S;
   const int32_t S = static_cast<int32_t>(D.S);
   auto W = [&](size_t off) { return static_cast<void*>(ws + off); };
@@ -830,7 +834,8 @@ int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float
                                  keep_override, keep, idx, count, r, s))
     return rc;
   ActPtrs act{c + ml.total, act_layout(D)};
-  return layer_forward(cfg, D, *w, MaskView{keep, idx, count, r}, act, x, s);
+  const int64_t hc = host_counts_if_profiling(count, 1, s)[0];
+  return layer_forward(cfg, D, *w, MaskView{keep, idx, count, r}, act, x, hc, s);
 }
 
 int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, void* dx,
@@ -848,7 +853,9 @@ int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, voi
   MaskView mv{reinterpret_cast<uint8_t*>(c + ml.keep), reinterpret_cast<int32_t*>(c + ml.idx),
               reinterpret_cast<int32_t*>(c + ml.count), reinterpret_cast<float*>(c + ml.r)};
   ActPtrs act{c + ml.total, act_layout(D)};
-  return layer_backward(D, *w, mv, act, BL, static_cast<char*>(ws), dx, *dw, as_stream(stream));
+  hipStream_t s = as_stream(stream);
+  const int64_t hc = host_counts_if_profiling(mv.count, 1, s)[0];
+  return layer_backward(D, *w, mv, act, BL, static_cast<char*>(ws), dx, *dw, hc, s);
 }
 
 int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const float* p,
@@ -886,13 +893,14 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
   auto view = [&](int64_t l) {
     return MaskView{keep + l * B, idx + l * B, count + l, r + l};
   };
+  const std::vector<int64_t> hc = host_counts_if_profiling(count, L, s);
   for (int64_t l = 0; l < L; ++l) {
     ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
-    if (int rc = layer_forward(cfg, D, w[l], view(l), act, x, s)) return rc;
+    if (int rc = layer_forward(cfg, D, w[l], view(l), act, x, hc[l], s)) return rc;
   }
   for (int64_t l = L - 1; l >= 0; --l) {
     ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
-    if (int rc = layer_backward(D, w[l], view(l), act, BL, bws, dx, dw[l], s)) return rc;
+    if (int rc = layer_backward(D, w[l], view(l), act, BL, bws, dx, dw[l], hc[l], s)) return rc;
   }
   if (keep_out) LD_HIP(hipMemcpyAsync(keep_out, keep, L * B, hipMemcpyDeviceToDevice, s));
   if (idx_out) LD_HIP(hipMemcpyAsync(idx_out, idx, 4 * L * B, hipMemcpyDeviceToDevice, s));
