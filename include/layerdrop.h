@@ -220,10 +220,17 @@ int ld_swiglu_bwd(int32_t dtype, int32_t rows, int32_t f, const void* uv, const 
  * C (and R) are [M, N] with leading dimension ldc (ldr); C is float32 when
  * c_f32 (R must then be NULL), else dtype.  Forward projections use
  * (1, 1); input gradients (1, 0); weight gradients (0, 0) with c_f32.
- * K may be 0 (C = R or 0).  For LD_BF16, K, lda, ldb must be multiples of 8. */
+ * K may be 0 (C = R or 0).  For LD_BF16, K, lda, ldb must be multiples of 8,
+ * and M (N) too when A (B) is not k-contiguous.
+ * ws: NULL, or device scratch of ws_bytes; with at least
+ * ld_gemm_ws_bytes(...) bytes a float32 GEMM without R may be split along K
+ * (partials summed in a fixed order).  Kernel-level diagnostics only. */
+size_t ld_gemm_ws_bytes(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int32_t N,
+                        int32_t K, int32_t ldc, int32_t c_f32);
 int ld_gemm(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int32_t N, int32_t K,
             const void* A, int32_t lda, const void* B, int32_t ldb, void* C, int32_t ldc,
-            int32_t c_f32, float alpha, const void* R, int32_t ldr, void* stream);
+            int32_t c_f32, float alpha, const void* R, int32_t ldr, void* ws, size_t ws_bytes,
+            void* stream);
 
 /* Causal multi-head attention over n_seq independent sequences.
  *   qkv: device [n_seq*S, 3*H*dh] as produced by x W_qkv^T;

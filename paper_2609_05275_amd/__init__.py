@@ -43,7 +43,7 @@ class ld_grads(C.Structure):
 
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_05275_amd.build`")
+    raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_05275_amd/build.py`")
 _lib = C.CDLL(LIB_PATH)
 
 _vp, _i32, _i64, _u64, _f32, _sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_float, C.c_size_t
@@ -70,8 +70,9 @@ _SIGS = {
                                  _vp]),
     "ld_swiglu_fwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp]),
     "ld_swiglu_bwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ld_gemm_ws_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32]),
     "ld_gemm": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _i32, _vp, _i32, _vp, _i32,
-                          _i32, _f32, _vp, _i32, _vp]),
+                          _i32, _f32, _vp, _i32, _vp, _sz, _vp]),
     "ld_attn_fwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "ld_attn_bwd_ws_bytes": (_sz, [_i32, _i32, _i32]),
     "ld_attn_bwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
@@ -230,11 +231,17 @@ def ld_swiglu_bwd(uv, gs, guv, stream=None):
                               _stream(stream)))
 
 
+def ld_gemm_ws_bytes(dtype, a_kcontig, b_kcontig, M, N, K, ldc, c_f32):
+    return _lib.ld_gemm_ws_bytes(dtype, int(a_kcontig), int(b_kcontig), M, N, K, ldc, int(c_f32))
+
+
 def ld_gemm(a_kcontig, b_kcontig, M, N, K, A, lda, B, ldb, Cm, ldc, alpha=1.0, R=None, ldr=0,
-            c_f32=False, dtype=None, stream=None):
+            c_f32=False, dtype=None, ws=None, stream=None):
     dt = _dtype_code(A) if dtype is None else dtype
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(_lib.ld_gemm(dt, int(a_kcontig), int(b_kcontig), M, N, K, _ptr(A), lda, _ptr(B), ldb,
-                        _ptr(Cm), ldc, int(c_f32), alpha, _ptr(R), ldr, _stream(stream)))
+                        _ptr(Cm), ldc, int(c_f32), alpha, _ptr(R), ldr, _ptr(ws), ws_bytes,
+                        _stream(stream)))
 
 
 def ld_attn_fwd(n_seq, seq, n_heads, d_head, qkv, o, lse, stream=None):

@@ -1,6 +1,6 @@
 """Build liblayerdrop.so (HIP for gfx950) in-tree.
 
-    python -m paper_2609_05275_amd.build
+    python paper_2609_05275_amd/build.py
 
 Each translation unit under csrc/ is compiled by hipcc into _build/ in
 parallel, then linked into paper_2609_05275_amd/liblayerdrop.so.

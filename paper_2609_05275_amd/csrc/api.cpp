@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -209,9 +210,27 @@ MaskLayout mask_layout(int64_t L, int64_t B) {
   return m;
 }
 
+// Split-K float32 scratch for the weight-gradient GEMMs (largest of the four).
+size_t splitk_bytes(const Dims& D) {
+  if (D.dtype != LD_BF16) return 0;
+  const int64_t shapes[4][2] = {{D.d, D.f}, {2 * D.f, D.d}, {D.d, D.d}, {3 * D.d, D.d}};
+  size_t best = 0;
+  for (const auto& sh : shapes) {
+    GemmArgs g;
+    std::memset(&g, 0, sizeof(g));
+    g.M = static_cast<int32_t>(sh[0]);
+    g.N = static_cast<int32_t>(sh[1]);
+    g.ldc = g.N;
+    g.c_f32 = 1;
+    const GemmPlan p = plan_gemm(D.dtype, 0, 0, g, sh[0], D.T, true);
+    best = std::max(best, gemm_part_bytes(p, sh[0], sh[1]));
+  }
+  return best;
+}
+
 // Backward scratch.
 struct BwdLayout {
-  size_t gk, gs, guv, gh, gz, ga, gqkv, delta, dg_part, total;
+  size_t gk, gs, guv, gh, gz, ga, gqkv, delta, dg_part, splitk, splitk_bytes, total;
 };
 
 BwdLayout bwd_layout(const Dims& D) {
@@ -232,6 +251,8 @@ BwdLayout bwd_layout(const Dims& D) {
   L.gqkv = take(es * T * 3 * D.d);
   L.delta = take(4 * T * D.H);
   L.dg_part = take(4 * rmsnorm_bwd_blocks(T) * D.d);
+  L.splitk_bytes = splitk_bytes(D);
+  L.splitk = take(L.splitk_bytes);
   L.total = o;
   return L;
 }
@@ -281,11 +302,18 @@ GemmArgs gemm_args() {
   return g;
 }
 
-int run_gemm(int dtype, int a_k, int b_k, const GemmArgs& g, int64_t max_m, int64_t host_m,
-             int64_t host_k, hipStream_t s) {
-  const char* name = gemm_kernel_name(dtype, a_k, b_k);
+// part: split-K scratch of part_bytes bytes (may be null / 0: no split).
+int run_gemm(int dtype, int a_k, int b_k, GemmArgs g, int64_t max_m, int64_t host_m,
+             int64_t host_k, hipStream_t s, float* part = nullptr, size_t part_bytes = 0,
+             int64_t max_k = 0) {
+  const GemmPlan plan = plan_gemm(dtype, a_k, b_k, g, max_m, max_k, part != nullptr);
+  if (plan.splits > 1) {
+    if (gemm_part_bytes(plan, g.M, g.N) > part_bytes) return fail(LD_E_WORKSPACE, "split-K scratch too small");
+    g.part = part;
+  }
+  const char* name = plan.name;
   ProfScope ps(name, s);
-  hipError_t e = launch_gemm(dtype, a_k, b_k, g, max_m, 0, s);
+  hipError_t e = launch_gemm_plan(dtype, a_k, b_k, plan, g, max_m, s);
   if (e != hipSuccess) return fail(LD_E_HIP, "%s launch: %s", name, hipGetErrorString(e));
   const double es = dtype == LD_BF16 ? 2.0 : 4.0;
   const double M = static_cast<double>(host_m), N = g.N, K = static_cast<double>(host_k);
@@ -441,6 +469,7 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
   const int64_t hm = hc * D.S;
   const int32_t S = static_cast<int32_t>(D.S);
   auto W = [&](size_t off) { return static_cast<void*>(ws + off); };
+  float* SK = BL.splitk_bytes ? reinterpret_cast<float*>(ws + BL.splitk) : nullptr;
   hipError_t e;
 
   // gk = dL/dX^{l+1} on the kept rows
@@ -488,7 +517,7 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     g.dev_count = mv.count;
     g.count_mult = S;
     g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s)) return rc;
+    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s, SK, BL.splitk_bytes, T)) return rc;
   }
   // guv = SwiGLU backward
   {
@@ -532,7 +561,7 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     g.dev_count = mv.count;
     g.count_mult = S;
     g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, 2 * D.f, 2 * D.f, hm, s)) return rc;
+    if (int rc = run_gemm(dt, 0, 0, g, 2 * D.f, 2 * D.f, hm, s, SK, BL.splitk_bytes, T)) return rc;
   }
   // gz = gk + RMSNorm_bwd(zk, g_mlp, gh2); dg_mlp
   {
@@ -583,7 +612,7 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     g.dev_count = mv.count;
     g.count_mult = S;
     g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s)) return rc;
+    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s, SK, BL.splitk_bytes, T)) return rc;
   }
   // attention backward -> gqkv
   {
@@ -632,7 +661,7 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     g.dev_count = mv.count;
     g.count_mult = S;
     g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, 3 * D.d, 3 * D.d, hm, s)) return rc;
+    if (int rc = run_gemm(dt, 0, 0, g, 3 * D.d, 3 * D.d, hm, s, SK, BL.splitk_bytes, T)) return rc;
   }
   // dL/dX^l[kept rows] = gz + RMSNorm_bwd(xk, g_attn, gh1); dg_attn
   {
@@ -997,9 +1026,24 @@ int ld_swiglu_bwd(int32_t dtype, int32_t rows, int32_t f, const void* uv, const 
   return LD_OK;
 }
 
+size_t ld_gemm_ws_bytes(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int32_t N,
+                        int32_t K, int32_t ldc, int32_t c_f32) {
+  if (M < 1 || N < 1 || K < 0) return 0;
+  GemmArgs g;
+  std::memset(&g, 0, sizeof(g));
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.ldc = ldc;
+  g.c_f32 = c_f32;
+  const GemmPlan p = plan_gemm(dtype, a_kcontig ? 1 : 0, b_kcontig ? 1 : 0, g, M, K, true);
+  return gemm_part_bytes(p, M, N);
+}
+
 int ld_gemm(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int32_t N, int32_t K,
             const void* A, int32_t lda, const void* B, int32_t ldb, void* C, int32_t ldc,
-            int32_t c_f32, float alpha, const void* R, int32_t ldr, void* stream) {
+            int32_t c_f32, float alpha, const void* R, int32_t ldr, void* ws, size_t ws_bytes,
+            void* stream) {
   t_err.clear();
   if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
   if (M < 0 || N < 0 || K < 0) return fail(LD_E_SHAPE, "negative extent");
@@ -1032,7 +1076,8 @@ int ld_gemm(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int3
   g.out_map = {nullptr, 1};
   g.alpha = alpha;
   g.c_f32 = c_f32;
-  return run_gemm(dtype, a_kcontig ? 1 : 0, b_kcontig ? 1 : 0, g, M, M, K, as_stream(stream));
+  return run_gemm(dtype, a_kcontig ? 1 : 0, b_kcontig ? 1 : 0, g, M, M, K, as_stream(stream),
+                  static_cast<float*>(ws), ws ? ws_bytes : 0, K);
 }
 
 int ld_attn_fwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,

@@ -16,6 +16,8 @@
 //
 // fp32: a plain SIMT kernel (64x64 tiles, 4x4 per thread) used by the fp32
 // configuration only.
+#include <algorithm>
+
 #include "ld_internal.h"
 
 namespace ld {
@@ -283,9 +285,321 @@ __global__ __launch_bounds__(256) void ld_gemm_f32_k(GemmArgs g) {
 
 constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 
+// ===================================================================== big
+// 256x256x64 workgroup tile, four waves in a 2x2 grid each owning 128x128
+// (4x4 MFMA blocks, 256 fp32 accumulators per lane).  LDS tiles are [row][64]
+// without padding; 16-byte chunks are XOR-swizzled by the row so that the
+// fragment reads (8 consecutive rows, one chunk) and the transposing writes
+// (rows 8 apart) spread over the banks.  The MFMA is issued as B x A so each
+// lane ends with 4 consecutive output columns of one row (vector stores).
+// Tiles are ordered XCD-aware: consecutive workgroup ids go to different XCDs,
+// so ids are remapped to give each XCD a contiguous range of tiles, walked in
+// groups of 8 tile-rows for L2 reuse.  Split-K (grid.y) writes fp32 partials
+// that a second kernel sums in split order.
+
+constexpr int GB = 256, GK = 64;
+constexpr int kBigTile = GB * GK;                          // elements per operand tile
+constexpr size_t kBigLds = 2ull * 2 * kBigTile * sizeof(bf16);  // A,B x double buffer
+
+__device__ __forceinline__ int swz_off(int row, int k) {
+  const int chunk = (k >> 3) ^ ((row & 7) ^ ((row >> 3) & 7));
+  return row * GK + (chunk << 3) + (k & 7);
+}
+
+struct BigRegs {
+  uint4 v[8];
+};
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// Buffer resource covering `bytes` from `base`: loads past it return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0 ? 0 : (bytes > 0xFFFFFFFFll ? 0xFFFFFFFFll : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(static_cast<uint32_t>(n)), 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  const v4i t = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+  return make_uint4(t[0], t[1], t[2], t[3]);
+}
+
+// Tile loads through a buffer descriptor that ends at the operand's last valid
+// row: rows (k-contiguous) or k-rows (mn-contiguous) past the end read 0.
+// Columns past the end inside a valid row read real memory; they only reach
+// outputs that are never stored, except a k tail of a k-contiguous operand,
+// which is zeroed per lane.
+template <bool KC>
+__device__ __forceinline__ void big_load(BigRegs& t, const bf16* X, int64_t ld, int r0, int R, int k0,
+                                         int K, int tid) {
+  if constexpr (KC) {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
+    const bool full_k = k0 + GK <= K;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      const int c = p * 256 + tid;
+      const int row = c >> 3, kk = k0 + (c & 7) * 8;
+      uint4 v = buf_load16(rs, static_cast<int>((static_cast<int64_t>(row) * ld + kk) * 2));
+      if (!full_k && kk >= K) v = make_uint4(0, 0, 0, 0);
+      t.v[p] = v;
+    }
+  } else {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(X + static_cast<int64_t>(k0) * ld, (static_cast<int64_t>(K) - k0) * ld * 2);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int gidx = q * 256 + tid;
+      const int rch = gidx & 31, kg = gidx >> 5;  // 32 row chunks of 8, 16 k groups of 4
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+        t.v[q * 4 + kk] = buf_load16(rs, static_cast<int>((static_cast<int64_t>(kg * 4 + kk) * ld + r0 + rch * 8) * 2));
+    }
+  }
+  (void)R;
+}
+
+template <bool KC>
+__device__ __forceinline__ void big_store(const BigRegs& t, bf16* lds, int tid) {
+  if constexpr (KC) {
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      const int c = p * 256 + tid;
+      const int row = c >> 3;
+      *reinterpret_cast<uint4*>(lds + swz_off(row, (c & 7) * 8)) = t.v[p];
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int gidx = q * 256 + tid;
+      const int rch = gidx & 31, kg = gidx >> 5;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        uint2 o;
+        o.x = half_of(t.v[q * 4 + 0], i) | (half_of(t.v[q * 4 + 1], i) << 16);
+        o.y = half_of(t.v[q * 4 + 2], i) | (half_of(t.v[q * 4 + 3], i) << 16);
+        *reinterpret_cast<uint2*>(lds + swz_off(rch * 8 + i, kg * 4)) = o;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void tile_coords(int pid, int n_wg, int tiles_m, int tiles_n, int& tm,
+                                            int& tn) {
+  if ((n_wg & 7) == 0) pid = (pid & 7) * (n_wg >> 3) + (pid >> 3);
+  constexpr int G = 8;
+  const int group = G * tiles_n;
+  const int first_m = (pid / group) * G;
+  const int gsz = min(tiles_m - first_m, G);
+  const int in = pid % group;
+  tm = first_m + in % gsz;
+  tn = in / gsz;
+}
+
+template <bool AK, bool BKC>
+__device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
+  extern __shared__ __align__(16) bf16 smem[];
+  bf16* As = smem;                 // [2][GB*GK]
+  bf16* Bs = smem + 2 * kBigTile;  // [2][GB*GK]
+  int M, K;
+  resolve_counts(g, M, K);
+  const int tiles_n = (g.N + GB - 1) / GB;
+  const int tiles_m = static_cast<int>(gridDim.x) / tiles_n;
+  int tm, tn;
+  tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * GB, n0 = tn * GB;
+  if (m0 >= M) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const bf16* A = static_cast<const bf16*>(g.A);
+  const bf16* B = static_cast<const bf16*>(g.B);
+
+  // k range of this split
+  const int nkt_all = (K + GK - 1) / GK;
+  const int splits = gridDim.y, sp = blockIdx.y;
+  const int kt0 = static_cast<int>((static_cast<int64_t>(nkt_all) * sp) / splits);
+  const int kt1 = static_cast<int>((static_cast<int64_t>(nkt_all) * (sp + 1)) / splits);
+  const int nk = kt1 - kt0;
+
+  floatx16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  if (nk > 0) {
+    BigRegs ra, rb;
+    big_load<AK>(ra, A, g.lda, m0, M, kt0 * GK, K, tid);
+    big_load<BKC>(rb, B, g.ldb, n0, g.N, kt0 * GK, K, tid);
+    big_store<AK>(ra, As, tid);
+    big_store<BKC>(rb, Bs, tid);
+    __syncthreads();
+    const int lrow = lane & 31, lk = (lane >> 5) * 8;
+    const int arow = wm * 128 + lrow, brow = wn * 128 + lrow;
+    for (int kt = 0; kt < nk; ++kt) {
+      const int buf = kt & 1;
+      if (kt + 1 < nk) {
+        big_load<AK>(ra, A, g.lda, m0, M, (kt0 + kt + 1) * GK, K, tid);
+        big_load<BKC>(rb, B, g.ldb, n0, g.N, (kt0 + kt + 1) * GK, K, tid);
+      }
+      const bf16* as = As + buf * kBigTile;
+      const bf16* bs = Bs + buf * kBigTile;
+      bf16x8 af[2][4], bfr[2][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        af[0][i] = *reinterpret_cast<const bf16x8*>(as + swz_off(arow + i * 32, lk));
+        bfr[0][i] = *reinterpret_cast<const bf16x8*>(bs + swz_off(brow + i * 32, lk));
+      }
+#pragma unroll
+      for (int ks = 0; ks < GK / 16; ++ks) {
+        const int cur = ks & 1;
+        if (ks + 1 < GK / 16) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(as + swz_off(arow + i * 32, (ks + 1) * 16 + lk));
+            bfr[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(bs + swz_off(brow + i * 32, (ks + 1) * 16 + lk));
+          }
+        }
+        if (ks == GK / 16 - 1 && kt + 1 < nk) {
+          big_store<AK>(ra, As + (buf ^ 1) * kBigTile, tid);
+          big_store<BKC>(rb, Bs + (buf ^ 1) * kBigTile, tid);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
+      }
+      __syncthreads();
+    }
+  }
+
+  // epilogue: lane holds rows m (its column of B x A) and 4 consecutive n
+  const float alpha = g.alpha * (g.alpha_dev ? *g.alpha_dev : 1.f);
+  const int half = lane >> 5, lm = lane & 31;
+  float* part = g.part ? g.part + static_cast<int64_t>(sp) * g.M * g.N : nullptr;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + wm * 128 + i * 32 + lm;
+    if (m >= M) continue;
+    const int64_t orow = map_row(g.out_map, m);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wn * 128 + j * 32 + 8 * q + 4 * half;
+        if (n >= g.N) continue;
+        float v4[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = alpha * acc[i][j][4 * q + e];
+        if (part) {
+          *reinterpret_cast<float4*>(part + static_cast<int64_t>(m) * g.N + n) =
+              make_float4(v4[0], v4[1], v4[2], v4[3]);
+          continue;
+        }
+        if (g.R) {
+          const int64_t rrow = g.r_mapped ? orow : m;
+          if (g.c_f32) {
+            const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(g.R) + rrow * g.ldr + n);
+            v4[0] += r.x; v4[1] += r.y; v4[2] += r.z; v4[3] += r.w;
+          } else {
+            const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(g.R) + rrow * g.ldr + n);
+            const bf16* rb = reinterpret_cast<const bf16*>(&r);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v4[e] += static_cast<float>(rb[e]);
+          }
+        }
+        if (g.c_f32) {
+          *reinterpret_cast<float4*>(static_cast<float*>(g.C) + orow * g.ldc + n) =
+              make_float4(v4[0], v4[1], v4[2], v4[3]);
+        } else {
+          __attribute__((aligned(8))) bf16 o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(v4[e]);
+          *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + orow * g.ldc + n) =
+              *reinterpret_cast<const uint2*>(o);
+        }
+      }
+  }
+}
+
+#define LD_BIG_ATTRS __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+LD_BIG_ATTRS void ld_gemm_bf16_nt_256(GemmArgs g) { gemm_big_body<true, true>(g); }
+LD_BIG_ATTRS void ld_gemm_bf16_nn_256(GemmArgs g) { gemm_big_body<true, false>(g); }
+LD_BIG_ATTRS void ld_gemm_bf16_tn_256(GemmArgs g) { gemm_big_body<false, false>(g); }
+LD_BIG_ATTRS void ld_gemm_bf16_tt_256(GemmArgs g) { gemm_big_body<false, true>(g); }
+
+// C[i] = R[i] + sum over splits of part[s][i], float32, in split order.
+__global__ __launch_bounds__(256) void ld_splitk_reduce(const float* part, int splits, int64_t mn,
+                                                        const int32_t* dev_m_unused, float* C) {
+  (void)dev_m_unused;
+  for (int64_t i4 = blockIdx.x * 256ll + threadIdx.x; i4 < mn / 4; i4 += gridDim.x * 256ll) {
+    float4 s = reinterpret_cast<const float4*>(part)[i4];
+    for (int k = 1; k < splits; ++k) {
+      const float4 t = reinterpret_cast<const float4*>(part + static_cast<int64_t>(k) * mn)[i4];
+      s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+    }
+    reinterpret_cast<float4*>(C)[i4] = s;
+  }
+}
+
 bool g_attr_done = false;
 
+void set_attrs() {
+  if (g_attr_done) return;
+  const void* small[] = {reinterpret_cast<const void*>(ld_gemm_bf16_nt), reinterpret_cast<const void*>(ld_gemm_bf16_nn),
+                         reinterpret_cast<const void*>(ld_gemm_bf16_tn), reinterpret_cast<const void*>(ld_gemm_bf16_tt)};
+  const void* big[] = {reinterpret_cast<const void*>(ld_gemm_bf16_nt_256), reinterpret_cast<const void*>(ld_gemm_bf16_nn_256),
+                       reinterpret_cast<const void*>(ld_gemm_bf16_tn_256), reinterpret_cast<const void*>(ld_gemm_bf16_tt_256)};
+  for (const void* f : small) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+  for (const void* f : big) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
+  g_attr_done = true;
+}
+
 }  // namespace
+
+GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,
+                   int64_t max_k, bool allow_split) {
+  GemmPlan p{};
+  p.splits = 1;
+  if (dtype != LD_BF16) {
+    p.name = "ld_gemm_f32_k";
+    return p;
+  }
+  const int64_t big_tiles = ((max_m + GB - 1) / GB) * ((g.N + GB - 1) / GB);
+  // the big tile needs N % 4 == 0 for its vector epilogue
+  // the big tile's epilogue stores 4 consecutive columns at once
+  p.big = (g.N % 4 == 0) && (g.ldc % 4 == 0) && (!g.R || g.ldr % 4 == 0) && max_m >= 512 &&
+          g.N >= 512 && big_tiles >= 32;
+  if (p.big) {
+    // split-K only for float32 outputs without a residual (weight gradients)
+    if (allow_split && g.c_f32 && !g.R && !g.out_map.idx && g.ldc == g.N && max_k >= 8 * GK) {
+      double best = 0;
+      for (int s = 1; s <= 8; ++s) {
+        const int64_t wg = big_tiles * s;
+        const double eff = static_cast<double>(wg) / (256.0 * ((wg + 255) / 256)) - 0.02 * (s - 1);
+        if (eff > best + 1e-9 && max_k / s >= 4 * GK) {
+          best = eff;
+          p.splits = s;
+        }
+      }
+    }
+    p.name = a_kcontig && b_kcontig ? "ld_gemm_bf16_nt_256"
+             : a_kcontig            ? "ld_gemm_bf16_nn_256"
+             : b_kcontig            ? "ld_gemm_bf16_tt_256"
+                                    : "ld_gemm_bf16_tn_256";
+  } else {
+    p.name = a_kcontig && b_kcontig ? "ld_gemm_bf16_nt"
+             : a_kcontig            ? "ld_gemm_bf16_nn"
+             : b_kcontig            ? "ld_gemm_bf16_tt"
+                                    : "ld_gemm_bf16_tn";
+  }
+  return p;
+}
+
+size_t gemm_part_bytes(const GemmPlan& p, int64_t M, int64_t N) {
+  return p.splits > 1 ? 4ull * p.splits * M * N : 0;
+}
 
 const char* gemm_kernel_name(int dtype, int a_kcontig, int b_kcontig) {
   if (dtype == LD_BF16) {
@@ -297,22 +611,44 @@ const char* gemm_kernel_name(int dtype, int a_kcontig, int b_kcontig) {
   return "ld_gemm_f32_k";
 }
 
+hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmPlan& p, GemmArgs g,
+                            int64_t max_m, hipStream_t s) {
+  if (max_m <= 0 || g.N <= 0) return hipSuccess;
+  if (dtype == LD_BF16 && p.big) {
+    set_attrs();
+    const int64_t tiles = ((max_m + GB - 1) / GB) * ((g.N + GB - 1) / GB);
+    float* C = static_cast<float*>(g.C);
+    if (p.splits > 1) {
+      if (!g.part) return hipErrorInvalidValue;
+    } else {
+      g.part = nullptr;
+    }
+    const dim3 grid(static_cast<unsigned>(tiles), p.splits), block(256);
+    if (a_kcontig && b_kcontig)
+      hipLaunchKernelGGL(ld_gemm_bf16_nt_256, grid, block, kBigLds, s, g);
+    else if (a_kcontig)
+      hipLaunchKernelGGL(ld_gemm_bf16_nn_256, grid, block, kBigLds, s, g);
+    else if (b_kcontig)
+      hipLaunchKernelGGL(ld_gemm_bf16_tt_256, grid, block, kBigLds, s, g);
+    else
+      hipLaunchKernelGGL(ld_gemm_bf16_tn_256, grid, block, kBigLds, s, g);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.splits == 1) return e;
+    const int64_t mn = static_cast<int64_t>(g.M) * g.N;
+    int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 4096));
+    hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, g.part, p.splits, mn,
+                       nullptr, C);
+    return hipGetLastError();
+  }
+  return launch_gemm(dtype, a_kcontig, b_kcontig, g, max_m, 0, s);
+}
+
 hipError_t launch_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,
                        int64_t max_k, hipStream_t s) {
   (void)max_k;
   if (max_m <= 0 || g.N <= 0) return hipSuccess;
   if (dtype == LD_BF16) {
-    if (!g_attr_done) {
-      hipFuncSetAttribute(reinterpret_cast<const void*>(ld_gemm_bf16_nt),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
-      hipFuncSetAttribute(reinterpret_cast<const void*>(ld_gemm_bf16_nn),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
-      hipFuncSetAttribute(reinterpret_cast<const void*>(ld_gemm_bf16_tn),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
-      hipFuncSetAttribute(reinterpret_cast<const void*>(ld_gemm_bf16_tt),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
-      g_attr_done = true;
-    }
+    set_attrs();
     const int64_t tiles = ((max_m + BM - 1) / BM) * ((g.N + BN - 1) / BN);
     const dim3 grid(static_cast<unsigned>(tiles)), block(256);
     if (a_kcontig && b_kcontig)

@@ -102,6 +102,15 @@ struct GemmArgs {
   float alpha;
   const float* alpha_dev;    // when set, alpha is multiplied by *alpha_dev
   int32_t c_f32;
+  float* part;               // split-K float32 partials [splits][M][N] (plan.splits > 1)
+};
+
+// Kernel choice for one GEMM: the 256x256 MFMA kernel (optionally split
+// along K) or the 128x128 one; fp32 uses the SIMT kernel.
+struct GemmPlan {
+  const char* name;
+  int big;
+  int splits;
 };
 
 struct AttnArgs {
@@ -133,6 +142,13 @@ hipError_t launch_swiglu_bwd(int dtype, const EltArgs& a, hipStream_t s);
 hipError_t launch_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,
                        int64_t max_k, hipStream_t s);
 const char* gemm_kernel_name(int dtype, int a_kcontig, int b_kcontig);
+// allow_split: split-K may be chosen (the caller then provides g.part of
+// gemm_part_bytes bytes).
+GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,
+                   int64_t max_k, bool allow_split);
+size_t gemm_part_bytes(const GemmPlan& p, int64_t M, int64_t N);
+hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmPlan& p, GemmArgs g,
+                            int64_t max_m, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
 const char* attn_fwd_kernel_name(int dtype);

@@ -148,6 +148,51 @@ def test_gemm_bf16(layout, shape):
         assert not Cf.any()
 
 
+@pytest.mark.parametrize("layout", [(1, 1), (1, 0), (0, 0), (0, 1)])
+@pytest.mark.parametrize("shape", [(2048, 2048, 2048), (2048, 2048, 2000), (4096, 1000, 512),
+                                   (1536, 2304, 1024)])
+def test_gemm_bf16_big_tiles(layout, shape):
+    """Shapes routed to the 256x256 kernel: K tail, ragged N, M not a tile multiple."""
+    ak, bk = layout
+    M, N, K = shape
+    g = torch.Generator().manual_seed(6)
+    A = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    B = torch.randn(N, K, generator=g).to(torch.bfloat16)
+    R = torch.randn(M, N, generator=g).to(torch.bfloat16)
+    Ad = (A if ak else A.t().contiguous()).to(DEV)
+    Bd = (B if bk else B.t().contiguous()).to(DEV)
+    Cd = torch.empty(M, N, dtype=torch.bfloat16, device=DEV)
+    ld.ld_gemm(ak, bk, M, N, K, Ad, K if ak else M, Bd, K if bk else N, Cd, N, alpha=-1.5,
+               R=R.to(DEV), ldr=N)
+    torch.cuda.synchronize()
+    ref = f64(A) @ f64(B).T
+    assert rel(f64(Cd), f64(R) - 1.5 * ref) < TOL_BF16
+
+
+@pytest.mark.parametrize("layout", [(0, 0), (1, 0)])
+def test_gemm_bf16_split_k(layout):
+    """float32 output with split-K partials summed in a fixed order."""
+    ak, bk = layout
+    M, N, K = 2048, 2048, 8192
+    g = torch.Generator().manual_seed(7)
+    A = torch.randn(M, K, generator=g).to(torch.bfloat16)
+    B = torch.randn(N, K, generator=g).to(torch.bfloat16)
+    Ad = (A if ak else A.t().contiguous()).to(DEV)
+    Bd = (B if bk else B.t().contiguous()).to(DEV)
+    wsb = ld.ld_gemm_ws_bytes(ld.LD_BF16, ak, bk, M, N, K, N, 1)
+    assert wsb > 0
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    outs = []
+    for _ in range(2):
+        Cd = torch.full((M, N), 3.0, dtype=torch.float32, device=DEV)
+        ld.ld_gemm(ak, bk, M, N, K, Ad, K if ak else M, Bd, K if bk else N, Cd, N, alpha=0.25,
+                   c_f32=True, ws=ws)
+        torch.cuda.synchronize()
+        outs.append(Cd.cpu())
+    assert torch.equal(outs[0], outs[1])
+    assert rel(outs[0].double().numpy(), 0.25 * (f64(A) @ f64(B).T)) < 1e-5
+
+
 @pytest.mark.parametrize("layout", [(1, 1), (1, 0), (0, 0)])
 def test_gemm_f32(layout):
     ak, bk = layout

@@ -15,6 +15,8 @@ pytestmark = pytest.mark.gpu
 
 SMALL_BF16 = inp.Shape(3, 256, 4, 704, 192, 5, "bf16")      # d_head 64, ragged q tile
 SMALL_BF16_128 = inp.Shape(2, 256, 2, 512, 128, 3, "bf16")  # d_head 128
+# large enough that every projection GEMM takes the 256x256 kernel path
+MID_BF16 = inp.Shape(2, 1024, 8, 2816, 512, 4, "bf16")
 
 
 def _cfg(sh, **kw):
@@ -39,8 +41,8 @@ def _check_grads(got, want, t, where=""):
             assert rel(g, w) < t, (where, k, rel(g, w))
 
 
-@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16, SMALL_BF16_128],
-                         ids=["tiny_f32", "small_bf16", "small_bf16_dh128"])
+@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16, SMALL_BF16_128, MID_BF16],
+                         ids=["tiny_f32", "small_bf16", "small_bf16_dh128", "mid_bf16"])
 @pytest.mark.parametrize("forced", [None, "none", "one", "ragged", "all"])
 def test_layer_fwd_bwd(sh, forced):
     cfg = _cfg(sh)
