@@ -299,7 +299,11 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 
 constexpr int GB = 256, GK = 64;
 constexpr int kBigTile = GB * GK;                          // elements per operand tile
-constexpr size_t kBigLds = 2ull * 2 * kBigTile * sizeof(bf16);  // A,B x double buffer
+constexpr int kStagePitch = 132;  // floats per staged epilogue row (128 + 4 pad)
+// A,B x double buffer for the main loop; four 64 x kStagePitch float blocks
+// for the epilogue (the larger of the two).
+constexpr size_t kBigLds = std::max<size_t>(2ull * 2 * kBigTile * sizeof(bf16),
+                                            4ull * 64 * kStagePitch * sizeof(float));
 
 __device__ __forceinline__ int swz_off(int row, int k) {
   const int chunk = (k >> 3) ^ ((row & 7) ^ ((row >> 3) & 7));
@@ -324,6 +328,17 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, int byte_o
   return make_uint4(t[0], t[1], t[2], t[3]);
 }
 
+// Transposing loader groups: 32 row chunks of 8 x 16 k groups of 4, two per
+// thread.  In a wave, lanes 0-15 and 32-47 cover 32 consecutive row chunks of
+// one k row (512 contiguous bytes) and lanes 16-31, 48-63 the next k row, so
+// the transposed 8-byte LDS writes of a half-wave land on both halves of the
+// swizzled 16-byte chunks and use every bank.
+__device__ __forceinline__ void mn_group(int q, int tid, int& rch, int& kg) {
+  const int l = tid & 63, w = tid >> 6;
+  kg = (q * 4 + w) * 2 + ((l >> 4) & 1);
+  rch = (l & 15) | ((l >> 5) << 4);
+}
+
 // Tile loads through a buffer descriptor that ends at the operand's last valid
 // row: rows (k-contiguous) or k-rows (mn-contiguous) past the end read 0.
 // Columns past the end inside a valid row read real memory; they only reach
@@ -334,21 +349,18 @@ __device__ __forceinline__ void big_load(BigRegs& t, const bf16* X, int64_t ld, 
                                          int K, int tid) {
   if constexpr (KC) {
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
-    const bool full_k = k0 + GK <= K;
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       const int c = p * 256 + tid;
       const int row = c >> 3, kk = k0 + (c & 7) * 8;
-      uint4 v = buf_load16(rs, static_cast<int>((static_cast<int64_t>(row) * ld + kk) * 2));
-      if (!full_k && kk >= K) v = make_uint4(0, 0, 0, 0);
-      t.v[p] = v;
+      t.v[p] = buf_load16(rs, static_cast<int>((static_cast<int64_t>(row) * ld + kk) * 2));
     }
   } else {
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(X + static_cast<int64_t>(k0) * ld, (static_cast<int64_t>(K) - k0) * ld * 2);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int gidx = q * 256 + tid;
-      const int rch = gidx & 31, kg = gidx >> 5;  // 32 row chunks of 8, 16 k groups of 4
+      int rch, kg;
+      mn_group(q, tid, rch, kg);
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
         t.v[q * 4 + kk] = buf_load16(rs, static_cast<int>((static_cast<int64_t>(kg * 4 + kk) * ld + r0 + rch * 8) * 2));
@@ -357,20 +369,24 @@ __device__ __forceinline__ void big_load(BigRegs& t, const bf16* X, int64_t ld, 
   (void)R;
 }
 
+// k0, K: the tile's first k and the reduction length; a k-contiguous tile
+// that crosses K has its columns past K zeroed here, once the loads landed.
 template <bool KC>
-__device__ __forceinline__ void big_store(const BigRegs& t, bf16* lds, int tid) {
+__device__ __forceinline__ void big_store(const BigRegs& t, bf16* lds, int tid, int k0, int K) {
   if constexpr (KC) {
+    const bool ok = k0 + (tid & 7) * 8 < K;  // the same k chunk for every p
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       const int c = p * 256 + tid;
-      const int row = c >> 3;
-      *reinterpret_cast<uint4*>(lds + swz_off(row, (c & 7) * 8)) = t.v[p];
+      const uint4 v = t.v[p];
+      *reinterpret_cast<uint4*>(lds + swz_off(c >> 3, (c & 7) * 8)) =
+          make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
     }
   } else {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int gidx = q * 256 + tid;
-      const int rch = gidx & 31, kg = gidx >> 5;
+      int rch, kg;
+      mn_group(q, tid, rch, kg);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         uint2 o;
@@ -428,98 +444,142 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   if (nk > 0) {
-    BigRegs ra, rb;
-    big_load<AK>(ra, A, g.lda, m0, M, kt0 * GK, K, tid);
-    big_load<BKC>(rb, B, g.ldb, n0, g.N, kt0 * GK, K, tid);
-    big_store<AK>(ra, As, tid);
-    big_store<BKC>(rb, Bs, tid);
+    // Global data is prefetched one k tile ahead in registers (a second set
+    // for two tiles ahead does not fit next to the 256 accumulators).
+    BigRegs ra0, rb0;
+    big_load<AK>(ra0, A, g.lda, m0, M, kt0 * GK, K, tid);
+    big_load<BKC>(rb0, B, g.ldb, n0, g.N, kt0 * GK, K, tid);
+    big_store<AK>(ra0, As, tid, kt0 * GK, K);
+    big_store<BKC>(rb0, Bs, tid, kt0 * GK, K);
     __syncthreads();
     const int lrow = lane & 31, lk = (lane >> 5) * 8;
     const int arow = wm * 128 + lrow, brow = wn * 128 + lrow;
-    for (int kt = 0; kt < nk; ++kt) {
+    bf16x8 af[2][4], bfr[2][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      af[0][i] = *reinterpret_cast<const bf16x8*>(As + swz_off(arow + i * 32, lk));
+      bfr[0][i] = *reinterpret_cast<const bf16x8*>(Bs + swz_off(brow + i * 32, lk));
+    }
+    // One k tile per step, a single basic block: the loads of tile kt+1 go
+    // out first (unconditionally: past the end they read zeros or unused
+    // data), steps 0-2 read the next step's fragments while their 16 MFMAs
+    // run (front-loaded, one LDS read per MFMA), step 3 writes tile kt+1 into
+    // the other LDS buffer between its MFMAs, then one barrier and the first
+    // fragments of tile kt+1.
+    auto tile_step = [&](BigRegs& la, BigRegs& lb, const BigRegs& sa, const BigRegs& sb, int kt) {
       const int buf = kt & 1;
-      if (kt + 1 < nk) {
-        big_load<AK>(ra, A, g.lda, m0, M, (kt0 + kt + 1) * GK, K, tid);
-        big_load<BKC>(rb, B, g.ldb, n0, g.N, (kt0 + kt + 1) * GK, K, tid);
-      }
+      big_load<AK>(la, A, g.lda, m0, M, (kt0 + kt + 1) * GK, K, tid);
+      big_load<BKC>(lb, B, g.ldb, n0, g.N, (kt0 + kt + 1) * GK, K, tid);
+      __builtin_amdgcn_sched_barrier(0);
       const bf16* as = As + buf * kBigTile;
       const bf16* bs = Bs + buf * kBigTile;
-      bf16x8 af[2][4], bfr[2][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        af[0][i] = *reinterpret_cast<const bf16x8*>(as + swz_off(arow + i * 32, lk));
-        bfr[0][i] = *reinterpret_cast<const bf16x8*>(bs + swz_off(brow + i * 32, lk));
-      }
-#pragma unroll
-      for (int ks = 0; ks < GK / 16; ++ks) {
+      for (int ks = 0; ks < 3; ++ks) {
         const int cur = ks & 1;
-        if (ks + 1 < GK / 16) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(as + swz_off(arow + i * 32, (ks + 1) * 16 + lk));
-            bfr[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(bs + swz_off(brow + i * 32, (ks + 1) * 16 + lk));
-          }
-        }
-        if (ks == GK / 16 - 1 && kt + 1 < nk) {
-          big_store<AK>(ra, As + (buf ^ 1) * kBigTile, tid);
-          big_store<BKC>(rb, Bs + (buf ^ 1) * kBigTile, tid);
+        for (int i = 0; i < 4; ++i) {
+          af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(as + swz_off(arow + i * 32, (ks + 1) * 16 + lk));
+          bfr[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(bs + swz_off(brow + i * 32, (ks + 1) * 16 + lk));
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
+      const int knext = (kt0 + kt + 1) * GK;
+      big_store<AK>(sa, As + (buf ^ 1) * kBigTile, tid, knext, K);
+      big_store<BKC>(sb, Bs + (buf ^ 1) * kBigTile, tid, knext, K);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[1][j], af[1][i], acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU (transposes)
+        __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);  // LDS writes
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      }
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
-    }
+      const bf16* an = As + (buf ^ 1) * kBigTile;
+      const bf16* bn = Bs + (buf ^ 1) * kBigTile;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        af[0][i] = *reinterpret_cast<const bf16x8*>(an + swz_off(arow + i * 32, lk));
+        bfr[0][i] = *reinterpret_cast<const bf16x8*>(bn + swz_off(brow + i * 32, lk));
+      }
+    };
+    for (int kt = 0; kt < nk; ++kt) tile_step(ra0, rb0, ra0, rb0, kt);
   }
 
-  // epilogue: lane holds rows m (its column of B x A) and 4 consecutive n
+  // Epilogue staged through LDS (the operand tiles are dead by now).  A lane
+  // holds, per 32x32 block, one output row and 4 consecutive columns; stored
+  // directly that scatters every store over 32 rows.  Instead each wave writes
+  // half of its 128x128 float32 results (alpha applied) into a private
+  // [64][kStagePitch] block and reads it back row-major: a half-wave then
+  // covers 128 contiguous columns of one row, so the residual loads and the
+  // output stores (one rounding, after the residual) are fully coalesced.
   const float alpha = g.alpha * (g.alpha_dev ? *g.alpha_dev : 1.f);
   const int half = lane >> 5, lm = lane & 31;
   float* part = g.part ? g.part + static_cast<int64_t>(sp) * g.M * g.N : nullptr;
+  float* stage = reinterpret_cast<float*>(smem) + wave * (64 * kStagePitch);
+  __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + wm * 128 + i * 32 + lm;
-    if (m >= M) continue;
-    const int64_t orow = map_row(g.out_map, m);
+  for (int hi = 0; hi < 2; ++hi) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * 128 + j * 32 + 8 * q + 4 * half;
-        if (n >= g.N) continue;
-        float v4[4];
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = alpha * acc[i][j][4 * q + e];
-        if (part) {
-          *reinterpret_cast<float4*>(part + static_cast<int64_t>(m) * g.N + n) =
-              make_float4(v4[0], v4[1], v4[2], v4[3]);
-          continue;
+        for (int q = 0; q < 4; ++q) {
+          const floatx16& a = acc[2 * hi + ii][j];
+          *reinterpret_cast<float4*>(stage + (ii * 32 + lm) * kStagePitch + j * 32 + 8 * q + 4 * half) =
+              make_float4(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
         }
-        if (g.R) {
-          const int64_t rrow = g.r_mapped ? orow : m;
-          if (g.c_f32) {
-            const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(g.R) + rrow * g.ldr + n);
-            v4[0] += r.x; v4[1] += r.y; v4[2] += r.z; v4[3] += r.w;
-          } else {
-            const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(g.R) + rrow * g.ldr + n);
-            const bf16* rb = reinterpret_cast<const bf16*>(&r);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v4[e] += static_cast<float>(rb[e]);
-          }
-        }
+    __syncthreads();
+    const int c = (lane & 31) * 4;
+    const int n = n0 + wn * 128 + c;
+#pragma unroll 4
+    for (int it = 0; it < 32; ++it) {
+      const int rl = 2 * it + half;
+      const int m = m0 + wm * 128 + hi * 64 + rl;
+      if (m >= M || n >= g.N) continue;
+      float4 v = *reinterpret_cast<const float4*>(stage + rl * kStagePitch + c);
+      if (part) {
+        *reinterpret_cast<float4*>(part + static_cast<int64_t>(m) * g.N + n) = v;
+        continue;
+      }
+      const int64_t orow = map_row(g.out_map, m);
+      if (g.R) {
+        const int64_t rrow = g.r_mapped ? orow : m;
         if (g.c_f32) {
-          *reinterpret_cast<float4*>(static_cast<float*>(g.C) + orow * g.ldc + n) =
-              make_float4(v4[0], v4[1], v4[2], v4[3]);
+          const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(g.R) + rrow * g.ldr + n);
+          v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
         } else {
-          __attribute__((aligned(8))) bf16 o[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = static_cast<bf16>(v4[e]);
-          *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + orow * g.ldc + n) =
-              *reinterpret_cast<const uint2*>(o);
+          const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(g.R) + rrow * g.ldr + n);
+          const bf16* rb = reinterpret_cast<const bf16*>(&r);
+          v.x += static_cast<float>(rb[0]); v.y += static_cast<float>(rb[1]);
+          v.z += static_cast<float>(rb[2]); v.w += static_cast<float>(rb[3]);
         }
       }
+      if (g.c_f32) {
+        *reinterpret_cast<float4*>(static_cast<float*>(g.C) + orow * g.ldc + n) = v;
+      } else {
+        __attribute__((aligned(8))) bf16 o[4] = {static_cast<bf16>(v.x), static_cast<bf16>(v.y),
+                                                 static_cast<bf16>(v.z), static_cast<bf16>(v.w)};
+        *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + orow * g.ldc + n) = *reinterpret_cast<const uint2*>(o);
+      }
+    }
+    __syncthreads();
   }
 }
 
