@@ -629,7 +629,16 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     a.H = static_cast<int32_t>(D.H);
     a.dh = static_cast<int32_t>(D.dh);
     a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.dh)));
-    if ((e = launch_attn_bwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "attn_bwd: %s", hipGetErrorString(e));
+    // algorithmic FLOPs of the backward (2x the forward), split over the two
+    // MFMA kernels in proportion to the products each forms (4 and 3)
+    const double fl_bwd = 4.0 * hc * D.d * D.S * (D.S + 1.0);
+    const double parts_fl[3] = {0.0, fl_bwd * 4.0 / 7.0, fl_bwd * 3.0 / 7.0};
+    for (int part = 0; part < 3; ++part) {
+      ProfScope ps(attn_bwd_kernel_name(dt, part), s);
+      if ((e = launch_attn_bwd_part(dt, part, a, s)) != hipSuccess)
+        return fail(LD_E_HIP, "attn_bwd: %s", hipGetErrorString(e));
+      ps.end(parts_fl[part], D.es * hm * D.d * (part == 0 ? 2.0 : 5.0));
+    }
   }
   // gh1 = gqkv W_qkv   [M, d]
   {

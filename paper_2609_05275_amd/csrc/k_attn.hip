@@ -47,6 +47,15 @@ __device__ __forceinline__ bf16x8 zero8() {
   return z;
 }
 
+// Transposed LDS tiles ([d][key] or [d][query], 64 columns) are unpadded
+// 128-byte rows whose 16-byte chunks are XOR-swizzled by the row, so that 32
+// consecutive rows read at one column and 16 rows written 8 apart both spread
+// over the banks.
+__device__ __forceinline__ int tr_off(int row, int col) {
+  const int chunk = (col >> 3) ^ ((row & 7) ^ ((row >> 3) & 7));
+  return row * 64 + (chunk << 3) + (col & 7);
+}
+
 // Two 4-element pieces of an LDS row -> one 8-element fragment.
 __device__ __forceinline__ bf16x8 load4x2(const bf16* lo, const bf16* hi) {
   const uint2 a = *reinterpret_cast<const uint2*>(lo);
@@ -97,21 +106,83 @@ __device__ __forceinline__ void stage_rows(const bf16* src, int64_t ld, int r0, 
 
 // ---------------------------------------------------------------- forward
 
-constexpr int FQ = 128, FKV = 64;
+constexpr int FQ = 128, FKV = 64;   // dQ kernel tiles
+constexpr int FWQ = 256;            // forward: query rows per workgroup (4 waves x 64)
 
+// Registers holding one K/V block (64 keys x DH) on its way to LDS.
+template <int DH>
+struct KvRegs {
+  static constexpr int NK = 64 * DH / 8 / 256;       // 16-byte K chunks per thread
+  static constexpr int NV = (64 / 4) * (DH / 8);     // V groups of 4 keys x 8 d
+  static constexpr int NVT = (NV + 255) / 256;       // per thread
+  uint4 k[NK];
+  uint4 v[NVT][4];
+};
+
+// The block [k0, k0+64) must lie inside the sequence (S % 64 == 0).
+template <int DH>
+__device__ __forceinline__ void kv_load(KvRegs<DH>& r, const bf16* Kp, const bf16* Vp, int64_t ld,
+                                        int k0, int tid) {
+#pragma unroll
+  for (int p = 0; p < KvRegs<DH>::NK; ++p) {
+    const int c = p * 256 + tid;
+    const int row = c / (DH / 8), dc = (c % (DH / 8)) * 8;
+    r.k[p] = *reinterpret_cast<const uint4*>(Kp + static_cast<int64_t>(k0 + row) * ld + dc);
+  }
+#pragma unroll
+  for (int p = 0; p < KvRegs<DH>::NVT; ++p) {
+    const int c = p * 256 + tid;
+    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      r.v[p][k] = c < KvRegs<DH>::NV
+                      ? *reinterpret_cast<const uint4*>(Vp + static_cast<int64_t>(k0 + rg + k) * ld + dc)
+                      : make_uint4(0, 0, 0, 0);
+  }
+}
+
+// K as [key][d] (pitch DH+8), V transposed as [d][key] (swizzled, tr_off).
+template <int DH>
+__device__ __forceinline__ void kv_store(const KvRegs<DH>& r, bf16* Ks, bf16* Vt, int tid) {
+#pragma unroll
+  for (int p = 0; p < KvRegs<DH>::NK; ++p) {
+    const int c = p * 256 + tid;
+    const int row = c / (DH / 8), dc = (c % (DH / 8)) * 8;
+    *reinterpret_cast<uint4*>(Ks + row * (DH + 8) + dc) = r.k[p];
+  }
+#pragma unroll
+  for (int p = 0; p < KvRegs<DH>::NVT; ++p) {
+    const int c = p * 256 + tid;
+    if (c >= KvRegs<DH>::NV) continue;
+    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      uint2 o;
+      o.x = half_of(r.v[p][0], i) | (half_of(r.v[p][1], i) << 16);
+      o.y = half_of(r.v[p][2], i) | (half_of(r.v[p][3], i) << 16);
+      *reinterpret_cast<uint2*>(Vt + tr_off(dc + i, rg)) = o;
+    }
+  }
+}
+
+// Forward.  Each wave owns 64 query rows as two 32-row MFMA blocks that share
+// every K and V fragment it reads from LDS.  K/V blocks of 64 keys are double
+// buffered in LDS and the next block is fetched into registers while the
+// current one is used, so there is one barrier per block.
 template <int DH>
 __global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
-  __shared__ __align__(16) bf16 Ks[FKV * (DH + 8)];
-  __shared__ __align__(16) bf16 Vt[DH * (FKV + 8)];
+  constexpr int KT = FKV * (DH + 8), VT = DH * FKV;
+  __shared__ __align__(16) bf16 lds[2 * (KT + VT)];
   const int S = a.S, H = a.H;
-  const int n_qt = (S + FQ - 1) / FQ;
-  const int qt = n_qt - 1 - static_cast<int>(blockIdx.x);
-  const int head = blockIdx.y, seq = blockIdx.z;
+  const int n_qt = (S + FWQ - 1) / FWQ;
+  // grid (head, sequence, tile): the tile index varies slowest, so every
+  // (heaviest) last query tile is dispatched before any lighter one
+  const int qt = n_qt - 1 - static_cast<int>(blockIdx.z);
+  const int head = blockIdx.x, seq = blockIdx.y;
   if (seq >= seq_count(a)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hf = lane >> 5, cl = lane & 31;
-  const int q0 = qt * FQ, qw = q0 + wave * 32, qrow = qw + cl;
-  const bool active = qw < S;
+  const int q0 = qt * FWQ, qw = q0 + wave * 64;
   const int64_t ldq = 3ll * H * DH;
   const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
   const bf16* Qp = base + head * DH;
@@ -119,95 +190,144 @@ __global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
   const bf16* Vp = base + 2ll * H * DH + head * DH;
   const float sl2 = a.scale * kLog2e;
 
-  bf16x8 qf[DH / 16];
+  bf16x8 qf[2][DH / 16];
+  floatx16 o[2][DH / 32];
+  float m[2], l[2];
 #pragma unroll
-  for (int ks = 0; ks < DH / 16; ++ks)
-    qf[ks] = qrow < S ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
-  floatx16 o[DH / 32];
+  for (int sb = 0; sb < 2; ++sb) {
+    const int qrow = qw + sb * 32 + cl;
 #pragma unroll
-  for (int db = 0; db < DH / 32; ++db)
+    for (int ks = 0; ks < DH / 16; ++ks)
+      qf[sb][ks] = qrow < S ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
 #pragma unroll
-    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
-  float m = -INFINITY, l = 0.f;
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[sb][db][v] = 0.f;
+    m[sb] = -INFINITY;
+    l[sb] = 0.f;
+  }
 
-  const int kv_end = min(S, q0 + FQ);
-  for (int k0 = 0; k0 < kv_end; k0 += FKV) {
-    stage_rows<FKV, DH>(Kp, ldq, k0, S, Ks, nullptr, tid);
-    stage_rows<FKV, DH>(Vp, ldq, k0, S, nullptr, Vt, tid);
-    __syncthreads();
-    if (active && k0 <= qw + 31) {
-      floatx16 s[2];
+  const int kv_end = min(S, q0 + FWQ);
+  const int nkb = (kv_end + FKV - 1) / FKV;
+  KvRegs<DH> kr;
+  kv_load<DH>(kr, Kp, Vp, ldq, 0, tid);
+  kv_store<DH>(kr, lds, lds + KT, tid);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int k0 = kb * FKV;
+    bf16* Ks = lds + (kb & 1) * (KT + VT);
+    bf16* Vt = Ks + KT;
+    if (kb + 1 < nkb) kv_load<DH>(kr, Kp, Vp, ldq, k0 + FKV, tid);
+    if (qw < S && k0 <= qw + 63) {
+      const bool diag = k0 + FKV - 1 > qw;  // some key of the block is past some row
+      // scores of both 32-row blocks: each K fragment feeds two MFMA chains
+      floatx16 sc[2][2];
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh) {
+      for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[kh][v] = 0.f;
+        for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-        for (int ks = 0; ks < DH / 16; ++ks)
-          s[kh] = mfma(load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), qf[ks], s[kh]);
+          for (int v = 0; v < 16; ++v) sc[sb][kh][v] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < DH / 16; ++ks)
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh) {
+          const bf16x8 kf = load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8);
+          sc[0][kh] = mfma(kf, qf[0][ks], sc[0][kh]);
+          sc[1][kh] = mfma(kf, qf[1][ks], sc[1][kh]);
+        }
+      bf16x8 pb[2][2][2];
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) {
+        const int qrow = qw + sb * 32 + cl;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            float x = sc[sb][kh][v] * sl2;
+            if (diag) {
+              const int key = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+              if (key > qrow) x = -INFINITY;
+            }
+            sc[sb][kh][v] = x;
+            mx = fmaxf(mx, x);
+          }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        // Lazy rescaling: the running maximum only moves (and O, l are only
+        // rescaled) when a row's maximum grows by more than 8 in log2 units;
+        // otherwise p = 2^(s - m) stays below 2^8, exact enough in bf16 and
+        // far from float overflow, and the result O / l is unchanged.
+        const bool grow = mx > m[sb] + 8.f;
+        if (__builtin_amdgcn_read_exec() & __ballot(grow)) {
+          const float m_new = grow ? mx : m[sb];
+          const float alpha = __builtin_amdgcn_exp2f(m[sb] - m_new);
+          m[sb] = m_new;
+          l[sb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) o[sb][db][v] *= alpha;
+        }
+        float ls = 0.f;
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float p = __builtin_amdgcn_exp2f(sc[sb][kh][v] - m[sb]);
+            ls += p;
+            pb[sb][kh][v >> 3][v & 7] = static_cast<bf16>(p);
+          }
+        l[sb] += ls;
       }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-          float x = s[kh][v] * sl2;
-          if (key > qrow || key >= S) x = -INFINITY;
-          s[kh][v] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m, mx);
-      const float alpha = exp2f(m - m_new);
-      m = m_new;
-      float ls = 0.f;
-      bf16x8 pb[2][2];
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float p = exp2f(s[kh][v] - m_new);
-          ls += p;
-          pb[kh][v >> 3][v & 7] = static_cast<bf16>(p);
-        }
-      l = l * alpha + ls;
+      // O^T += V^T P^T for both blocks: each V fragment feeds two chains
 #pragma unroll
       for (int db = 0; db < DH / 32; ++db) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
-        const bf16* vrow = Vt + (db * 32 + cl) * (FKV + 8);
+        const int vr = db * 32 + cl;
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
-            const int kb = kh * 32 + 16 * c + 4 * hf;
-            o[db] = mfma(load4x2(vrow + kb, vrow + kb + 8), pb[kh][c], o[db]);
+            const int kbb = kh * 32 + 16 * c + 4 * hf;
+            const bf16x8 vf = load4x2(Vt + tr_off(vr, kbb), Vt + tr_off(vr, kbb + 8));
+            o[0][db] = mfma(vf, pb[0][kh][c], o[0][db]);
+            o[1][db] = mfma(vf, pb[1][kh][c], o[1][db]);
           }
       }
     }
+    if (kb + 1 < nkb) {
+      bf16* Kn = lds + ((kb + 1) & 1) * (KT + VT);
+      kv_store<DH>(kr, Kn, Kn + KT, tid);
+    }
     __syncthreads();
   }
-  const float lt = l + __shfl_xor(l, 32, 64);
-  if (active && qrow < S) {
-    const float inv = 1.f / lt;
-    bf16* Op = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * (static_cast<int64_t>(H) * DH) + head * DH;
 #pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
+  for (int sb = 0; sb < 2; ++sb) {
+    const int qrow = qw + sb * 32 + cl;
+    const float lt = l[sb] + __shfl_xor(l[sb], 32, 64);
+    if (qrow < S) {
+      const float inv = 1.f / lt;
+      bf16* Op = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * (static_cast<int64_t>(H) * DH) + head * DH;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        __attribute__((aligned(8))) bf16 t[4];
+      for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(o[db][4 * g + i] * inv);
-        *reinterpret_cast<uint2*>(Op + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(t);
-      }
-    if (hf == 0) a.lse[(static_cast<int64_t>(seq) * H + head) * S + qrow] = (m + log2f(lt)) * kLn2;
+        for (int g = 0; g < 4; ++g) {
+          __attribute__((aligned(8))) bf16 t[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(o[sb][db][4 * g + i] * inv);
+          *reinterpret_cast<uint2*>(Op + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(t);
+        }
+      if (hf == 0) a.lse[(static_cast<int64_t>(seq) * H + head) * S + qrow] = (m[sb] + log2f(lt)) * kLn2;
+    }
   }
 }
 
 // --------------------------------------------------------------- backward
 
+// delta[seq, head, q] = sum_d dO * O (float32), one thread per (token, head).
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
+  constexpr int VN = 16 / sizeof(T);
   const int64_t rows = static_cast<int64_t>(seq_count(a)) * a.S * a.H;
   const int64_t id = blockIdx.x * 256ll + threadIdx.x;
   if (id >= rows) return;
@@ -217,27 +337,91 @@ __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
   const T* o = static_cast<const T*>(a.o) + tok * ld + head * DH;
   const T* go = static_cast<const T*>(a.go) + tok * ld + head * DH;
   float s = 0.f;
-  for (int i = 0; i < DH; ++i) s = __builtin_fmaf(static_cast<float>(o[i]), static_cast<float>(go[i]), s);
+#pragma unroll
+  for (int c = 0; c < DH; c += VN) {
+    const uint4 ov = *reinterpret_cast<const uint4*>(o + c);
+    const uint4 gv = *reinterpret_cast<const uint4*>(go + c);
+    const T* op = reinterpret_cast<const T*>(&ov);
+    const T* gp = reinterpret_cast<const T*>(&gv);
+#pragma unroll
+    for (int i = 0; i < VN; ++i) s = __builtin_fmaf(static_cast<float>(op[i]), static_cast<float>(gp[i]), s);
+  }
   const int64_t seq = tok / a.S, q = tok % a.S;
   a.delta[(seq * a.H + head) * a.S + q] = s;
 }
 
-constexpr int BQ = 32;       // query rows per step of the dK/dV kernel
-constexpr int BKEYS = 128;   // keys per dK/dV workgroup (4 waves x 32)
+// Registers holding 64 rows x DH of one operand as groups of 4 rows x 8
+// columns, from which both the [row][d] and the transposed [d][row] LDS
+// copies are written.
+template <int DH>
+struct RowGroups {
+  static constexpr int NG = (64 / 4) * (DH / 8);
+  static constexpr int NGT = (NG + 255) / 256;
+  uint4 v[NGT][4];
+};
+
+// Rows [r0, r0+64) must lie inside the sequence (S % 64 == 0).
+template <int DH>
+__device__ __forceinline__ void rg_load(RowGroups<DH>& t, const bf16* src, int64_t ld, int r0, int tid) {
+#pragma unroll
+  for (int p = 0; p < RowGroups<DH>::NGT; ++p) {
+    const int c = p * 256 + tid;
+    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      t.v[p][k] = c < RowGroups<DH>::NG
+                      ? *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r0 + rg + k) * ld + dc)
+                      : make_uint4(0, 0, 0, 0);
+  }
+}
 
 template <int DH>
+__device__ __forceinline__ void rg_store(const RowGroups<DH>& t, bf16* direct, bf16* trans, int tid) {
+#pragma unroll
+  for (int p = 0; p < RowGroups<DH>::NGT; ++p) {
+    const int c = p * 256 + tid;
+    if (c >= RowGroups<DH>::NG) continue;
+    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
+    if (direct) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) *reinterpret_cast<uint4*>(direct + (rg + k) * (DH + 8) + dc) = t.v[p][k];
+    }
+    if (trans) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        uint2 o;
+        o.x = half_of(t.v[p][0], i) | (half_of(t.v[p][1], i) << 16);
+        o.y = half_of(t.v[p][2], i) | (half_of(t.v[p][3], i) << 16);
+        *reinterpret_cast<uint2*>(trans + tr_off(dc + i, rg)) = o;
+      }
+    }
+  }
+}
+
+constexpr int BQ = 64;       // query rows per step of the dK/dV kernel
+constexpr int BKEYS = 128;   // keys per dK/dV workgroup (4 waves x 32)
+
+// dK, dV.  A workgroup owns 128 keys (32 per wave, K and V fragments in
+// registers) and walks the 64-row query blocks from the diagonal to the end;
+// Q, dO (both as [q][d] and transposed [d][q]), the log-sum-exp and delta of
+// the block are double buffered in LDS with the next block prefetched in
+// registers.  P = 2^(s*scale*log2e - lse*log2e) is recomputed, dS = P (dP -
+// delta); dV^T += dO^T P and dK^T += Q^T dS take P and dS straight from the
+// score accumulators (their rows are a fixed permutation of the MFMA k index,
+// matched when the transposed tiles are read).
+template <int DH>
 __global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
-  __shared__ __align__(16) bf16 Qs[BQ * (DH + 8)];
-  __shared__ __align__(16) bf16 Qt[DH * (BQ + 8)];
-  __shared__ __align__(16) bf16 Os[BQ * (DH + 8)];   // dO [q][d]
-  __shared__ __align__(16) bf16 Ot[DH * (BQ + 8)];   // dO^T [d][q]
-  __shared__ float lse_s[BQ], del_s[BQ];
+  constexpr int DT = BQ * (DH + 8), TT = DH * BQ;
+  constexpr int STAGE = 2 * DT + 2 * TT;  // bf16 elements per buffer
+  extern __shared__ __align__(16) bf16 lds[];
+  float* lse_s = reinterpret_cast<float*>(lds + 2 * STAGE);  // [2][BQ]
+  float* del_s = lse_s + 2 * BQ;                              // [2][BQ]
   const int S = a.S, H = a.H;
-  const int n_kt = (S + BKEYS - 1) / BKEYS;
-  const int kt = static_cast<int>(blockIdx.x);  // early key tiles see the most queries
-  const int head = blockIdx.y, seq = blockIdx.z;
+  // grid (head, sequence, tile), tile slowest: early key tiles see the most
+  // queries and go first
+  const int kt = static_cast<int>(blockIdx.z);
+  const int head = blockIdx.x, seq = blockIdx.y;
   if (seq >= seq_count(a)) return;
-  (void)n_kt;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hf = lane >> 5, cl = lane & 31;
   const int k0 = kt * BKEYS, kw = k0 + wave * 32, key = kw + cl;
@@ -264,47 +448,77 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) dv[db][v] = dk[db][v] = 0.f;
 
-  for (int q0 = k0; q0 < S; q0 += BQ) {
-    stage_rows<BQ, DH>(Qp, ldq, q0, S, Qs, Qt, tid);
-    stage_rows<BQ, DH>(dOp, ldo, q0, S, Os, Ot, tid);
+  const int q_first = k0;  // the first query that can see key k0
+  const int nqb = q_first < S ? (S - q_first) / BQ : 0;
+  RowGroups<DH> rq, ro;
+  float lse_r = 0.f, del_r = 0.f;
+  auto fetch = [&](int qb) {
+    rg_load<DH>(rq, Qp, ldq, qb, tid);
+    rg_load<DH>(ro, dOp, ldo, qb, tid);
     if (tid < BQ) {
-      const bool ok = q0 + tid < S;
-      lse_s[tid] = ok ? lse[q0 + tid] * kLog2e : 0.f;
-      del_s[tid] = ok ? del[q0 + tid] : 0.f;
+      lse_r = lse[qb + tid] * kLog2e;
+      del_r = del[qb + tid];
     }
-    __syncthreads();
-    if (active && kw <= q0 + BQ - 1) {
-      floatx16 s, dp;
+  };
+  auto put = [&](int buf) {
+    bf16* st = lds + buf * STAGE;
+    rg_store<DH>(rq, st, st + 2 * DT, tid);
+    rg_store<DH>(ro, st + DT, st + 2 * DT + TT, tid);
+    if (tid < BQ) {
+      lse_s[buf * BQ + tid] = lse_r;
+      del_s[buf * BQ + tid] = del_r;
+    }
+  };
+  if (nqb > 0) {
+    fetch(q_first);
+    put(0);
+  }
+  __syncthreads();
+  for (int ib = 0; ib < nqb; ++ib) {
+    const int qb = q_first + ib * BQ, buf = ib & 1;
+    if (ib + 1 < nqb) fetch(qb + BQ);
+    const bf16* Qs = lds + buf * STAGE;
+    const bf16* Os = Qs + DT;
+    const bf16* Qt = Qs + 2 * DT;
+    const bf16* Ot = Qt + TT;
+    const float* ls = lse_s + buf * BQ;
+    const float* dl = del_s + buf * BQ;
+    if (active && kw <= qb + BQ - 1) {
+      const bool diag = kw + 31 > qb;  // some key of the wave is past some query of the block
+      bf16x8 pb[2][2], dsb[2][2];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
+      for (int qh = 0; qh < 2; ++qh) {
+        floatx16 sc, dp;
 #pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks) {
-        s = mfma(load8(Qs + cl * (DH + 8) + ks * 16 + hf * 8), kf[ks], s);
-        dp = mfma(load8(Os + cl * (DH + 8) + ks * 16 + hf * 8), vf[ks], dp);
-      }
-      bf16x8 pb[2], db8[2];
+        for (int v = 0; v < 16; ++v) sc[v] = dp[v] = 0.f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int ql = 8 * (v >> 2) + 4 * hf + (v & 3);
-        const int q = q0 + ql;
-        float p = 0.f;
-        if (q < S && key <= q) p = exp2f(s[v] * sl2 - lse_s[ql]);
-        const float ds = p * (dp[v] - del_s[ql]);
-        pb[v >> 3][v & 7] = static_cast<bf16>(p);
-        db8[v >> 3][v & 7] = static_cast<bf16>(ds);
+        for (int ks = 0; ks < DH / 16; ++ks) {
+          sc = mfma(load8(Qs + (qh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), kf[ks], sc);
+          dp = mfma(load8(Os + (qh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), vf[ks], dp);
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int ql = qh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+          float p = __builtin_amdgcn_exp2f(sc[v] * sl2 - ls[ql]);
+          if (diag && key > qb + ql) p = 0.f;
+          pb[qh][v >> 3][v & 7] = static_cast<bf16>(p);
+          dsb[qh][v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dl[ql]));
+        }
       }
 #pragma unroll
       for (int db = 0; db < DH / 32; ++db) {
-        const bf16* orow = Ot + (db * 32 + cl) * (BQ + 8);
-        const bf16* qrow = Qt + (db * 32 + cl) * (BQ + 8);
+        const int dr = db * 32 + cl;
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int qb = 16 * c + 4 * hf;
-          dv[db] = mfma(load4x2(orow + qb, orow + qb + 8), pb[c], dv[db]);
-          dk[db] = mfma(load4x2(qrow + qb, qrow + qb + 8), db8[c], dk[db]);
-        }
+        for (int qh = 0; qh < 2; ++qh)
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const int qq = qh * 32 + 16 * c + 4 * hf;
+            dv[db] = mfma(load4x2(Ot + tr_off(dr, qq), Ot + tr_off(dr, qq + 8)), pb[qh][c], dv[db]);
+            dk[db] = mfma(load4x2(Qt + tr_off(dr, qq), Qt + tr_off(dr, qq + 8)), dsb[qh][c], dk[db]);
+          }
       }
     }
+    if (ib + 1 < nqb) put(buf ^ 1);
     __syncthreads();
   }
   if (active && key < S) {
@@ -328,19 +542,32 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
 }
 
 template <int DH>
+constexpr size_t dkdv_lds_bytes() {
+  return (2ull * (2 * BQ * (DH + 8) + 2 * DH * BQ)) * sizeof(bf16) + 4ull * BQ * sizeof(float);
+}
+
+constexpr int DQ_ROWS = 256;  // query rows per dQ workgroup (4 waves x 64)
+
+// dQ.  A workgroup owns 256 query rows (64 per wave as two 32-row MFMA blocks
+// sharing every fragment read) and walks the 64-key blocks up to the
+// diagonal; K ([key][d] and transposed [d][key]) and V are double buffered in
+// LDS with the next block prefetched in registers.  Scores are formed
+// transposed (S^T = K Q^T), so the query's log-sum-exp and delta are per lane
+// and dS^T feeds dQ^T += K^T dS^T directly.
+template <int DH>
 __global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
-  __shared__ __align__(16) bf16 Ks[FKV * (DH + 8)];
-  __shared__ __align__(16) bf16 Kt[DH * (FKV + 8)];
-  __shared__ __align__(16) bf16 Vs[FKV * (DH + 8)];
+  constexpr int DT = FKV * (DH + 8), TT = DH * FKV;
+  constexpr int STAGE = 2 * DT + TT;  // Ks, Vs, Kt
+  extern __shared__ __align__(16) bf16 lds[];
   const int S = a.S, H = a.H;
-  const int n_qt = (S + FQ - 1) / FQ;
-  const int qt = n_qt - 1 - static_cast<int>(blockIdx.x);
-  const int head = blockIdx.y, seq = blockIdx.z;
+  const int n_qt = (S + DQ_ROWS - 1) / DQ_ROWS;
+  // grid (head, sequence, tile), tile slowest: heavy (late) query tiles first
+  const int qt = n_qt - 1 - static_cast<int>(blockIdx.z);
+  const int head = blockIdx.x, seq = blockIdx.y;
   if (seq >= seq_count(a)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hf = lane >> 5, cl = lane & 31;
-  const int q0 = qt * FQ, qw = q0 + wave * 32, qrow = qw + cl;
-  const bool active = qw < S;
+  const int q0 = qt * DQ_ROWS, qw = q0 + wave * 64;
   const int64_t ldq = 3ll * H * DH, ldo = static_cast<int64_t>(H) * DH;
   const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
   const bf16* Qp = base + head * DH;
@@ -348,63 +575,105 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   const bf16* Vp = base + 2ll * H * DH + head * DH;
   const bf16* dOp = static_cast<const bf16*>(a.go) + static_cast<int64_t>(seq) * S * ldo + head * DH;
   const float sl2 = a.scale * kLog2e;
-  const bool qok = qrow < S;
-  const int64_t srow = (static_cast<int64_t>(seq) * H + head) * S + (qok ? qrow : 0);
-  const float lse2 = qok ? a.lse[srow] * kLog2e : 0.f;
-  const float dl = qok ? a.delta[srow] : 0.f;
 
-  bf16x8 qf[DH / 16], of[DH / 16];
+  bf16x8 qf[2][DH / 16], of[2][DH / 16];
+  float lse2[2], dl[2];
+  floatx16 dq[2][DH / 32];
 #pragma unroll
-  for (int ks = 0; ks < DH / 16; ++ks) {
-    qf[ks] = qok ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
-    of[ks] = qok ? load8(dOp + static_cast<int64_t>(qrow) * ldo + ks * 16 + hf * 8) : zero8();
+  for (int sb = 0; sb < 2; ++sb) {
+    const int qrow = qw + sb * 32 + cl;
+    const bool qok = qrow < S;
+    const int64_t srow = (static_cast<int64_t>(seq) * H + head) * S + (qok ? qrow : 0);
+    lse2[sb] = qok ? a.lse[srow] * kLog2e : 0.f;
+    dl[sb] = qok ? a.delta[srow] : 0.f;
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) {
+      qf[sb][ks] = qok ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
+      of[sb][ks] = qok ? load8(dOp + static_cast<int64_t>(qrow) * ldo + ks * 16 + hf * 8) : zero8();
+    }
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dq[sb][db][v] = 0.f;
   }
-  floatx16 dq[DH / 32];
-#pragma unroll
-  for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) dq[db][v] = 0.f;
 
-  const int kv_end = min(S, q0 + FQ);
-  for (int k0 = 0; k0 < kv_end; k0 += FKV) {
-    stage_rows<FKV, DH>(Kp, ldq, k0, S, Ks, Kt, tid);
-    stage_rows<FKV, DH>(Vp, ldq, k0, S, Vs, nullptr, tid);
-    __syncthreads();
-    if (active && k0 <= qw + 31) {
-      bf16x8 dsb[2][2];
+  const int kv_end = min(S, q0 + DQ_ROWS);
+  const int nkb = kv_end / FKV;
+  RowGroups<DH> rk, rv;
+  auto put = [&](int buf) {
+    bf16* st = lds + buf * STAGE;
+    rg_store<DH>(rk, st, st + 2 * DT, tid);
+    rg_store<DH>(rv, st + DT, nullptr, tid);
+  };
+  rg_load<DH>(rk, Kp, ldq, 0, tid);
+  rg_load<DH>(rv, Vp, ldq, 0, tid);
+  put(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int k0 = kb * FKV, buf = kb & 1;
+    if (kb + 1 < nkb) {
+      rg_load<DH>(rk, Kp, ldq, k0 + FKV, tid);
+      rg_load<DH>(rv, Vp, ldq, k0 + FKV, tid);
+    }
+    const bf16* Ks = lds + buf * STAGE;
+    const bf16* Vs = Ks + DT;
+    const bf16* Kt = Ks + 2 * DT;
+    if (qw < S && k0 <= qw + 63) {
+      const bool diag = k0 + FKV - 1 > qw;
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
-        floatx16 s, dp;
+        // scores and dP^T of this 32-key half for both query blocks, then its
+        // dS^T is consumed right away (only one half's dS is ever live)
+        floatx16 st[2], dpt[2];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) st[sb][v] = dpt[sb][v] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < DH / 16; ++ks) {
-          s = mfma(load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), qf[ks], s);
-          dp = mfma(load8(Vs + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), of[ks], dp);
+          const bf16x8 kfr = load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8);
+          const bf16x8 vfr = load8(Vs + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8);
+#pragma unroll
+          for (int sb = 0; sb < 2; ++sb) {
+            st[sb] = mfma(kfr, qf[sb][ks], st[sb]);
+            dpt[sb] = mfma(vfr, of[sb][ks], dpt[sb]);
+          }
+        }
+        bf16x8 dsb[2][2];
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb) {
+          const int qrow = qw + sb * 32 + cl;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            float p = __builtin_amdgcn_exp2f(st[sb][v] * sl2 - lse2[sb]);
+            if (diag) {
+              const int keyi = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+              if (keyi > qrow) p = 0.f;
+            }
+            dsb[sb][v >> 3][v & 7] = static_cast<bf16>(p * (dpt[sb][v] - dl[sb]));
+          }
         }
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-          float p = 0.f;
-          if (qok && key <= qrow) p = exp2f(s[v] * sl2 - lse2);
-          dsb[kh][v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dl));
-        }
-      }
-#pragma unroll
-      for (int db = 0; db < DH / 32; ++db) {
-        const bf16* krow = Kt + (db * 32 + cl) * (FKV + 8);
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
+        for (int db = 0; db < DH / 32; ++db) {
+          const int dr = db * 32 + cl;
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
-            const int kb = kh * 32 + 16 * c + 4 * hf;
-            dq[db] = mfma(load4x2(krow + kb, krow + kb + 8), dsb[kh][c], dq[db]);
+            const int kk = kh * 32 + 16 * c + 4 * hf;
+            const bf16x8 kt = load4x2(Kt + tr_off(dr, kk), Kt + tr_off(dr, kk + 8));
+            dq[0][db] = mfma(kt, dsb[0][c], dq[0][db]);
+            dq[1][db] = mfma(kt, dsb[1][c], dq[1][db]);
           }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep the two halves' live ranges apart
       }
     }
+    if (kb + 1 < nkb) put(buf ^ 1);
     __syncthreads();
   }
-  if (active && qok) {
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb) {
+    const int qrow = qw + sb * 32 + cl;
+    if (qrow >= S) continue;
     bf16* G = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * ldq + head * DH;
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db)
@@ -412,10 +681,15 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
       for (int g = 0; g < 4; ++g) {
         __attribute__((aligned(8))) bf16 t[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(dq[db][4 * g + i] * a.scale);
+        for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(dq[sb][db][4 * g + i] * a.scale);
         *reinterpret_cast<uint2*>(G + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(t);
       }
   }
+}
+
+template <int DH>
+constexpr size_t dq_lds_bytes() {
+  return 2ull * (2 * FKV * (DH + 8) + DH * FKV) * sizeof(bf16);
 }
 
 // ------------------------------------------------------------ fp32 (SIMT)
@@ -578,7 +852,7 @@ template <int DH>
 hipError_t fwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
   if constexpr (DH >= 64) {
     if (dtype == LD_BF16) {
-      const dim3 grid((a.S + FQ - 1) / FQ, a.H, a.n_seq);
+      const dim3 grid(a.H, a.n_seq, (a.S + FWQ - 1) / FWQ);
       hipLaunchKernelGGL(ld_attn_fwd_bf16<DH>, grid, dim3(256), 0, s, a);
       return hipGetLastError();
     }
@@ -591,24 +865,30 @@ hipError_t fwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
 }
 
 template <int DH>
-hipError_t bwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
+hipError_t bwd_dh(int dtype, int part, const AttnArgs& a, hipStream_t s) {
   const int64_t rows = static_cast<int64_t>(a.n_seq) * a.S * a.H;
   const dim3 dgrid(static_cast<unsigned>((rows + 255) / 256));
   if constexpr (DH >= 64) {
     if (dtype == LD_BF16) {
-      hipLaunchKernelGGL((ld_attn_delta<bf16, DH>), dgrid, dim3(256), 0, s, a);
-      hipLaunchKernelGGL(ld_attn_bwd_dkdv_bf16<DH>, dim3((a.S + BKEYS - 1) / BKEYS, a.H, a.n_seq),
-                         dim3(256), 0, s, a);
-      hipLaunchKernelGGL(ld_attn_bwd_dq_bf16<DH>, dim3((a.S + FQ - 1) / FQ, a.H, a.n_seq),
-                         dim3(256), 0, s, a);
+      if (part == 0)
+        hipLaunchKernelGGL((ld_attn_delta<bf16, DH>), dgrid, dim3(256), 0, s, a);
+      else if (part == 1)
+        hipLaunchKernelGGL(ld_attn_bwd_dkdv_bf16<DH>, dim3(a.H, a.n_seq, (a.S + BKEYS - 1) / BKEYS),
+                           dim3(256), dkdv_lds_bytes<DH>(), s, a);
+      else
+        hipLaunchKernelGGL(ld_attn_bwd_dq_bf16<DH>, dim3(a.H, a.n_seq, (a.S + DQ_ROWS - 1) / DQ_ROWS),
+                           dim3(256), dq_lds_bytes<DH>(), s, a);
       return hipGetLastError();
     }
   }
   if constexpr (DH <= 64) {
-    hipLaunchKernelGGL((ld_attn_delta<float, DH>), dgrid, dim3(256), 0, s, a);
     const dim3 grid((a.S + ST - 1) / ST, a.H, a.n_seq);
-    hipLaunchKernelGGL(ld_attn_bwd_dkdv_f32<DH>, grid, dim3(64), 0, s, a);
-    hipLaunchKernelGGL(ld_attn_bwd_dq_f32<DH>, grid, dim3(64), 0, s, a);
+    if (part == 0)
+      hipLaunchKernelGGL((ld_attn_delta<float, DH>), dgrid, dim3(256), 0, s, a);
+    else if (part == 1)
+      hipLaunchKernelGGL(ld_attn_bwd_dkdv_f32<DH>, grid, dim3(64), 0, s, a);
+    else
+      hipLaunchKernelGGL(ld_attn_bwd_dq_f32<DH>, grid, dim3(64), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -634,19 +914,33 @@ hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
+const char* attn_bwd_kernel_name(int dtype, int part) {
+  static const char* names[2][3] = {{"ld_attn_delta", "ld_attn_bwd_dkdv_f32", "ld_attn_bwd_dq_f32"},
+                                    {"ld_attn_delta", "ld_attn_bwd_dkdv_bf16", "ld_attn_bwd_dq_bf16"}};
+  return names[dtype == LD_BF16 ? 1 : 0][part];
+}
+
+hipError_t launch_attn_bwd_part(int dtype, int part, const AttnArgs& a, hipStream_t s) {
   if (a.n_seq <= 0) return hipSuccess;
   if (dtype == LD_BF16) {
-    if (a.dh == 64) return bwd_dh<64>(dtype, a, s);
-    if (a.dh == 128) return bwd_dh<128>(dtype, a, s);
+    if (a.dh == 64) return bwd_dh<64>(dtype, part, a, s);
+    if (a.dh == 128) return bwd_dh<128>(dtype, part, a, s);
     return hipErrorInvalidValue;
   }
   switch (a.dh) {
-    case 16: return bwd_dh<16>(dtype, a, s);
-    case 32: return bwd_dh<32>(dtype, a, s);
-    case 64: return bwd_dh<64>(dtype, a, s);
+    case 16: return bwd_dh<16>(dtype, part, a, s);
+    case 32: return bwd_dh<32>(dtype, part, a, s);
+    case 64: return bwd_dh<64>(dtype, part, a, s);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  for (int part = 0; part < 3; ++part) {
+    const hipError_t e = launch_attn_bwd_part(dtype, part, a, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace ld

@@ -151,6 +151,9 @@ hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmP
                             int64_t max_m, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
+// The three backward kernels one at a time: 0 delta, 1 dK/dV, 2 dQ.
+hipError_t launch_attn_bwd_part(int dtype, int part, const AttnArgs& a, hipStream_t s);
+const char* attn_bwd_kernel_name(int dtype, int part);
 const char* attn_fwd_kernel_name(int dtype);
 
 }  // namespace ld
