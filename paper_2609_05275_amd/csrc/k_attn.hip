@@ -107,53 +107,61 @@ __device__ __forceinline__ void stage_rows(const bf16* src, int64_t ld, int r0, 
 // ---------------------------------------------------------------- forward
 
 constexpr int FQ = 128, FKV = 64;   // dQ kernel tiles
-constexpr int FWQ = 256;            // forward: query rows per workgroup (4 waves x 64)
+constexpr int FWQ = 256;            // forward: query rows per workgroup
+#ifndef FWD_RPW
+#define FWD_RPW 32                  // forward: query rows per wave (8 waves)
+#endif
 
-// Registers holding one K/V block (64 keys x DH) on its way to LDS.
-template <int DH>
+// Registers holding one K/V block (64 keys x DH) on its way to LDS, split
+// over NT threads.
+template <int DH, int NT>
 struct KvRegs {
-  static constexpr int NK = 64 * DH / 8 / 256;       // 16-byte K chunks per thread
+  static constexpr int NKC = 64 * DH / 8;            // 16-byte K chunks
+  static constexpr int NK = (NKC + NT - 1) / NT;     // per thread
   static constexpr int NV = (64 / 4) * (DH / 8);     // V groups of 4 keys x 8 d
-  static constexpr int NVT = (NV + 255) / 256;       // per thread
+  static constexpr int NVT = (NV + NT - 1) / NT;     // per thread
   uint4 k[NK];
   uint4 v[NVT][4];
 };
 
 // The block [k0, k0+64) must lie inside the sequence (S % 64 == 0).
-template <int DH>
-__device__ __forceinline__ void kv_load(KvRegs<DH>& r, const bf16* Kp, const bf16* Vp, int64_t ld,
+template <int DH, int NT>
+__device__ __forceinline__ void kv_load(KvRegs<DH, NT>& r, const bf16* Kp, const bf16* Vp, int64_t ld,
                                         int k0, int tid) {
 #pragma unroll
-  for (int p = 0; p < KvRegs<DH>::NK; ++p) {
-    const int c = p * 256 + tid;
+  for (int p = 0; p < KvRegs<DH, NT>::NK; ++p) {
+    const int c = p * NT + tid;
     const int row = c / (DH / 8), dc = (c % (DH / 8)) * 8;
-    r.k[p] = *reinterpret_cast<const uint4*>(Kp + static_cast<int64_t>(k0 + row) * ld + dc);
+    r.k[p] = c < KvRegs<DH, NT>::NKC
+                 ? *reinterpret_cast<const uint4*>(Kp + static_cast<int64_t>(k0 + row) * ld + dc)
+                 : make_uint4(0, 0, 0, 0);
   }
 #pragma unroll
-  for (int p = 0; p < KvRegs<DH>::NVT; ++p) {
-    const int c = p * 256 + tid;
+  for (int p = 0; p < KvRegs<DH, NT>::NVT; ++p) {
+    const int c = p * NT + tid;
     const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      r.v[p][k] = c < KvRegs<DH>::NV
+      r.v[p][k] = c < KvRegs<DH, NT>::NV
                       ? *reinterpret_cast<const uint4*>(Vp + static_cast<int64_t>(k0 + rg + k) * ld + dc)
                       : make_uint4(0, 0, 0, 0);
   }
 }
 
 // K as [key][d] (pitch DH+8), V transposed as [d][key] (swizzled, tr_off).
-template <int DH>
-__device__ __forceinline__ void kv_store(const KvRegs<DH>& r, bf16* Ks, bf16* Vt, int tid) {
+template <int DH, int NT>
+__device__ __forceinline__ void kv_store(const KvRegs<DH, NT>& r, bf16* Ks, bf16* Vt, int tid) {
 #pragma unroll
-  for (int p = 0; p < KvRegs<DH>::NK; ++p) {
-    const int c = p * 256 + tid;
+  for (int p = 0; p < KvRegs<DH, NT>::NK; ++p) {
+    const int c = p * NT + tid;
+    if (c >= KvRegs<DH, NT>::NKC) continue;
     const int row = c / (DH / 8), dc = (c % (DH / 8)) * 8;
     *reinterpret_cast<uint4*>(Ks + row * (DH + 8) + dc) = r.k[p];
   }
 #pragma unroll
-  for (int p = 0; p < KvRegs<DH>::NVT; ++p) {
-    const int c = p * 256 + tid;
-    if (c >= KvRegs<DH>::NV) continue;
+  for (int p = 0; p < KvRegs<DH, NT>::NVT; ++p) {
+    const int c = p * NT + tid;
+    if (c >= KvRegs<DH, NT>::NV) continue;
     const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -165,12 +173,15 @@ __device__ __forceinline__ void kv_store(const KvRegs<DH>& r, bf16* Ks, bf16* Vt
   }
 }
 
-// Forward.  Each wave owns 64 query rows as two 32-row MFMA blocks that share
-// every K and V fragment it reads from LDS.  K/V blocks of 64 keys are double
-// buffered in LDS and the next block is fetched into registers while the
-// current one is used, so there is one barrier per block.
-template <int DH>
-__global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
+// Forward.  A workgroup owns 256 query rows; each wave owns RPW of them as
+// RPW/32 MFMA blocks that share every K and V fragment it reads from LDS
+// (64 rows: 4 waves, fewer LDS reads per FLOP; 32 rows: 8 waves, two per
+// SIMD).  K/V blocks of 64 keys are double buffered in LDS and the next block
+// is fetched into registers while the current one is used, so there is one
+// barrier per block.
+template <int DH, int RPW>
+__global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a) {
+  constexpr int NSB = RPW / 32, NT = 64 * (FWQ / RPW);
   constexpr int KT = FKV * (DH + 8), VT = DH * FKV;
   __shared__ __align__(16) bf16 lds[2 * (KT + VT)];
   const int S = a.S, H = a.H;
@@ -182,7 +193,7 @@ __global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
   if (seq >= seq_count(a)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hf = lane >> 5, cl = lane & 31;
-  const int q0 = qt * FWQ, qw = q0 + wave * 64;
+  const int q0 = qt * FWQ, qw = q0 + wave * RPW;
   const int64_t ldq = 3ll * H * DH;
   const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
   const bf16* Qp = base + head * DH;
@@ -190,11 +201,11 @@ __global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
   const bf16* Vp = base + 2ll * H * DH + head * DH;
   const float sl2 = a.scale * kLog2e;
 
-  bf16x8 qf[2][DH / 16];
-  floatx16 o[2][DH / 32];
-  float m[2], l[2];
+  bf16x8 qf[NSB][DH / 16];
+  floatx16 o[NSB][DH / 32];
+  float m[NSB], l[NSB];
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
+  for (int sb = 0; sb < NSB; ++sb) {
     const int qrow = qw + sb * 32 + cl;
 #pragma unroll
     for (int ks = 0; ks < DH / 16; ++ks)
@@ -209,21 +220,21 @@ __global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
 
   const int kv_end = min(S, q0 + FWQ);
   const int nkb = (kv_end + FKV - 1) / FKV;
-  KvRegs<DH> kr;
-  kv_load<DH>(kr, Kp, Vp, ldq, 0, tid);
-  kv_store<DH>(kr, lds, lds + KT, tid);
+  KvRegs<DH, NT> kr;
+  kv_load<DH, NT>(kr, Kp, Vp, ldq, 0, tid);
+  kv_store<DH, NT>(kr, lds, lds + KT, tid);
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
     const int k0 = kb * FKV;
     bf16* Ks = lds + (kb & 1) * (KT + VT);
     bf16* Vt = Ks + KT;
-    if (kb + 1 < nkb) kv_load<DH>(kr, Kp, Vp, ldq, k0 + FKV, tid);
-    if (qw < S && k0 <= qw + 63) {
+    if (kb + 1 < nkb) kv_load<DH, NT>(kr, Kp, Vp, ldq, k0 + FKV, tid);
+    if (qw < S && k0 <= qw + RPW - 1) {
       const bool diag = k0 + FKV - 1 > qw;  // some key of the block is past some row
-      // scores of both 32-row blocks: each K fragment feeds two MFMA chains
-      floatx16 sc[2][2];
+      // scores of every 32-row block: each K fragment feeds NSB MFMA chains
+      floatx16 sc[NSB][2];
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+      for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
@@ -233,12 +244,12 @@ __global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh) {
           const bf16x8 kf = load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8);
-          sc[0][kh] = mfma(kf, qf[0][ks], sc[0][kh]);
-          sc[1][kh] = mfma(kf, qf[1][ks], sc[1][kh]);
-        }
-      bf16x8 pb[2][2][2];
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
+          for (int sb = 0; sb < NSB; ++sb) sc[sb][kh] = mfma(kf, qf[sb][ks], sc[sb][kh]);
+        }
+      bf16x8 pb[NSB][2][2];
+#pragma unroll
+      for (int sb = 0; sb < NSB; ++sb) {
         const int qrow = qw + sb * 32 + cl;
         float mx = -INFINITY;
 #pragma unroll
@@ -290,19 +301,19 @@ __global__ __launch_bounds__(256) void ld_attn_fwd_bf16(AttnArgs a) {
           for (int c = 0; c < 2; ++c) {
             const int kbb = kh * 32 + 16 * c + 4 * hf;
             const bf16x8 vf = load4x2(Vt + tr_off(vr, kbb), Vt + tr_off(vr, kbb + 8));
-            o[0][db] = mfma(vf, pb[0][kh][c], o[0][db]);
-            o[1][db] = mfma(vf, pb[1][kh][c], o[1][db]);
+#pragma unroll
+            for (int sb = 0; sb < NSB; ++sb) o[sb][db] = mfma(vf, pb[sb][kh][c], o[sb][db]);
           }
       }
     }
     if (kb + 1 < nkb) {
       bf16* Kn = lds + ((kb + 1) & 1) * (KT + VT);
-      kv_store<DH>(kr, Kn, Kn + KT, tid);
+      kv_store<DH, NT>(kr, Kn, Kn + KT, tid);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
+  for (int sb = 0; sb < NSB; ++sb) {
     const int qrow = qw + sb * 32 + cl;
     const float lt = l[sb] + __shfl_xor(l[sb], 32, 64);
     if (qrow < S) {
@@ -351,41 +362,41 @@ __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
 }
 
 // Registers holding 64 rows x DH of one operand as groups of 4 rows x 8
-// columns, from which both the [row][d] and the transposed [d][row] LDS
-// copies are written.
-template <int DH>
-struct RowGroups {
+// columns, split over NT threads, from which both the [row][d] and the
+// transposed [d][row] LDS copies are written.  Rows [r0, r0+64) must lie
+// inside the sequence (S % 64 == 0).
+template <int DH, int NT>
+struct RowGroupsN {
   static constexpr int NG = (64 / 4) * (DH / 8);
-  static constexpr int NGT = (NG + 255) / 256;
+  static constexpr int NGT = (NG + NT - 1) / NT;
   uint4 v[NGT][4];
 };
 
-// Rows [r0, r0+64) must lie inside the sequence (S % 64 == 0).
-template <int DH>
-__device__ __forceinline__ void rg_load(RowGroups<DH>& t, const bf16* src, int64_t ld, int r0, int tid) {
+template <int DH, int NT>
+__device__ __forceinline__ void rgn_load(RowGroupsN<DH, NT>& t, const bf16* src, int64_t ld, int r0,
+                                         int tid) {
 #pragma unroll
-  for (int p = 0; p < RowGroups<DH>::NGT; ++p) {
-    const int c = p * 256 + tid;
+  for (int p = 0; p < RowGroupsN<DH, NT>::NGT; ++p) {
+    const int c = p * NT + tid;
     const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      t.v[p][k] = c < RowGroups<DH>::NG
+      t.v[p][k] = c < RowGroupsN<DH, NT>::NG
                       ? *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r0 + rg + k) * ld + dc)
                       : make_uint4(0, 0, 0, 0);
   }
 }
 
-template <int DH>
-__device__ __forceinline__ void rg_store(const RowGroups<DH>& t, bf16* direct, bf16* trans, int tid) {
+template <int DH, int NT>
+__device__ __forceinline__ void rgn_store(const RowGroupsN<DH, NT>& t, bf16* direct, bf16* trans,
+                                          int tid) {
 #pragma unroll
-  for (int p = 0; p < RowGroups<DH>::NGT; ++p) {
-    const int c = p * 256 + tid;
-    if (c >= RowGroups<DH>::NG) continue;
+  for (int p = 0; p < RowGroupsN<DH, NT>::NGT; ++p) {
+    const int c = p * NT + tid;
+    if (c >= RowGroupsN<DH, NT>::NG) continue;
     const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
-    if (direct) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) *reinterpret_cast<uint4*>(direct + (rg + k) * (DH + 8) + dc) = t.v[p][k];
-    }
+    for (int k = 0; k < 4; ++k) *reinterpret_cast<uint4*>(direct + (rg + k) * (DH + 8) + dc) = t.v[p][k];
     if (trans) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -399,18 +410,26 @@ __device__ __forceinline__ void rg_store(const RowGroups<DH>& t, bf16* direct, b
 }
 
 constexpr int BQ = 64;       // query rows per step of the dK/dV kernel
-constexpr int BKEYS = 128;   // keys per dK/dV workgroup (4 waves x 32)
 
-// dK, dV.  A workgroup owns 128 keys (32 per wave, K and V fragments in
-// registers) and walks the 64-row query blocks from the diagonal to the end;
-// Q, dO (both as [q][d] and transposed [d][q]), the log-sum-exp and delta of
-// the block are double buffered in LDS with the next block prefetched in
-// registers.  P = 2^(s*scale*log2e - lse*log2e) is recomputed, dS = P (dP -
-// delta); dV^T += dO^T P and dK^T += Q^T dS take P and dS straight from the
-// score accumulators (their rows are a fixed permutation of the MFMA k index,
-// matched when the transposed tiles are read).
+// Waves per dK/dV workgroup: 8 (two per SIMD) where the per-wave state fits
+// in 256 registers (d_head 64); 4 for d_head 128, whose K/V fragments and
+// dK/dV accumulators need the whole register file of a SIMD.
 template <int DH>
-__global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
+constexpr int dkdv_waves() { return DH <= 64 ? 8 : 4; }
+
+// dK, dV.  A workgroup of NW waves owns 32 NW keys (32 per wave, K and V
+// fragments in registers) and walks the 64-row query
+// blocks from the diagonal to the end; Q, dO (both as [q][d] and transposed
+// [d][q]), the log-sum-exp and delta of the block are double buffered in LDS
+// with the next block prefetched in registers.  P = 2^(s*scale*log2e -
+// lse*log2e) is recomputed, dS = P (dP - delta); dV^T += dO^T P and
+// dK^T += Q^T dS take P and dS straight from the score accumulators (their
+// rows are a fixed permutation of the MFMA k index, matched when the
+// transposed tiles are read).  The two 32-row halves of a query block are
+// processed one after the other so only one half's scores are live.
+template <int DH, int NW = dkdv_waves<DH>()>
+__global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
+  constexpr int NT = 64 * NW, BKEYS = 32 * NW;
   constexpr int DT = BQ * (DH + 8), TT = DH * BQ;
   constexpr int STAGE = 2 * DT + 2 * TT;  // bf16 elements per buffer
   extern __shared__ __align__(16) bf16 lds[];
@@ -450,11 +469,11 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
 
   const int q_first = k0;  // the first query that can see key k0
   const int nqb = q_first < S ? (S - q_first) / BQ : 0;
-  RowGroups<DH> rq, ro;
+  RowGroupsN<DH, NT> rq, ro;
   float lse_r = 0.f, del_r = 0.f;
   auto fetch = [&](int qb) {
-    rg_load<DH>(rq, Qp, ldq, qb, tid);
-    rg_load<DH>(ro, dOp, ldo, qb, tid);
+    rgn_load<DH, NT>(rq, Qp, ldq, qb, tid);
+    rgn_load<DH, NT>(ro, dOp, ldo, qb, tid);
     if (tid < BQ) {
       lse_r = lse[qb + tid] * kLog2e;
       del_r = del[qb + tid];
@@ -462,8 +481,8 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   };
   auto put = [&](int buf) {
     bf16* st = lds + buf * STAGE;
-    rg_store<DH>(rq, st, st + 2 * DT, tid);
-    rg_store<DH>(ro, st + DT, st + 2 * DT + TT, tid);
+    rgn_store<DH, NT>(rq, st, st + 2 * DT, tid);
+    rgn_store<DH, NT>(ro, st + DT, st + 2 * DT + TT, tid);
     if (tid < BQ) {
       lse_s[buf * BQ + tid] = lse_r;
       del_s[buf * BQ + tid] = del_r;
@@ -484,10 +503,10 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     const float* ls = lse_s + buf * BQ;
     const float* dl = del_s + buf * BQ;
     if (active && kw <= qb + BQ - 1) {
-      const bool diag = kw + 31 > qb;  // some key of the wave is past some query of the block
-      bf16x8 pb[2][2], dsb[2][2];
 #pragma unroll
       for (int qh = 0; qh < 2; ++qh) {
+        if (kw > qb + qh * 32 + 31) continue;  // every key of the wave is past this half
+        const bool diag = kw + 31 > qb + qh * 32;
         floatx16 sc, dp;
 #pragma unroll
         for (int v = 0; v < 16; ++v) sc[v] = dp[v] = 0.f;
@@ -496,26 +515,26 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
           sc = mfma(load8(Qs + (qh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), kf[ks], sc);
           dp = mfma(load8(Os + (qh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), vf[ks], dp);
         }
+        bf16x8 pb[2], dsb[2];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int ql = qh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
           float p = __builtin_amdgcn_exp2f(sc[v] * sl2 - ls[ql]);
           if (diag && key > qb + ql) p = 0.f;
-          pb[qh][v >> 3][v & 7] = static_cast<bf16>(p);
-          dsb[qh][v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dl[ql]));
+          pb[v >> 3][v & 7] = static_cast<bf16>(p);
+          dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dl[ql]));
         }
-      }
 #pragma unroll
-      for (int db = 0; db < DH / 32; ++db) {
-        const int dr = db * 32 + cl;
-#pragma unroll
-        for (int qh = 0; qh < 2; ++qh)
+        for (int db = 0; db < DH / 32; ++db) {
+          const int dr = db * 32 + cl;
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
             const int qq = qh * 32 + 16 * c + 4 * hf;
-            dv[db] = mfma(load4x2(Ot + tr_off(dr, qq), Ot + tr_off(dr, qq + 8)), pb[qh][c], dv[db]);
-            dk[db] = mfma(load4x2(Qt + tr_off(dr, qq), Qt + tr_off(dr, qq + 8)), dsb[qh][c], dk[db]);
+            dv[db] = mfma(load4x2(Ot + tr_off(dr, qq), Ot + tr_off(dr, qq + 8)), pb[c], dv[db]);
+            dk[db] = mfma(load4x2(Qt + tr_off(dr, qq), Qt + tr_off(dr, qq + 8)), dsb[c], dk[db]);
           }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep the two halves' live ranges apart
       }
     }
     if (ib + 1 < nqb) put(buf ^ 1);
@@ -546,16 +565,16 @@ constexpr size_t dkdv_lds_bytes() {
   return (2ull * (2 * BQ * (DH + 8) + 2 * DH * BQ)) * sizeof(bf16) + 4ull * BQ * sizeof(float);
 }
 
-constexpr int DQ_ROWS = 256;  // query rows per dQ workgroup (4 waves x 64)
+constexpr int DQ_ROWS = 256;  // query rows per dQ workgroup (8 waves x 32)
 
-// dQ.  A workgroup owns 256 query rows (64 per wave as two 32-row MFMA blocks
-// sharing every fragment read) and walks the 64-key blocks up to the
-// diagonal; K ([key][d] and transposed [d][key]) and V are double buffered in
-// LDS with the next block prefetched in registers.  Scores are formed
-// transposed (S^T = K Q^T), so the query's log-sum-exp and delta are per lane
-// and dS^T feeds dQ^T += K^T dS^T directly.
+// dQ.  A workgroup of 8 waves owns 256 query rows (32 per wave, two waves per
+// SIMD) and walks the 64-key blocks up to the diagonal; K ([key][d] and
+// transposed [d][key]) and V are double buffered in LDS with the next block
+// prefetched in registers.  Scores are formed transposed (S^T = K Q^T), so the
+// query's log-sum-exp and delta are per lane and dS^T feeds dQ^T += K^T dS^T
+// directly.
 template <int DH>
-__global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
+__global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   constexpr int DT = FKV * (DH + 8), TT = DH * FKV;
   constexpr int STAGE = 2 * DT + TT;  // Ks, Vs, Kt
   extern __shared__ __align__(16) bf16 lds[];
@@ -567,7 +586,7 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   if (seq >= seq_count(a)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hf = lane >> 5, cl = lane & 31;
-  const int q0 = qt * DQ_ROWS, qw = q0 + wave * 64;
+  const int q0 = qt * DQ_ROWS, qw = q0 + wave * 32, qrow = qw + cl;
   const int64_t ldq = 3ll * H * DH, ldo = static_cast<int64_t>(H) * DH;
   const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
   const bf16* Qp = base + head * DH;
@@ -576,82 +595,64 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   const bf16* dOp = static_cast<const bf16*>(a.go) + static_cast<int64_t>(seq) * S * ldo + head * DH;
   const float sl2 = a.scale * kLog2e;
 
-  bf16x8 qf[2][DH / 16], of[2][DH / 16];
-  float lse2[2], dl[2];
-  floatx16 dq[2][DH / 32];
+  const bool qok = qrow < S;
+  const int64_t srow = (static_cast<int64_t>(seq) * H + head) * S + (qok ? qrow : 0);
+  const float lse2 = qok ? a.lse[srow] * kLog2e : 0.f;
+  const float dl = qok ? a.delta[srow] : 0.f;
+  bf16x8 qf[DH / 16], of[DH / 16];
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int qrow = qw + sb * 32 + cl;
-    const bool qok = qrow < S;
-    const int64_t srow = (static_cast<int64_t>(seq) * H + head) * S + (qok ? qrow : 0);
-    lse2[sb] = qok ? a.lse[srow] * kLog2e : 0.f;
-    dl[sb] = qok ? a.delta[srow] : 0.f;
-#pragma unroll
-    for (int ks = 0; ks < DH / 16; ++ks) {
-      qf[sb][ks] = qok ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
-      of[sb][ks] = qok ? load8(dOp + static_cast<int64_t>(qrow) * ldo + ks * 16 + hf * 8) : zero8();
-    }
-#pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) dq[sb][db][v] = 0.f;
+  for (int ks = 0; ks < DH / 16; ++ks) {
+    qf[ks] = qok ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
+    of[ks] = qok ? load8(dOp + static_cast<int64_t>(qrow) * ldo + ks * 16 + hf * 8) : zero8();
   }
+  floatx16 dq[DH / 32];
+#pragma unroll
+  for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dq[db][v] = 0.f;
 
   const int kv_end = min(S, q0 + DQ_ROWS);
   const int nkb = kv_end / FKV;
-  RowGroups<DH> rk, rv;
+  RowGroupsN<DH, 512> rk, rv;
   auto put = [&](int buf) {
     bf16* st = lds + buf * STAGE;
-    rg_store<DH>(rk, st, st + 2 * DT, tid);
-    rg_store<DH>(rv, st + DT, nullptr, tid);
+    rgn_store<DH, 512>(rk, st, st + 2 * DT, tid);
+    rgn_store<DH, 512>(rv, st + DT, nullptr, tid);
   };
-  rg_load<DH>(rk, Kp, ldq, 0, tid);
-  rg_load<DH>(rv, Vp, ldq, 0, tid);
+  rgn_load<DH, 512>(rk, Kp, ldq, 0, tid);
+  rgn_load<DH, 512>(rv, Vp, ldq, 0, tid);
   put(0);
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
     const int k0 = kb * FKV, buf = kb & 1;
     if (kb + 1 < nkb) {
-      rg_load<DH>(rk, Kp, ldq, k0 + FKV, tid);
-      rg_load<DH>(rv, Vp, ldq, k0 + FKV, tid);
+      rgn_load<DH, 512>(rk, Kp, ldq, k0 + FKV, tid);
+      rgn_load<DH, 512>(rv, Vp, ldq, k0 + FKV, tid);
     }
     const bf16* Ks = lds + buf * STAGE;
     const bf16* Vs = Ks + DT;
     const bf16* Kt = Ks + 2 * DT;
-    if (qw < S && k0 <= qw + 63) {
+    if (qw < S && k0 <= qw + 31) {
       const bool diag = k0 + FKV - 1 > qw;
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
-        // scores and dP^T of this 32-key half for both query blocks, then its
-        // dS^T is consumed right away (only one half's dS is ever live)
-        floatx16 st[2], dpt[2];
+        floatx16 st, dpt;
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) st[sb][v] = dpt[sb][v] = 0.f;
+        for (int v = 0; v < 16; ++v) st[v] = dpt[v] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < DH / 16; ++ks) {
-          const bf16x8 kfr = load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8);
-          const bf16x8 vfr = load8(Vs + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8);
-#pragma unroll
-          for (int sb = 0; sb < 2; ++sb) {
-            st[sb] = mfma(kfr, qf[sb][ks], st[sb]);
-            dpt[sb] = mfma(vfr, of[sb][ks], dpt[sb]);
-          }
+          st = mfma(load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), qf[ks], st);
+          dpt = mfma(load8(Vs + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), of[ks], dpt);
         }
-        bf16x8 dsb[2][2];
+        bf16x8 dsb[2];
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb) {
-          const int qrow = qw + sb * 32 + cl;
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float p = __builtin_amdgcn_exp2f(st[sb][v] * sl2 - lse2[sb]);
-            if (diag) {
-              const int keyi = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-              if (keyi > qrow) p = 0.f;
-            }
-            dsb[sb][v >> 3][v & 7] = static_cast<bf16>(p * (dpt[sb][v] - dl[sb]));
+        for (int v = 0; v < 16; ++v) {
+          float p = __builtin_amdgcn_exp2f(st[v] * sl2 - lse2);
+          if (diag) {
+            const int keyi = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+            if (keyi > qrow) p = 0.f;
           }
+          dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dpt[v] - dl));
         }
 #pragma unroll
         for (int db = 0; db < DH / 32; ++db) {
@@ -659,21 +660,15 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
             const int kk = kh * 32 + 16 * c + 4 * hf;
-            const bf16x8 kt = load4x2(Kt + tr_off(dr, kk), Kt + tr_off(dr, kk + 8));
-            dq[0][db] = mfma(kt, dsb[0][c], dq[0][db]);
-            dq[1][db] = mfma(kt, dsb[1][c], dq[1][db]);
+            dq[db] = mfma(load4x2(Kt + tr_off(dr, kk), Kt + tr_off(dr, kk + 8)), dsb[c], dq[db]);
           }
         }
-        __builtin_amdgcn_sched_barrier(0);  // keep the two halves' live ranges apart
       }
     }
     if (kb + 1 < nkb) put(buf ^ 1);
     __syncthreads();
   }
-#pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int qrow = qw + sb * 32 + cl;
-    if (qrow >= S) continue;
+  if (qok) {
     bf16* G = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * ldq + head * DH;
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db)
@@ -681,7 +676,7 @@ __global__ __launch_bounds__(256) void ld_attn_bwd_dq_bf16(AttnArgs a) {
       for (int g = 0; g < 4; ++g) {
         __attribute__((aligned(8))) bf16 t[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(dq[sb][db][4 * g + i] * a.scale);
+        for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(dq[db][4 * g + i] * a.scale);
         *reinterpret_cast<uint2*>(G + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(t);
       }
   }
@@ -853,7 +848,8 @@ hipError_t fwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
   if constexpr (DH >= 64) {
     if (dtype == LD_BF16) {
       const dim3 grid(a.H, a.n_seq, (a.S + FWQ - 1) / FWQ);
-      hipLaunchKernelGGL(ld_attn_fwd_bf16<DH>, grid, dim3(256), 0, s, a);
+      constexpr int rpw = FWD_RPW;
+      hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw>), grid, dim3(64 * (FWQ / rpw)), 0, s, a);
       return hipGetLastError();
     }
   }
@@ -872,12 +868,13 @@ hipError_t bwd_dh(int dtype, int part, const AttnArgs& a, hipStream_t s) {
     if (dtype == LD_BF16) {
       if (part == 0)
         hipLaunchKernelGGL((ld_attn_delta<bf16, DH>), dgrid, dim3(256), 0, s, a);
-      else if (part == 1)
-        hipLaunchKernelGGL(ld_attn_bwd_dkdv_bf16<DH>, dim3(a.H, a.n_seq, (a.S + BKEYS - 1) / BKEYS),
-                           dim3(256), dkdv_lds_bytes<DH>(), s, a);
-      else
+      else if (part == 1) {
+        constexpr int nw = dkdv_waves<DH>();
+        hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw>), dim3(a.H, a.n_seq, (a.S + 32 * nw - 1) / (32 * nw)),
+                           dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
+      } else
         hipLaunchKernelGGL(ld_attn_bwd_dq_bf16<DH>, dim3(a.H, a.n_seq, (a.S + DQ_ROWS - 1) / DQ_ROWS),
-                           dim3(256), dq_lds_bytes<DH>(), s, a);
+                           dim3(512), dq_lds_bytes<DH>(), s, a);
       return hipGetLastError();
     }
   }
