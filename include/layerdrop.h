@@ -63,7 +63,7 @@ typedef enum { LD_F32 = 0, LD_BF16 = 1 } ld_dtype;
  *   batch B, seq S, d_model d, n_heads H (d % H == 0), d_ff f.
  *   LD_BF16 requires d_head = d/H in {64, 128}, d % 8 == 0, f % 8 == 0,
  *   S % 64 == 0.  LD_F32 requires d_head in {16, 32, 64}, d % 4 == 0, f % 4 == 0.
- *   Both require d <= 8192 (bf16) or d <= 4096 (fp32).
+ *   d <= 4096 (bf16) or d <= 2048 (fp32).
  *   rms_eps: RMSNorm epsilon (the paper fixes none; 1e-5 is the default).
  *   rescale: 1 -> r = res_scale / (1 - p); 0 -> r = res_scale.
  *   res_scale: constant residual-branch multiplier (the depth multiplier of
@@ -195,7 +195,7 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
  * host values. */
 
 /* y = x * rsqrt(mean_d(x^2) + eps) * g; rstd[row] = that rsqrt (float32).
- * x, y: device [rows, d]; g: device [d]. */
+ * x, y: device [rows, d]; g: device [d].  d <= 4096 (bf16) / 2048 (fp32). */
 int ld_rmsnorm_fwd(int32_t dtype, int32_t rows, int32_t d, float eps, const void* x, const void* g,
                    void* y, float* rstd, void* stream);
 

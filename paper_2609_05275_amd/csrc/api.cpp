@@ -107,12 +107,12 @@ int check_cfg(const ld_config* c, Dims* out) {
     if (dh != 64 && dh != 128) return fail(LD_E_UNSUPPORTED, "bf16 needs d_head 64 or 128, got %d", dh);
     if (c->d_model % 8 || c->d_ff % 8) return fail(LD_E_SHAPE, "bf16 needs d_model, d_ff multiples of 8");
     if (c->seq % 64) return fail(LD_E_SHAPE, "bf16 needs seq %% 64 == 0");
-    if (c->d_model > 8192) return fail(LD_E_UNSUPPORTED, "d_model > 8192");
+    if (c->d_model > 4096) return fail(LD_E_UNSUPPORTED, "d_model > 4096");
   } else {
     if (dh != 16 && dh != 32 && dh != 64)
       return fail(LD_E_UNSUPPORTED, "fp32 needs d_head 16, 32 or 64, got %d", dh);
     if (c->d_model % 4 || c->d_ff % 4) return fail(LD_E_SHAPE, "fp32 needs d_model, d_ff multiples of 4");
-    if (c->d_model > 4096) return fail(LD_E_UNSUPPORTED, "d_model > 4096");
+    if (c->d_model > 2048) return fail(LD_E_UNSUPPORTED, "d_model > 2048");
   }
   const int64_t T = static_cast<int64_t>(c->batch) * c->seq;
   if (T * std::max<int64_t>(3ll * c->d_model, 2ll * c->d_ff) >= (1ll << 40) || T >= (1ll << 30))
@@ -953,7 +953,7 @@ int ld_rmsnorm_fwd(int32_t dtype, int32_t rows, int32_t d, float eps, const void
   t_err.clear();
   if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
   if (rows < 0 || d < 1) return fail(LD_E_SHAPE, "bad shape");
-  if (d % (dtype == LD_BF16 ? 8 : 4) || d > (dtype == LD_BF16 ? 8192 : 4096)) return fail(LD_E_SHAPE, "unsupported d");
+  if (d % (dtype == LD_BF16 ? 8 : 4) || d > (dtype == LD_BF16 ? 4096 : 2048)) return fail(LD_E_SHAPE, "unsupported d");
   if (!(eps > 0.f)) return fail(LD_E_INVALID, "eps must be > 0");
   if (rows == 0) return LD_OK;
   if (!x || !g || !y || !rstd) return fail(LD_E_INVALID, "NULL pointer");
@@ -982,7 +982,7 @@ int ld_rmsnorm_bwd(int32_t dtype, int32_t rows, int32_t d, const void* x, const 
   t_err.clear();
   if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
   if (rows < 0 || d < 1) return fail(LD_E_SHAPE, "bad shape");
-  if (d % (dtype == LD_BF16 ? 8 : 4) || d > (dtype == LD_BF16 ? 8192 : 4096)) return fail(LD_E_SHAPE, "unsupported d");
+  if (d % (dtype == LD_BF16 ? 8 : 4) || d > (dtype == LD_BF16 ? 4096 : 2048)) return fail(LD_E_SHAPE, "unsupported d");
   if (!g || !dg || !ws || (rows > 0 && (!x || !rstd || !gy || !gx))) return fail(LD_E_INVALID, "NULL pointer");
   if (ws_bytes < ld_rmsnorm_bwd_ws_bytes(rows, d)) return fail(LD_E_WORKSPACE, "workspace too small");
   RmsBwdArgs a{};

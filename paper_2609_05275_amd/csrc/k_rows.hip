@@ -193,12 +193,37 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_fwd_k(RmsFwdArgs a) {
   if (lane == 0) a.rstd[row] = rstd;
 }
 
-constexpr int kBwdRowsPerWave = 16;
+constexpr int kBwdRowsPerWave = 8;
 constexpr int kBwdRowsPerBlock = 4 * kBwdRowsPerWave;
+
+template <typename T, int NCH>
+struct NormRow {
+  Pack<T> x[NCH], gy[NCH], res[NCH];
+  float rstd;
+};
+
+template <typename T, int NCH>
+__device__ __forceinline__ void norm_row_load(NormRow<T, NCH>& r, const RmsBwdArgs& a, int64_t row,
+                                              int lane) {
+  const T* x = static_cast<const T*>(a.x) + row * a.d;
+  const T* gy = static_cast<const T*>(a.gy) + row * a.d;
+  const T* gres = a.gres ? static_cast<const T*>(a.gres) + row * a.d : nullptr;
+  r.rstd = a.rstd[row];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 64 + lane) * Pack<T>::N;
+    if (col < a.d) {
+      r.x[c] = load16(x + col);
+      r.gy[c] = load16(gy + col);
+      if (gres) r.res[c] = load16(gres + col);
+    }
+  }
+}
 
 // gx = gres + rstd*(g*gy) - x*rstd^3*mean_d(x*g*gy); per-block dg partials
 // summed over the block's rows in a fixed order (rows in sequence inside a
-// wave, then waves 0..3 through LDS).
+// wave, then waves 0..3 through LDS).  The next row's loads are issued
+// before the current row's reduction so a wave keeps two rows in flight.
 template <typename T, int NCH>
 __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
   constexpr int VN = Pack<T>::N;
@@ -220,47 +245,48 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
   }
   const float inv_d = 1.f / static_cast<float>(a.d);
   const int64_t r0 = blockIdx.x * static_cast<int64_t>(kBwdRowsPerBlock) + wave * kBwdRowsPerWave;
-  for (int k = 0; k < kBwdRowsPerWave; ++k) {
-    const int64_t row = r0 + k;
-    if (row >= rows) break;
-    const T* x = static_cast<const T*>(a.x) + row * a.d;
-    const T* gy = static_cast<const T*>(a.gy) + row * a.d;
-    const float rstd = a.rstd[row];
-    Pack<T> xv[NCH], gyv[NCH];
+  const int64_t r1 = min(r0 + kBwdRowsPerWave, rows);
+  // two rows in flight when they fit in registers (up to 4 chunks per lane)
+  constexpr bool kPrefetch = NCH <= 4;
+  NormRow<T, NCH> cur, nxt;
+  if (kPrefetch && r0 < r1) norm_row_load(cur, a, r0, lane);
+  for (int64_t row = r0; row < r1; ++row) {
+    if (kPrefetch) {
+      if (row + 1 < r1) norm_row_load(nxt, a, row + 1, lane);
+    } else {
+      norm_row_load(cur, a, row, lane);
+    }
     float dot = 0.f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int col = (c * 64 + lane) * VN;
       if (col < a.d) {
-        xv[c] = load16(x + col);
-        gyv[c] = load16(gy + col);
 #pragma unroll
         for (int i = 0; i < VN; ++i)
-          dot = __builtin_fmaf(to_f(xv[c].v[i]) * gf[c][i], to_f(gyv[c].v[i]), dot);
+          dot = __builtin_fmaf(to_f(cur.x[c].v[i]) * gf[c][i], to_f(cur.gy[c].v[i]), dot);
       }
     }
     dot = wave_sum(dot);
+    const float rstd = cur.rstd;
     const float coef = rstd * rstd * rstd * dot * inv_d;
     T* gx = static_cast<T*>(a.gx) + map_row(a.dst, row) * a.d;
-    const T* gres = a.gres ? static_cast<const T*>(a.gres) + row * a.d : nullptr;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int col = (c * 64 + lane) * VN;
       if (col < a.d) {
-        Pack<T> rv{};
-        if (gres) rv = load16(gres + col);
         Pack<T> o;
 #pragma unroll
         for (int i = 0; i < VN; ++i) {
-          const float xf = to_f(xv[c].v[i]), gyf = to_f(gyv[c].v[i]);
+          const float xf = to_f(cur.x[c].v[i]), gyf = to_f(cur.gy[c].v[i]);
           float val = rstd * gf[c][i] * gyf - xf * coef;
-          if (gres) val += to_f(rv.v[i]);
+          if (a.gres) val += to_f(cur.res[c].v[i]);
           o.v[i] = from_f<T>(val);
           dga[c][i] = __builtin_fmaf(gyf * xf, rstd, dga[c][i]);
         }
         store16(gx + col, o);
       }
     }
+    if (kPrefetch) cur = nxt;
   }
   for (int w = 0; w < 4; ++w) {
     if (wave == w) {
@@ -279,13 +305,19 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
   for (int col = threadIdx.x; col < a.d; col += 256) part[col] = dg_lds[col];
 }
 
+// dg[c] = sum over blocks of part[b][c] in a fixed order: four row-strided
+// partial sums per column (b = r, r+4, ...), then those four in order.
 __global__ __launch_bounds__(256) void ld_dg_reduce_k(const float* part, int64_t n_blocks, int d,
                                                       float* dg) {
-  const int col = blockIdx.x * 256 + threadIdx.x;
-  if (col >= d) return;
+  __shared__ float acc[4][64];
+  const int c = threadIdx.x & 63, r = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + c;
   float s = 0.f;
-  for (int64_t b = 0; b < n_blocks; ++b) s += part[b * d + col];
-  dg[col] = s;
+  if (col < d)
+    for (int64_t b = r; b < n_blocks; b += 4) s += part[b * d + col];
+  acc[r][c] = s;
+  __syncthreads();
+  if (r == 0 && col < d) dg[col] = ((acc[0][c] + acc[1][c]) + acc[2][c]) + acc[3][c];
 }
 
 // ----------------------------------------------------------------- SwiGLU
@@ -360,8 +392,8 @@ hipError_t rms_fwd_t(const RmsFwdArgs& a, hipStream_t s) {
   if (max_rows == 0) return hipSuccess;
 #define LD_RF(N) \
   case N: hipLaunchKernelGGL((ld_rmsnorm_fwd_k<T, N>), grid, dim3(256), 0, s, a); break;
-  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : nch <= 8 ? 8 : 16) {
-    LD_RF(1) LD_RF(2) LD_RF(4) LD_RF(8) LD_RF(16)
+  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : 8) {
+    LD_RF(1) LD_RF(2) LD_RF(4) LD_RF(8)
   }
 #undef LD_RF
   return hipGetLastError();
@@ -374,13 +406,13 @@ hipError_t rms_bwd_t(const RmsBwdArgs& a, float* dg, hipStream_t s) {
   const size_t lds = static_cast<size_t>(a.d) * sizeof(float);
 #define LD_RB(N) \
   case N: hipLaunchKernelGGL((ld_rmsnorm_bwd_k<T, N>), dim3(nblk), dim3(256), lds, s, a); break;
-  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : nch <= 8 ? 8 : 16) {
-    LD_RB(1) LD_RB(2) LD_RB(4) LD_RB(8) LD_RB(16)
+  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : 8) {
+    LD_RB(1) LD_RB(2) LD_RB(4) LD_RB(8)
   }
 #undef LD_RB
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(ld_dg_reduce_k, dim3((a.d + 255) / 256), dim3(256), 0, s, a.dg_part, nblk,
+  hipLaunchKernelGGL(ld_dg_reduce_k, dim3((a.d + 63) / 64), dim3(256), 0, s, a.dg_part, nblk,
                      a.d, dg);
   return hipGetLastError();
 }
