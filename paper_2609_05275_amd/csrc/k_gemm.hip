@@ -287,114 +287,176 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 
 // ===================================================================== big
 // 256x256x64 workgroup tile, four waves in a 2x2 grid each owning 128x128
-// (4x4 MFMA blocks, 256 fp32 accumulators per lane).  LDS tiles are [row][64]
-// without padding; 16-byte chunks are XOR-swizzled by the row so that the
-// fragment reads (8 consecutive rows, one chunk) and the transposing writes
-// (rows 8 apart) spread over the banks.  The MFMA is issued as B x A so each
-// lane ends with 4 consecutive output columns of one row (vector stores).
-// Tiles are ordered XCD-aware: consecutive workgroup ids go to different XCDs,
-// so ids are remapped to give each XCD a contiguous range of tiles, walked in
-// groups of 8 tile-rows for L2 reuse.  Split-K (grid.y) writes fp32 partials
-// that a second kernel sums in split order.
+// (4x4 MFMA blocks, 256 fp32 accumulators per lane).
+//
+// Operand tiles go from global memory straight into LDS: buffer loads with an
+// LDS destination, so no register staging and no LDS write instructions.  Two
+// stages, each a separate LDS object, so the compiler can tell that fragment
+// reads of one stage need not wait for the loads in flight into the other.
+// Such a load writes the 16 bytes of lane i at LDS offset 16*i from a
+// wave-uniform base, so the LDS layout is set by which global chunk each lane
+// fetches:
+//   k-contiguous operand: [256 rows][64 k], the 16-byte chunks of a row
+//     XOR-swizzled by the row; a fragment is one 16-byte read per lane.
+//   mn-contiguous operand: [64 k][256 mn] as in memory, chunks XOR-swizzled
+//     by k; a fragment is two transposing reads (ds_read_b64_tr_b16: in each
+//     group of 16 lanes, lane j receives element j%4 of the four-element rows
+//     read by lanes j/4, j/4+4, j/4+8 and j/4+12, so 16 lanes reading rows
+//     k..k+3 at mn offsets 0, 4, 8, 12 give lane j the values k..k+3 at mn j).
+// Rows past the operand's end, and k chunks past K, are fetched from an
+// offset outside the buffer descriptor's range and land in LDS as zeros.
+//
+// Per k tile: the fragments of k-substeps 1-3 are read while the MFMAs of the
+// previous substep run; before substep 3 every wave waits for its loads of the
+// next tile and meets the others at the one barrier of the tile; after it the
+// loads of the tile after next go into the stage just released, and the first
+// fragments of the next tile are read while the MFMAs of substep 3 run.
+//
+// The MFMA is issued as B x A so each lane ends with 4 consecutive output
+// columns of one row.  Tiles are ordered XCD-aware: consecutive workgroup ids
+// go to different XCDs, so ids are remapped to give each XCD a contiguous
+// range of tiles, walked in groups of 8 tile-rows for L2 reuse.  Split-K
+// (grid.y) writes fp32 partials that a second kernel sums in split order.
 
 constexpr int GB = 256, GK = 64;
-constexpr int kBigTile = GB * GK;                          // elements per operand tile
-constexpr int kStagePitch = 132;  // floats per staged epilogue row (128 + 4 pad)
-// A,B x double buffer for the main loop; four 64 x kStagePitch float blocks
-// for the epilogue (the larger of the two).
-constexpr size_t kBigLds = std::max<size_t>(2ull * 2 * kBigTile * sizeof(bf16),
-                                            4ull * 64 * kStagePitch * sizeof(float));
+constexpr int kBigTile = GB * GK;  // elements per operand tile
+constexpr int kStagePitch = 132;   // floats per staged epilogue row (128 + 4 pad)
+constexpr uint32_t kOob = 0x80000000u;  // buffer offset past every descriptor's range
+// Operand spans addressed by one descriptor stay below kOob bytes.
+constexpr int64_t kBigMaxSpan = 0x7FFFFFFFll;
 
+typedef short v4s __attribute__((ext_vector_type(4)));
+#define LD_LDS(T, p) ((__attribute__((address_space(3))) T*)(p))
+
+// k-contiguous tile: element (row, k) of a [256][64] tile.  The chunk
+// swizzle depends on row bits 1-3 only, so 16 lanes reading one chunk of 16
+// consecutive rows hit 16 different 16-byte bank groups, and moving by a
+// multiple of 32 rows is a plain offset.
+__device__ __forceinline__ int kc_swz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int swz_off(int row, int k) {
-  const int chunk = (k >> 3) ^ ((row & 7) ^ ((row >> 3) & 7));
-  return row * GK + (chunk << 3) + (k & 7);
+  return row * GK + ((((k >> 3) ^ kc_swz(row))) << 3) + (k & 7);
 }
 
-struct BigRegs {
-  uint4 v[8];
+// mn-contiguous tile: element (k, m) of a [64][256] tile.  The swizzle puts
+// the 4 k rows a 16-lane transposing read touches (32 bytes each) on 4
+// different 64-byte bank groups, and rows k and k+8 on different halves; it
+// depends on k bits 0, 1 and 3 only, so k steps of 4 and 16 are plain offsets.
+__device__ __forceinline__ int mc_swz(int k) { return ((k & 3) << 2) | (((k >> 3) & 1) << 1); }
+__device__ __forceinline__ int mc_off(int k, int m) {
+  return k * GB + ((((m >> 3) ^ mc_swz(k)) << 3) | (m & 7));
+}
+
+// Buffer descriptor covering `bytes` from `base` (raw, no stride): loads
+// past it return 0.
+typedef int v4i __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4i make_rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0 ? 0 : (bytes > kBigMaxSpan ? kBigMaxSpan : bytes);
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return v4i{static_cast<int>(static_cast<uint32_t>(a)), static_cast<int>((a >> 32) & 0xFFFF),
+             static_cast<int>(n), 0x00020000};
+}
+
+// 16 bytes per lane from buffer offset `voff` into LDS at `lds` + 16 * lane
+// (`lds` wave-uniform).  Written as inline assembly on purpose: the compiler
+// then does not count these loads against later LDS reads (it cannot tell the
+// stages apart for the transposing reads and would wait for every load in
+// flight), so the kernel waits for them itself before each barrier.  No other
+// code in these kernels reads m0.
+__device__ __forceinline__ void dma16(v4i rs, const bf16* lds, uint32_t voff) {
+  const uint32_t m = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LD_LDS(const void, lds)));
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m), "v"(voff),
+               "s"(rs)
+               : "memory");
+}
+
+// Waits until this wave's LDS loads have landed, then meets the workgroup.
+__device__ __forceinline__ void dma_barrier() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  __syncthreads();
+}
+
+// Per-lane constants of one operand's tile loads and fragment reads.
+template <bool KC>
+struct OpLanes {
+  uint32_t ld_off[2];  // byte offset of the lane's first 16-byte chunk (mn: per k-row parity)
+  int kchunk;          // k-contiguous: k offset of the lane's chunk in the tile
+  int frag[4];         // element offsets of fragment reads: per k-substep (KC) or block (MC)
 };
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-// Buffer resource covering `bytes` from `base`: loads past it return 0.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
-  const int64_t n = bytes < 0 ? 0 : (bytes > 0xFFFFFFFFll ? 0xFFFFFFFFll : bytes);
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
-                                           static_cast<int>(static_cast<uint32_t>(n)), 0x00020000);
-}
-
-__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
-  const v4i t = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
-  return make_uint4(t[0], t[1], t[2], t[3]);
-}
-
-// Transposing loader groups: 32 row chunks of 8 x 16 k groups of 4, two per
-// thread.  In a wave, lanes 0-15 and 32-47 cover 32 consecutive row chunks of
-// one k row (512 contiguous bytes) and lanes 16-31, 48-63 the next k row, so
-// the transposed 8-byte LDS writes of a half-wave land on both halves of the
-// swizzled 16-byte chunks and use every bank.
-__device__ __forceinline__ void mn_group(int q, int tid, int& rch, int& kg) {
-  const int l = tid & 63, w = tid >> 6;
-  kg = (q * 4 + w) * 2 + ((l >> 4) & 1);
-  rch = (l & 15) | ((l >> 5) << 4);
-}
-
-// Tile loads through a buffer descriptor that ends at the operand's last valid
-// row: rows (k-contiguous) or k-rows (mn-contiguous) past the end read 0.
-// Columns past the end inside a valid row read real memory; they only reach
-// outputs that are never stored, except a k tail of a k-contiguous operand,
-// which is zeroed per lane.
+// `r`: the first of the wave's 128 fragment rows (0 or 128).
 template <bool KC>
-__device__ __forceinline__ void big_load(BigRegs& t, const bf16* X, int64_t ld, int r0, int R, int k0,
-                                         int K, int tid) {
+__device__ __forceinline__ OpLanes<KC> op_lanes(int64_t ld, int lane, int wave, int r) {
+  OpLanes<KC> o;
   if constexpr (KC) {
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
+    // load instruction p fills rows (4p + wave)*8 .. +7, lane -> row + lane/8,
+    // physical chunk lane%8; the swizzle is the same for every p
+    const int rl = lane >> 3;
+    const int row = wave * 8 + rl;
+    o.kchunk = ((lane & 7) ^ kc_swz(row)) << 3;
+    o.ld_off[0] = o.ld_off[1] = static_cast<uint32_t>((static_cast<int64_t>(row) * ld + o.kchunk) * 2);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) o.frag[ks] = swz_off(r + (lane & 31), ks * 16 + (lane >> 5) * 8);
+  } else {
+    // load instruction p fills k rows 8p + 2*wave + lane/32, physical chunk
+    // lane%32; the swizzle depends on p only through its parity (k bit 3)
+    const int kr = 2 * wave + (lane >> 5);
+#pragma unroll
+    for (int par = 0; par < 2; ++par) {
+      const int m = ((lane & 31) ^ mc_swz(8 * par + kr)) << 3;
+      o.ld_off[par] = static_cast<uint32_t>((static_cast<int64_t>(kr) * ld + m) * 2);
+    }
+    o.kchunk = 0;
+    // transposing reads: lane reads k row kl, 4 elements from mn ml
+    const int kl = (lane >> 5) * 8 + ((lane >> 2) & 3);
+    const int ml = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o.frag[i] = mc_off(kl, r + ml + 32 * i);
+  }
+  return o;
+}
+
+// Loads the tile (rows r0.., k0..) of operand X into `lds`, 16 bytes per lane
+// and 8 instructions per wave.  k-contiguous: one instruction fills 8 rows;
+// mn-contiguous: 2 k rows.  Columns past the end of a valid row read real
+// memory; they only reach outputs that are never stored, except a k tail of a
+// k-contiguous operand, which is fetched out of range (zeros).
+template <bool KC>
+__device__ __forceinline__ void tile_to_lds(bf16* lds, const OpLanes<KC>& o, const bf16* X, int64_t ld,
+                                            int r0, int R, int k0, int K, int wave) {
+  if constexpr (KC) {
+    const v4i rs = make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
+    const bool in_k = k0 + o.kchunk < K;
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
-      const int c = p * 256 + tid;
-      const int row = c >> 3, kk = k0 + (c & 7) * 8;
-      t.v[p] = buf_load16(rs, static_cast<int>((static_cast<int64_t>(row) * ld + kk) * 2));
+      const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 32 * ld + k0) * 2);
+      const uint32_t off = in_k ? o.ld_off[0] + u : kOob;
+      dma16(rs, lds + (p * 4 + wave) * 512, off);
     }
   } else {
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(X + static_cast<int64_t>(k0) * ld, (static_cast<int64_t>(K) - k0) * ld * 2);
+    const v4i rs = make_rsrc(X + static_cast<int64_t>(k0) * ld, (static_cast<int64_t>(K) - k0) * ld * 2);
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      int rch, kg;
-      mn_group(q, tid, rch, kg);
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        t.v[q * 4 + kk] = buf_load16(rs, static_cast<int>((static_cast<int64_t>(kg * 4 + kk) * ld + r0 + rch * 8) * 2));
+    for (int p = 0; p < 8; ++p) {
+      const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 8 * ld + r0) * 2);
+      const uint32_t off = o.ld_off[p & 1] + u;
+      dma16(rs, lds + (p * 4 + wave) * 512, off);
     }
   }
   (void)R;
 }
 
-// k0, K: the tile's first k and the reduction length; a k-contiguous tile
-// that crosses K has its columns past K zeroed here, once the loads landed.
+// Fragment of block i of the wave's 128 rows for k-substep ks: the lane's
+// MFMA row is r + 32 i + lane % 32 (r as given to op_lanes), its 8 k values
+// start at ks*16 + (lane/32)*8.  Only the per-lane offset is a register; the
+// rest is a constant offset of the LDS instruction.
 template <bool KC>
-__device__ __forceinline__ void big_store(const BigRegs& t, bf16* lds, int tid, int k0, int K) {
+__device__ __forceinline__ bf16x8 frag(const bf16* t, const OpLanes<KC>& o, int i, int ks) {
   if constexpr (KC) {
-    const bool ok = k0 + (tid & 7) * 8 < K;  // the same k chunk for every p
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      const int c = p * 256 + tid;
-      const uint4 v = t.v[p];
-      *reinterpret_cast<uint4*>(lds + swz_off(c >> 3, (c & 7) * 8)) =
-          make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
-    }
+    return *reinterpret_cast<const bf16x8*>(t + 32 * i * GK + o.frag[ks]);
   } else {
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      int rch, kg;
-      mn_group(q, tid, rch, kg);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        uint2 o;
-        o.x = half_of(t.v[q * 4 + 0], i) | (half_of(t.v[q * 4 + 1], i) << 16);
-        o.y = half_of(t.v[q * 4 + 2], i) | (half_of(t.v[q * 4 + 3], i) << 16);
-        *reinterpret_cast<uint2*>(lds + swz_off(rch * 8 + i, kg * 4)) = o;
-      }
-    }
+    const bf16* p = t + o.frag[i] + ks * 16 * GB;
+    const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LD_LDS(v4s, p));
+    const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LD_LDS(v4s, p + 4 * GB));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   }
 }
 
@@ -412,9 +474,7 @@ __device__ __forceinline__ void tile_coords(int pid, int n_wg, int tiles_m, int 
 
 template <bool AK, bool BKC>
 __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
-  extern __shared__ __align__(16) bf16 smem[];
-  bf16* As = smem;                 // [2][GB*GK]
-  bf16* Bs = smem + 2 * kBigTile;  // [2][GB*GK]
+  __shared__ __align__(16) bf16 sA0[kBigTile], sA1[kBigTile], sB0[kBigTile], sB1[kBigTile];
   int M, K;
   resolve_counts(g, M, K);
   const int tiles_n = (g.N + GB - 1) / GB;
@@ -423,7 +483,8 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
   tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * GB, n0 = tn * GB;
   if (m0 >= M) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const bf16* A = static_cast<const bf16*>(g.A);
   const bf16* B = static_cast<const bf16*>(g.B);
@@ -443,115 +504,108 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  // Tiles go in pairs, one per stage, with no branch around the MFMAs (a
+  // branch would merge 256 accumulators).  Loads past the split's last k
+  // read zeros, so a pair's phantom second tile adds nothing; a split with
+  // no tiles only runs the prologue.
+  const int kend = min(K, kt1 * GK);
+  const int nkp = (nk + 1) & ~1;  // tiles including the phantom one
+  const OpLanes<AK> oa = op_lanes<AK>(g.lda, lane, wave, wm * 128);
+  const OpLanes<BKC> ob = op_lanes<BKC>(g.ldb, lane, wave, wn * 128);
+  auto load = [&](bf16* sa, bf16* sb, int kt) {
+    tile_to_lds<AK>(sa, oa, A, g.lda, m0, M, (kt0 + kt) * GK, kend, wave);
+    tile_to_lds<BKC>(sb, ob, B, g.ldb, n0, g.N, (kt0 + kt) * GK, kend, wave);
+  };
   if (nk > 0) {
-    // Global data is prefetched one k tile ahead in registers (a second set
-    // for two tiles ahead does not fit next to the 256 accumulators).
-    BigRegs ra0, rb0;
-    big_load<AK>(ra0, A, g.lda, m0, M, kt0 * GK, K, tid);
-    big_load<BKC>(rb0, B, g.ldb, n0, g.N, kt0 * GK, K, tid);
-    big_store<AK>(ra0, As, tid, kt0 * GK, K);
-    big_store<BKC>(rb0, Bs, tid, kt0 * GK, K);
-    __syncthreads();
-    const int lrow = lane & 31, lk = (lane >> 5) * 8;
-    const int arow = wm * 128 + lrow, brow = wn * 128 + lrow;
-    bf16x8 af[2][4], bfr[2][4];
+    load(sA0, sB0, 0);
+    load(sA1, sB1, 1);
+  }
+  dma_barrier();  // waits for both tiles: once per launch
+  bf16x8 af[2][4], bfr[2][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[0][i] = *reinterpret_cast<const bf16x8*>(As + swz_off(arow + i * 32, lk));
-      bfr[0][i] = *reinterpret_cast<const bf16x8*>(Bs + swz_off(brow + i * 32, lk));
-    }
-    // One k tile per step, a single basic block: the loads of tile kt+1 go
-    // out first (unconditionally: past the end they read zeros or unused
-    // data), steps 0-2 read the next step's fragments while their 16 MFMAs
-    // run (front-loaded, one LDS read per MFMA), step 3 writes tile kt+1 into
-    // the other LDS buffer between its MFMAs, then one barrier and the first
-    // fragments of tile kt+1.
-    auto tile_step = [&](BigRegs& la, BigRegs& lb, const BigRegs& sa, const BigRegs& sb, int kt) {
-      const int buf = kt & 1;
-      big_load<AK>(la, A, g.lda, m0, M, (kt0 + kt + 1) * GK, K, tid);
-      big_load<BKC>(lb, B, g.ldb, n0, g.N, (kt0 + kt + 1) * GK, K, tid);
-      __builtin_amdgcn_sched_barrier(0);
-      const bf16* as = As + buf * kBigTile;
-      const bf16* bs = Bs + buf * kBigTile;
+  for (int i = 0; i < 4; ++i) {
+    af[0][i] = frag<AK>(sA0, oa, i, 0);
+    bfr[0][i] = frag<BKC>(sB0, ob, i, 0);
+  }
+  constexpr int kReads = (AK ? 4 : 8) + (BKC ? 4 : 8);  // LDS read instructions per substep
+  // tile kt from stage (sa, sb); the next tile is in (na, nb)
+  auto tile = [&](bf16* sa, bf16* sb, bf16* na, bf16* nb, int kt) {
 #pragma unroll
-      for (int ks = 0; ks < 3; ++ks) {
-        const int cur = ks & 1;
+    for (int ks = 0; ks < 3; ++ks) {
+      const int cur = ks & 1;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          af[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(as + swz_off(arow + i * 32, (ks + 1) * 16 + lk));
-          bfr[cur ^ 1][i] = *reinterpret_cast<const bf16x8*>(bs + swz_off(brow + i * 32, (ks + 1) * 16 + lk));
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-        __builtin_amdgcn_sched_barrier(0);
+      for (int i = 0; i < 4; ++i) {
+        af[cur ^ 1][i] = frag<AK>(sa, oa, i, ks + 1);
+        bfr[cur ^ 1][i] = frag<BKC>(sb, ob, i, ks + 1);
       }
-      const int knext = (kt0 + kt + 1) * GK;
-      big_store<AK>(sa, As + (buf ^ 1) * kBigTile, tid, knext, K);
-      big_store<BKC>(sb, Bs + (buf ^ 1) * kBigTile, tid, knext, K);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[1][j], af[1][i], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU (transposes)
-        __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);  // LDS writes
+      for (int r = 0; r < kReads; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
       }
+      __builtin_amdgcn_sched_group_barrier(0x008, 16 - kReads, 0);
       __builtin_amdgcn_sched_barrier(0);
-      __syncthreads();
-      const bf16* an = As + (buf ^ 1) * kBigTile;
-      const bf16* bn = Bs + (buf ^ 1) * kBigTile;
+    }
+    // the next tile has landed everywhere; this stage is no longer read
+    dma_barrier();
+    if (kt + 2 < nkp) load(sa, sb, kt + 2);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        af[0][i] = *reinterpret_cast<const bf16x8*>(an + swz_off(arow + i * 32, lk));
-        bfr[0][i] = *reinterpret_cast<const bf16x8*>(bn + swz_off(brow + i * 32, lk));
-      }
-    };
-    for (int kt = 0; kt < nk; ++kt) tile_step(ra0, rb0, ra0, rb0, kt);
+    for (int i = 0; i < 4; ++i) {
+      af[0][i] = frag<AK>(na, oa, i, 0);
+      bfr[0][i] = frag<BKC>(nb, ob, i, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[1][j], af[1][i], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int r = 0; r < kReads; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 16 - kReads, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int kt = 0; kt < nk; kt += 2) {
+    tile(sA0, sB0, sA1, sB1, kt);
+    tile(sA1, sB1, sA0, sB0, kt + 1);
   }
 
   // Epilogue staged through LDS (the operand tiles are dead by now).  A lane
   // holds, per 32x32 block, one output row and 4 consecutive columns; stored
   // directly that scatters every store over 32 rows.  Instead each wave writes
-  // half of its 128x128 float32 results (alpha applied) into a private
-  // [64][kStagePitch] block and reads it back row-major: a half-wave then
-  // covers 128 contiguous columns of one row, so the residual loads and the
-  // output stores (one rounding, after the residual) are fully coalesced.
+  // one block row of its results (32 x 128 float32, alpha applied) into a
+  // private [32][kStagePitch] block and reads it back row-major: a half-wave
+  // then covers 128 contiguous columns of one row, so the residual loads and
+  // the output stores (one rounding, after the residual) are fully coalesced.
   const float alpha = g.alpha * (g.alpha_dev ? *g.alpha_dev : 1.f);
   const int half = lane >> 5, lm = lane & 31;
   float* part = g.part ? g.part + static_cast<int64_t>(sp) * g.M * g.N : nullptr;
-  float* stage = reinterpret_cast<float*>(smem) + wave * (64 * kStagePitch);
+  float* stage = reinterpret_cast<float*>(wave == 0 ? sA0 : wave == 1 ? sA1 : wave == 2 ? sB0 : sB1);
   __syncthreads();
 #pragma unroll
-  for (int hi = 0; hi < 2; ++hi) {
+  for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int ii = 0; ii < 2; ++ii)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const floatx16& a = acc[2 * hi + ii][j];
-          *reinterpret_cast<float4*>(stage + (ii * 32 + lm) * kStagePitch + j * 32 + 8 * q + 4 * half) =
-              make_float4(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
-        }
+      for (int q = 0; q < 4; ++q) {
+        const floatx16& a = acc[i][j];
+        *reinterpret_cast<float4*>(stage + lm * kStagePitch + j * 32 + 8 * q + 4 * half) =
+            make_float4(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
+      }
     __syncthreads();
     const int c = (lane & 31) * 4;
     const int n = n0 + wn * 128 + c;
 #pragma unroll 4
-    for (int it = 0; it < 32; ++it) {
+    for (int it = 0; it < 16; ++it) {
       const int rl = 2 * it + half;
-      const int m = m0 + wm * 128 + hi * 64 + rl;
+      const int m = m0 + wm * 128 + i * 32 + rl;
       if (m >= M || n >= g.N) continue;
       float4 v = *reinterpret_cast<const float4*>(stage + rl * kStagePitch + c);
       if (part) {
@@ -609,10 +663,7 @@ void set_attrs() {
   if (g_attr_done) return;
   const void* small[] = {reinterpret_cast<const void*>(ld_gemm_bf16_nt), reinterpret_cast<const void*>(ld_gemm_bf16_nn),
                          reinterpret_cast<const void*>(ld_gemm_bf16_tn), reinterpret_cast<const void*>(ld_gemm_bf16_tt)};
-  const void* big[] = {reinterpret_cast<const void*>(ld_gemm_bf16_nt_256), reinterpret_cast<const void*>(ld_gemm_bf16_nn_256),
-                       reinterpret_cast<const void*>(ld_gemm_bf16_tn_256), reinterpret_cast<const void*>(ld_gemm_bf16_tt_256)};
   for (const void* f : small) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
-  for (const void* f : big) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
   g_attr_done = true;
 }
 
@@ -627,10 +678,12 @@ GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, i
     return p;
   }
   const int64_t big_tiles = ((max_m + GB - 1) / GB) * ((g.N + GB - 1) / GB);
-  // the big tile needs N % 4 == 0 for its vector epilogue
   // the big tile's epilogue stores 4 consecutive columns at once
+  // each operand is addressed through one buffer descriptor: spans < 2 GiB
+  const int64_t a_span = 2 * g.lda * (a_kcontig ? max_m : max_k);
+  const int64_t b_span = 2 * g.ldb * (b_kcontig ? static_cast<int64_t>(g.N) : max_k);
   p.big = (g.N % 4 == 0) && (g.ldc % 4 == 0) && (!g.R || g.ldr % 4 == 0) && max_m >= 512 &&
-          g.N >= 512 && big_tiles >= 32;
+          g.N >= 512 && big_tiles >= 32 && a_span < kBigMaxSpan && b_span < kBigMaxSpan;
   if (p.big) {
     // split-K only for float32 outputs without a residual (weight gradients)
     if (allow_split && g.c_f32 && !g.R && !g.out_map.idx && g.ldc == g.N && max_k >= 8 * GK) {
@@ -685,13 +738,13 @@ hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmP
     }
     const dim3 grid(static_cast<unsigned>(tiles), p.splits), block(256);
     if (a_kcontig && b_kcontig)
-      hipLaunchKernelGGL(ld_gemm_bf16_nt_256, grid, block, kBigLds, s, g);
+      hipLaunchKernelGGL(ld_gemm_bf16_nt_256, grid, block, 0, s, g);
     else if (a_kcontig)
-      hipLaunchKernelGGL(ld_gemm_bf16_nn_256, grid, block, kBigLds, s, g);
+      hipLaunchKernelGGL(ld_gemm_bf16_nn_256, grid, block, 0, s, g);
     else if (b_kcontig)
-      hipLaunchKernelGGL(ld_gemm_bf16_tt_256, grid, block, kBigLds, s, g);
+      hipLaunchKernelGGL(ld_gemm_bf16_tt_256, grid, block, 0, s, g);
     else
-      hipLaunchKernelGGL(ld_gemm_bf16_tn_256, grid, block, kBigLds, s, g);
+      hipLaunchKernelGGL(ld_gemm_bf16_tn_256, grid, block, 0, s, g);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t mn = static_cast<int64_t>(g.M) * g.N;
