@@ -286,31 +286,33 @@ __global__ __launch_bounds__(256) void ld_gemm_f32_k(GemmArgs g) {
 constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 
 // ===================================================================== big
-// 256x256x64 workgroup tile, four waves in a 2x2 grid each owning 128x128
-// (4x4 MFMA blocks, 256 fp32 accumulators per lane).
+// 256x256 workgroup tile, four waves in a 2x2 grid each owning 128x128 (4x4
+// MFMA blocks, 256 fp32 accumulators per lane), k walked in tiles of 32.
 //
 // Operand tiles go from global memory straight into LDS: buffer loads with an
-// LDS destination, so no register staging and no LDS write instructions.  Two
-// stages, each a separate LDS object, so the compiler can tell that fragment
-// reads of one stage need not wait for the loads in flight into the other.
-// Such a load writes the 16 bytes of lane i at LDS offset 16*i from a
-// wave-uniform base, so the LDS layout is set by which global chunk each lane
-// fetches:
-//   k-contiguous operand: [256 rows][64 k], the 16-byte chunks of a row
+// LDS destination, so no register staging and no LDS write instructions, in a
+// ring of four stages (32 KB each: the A and B tiles), so the loads of a tile
+// have three tile-times to land.  Such a load writes the 16 bytes of lane i
+// at LDS offset 16*i from a wave-uniform base, so the LDS layout is set by
+// which global chunk each lane fetches:
+//   k-contiguous operand: [256 rows][32 k], the 16-byte chunks of a row
 //     XOR-swizzled by the row; a fragment is one 16-byte read per lane.
-//   mn-contiguous operand: [64 k][256 mn] as in memory, chunks XOR-swizzled
+//   mn-contiguous operand: [32 k][256 mn] as in memory, chunks XOR-swizzled
 //     by k; a fragment is two transposing reads (ds_read_b64_tr_b16: in each
 //     group of 16 lanes, lane j receives element j%4 of the four-element rows
 //     read by lanes j/4, j/4+4, j/4+8 and j/4+12, so 16 lanes reading rows
 //     k..k+3 at mn offsets 0, 4, 8, 12 give lane j the values k..k+3 at mn j).
-// Rows past the operand's end, and k chunks past K, are fetched from an
-// offset outside the buffer descriptor's range and land in LDS as zeros.
+// Rows past the operand's end, and k chunks past the split's end, are
+// fetched from an offset outside the buffer descriptor's range and land in
+// LDS as zeros.  The loads are issued as inline assembly, so the compiler
+// does not track them; the kernel waits for them itself (s_waitcnt vmcnt)
+// before the barriers.
 //
-// Per k tile: the fragments of k-substeps 1-3 are read while the MFMAs of the
-// previous substep run; before substep 3 every wave waits for its loads of the
-// next tile and meets the others at the one barrier of the tile; after it the
-// loads of the tile after next go into the stage just released, and the first
-// fragments of the next tile are read while the MFMAs of substep 3 run.
+// Per k tile (two k-substeps of 16): the second substep's fragments are read
+// while the first substep's MFMAs run; then each wave waits until the next
+// tile has landed and meets the others at the tile's one barrier; the second
+// substep's MFMAs then run next to the loads of the tile four ahead (into the
+// stage just released) and the reads of the next tile's first fragments.
 //
 // The MFMA is issued as B x A so each lane ends with 4 consecutive output
 // columns of one row.  Tiles are ordered XCD-aware: consecutive workgroup ids
@@ -318,26 +320,30 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 // range of tiles, walked in groups of 8 tile-rows for L2 reuse.  Split-K
 // (grid.y) writes fp32 partials that a second kernel sums in split order.
 
-constexpr int GB = 256, GK = 64;
-constexpr int kBigTile = GB * GK;  // elements per operand tile
-constexpr int kStagePitch = 132;   // floats per staged epilogue row (128 + 4 pad)
+constexpr int GB = 256, GK = 32, NSTAGE = 4;
+constexpr int kBigTile = GB * GK;      // elements per operand tile
+constexpr int kStage = 2 * kBigTile;   // A and B tiles of one stage
+constexpr int kLoads = 4;              // load instructions per wave per operand tile
+constexpr int kStagePitch = 132;       // floats per staged epilogue row (128 + 4 pad)
 constexpr uint32_t kOob = 0x80000000u;  // buffer offset past every descriptor's range
 // Operand spans addressed by one descriptor stay below kOob bytes.
 constexpr int64_t kBigMaxSpan = 0x7FFFFFFFll;
+static_assert(NSTAGE * kStage * 2 >= 4 * 32 * kStagePitch * 4, "epilogue staging fits the stages");
 
 typedef short v4s __attribute__((ext_vector_type(4)));
+typedef int v4i __attribute__((ext_vector_type(4)));
 #define LD_LDS(T, p) ((__attribute__((address_space(3))) T*)(p))
 
-// k-contiguous tile: element (row, k) of a [256][64] tile.  The chunk
-// swizzle depends on row bits 1-3 only, so 16 lanes reading one chunk of 16
-// consecutive rows hit 16 different 16-byte bank groups, and moving by a
-// multiple of 32 rows is a plain offset.
-__device__ __forceinline__ int kc_swz(int row) { return (row >> 1) & 7; }
+// k-contiguous tile: element (row, k) of a [256][32] tile.  The chunk swizzle
+// depends on row bits 2-3 only: 16 lanes reading one chunk of 16 consecutive
+// rows hit 16 different 16-byte bank groups, and moving by a multiple of 32
+// rows is a plain offset.
+__device__ __forceinline__ int kc_swz(int row) { return (row >> 2) & 3; }
 __device__ __forceinline__ int swz_off(int row, int k) {
-  return row * GK + ((((k >> 3) ^ kc_swz(row))) << 3) + (k & 7);
+  return row * GK + (((k >> 3) ^ kc_swz(row)) << 3) + (k & 7);
 }
 
-// mn-contiguous tile: element (k, m) of a [64][256] tile.  The swizzle puts
+// mn-contiguous tile: element (k, m) of a [32][256] tile.  The swizzle puts
 // the 4 k rows a 16-lane transposing read touches (32 bytes each) on 4
 // different 64-byte bank groups, and rows k and k+8 on different halves; it
 // depends on k bits 0, 1 and 3 only, so k steps of 4 and 16 are plain offsets.
@@ -348,7 +354,6 @@ __device__ __forceinline__ int mc_off(int k, int m) {
 
 // Buffer descriptor covering `bytes` from `base` (raw, no stride): loads
 // past it return 0.
-typedef int v4i __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ v4i make_rsrc(const void* base, int64_t bytes) {
   const int64_t n = bytes < 0 ? 0 : (bytes > kBigMaxSpan ? kBigMaxSpan : bytes);
   const uint64_t a = reinterpret_cast<uint64_t>(base);
@@ -357,22 +362,19 @@ __device__ __forceinline__ v4i make_rsrc(const void* base, int64_t bytes) {
 }
 
 // 16 bytes per lane from buffer offset `voff` into LDS at `lds` + 16 * lane
-// (`lds` wave-uniform).  Written as inline assembly on purpose: the compiler
-// then does not count these loads against later LDS reads (it cannot tell the
-// stages apart for the transposing reads and would wait for every load in
-// flight), so the kernel waits for them itself before each barrier.  No other
-// code in these kernels reads m0.
+// (`lds` wave-uniform).  No other code in these kernels reads m0.
 __device__ __forceinline__ void dma16(v4i rs, const bf16* lds, uint32_t voff) {
   const uint32_t m = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LD_LDS(const void, lds)));
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m), "v"(voff),
-               "s"(rs)
-               : "memory");
+               "s"(rs));
 }
 
-// Waits until this wave's LDS loads have landed, then meets the workgroup.
+// Waits until at most N of this wave's LDS loads are in flight and its LDS
+// reads are done, then meets the workgroup.  A compiler barrier for memory.
+template <int N>
 __device__ __forceinline__ void dma_barrier() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-  __syncthreads();
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
 // Per-lane constants of one operand's tile loads and fragment reads.
@@ -388,14 +390,14 @@ template <bool KC>
 __device__ __forceinline__ OpLanes<KC> op_lanes(int64_t ld, int lane, int wave, int r) {
   OpLanes<KC> o;
   if constexpr (KC) {
-    // load instruction p fills rows (4p + wave)*8 .. +7, lane -> row + lane/8,
-    // physical chunk lane%8; the swizzle is the same for every p
-    const int rl = lane >> 3;
-    const int row = wave * 8 + rl;
-    o.kchunk = ((lane & 7) ^ kc_swz(row)) << 3;
+    // load instruction p fills rows (4p + wave)*16 .. +15, lane -> row +
+    // lane/4, physical chunk lane%4; the swizzle is the same for every p
+    const int row = wave * 16 + (lane >> 2);
+    o.kchunk = ((lane & 3) ^ kc_swz(row)) << 3;
     o.ld_off[0] = o.ld_off[1] = static_cast<uint32_t>((static_cast<int64_t>(row) * ld + o.kchunk) * 2);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) o.frag[ks] = swz_off(r + (lane & 31), ks * 16 + (lane >> 5) * 8);
+    for (int ks = 0; ks < 2; ++ks) o.frag[ks] = swz_off(r + (lane & 31), ks * 16 + (lane >> 5) * 8);
+    o.frag[2] = o.frag[3] = 0;
   } else {
     // load instruction p fills k rows 8p + 2*wave + lane/32, physical chunk
     // lane%32; the swizzle depends on p only through its parity (k bit 3)
@@ -415,31 +417,24 @@ __device__ __forceinline__ OpLanes<KC> op_lanes(int64_t ld, int lane, int wave, 
   return o;
 }
 
-// Loads the tile (rows r0.., k0..) of operand X into `lds`, 16 bytes per lane
-// and 8 instructions per wave.  k-contiguous: one instruction fills 8 rows;
-// mn-contiguous: 2 k rows.  Columns past the end of a valid row read real
-// memory; they only reach outputs that are never stored, except a k tail of a
-// k-contiguous operand, which is fetched out of range (zeros).
+// Load instruction p (0-3) of the tile (rows r0.., k0..) of operand X into
+// `lds`: 16 bytes per lane; all 4 fill the tile.  k-contiguous: instruction p
+// fills 16 rows per wave; mn-contiguous: 2 k rows.  Columns past the end of a
+// valid row read real memory; they only reach outputs that are never stored,
+// except a k tail of a k-contiguous operand, which is fetched out of range
+// (zeros), as is everything of a tile that starts at or past K.
 template <bool KC>
-__device__ __forceinline__ void tile_to_lds(bf16* lds, const OpLanes<KC>& o, const bf16* X, int64_t ld,
-                                            int r0, int R, int k0, int K, int wave) {
+__device__ __forceinline__ void tile_part(bf16* lds, const OpLanes<KC>& o, const bf16* X, int64_t ld,
+                                          int r0, int R, int k0, int K, int wave, int p) {
   if constexpr (KC) {
     const v4i rs = make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
-    const bool in_k = k0 + o.kchunk < K;
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 32 * ld + k0) * 2);
-      const uint32_t off = in_k ? o.ld_off[0] + u : kOob;
-      dma16(rs, lds + (p * 4 + wave) * 512, off);
-    }
+    const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 64 * ld + k0) * 2);
+    const uint32_t off = k0 + o.kchunk < K ? o.ld_off[0] + u : kOob;
+    dma16(rs, lds + (p * 4 + wave) * 512, off);
   } else {
     const v4i rs = make_rsrc(X + static_cast<int64_t>(k0) * ld, (static_cast<int64_t>(K) - k0) * ld * 2);
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 8 * ld + r0) * 2);
-      const uint32_t off = o.ld_off[p & 1] + u;
-      dma16(rs, lds + (p * 4 + wave) * 512, off);
-    }
+    const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 8 * ld + r0) * 2);
+    dma16(rs, lds + (p * 4 + wave) * 512, o.ld_off[p & 1] + u);
   }
   (void)R;
 }
@@ -474,7 +469,7 @@ __device__ __forceinline__ void tile_coords(int pid, int n_wg, int tiles_m, int 
 
 template <bool AK, bool BKC>
 __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
-  __shared__ __align__(16) bf16 sA0[kBigTile], sA1[kBigTile], sB0[kBigTile], sB1[kBigTile];
+  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
   int M, K;
   resolve_counts(g, M, K);
   const int tiles_n = (g.N + GB - 1) / GB;
@@ -495,6 +490,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
   const int kt0 = static_cast<int>((static_cast<int64_t>(nkt_all) * sp) / splits);
   const int kt1 = static_cast<int>((static_cast<int64_t>(nkt_all) * (sp + 1)) / splits);
   const int nk = kt1 - kt0;
+  const int kend = min(K, kt1 * GK);  // loads at or past it read zeros
 
   floatx16 acc[4][4];
 #pragma unroll
@@ -504,91 +500,84 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // Tiles go in pairs, one per stage, with no branch around the MFMAs (a
-  // branch would merge 256 accumulators).  Loads past the split's last k
-  // read zeros, so a pair's phantom second tile adds nothing; a split with
-  // no tiles only runs the prologue.
-  const int kend = min(K, kt1 * GK);
-  const int nkp = (nk + 1) & ~1;  // tiles including the phantom one
   const OpLanes<AK> oa = op_lanes<AK>(g.lda, lane, wave, wm * 128);
   const OpLanes<BKC> ob = op_lanes<BKC>(g.ldb, lane, wave, wn * 128);
-  auto load = [&](bf16* sa, bf16* sb, int kt) {
-    tile_to_lds<AK>(sa, oa, A, g.lda, m0, M, (kt0 + kt) * GK, kend, wave);
-    tile_to_lds<BKC>(sb, ob, B, g.ldb, n0, g.N, (kt0 + kt) * GK, kend, wave);
+  // load instruction q (0-7) of tile kt into stage st: A's 4, then B's 4
+  auto load_part = [&](int st, int kt, int q) {
+    bf16* sa = ring + st * kStage;
+    const int k0 = (kt0 + kt) * GK;
+    if (q < kLoads)
+      tile_part<AK>(sa, oa, A, g.lda, m0, M, k0, kend, wave, q);
+    else
+      tile_part<BKC>(sa + kBigTile, ob, B, g.ldb, n0, g.N, k0, kend, wave, q - kLoads);
   };
-  if (nk > 0) {
-    load(sA0, sB0, 0);
-    load(sA1, sB1, 1);
-  }
-  dma_barrier();  // waits for both tiles: once per launch
+  // The ring starts full: tiles 0-3 (zeros past the split's end).
+#pragma unroll
+  for (int st = 0; st < NSTAGE; ++st)
+#pragma unroll
+    for (int q = 0; q < 2 * kLoads; ++q) load_part(st, st, q);
+  dma_barrier<(NSTAGE - 1) * 2 * kLoads>();  // tile 0 has landed
   bf16x8 af[2][4], bfr[2][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    af[0][i] = frag<AK>(sA0, oa, i, 0);
-    bfr[0][i] = frag<BKC>(sB0, ob, i, 0);
+    af[0][i] = frag<AK>(ring, oa, i, 0);
+    bfr[0][i] = frag<BKC>(ring + kBigTile, ob, i, 0);
   }
   constexpr int kReads = (AK ? 4 : 8) + (BKC ? 4 : 8);  // LDS read instructions per substep
-  // tile kt from stage (sa, sb); the next tile is in (na, nb)
-  auto tile = [&](bf16* sa, bf16* sb, bf16* na, bf16* nb, int kt) {
-#pragma unroll
-    for (int ks = 0; ks < 3; ++ks) {
-      const int cur = ks & 1;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        af[cur ^ 1][i] = frag<AK>(sa, oa, i, ks + 1);
-        bfr[cur ^ 1][i] = frag<BKC>(sb, ob, i, ks + 1);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
-#pragma unroll
-      for (int r = 0; r < kReads; ++r) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 16 - kReads, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // the next tile has landed everywhere; this stage is no longer read
-    dma_barrier();
-    if (kt + 2 < nkp) load(sa, sb, kt + 2);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt & (NSTAGE - 1), nst = (kt + 1) & (NSTAGE - 1);
+    const bf16* sa = ring + st * kStage;
+    const bf16* na = ring + nst * kStage;
+    // substep 0: MFMAs on the fragments in hand, reads of substep 1's
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      af[0][i] = frag<AK>(na, oa, i, 0);
-      bfr[0][i] = frag<BKC>(nb, ob, i, 0);
+      af[1][i] = frag<AK>(sa, oa, i, 1);
+      bfr[1][i] = frag<BKC>(sa + kBigTile, ob, i, 1);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[1][j], af[1][i], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[0][j], af[0][i], acc[i][j], 0, 0, 0);
+    // MFMA first: its operands were read during the previous tile, and a
+    // read issued before it would be included in its wait
 #pragma unroll
     for (int r = 0; r < kReads; ++r) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 16 - kReads, 0);
     __builtin_amdgcn_sched_barrier(0);
-  };
-  for (int kt = 0; kt < nk; kt += 2) {
-    tile(sA0, sB0, sA1, sB1, kt);
-    tile(sA1, sB1, sA0, sB0, kt + 1);
+    // Tile kt+1 has landed (tiles kt+2, kt+3 may still be in flight) and
+    // this stage is no longer read.  Substep 1 issues next to its 16 MFMAs
+    // the 8 loads of tile kt+4 into this stage and the 8 fragments of the
+    // next tile's substep 0.
+    dma_barrier<(NSTAGE - 2) * 2 * kLoads>();
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int i = q >> 2, j = q & 3;
+      if (q < 4)
+        af[0][q] = frag<AK>(na, oa, q, 0);
+      else if (q < 8)
+        bfr[0][q - 4] = frag<BKC>(na + kBigTile, ob, q - 4, 0);
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[1][j], af[1][i], acc[i][j], 0, 0, 0);
+      if ((q & 1) == 0) load_part(st, kt + NSTAGE, q >> 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 
-  // Epilogue staged through LDS (the operand tiles are dead by now).  A lane
-  // holds, per 32x32 block, one output row and 4 consecutive columns; stored
-  // directly that scatters every store over 32 rows.  Instead each wave writes
-  // one block row of its results (32 x 128 float32, alpha applied) into a
-  // private [32][kStagePitch] block and reads it back row-major: a half-wave
-  // then covers 128 contiguous columns of one row, so the residual loads and
-  // the output stores (one rounding, after the residual) are fully coalesced.
+  // Epilogue staged through LDS.  A lane holds, per 32x32 block, one output
+  // row and 4 consecutive columns; stored directly that scatters every store
+  // over 32 rows.  Instead each wave writes one block row of its results
+  // (32 x 128 float32, alpha applied) into a private [32][kStagePitch] block
+  // and reads it back row-major: a half-wave then covers 128 contiguous
+  // columns of one row, so the residual loads and the output stores (one
+  // rounding, after the residual) are fully coalesced.
   const float alpha = g.alpha * (g.alpha_dev ? *g.alpha_dev : 1.f);
   const int half = lane >> 5, lm = lane & 31;
   float* part = g.part ? g.part + static_cast<int64_t>(sp) * g.M * g.N : nullptr;
-  float* stage = reinterpret_cast<float*>(wave == 0 ? sA0 : wave == 1 ? sA1 : wave == 2 ? sB0 : sB1);
-  __syncthreads();
+  float* stage = reinterpret_cast<float*>(ring) + wave * (32 * kStagePitch);
+  dma_barrier<0>();  // the loop's last loads (zeros) land before the ring is reused
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -686,12 +675,12 @@ GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, i
           g.N >= 512 && big_tiles >= 32 && a_span < kBigMaxSpan && b_span < kBigMaxSpan;
   if (p.big) {
     // split-K only for float32 outputs without a residual (weight gradients)
-    if (allow_split && g.c_f32 && !g.R && !g.out_map.idx && g.ldc == g.N && max_k >= 8 * GK) {
+    if (allow_split && g.c_f32 && !g.R && !g.out_map.idx && g.ldc == g.N && max_k >= 16 * GK) {
       double best = 0;
       for (int s = 1; s <= 8; ++s) {
         const int64_t wg = big_tiles * s;
         const double eff = static_cast<double>(wg) / (256.0 * ((wg + 255) / 256)) - 0.02 * (s - 1);
-        if (eff > best + 1e-9 && max_k / s >= 4 * GK) {
+        if (eff > best + 1e-9 && max_k / s >= 8 * GK) {
           best = eff;
           p.splits = s;
         }
