@@ -17,6 +17,7 @@
 // fp32: a plain SIMT kernel (64x64 tiles, 4x4 per thread) used by the fp32
 // configuration only.
 #include <algorithm>
+#include <type_traits>
 
 #include "ld_internal.h"
 
@@ -308,11 +309,12 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 // does not track them; the kernel waits for them itself (s_waitcnt vmcnt)
 // before the barriers.
 //
-// Per k tile (two k-substeps of 16): the second substep's fragments are read
-// while the first substep's MFMAs run; then each wave waits until the next
-// tile has landed and meets the others at the tile's one barrier; the second
-// substep's MFMAs then run next to the loads of the tile four ahead (into the
-// stage just released) and the reads of the next tile's first fragments.
+// Per k tile (two k-substeps of 16): one barrier at the top, where each wave
+// has waited until the next tile has landed; then the tile's 32 MFMAs run on
+// fragments read during the previous tile, next to the reads of all of the
+// next tile's fragments and the loads of the tile four ahead, which go into
+// the stage this tile was read from (its reads completed before the
+// barrier).  No MFMA waits on a recent LDS read.
 //
 // The MFMA is issued as B x A so each lane ends with 4 consecutive output
 // columns of one row.  Tiles are ordered XCD-aware: consecutive workgroup ids
@@ -517,53 +519,44 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
 #pragma unroll
     for (int q = 0; q < 2 * kLoads; ++q) load_part(st, st, q);
   dma_barrier<(NSTAGE - 1) * 2 * kLoads>();  // tile 0 has landed
-  bf16x8 af[2][4], bfr[2][4];
+  // Fragments are read one whole tile ahead: fa/fb[set][ks][block], the
+  // set alternating with the tile's parity.
+  bf16x8 fa[2][2][4], fb[2][2][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    af[0][i] = frag<AK>(ring, oa, i, 0);
-    bfr[0][i] = frag<BKC>(ring + kBigTile, ob, i, 0);
-  }
-  constexpr int kReads = (AK ? 4 : 8) + (BKC ? 4 : 8);  // LDS read instructions per substep
-  for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & (NSTAGE - 1), nst = (kt + 1) & (NSTAGE - 1);
-    const bf16* sa = ring + st * kStage;
-    const bf16* na = ring + nst * kStage;
-    // substep 0: MFMAs on the fragments in hand, reads of substep 1's
+  for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      af[1][i] = frag<AK>(sa, oa, i, 1);
-      bfr[1][i] = frag<BKC>(sa + kBigTile, ob, i, 1);
+      fa[0][ks][i] = frag<AK>(ring, oa, i, ks);
+      fb[0][ks][i] = frag<BKC>(ring + kBigTile, ob, i, ks);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[0][j], af[0][i], acc[i][j], 0, 0, 0);
-    // MFMA first: its operands were read during the previous tile, and a
-    // read issued before it would be included in its wait
-#pragma unroll
-    for (int r = 0; r < kReads; ++r) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 16 - kReads, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    // Tile kt+1 has landed (tiles kt+2, kt+3 may still be in flight) and
-    // this stage is no longer read.  Substep 1 issues next to its 16 MFMAs
-    // the 8 loads of tile kt+4 into this stage and the 8 fragments of the
-    // next tile's substep 0.
+  // Tile kt: one barrier at the top (tile kt+1 has landed; tile kt's stage,
+  // read during the previous tile, is free), then 32 MFMAs on fragments in
+  // hand; next to the first 16 the 16 fragment reads of tile kt+1, and one
+  // load instruction of tile kt+4 (into tile kt's stage) per 4 MFMAs.
+  auto tile = [&](auto parity, int kt) {
+    constexpr int P = decltype(parity)::value;
+    const int st = kt & (NSTAGE - 1);
+    const bf16* na = ring + ((kt + 1) & (NSTAGE - 1)) * kStage;
     dma_barrier<(NSTAGE - 2) * 2 * kLoads>();
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int i = q >> 2, j = q & 3;
-      if (q < 4)
-        af[0][q] = frag<AK>(na, oa, q, 0);
-      else if (q < 8)
-        bfr[0][q - 4] = frag<BKC>(na + kBigTile, ob, q - 4, 0);
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[1][j], af[1][i], acc[i][j], 0, 0, 0);
-      if ((q & 1) == 0) load_part(st, kt + NSTAGE, q >> 1);
+    for (int q = 0; q < 32; ++q) {
+      const int ks = q >> 4, i = (q >> 2) & 3, j = q & 3;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[P][ks][j], fa[P][ks][i], acc[i][j], 0, 0, 0);
+      if (q < 16) {  // read order per k-substep: B0 A0 B1 B2 B3 A1 A2 A3
+        const int rk = q >> 3, r = q & 7;
+        if (r == 0 || r == 2 || r == 3 || r == 4)
+          fb[P ^ 1][rk][r == 0 ? 0 : r - 1] = frag<BKC>(na + kBigTile, ob, r == 0 ? 0 : r - 1, rk);
+        else
+          fa[P ^ 1][rk][r == 1 ? 0 : r - 4] = frag<AK>(na, oa, r == 1 ? 0 : r - 4, rk);
+      }
+      if ((q & 3) == 3) load_part(st, kt + NSTAGE, q >> 2);
       __builtin_amdgcn_sched_barrier(0);
     }
+  };
+  // Tiles in pairs (a phantom tile past the end loads and multiplies zeros).
+  for (int kt = 0; kt < nk; kt += 2) {
+    tile(std::integral_constant<int, 0>(), kt);
+    tile(std::integral_constant<int, 1>(), kt + 1);
   }
 
   // Epilogue staged through LDS.  A lane holds, per 32x32 block, one output
@@ -572,7 +565,11 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
   // (32 x 128 float32, alpha applied) into a private [32][kStagePitch] block
   // and reads it back row-major: a half-wave then covers 128 contiguous
   // columns of one row, so the residual loads and the output stores (one
-  // rounding, after the residual) are fully coalesced.
+  // rounding, after the residual) are fully coalesced.  The blocks are
+  // private to the wave, so after one barrier (the ring's last loads have
+  // landed everywhere) only the wave's own LDS accesses are ordered: no
+  // workgroup barrier, whose memory fence would wait for every store in
+  // flight, and the stores drain while the wave goes on.
   const float alpha = g.alpha * (g.alpha_dev ? *g.alpha_dev : 1.f);
   const int half = lane >> 5, lm = lane & 31;
   float* part = g.part ? g.part + static_cast<int64_t>(sp) * g.M * g.N : nullptr;
@@ -588,7 +585,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
         *reinterpret_cast<float4*>(stage + lm * kStagePitch + j * 32 + 8 * q + 4 * half) =
             make_float4(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
       }
-    __syncthreads();
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // staged values visible to the wave
     const int c = (lane & 31) * 4;
     const int n = n0 + wn * 128 + c;
 #pragma unroll 4
@@ -622,7 +619,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
         *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + orow * g.ldc + n) = *reinterpret_cast<const uint2*>(o);
       }
     }
-    __syncthreads();
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // reads done before the block is rewritten
   }
 }
 
