@@ -30,10 +30,43 @@ sys.path.insert(0, ROOT)
 
 import ld_inputs as inp  # noqa: E402
 import paper_2609_05275_amd as ld  # noqa: E402
+from paper_2609_05275_amd import profsum  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 T_RAMP = 1001               # steps 0..1000 of the p_max ramp
+
+
+# Kernel -> source file it is built from (for the traffic record's hash check).
+KERNEL_SOURCES = {"ld_gemm": "paper_2609_05275_amd/csrc/k_gemm.hip",
+                  "ld_attn": "paper_2609_05275_amd/csrc/k_attn.hip"}
+
+
+def traffic_record(kernel):
+    """HBM bytes per launch of `kernel` from its committed counter summary,
+    or None when there is none or the kernel's source changed since."""
+    rec = profsum.read_traffic(os.path.join(ROOT, "profiles", f"{kernel}_1b_traffic.md"))
+    if not rec or rec.get("kernel") != kernel:
+        return None
+    src = next((v for k, v in KERNEL_SOURCES.items() if kernel.startswith(k)), None)
+    if src is None or rec.get("source") != src:
+        return None
+    if profsum.source_hash(os.path.join(ROOT, src)) != rec.get("source_sha256"):
+        return None
+    return rec
+
+
+def copy_calibration(mib):
+    """Elementwise y = 1 * x over float32 tensors of `mib` MiB, 3 times: the
+    known-size reference the HBM traffic counters are scaled by."""
+    n = mib * 2**20 // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.mul(x, 1.0, out=y)
+    torch.cuda.synchronize()
+    del x, y
 
 
 def f_sl(sh):
@@ -118,6 +151,8 @@ def main():
     ap.add_argument("--p-max", type=float, default=0.2)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="run the traffic-counter calibration copy of this size first")
     ap.add_argument("--prof-kernel", default=None,
                     help="kernel timed with HIP events for the roofline (default: every GEMM "
                          "variant is measured in a short pass and the slowest total is used)")
@@ -127,6 +162,8 @@ def main():
               "(the data-parallel sharding is described in DESIGN.md)", file=sys.stderr)
         sys.exit(2)
 
+    if args.copy_calib_mib > 0:
+        copy_calibration(args.copy_calib_mib)
     sh = inp.SHAPES["1b"]
     dev = "cuda:0"
     st = Stack(sh, dev)
@@ -169,6 +206,7 @@ def main():
           flush=True)
     exec_tflops = fsl * np.mean(kept) / (ms * 1e-3) / 1e12
     achieved = pr["flops"] / (pr["ms"] * 1e-3) / 1e12 if pr["ms"] > 0 else 0.0
+    trec = traffic_record(prof_kernel)
 
     sweep = []
     if not args.no_sweep:
@@ -223,7 +261,10 @@ def main():
         "drop_frac": round(1 - np.mean(kept) / (sh.n_layers * sh.batch), 4),
         "roofline": {"kernel": prof_kernel, "bound": "mfma", "achieved": round(achieved, 1),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": trec["hbm_bytes_per_launch"] if trec else None,
+                     "traffic_unit": "bytes per launch (HBM, counter-measured)",
+                     "algorithmic_bytes": round(pr["bytes"] / max(pr["launches"], 1)),
                      "launches": pr["launches"],
                      "avg_launch_us": round(pr["ms"] * 1e3 / max(pr["launches"], 1), 2)},
         "cpu_baseline": cpu,
