@@ -410,6 +410,7 @@ __device__ __forceinline__ void rgn_store(const RowGroupsN<DH, NT>& t, bf16* dir
 }
 
 constexpr int BQ = 64;       // query rows per step of the dK/dV kernel
+constexpr int DK_NST = 3;    // dK/dV ring stages (query blocks in LDS)
 
 // Waves per dK/dV workgroup: 8 (two per SIMD) where the per-wave state fits
 // in 256 registers (d_head 64); 4 for d_head 128, whose K/V fragments and
@@ -417,31 +418,60 @@ constexpr int BQ = 64;       // query rows per step of the dK/dV kernel
 template <int DH>
 constexpr int dkdv_waves() { return DH <= 64 ? 8 : 4; }
 
+// Q and dO blocks in the dK/dV ring are [64 q][DH] without padding, the
+// 16-byte chunks of a row XOR-swizzled by row bits 0-3: 16 lanes reading one
+// chunk of 16 consecutive rows, and the transposing reads (4 consecutive rows
+// x 64 bytes per half-wave), both hit every bank once.
+template <int DH>
+__device__ __forceinline__ int qd_swz(int r) {
+  if constexpr (DH == 128)
+    return ((r & 3) << 2) | ((r >> 2) & 3);
+  else
+    return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+template <int DH>
+__device__ __forceinline__ int qd_off(int r, int d) {
+  return r * DH + (((d >> 3) ^ qd_swz<DH>(r)) << 3) + (d & 7);
+}
+
+// One ring stage: the Q block, the dO block, then log-sum-exp and delta.
+template <int DH>
+constexpr int dk_stage_bytes() { return 4 * BQ * DH + 8 * BQ; }
+// Loads per wave per stage: Q and dO in 1 KB pieces split over the waves,
+// plus the log-sum-exp and delta rows (every wave loads both: same bytes).
+template <int DH, int NW>
+constexpr int dk_loads() { return 2 * (BQ * DH * 2 / 1024) / NW + 2; }
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+
 // dK, dV.  A workgroup of NW waves owns 32 NW keys (32 per wave, K and V
-// fragments in registers) and walks the 64-row query
-// blocks from the diagonal to the end; Q, dO (both as [q][d] and transposed
-// [d][q]), the log-sum-exp and delta of the block are double buffered in LDS
-// with the next block prefetched in registers.  P = 2^(s*scale*log2e -
-// lse*log2e) is recomputed, dS = P (dP - delta); dV^T += dO^T P and
-// dK^T += Q^T dS take P and dS straight from the score accumulators (their
-// rows are a fixed permutation of the MFMA k index, matched when the
-// transposed tiles are read).  The two 32-row halves of a query block are
-// processed one after the other so only one half's scores are live.
+// fragments in registers) and walks the 64-row query blocks from the diagonal
+// to the end.  Q, dO, log-sum-exp and delta of each block go from global
+// memory straight into a three-stage LDS ring (buffer loads with an LDS
+// destination, see ld_internal.h), so a block's loads have two block-times to
+// land; one barrier per block.  P = 2^(s*scale*log2e - lse*log2e) is
+// recomputed, dS = P (dP - delta); dV^T += dO^T P and dK^T += Q^T dS take P
+// and dS straight from the score accumulators (their rows are a fixed
+// permutation of the MFMA k index), and dO^T, Q^T come from the same [q][d]
+// blocks through transposing reads (ds_read_b64_tr_b16) in that
+// permutation.  The two 32-row halves of a query block are processed one
+// after the other so only one half's scores are live.  Fragment addresses
+// are per-lane offsets computed once; the loop has no branch around its
+// MFMAs.
 template <int DH, int NW = dkdv_waves<DH>()>
 __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
-  constexpr int NT = 64 * NW, BKEYS = 32 * NW;
-  constexpr int DT = BQ * (DH + 8), TT = DH * BQ;
-  constexpr int STAGE = 2 * DT + 2 * TT;  // bf16 elements per buffer
-  extern __shared__ __align__(16) bf16 lds[];
-  float* lse_s = reinterpret_cast<float*>(lds + 2 * STAGE);  // [2][BQ]
-  float* del_s = lse_s + 2 * BQ;                              // [2][BQ]
+  constexpr int BKEYS = 32 * NW, SB = dk_stage_bytes<DH>(), NL = dk_loads<DH, NW>();
+  constexpr int RPI = 512 / DH, LPR = 64 / RPI;   // rows per 1 KB load, lanes per row
+  constexpr int NPW = (BQ * DH * 2 / 1024) / NW;  // 1 KB loads per wave per tile
+  extern __shared__ __align__(16) char ring[];
   const int S = a.S, H = a.H;
   // grid (head, sequence, tile), tile slowest: early key tiles see the most
   // queries and go first
   const int kt = static_cast<int>(blockIdx.z);
   const int head = blockIdx.x, seq = blockIdx.y;
   if (seq >= seq_count(a)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hf = lane >> 5, cl = lane & 31;
   const int k0 = kt * BKEYS, kw = k0 + wave * 32, key = kw + cl;
   const bool active = kw < S;
@@ -461,85 +491,123 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     kf[ks] = key < S ? load8(Kp + static_cast<int64_t>(key) * ldq + ks * 16 + hf * 8) : zero8();
     vf[ks] = key < S ? load8(Vp + static_cast<int64_t>(key) * ldq + ks * 16 + hf * 8) : zero8();
   }
+  // The fragments must have arrived before the first LDS load is issued:
+  // the compiler does not see those loads, so a wait of its own for these
+  // inside the loop would wait for all of them, every iteration.
+#pragma unroll
+  for (int ks = 0; ks < DH / 16; ++ks) asm volatile("" ::"v"(kf[ks]), "v"(vf[ks]));
   floatx16 dv[DH / 32], dk[DH / 32];
 #pragma unroll
   for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) dv[db][v] = dk[db][v] = 0.f;
 
+  // Loads of query block qb into stage st.  Blocks past the end (qb >= S)
+  // read zeros; every wave issues NL loads per stage.
+  const dma_rsrc rq = dma_make_rsrc(Qp, static_cast<int64_t>(S) * ldq * 2);
+  const dma_rsrc ro = dma_make_rsrc(dOp, static_cast<int64_t>(S) * ldo * 2);
+  const dma_rsrc rl = dma_make_rsrc(lse, static_cast<int64_t>(S) * 4);
+  const dma_rsrc rd = dma_make_rsrc(del, static_cast<int64_t>(S) * 4);
+  const int lrow = wave * RPI + lane / LPR;                           // row of load 0
+  const int lchk = ((lane % LPR) ^ qd_swz<DH>(lrow)) << 3;            // its logical column
+  const uint32_t lq = static_cast<uint32_t>((lrow * ldq + lchk) * 2);
+  const uint32_t lo = static_cast<uint32_t>((lrow * ldo + lchk) * 2);
+  auto load_block = [&](int st, int qb) {
+    char* sb = ring + st * SB;
+    const bool in = qb < S;
+#pragma unroll
+    for (int i = 0; i < NPW; ++i) {
+      const int p = wave + NW * i;
+      const int64_t r = qb + static_cast<int64_t>(NW) * i * RPI;
+      dma16(rq, sb + p * 1024, in ? lq + static_cast<uint32_t>(r * ldq * 2) : kDmaOob);
+      dma16(ro, sb + BQ * DH * 2 + p * 1024, in ? lo + static_cast<uint32_t>(r * ldo * 2) : kDmaOob);
+    }
+    dma4(rl, sb + 4 * BQ * DH, in ? static_cast<uint32_t>((qb + lane) * 4) : kDmaOob);
+    dma4(rd, sb + 4 * BQ * DH + 4 * BQ, in ? static_cast<uint32_t>((qb + lane) * 4) : kDmaOob);
+  };
+
+  // Per-lane fragment offsets within a block; the row offsets of the halves
+  // and 16-row groups are instruction immediates.
+  int po[DH / 16];            // plain reads: row cl, 16-byte chunk 2ks + hf
+  int to0[DH / 32], to1[DH / 32];  // transposing reads, rows tr_r and tr_r + 8
+  {
+    const int sw_c = qd_swz<DH>(cl);
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) po[ks] = cl * DH + (((2 * ks + hf) ^ sw_c) << 3);
+    const int tr_r = 4 * hf + ((lane & 15) >> 2);
+    const int tr_d = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+    const int sw0 = qd_swz<DH>(tr_r), sw1 = qd_swz<DH>(tr_r + 8);
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) {
+      const int d0 = db * 32 + tr_d;
+      to0[db] = tr_r * DH + (((d0 >> 3) ^ sw0) << 3) + (d0 & 7);
+      to1[db] = (tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7);
+    }
+  }
+
   const int q_first = k0;  // the first query that can see key k0
   const int nqb = q_first < S ? (S - q_first) / BQ : 0;
-  RowGroupsN<DH, NT> rq, ro;
-  float lse_r = 0.f, del_r = 0.f;
-  auto fetch = [&](int qb) {
-    rgn_load<DH, NT>(rq, Qp, ldq, qb, tid);
-    rgn_load<DH, NT>(ro, dOp, ldo, qb, tid);
-    if (tid < BQ) {
-      lse_r = lse[qb + tid] * kLog2e;
-      del_r = del[qb + tid];
-    }
-  };
-  auto put = [&](int buf) {
-    bf16* st = lds + buf * STAGE;
-    rgn_store<DH, NT>(rq, st, st + 2 * DT, tid);
-    rgn_store<DH, NT>(ro, st + DT, st + 2 * DT + TT, tid);
-    if (tid < BQ) {
-      lse_s[buf * BQ + tid] = lse_r;
-      del_s[buf * BQ + tid] = del_r;
-    }
-  };
-  if (nqb > 0) {
-    fetch(q_first);
-    put(0);
-  }
-  __syncthreads();
+  load_block(0, q_first);
+  load_block(1, q_first + BQ);
+  // No branch around the MFMAs (a branch would merge the dK/dV accumulators
+  // across register files): query rows before a wave's keys are computed and
+  // masked to P = 0, and waves past the end compute on zero K/V and store
+  // nothing.
   for (int ib = 0; ib < nqb; ++ib) {
-    const int qb = q_first + ib * BQ, buf = ib & 1;
-    if (ib + 1 < nqb) fetch(qb + BQ);
-    const bf16* Qs = lds + buf * STAGE;
-    const bf16* Os = Qs + DT;
-    const bf16* Qt = Qs + 2 * DT;
-    const bf16* Ot = Qt + TT;
-    const float* ls = lse_s + buf * BQ;
-    const float* dl = del_s + buf * BQ;
-    if (active && kw <= qb + BQ - 1) {
+    const int qb = q_first + ib * BQ, st = ib % DK_NST;
+    // block ib has landed (block ib+1 may be in flight); the stage of block
+    // ib-1 is no longer read and takes block ib+2
+    dma_barrier<NL>();
+    load_block((ib + 2) % DK_NST, qb + 2 * BQ);
+    const char* sb = ring + st * SB;
+    const bf16* Qs = reinterpret_cast<const bf16*>(sb);
+    const bf16* Os = Qs + BQ * DH;
+    const float* ls = reinterpret_cast<const float*>(sb + 4 * BQ * DH);
+    const float* dl = ls + BQ;
 #pragma unroll
-      for (int qh = 0; qh < 2; ++qh) {
-        if (kw > qb + qh * 32 + 31) continue;  // every key of the wave is past this half
-        const bool diag = kw + 31 > qb + qh * 32;
-        floatx16 sc, dp;
+    for (int qh = 0; qh < 2; ++qh) {
+      floatx16 sc, dp;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sc[v] = dp[v] = 0.f;
+      for (int v = 0; v < 16; ++v) sc[v] = dp[v] = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < DH / 16; ++ks) {
-          sc = mfma(load8(Qs + (qh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), kf[ks], sc);
-          dp = mfma(load8(Os + (qh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), vf[ks], dp);
-        }
-        bf16x8 pb[2], dsb[2];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int ql = qh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-          float p = __builtin_amdgcn_exp2f(sc[v] * sl2 - ls[ql]);
-          if (diag && key > qb + ql) p = 0.f;
-          pb[v >> 3][v & 7] = static_cast<bf16>(p);
-          dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dl[ql]));
-        }
-#pragma unroll
-        for (int db = 0; db < DH / 32; ++db) {
-          const int dr = db * 32 + cl;
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int qq = qh * 32 + 16 * c + 4 * hf;
-            dv[db] = mfma(load4x2(Ot + tr_off(dr, qq), Ot + tr_off(dr, qq + 8)), pb[c], dv[db]);
-            dk[db] = mfma(load4x2(Qt + tr_off(dr, qq), Qt + tr_off(dr, qq + 8)), dsb[c], dk[db]);
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);  // keep the two halves' live ranges apart
+      for (int ks = 0; ks < DH / 16; ++ks) {
+        sc = mfma(load8(Qs + qh * 32 * DH + po[ks]), kf[ks], sc);
+        dp = mfma(load8(Os + qh * 32 * DH + po[ks]), vf[ks], dp);
       }
+      float4 l4[4], d4[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        l4[g] = *reinterpret_cast<const float4*>(ls + qh * 32 + 8 * g + 4 * hf);
+        d4[g] = *reinterpret_cast<const float4*>(dl + qh * 32 + 8 * g + 4 * hf);
+      }
+      bf16x8 pb[2], dsb[2];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int ql = qh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
+        const float lv = (&l4[v >> 2].x)[v & 3], dv_ = (&d4[v >> 2].x)[v & 3];
+        float p = __builtin_amdgcn_exp2f(sc[v] * sl2 - lv * kLog2e);
+        p = key > qb + ql ? 0.f : p;
+        pb[v >> 3][v & 7] = static_cast<bf16>(p);
+        dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dv_));
+      }
+#pragma unroll
+      for (int db = 0; db < DH / 32; ++db) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int rr = (qh * 32 + 16 * c) * DH;
+          typedef __attribute__((address_space(3))) v4s lds_v4s;
+          const v4s ol = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Os + rr + to0[db]));
+          const v4s oh = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Os + rr + to1[db]));
+          const v4s ql_ = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Qs + rr + to0[db]));
+          const v4s qh_ = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Qs + rr + to1[db]));
+          dv[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ol, oh, 0, 1, 2, 3, 4, 5, 6, 7)), pb[c], dv[db]);
+          dk[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ql_, qh_, 0, 1, 2, 3, 4, 5, 6, 7)), dsb[c], dk[db]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);  // keep the two halves' live ranges apart
     }
-    if (ib + 1 < nqb) put(buf ^ 1);
-    __syncthreads();
   }
+  dma_barrier<0>();  // no load may still write LDS when the workgroup ends
   if (active && key < S) {
     bf16* G = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + key) * ldq + head * DH;
     bf16* Gk = G + static_cast<int64_t>(H) * DH;
@@ -562,7 +630,7 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
 
 template <int DH>
 constexpr size_t dkdv_lds_bytes() {
-  return (2ull * (2 * BQ * (DH + 8) + 2 * DH * BQ)) * sizeof(bf16) + 4ull * BQ * sizeof(float);
+  return static_cast<size_t>(DK_NST) * dk_stage_bytes<DH>();
 }
 
 constexpr int DQ_ROWS = 256;  // query rows per dQ workgroup (8 waves x 32)

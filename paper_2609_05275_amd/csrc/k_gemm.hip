@@ -305,9 +305,9 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 //     k..k+3 at mn offsets 0, 4, 8, 12 give lane j the values k..k+3 at mn j).
 // Rows past the operand's end, and k chunks past the split's end, are
 // fetched from an offset outside the buffer descriptor's range and land in
-// LDS as zeros.  The loads are issued as inline assembly, so the compiler
-// does not track them; the kernel waits for them itself (s_waitcnt vmcnt)
-// before the barriers.
+// LDS as zeros.  The loads are issued as inline assembly (ld_internal.h),
+// so the compiler does not track them; the kernel waits for them itself
+// (s_waitcnt vmcnt) before the barriers.
 //
 // Per k tile (two k-substeps of 16): one barrier at the top, where each wave
 // has waited until the next tile has landed; then the tile's 32 MFMAs run on
@@ -327,13 +327,12 @@ constexpr int kBigTile = GB * GK;      // elements per operand tile
 constexpr int kStage = 2 * kBigTile;   // A and B tiles of one stage
 constexpr int kLoads = 4;              // load instructions per wave per operand tile
 constexpr int kStagePitch = 132;       // floats per staged epilogue row (128 + 4 pad)
-constexpr uint32_t kOob = 0x80000000u;  // buffer offset past every descriptor's range
-// Operand spans addressed by one descriptor stay below kOob bytes.
-constexpr int64_t kBigMaxSpan = 0x7FFFFFFFll;
+constexpr uint32_t kOob = kDmaOob;
+constexpr int64_t kBigMaxSpan = kDmaMaxSpan;
 static_assert(NSTAGE * kStage * 2 >= 4 * 32 * kStagePitch * 4, "epilogue staging fits the stages");
 
 typedef short v4s __attribute__((ext_vector_type(4)));
-typedef int v4i __attribute__((ext_vector_type(4)));
+typedef dma_rsrc v4i;
 #define LD_LDS(T, p) ((__attribute__((address_space(3))) T*)(p))
 
 // k-contiguous tile: element (row, k) of a [256][32] tile.  The chunk swizzle
@@ -352,31 +351,6 @@ __device__ __forceinline__ int swz_off(int row, int k) {
 __device__ __forceinline__ int mc_swz(int k) { return ((k & 3) << 2) | (((k >> 3) & 1) << 1); }
 __device__ __forceinline__ int mc_off(int k, int m) {
   return k * GB + ((((m >> 3) ^ mc_swz(k)) << 3) | (m & 7));
-}
-
-// Buffer descriptor covering `bytes` from `base` (raw, no stride): loads
-// past it return 0.
-__device__ __forceinline__ v4i make_rsrc(const void* base, int64_t bytes) {
-  const int64_t n = bytes < 0 ? 0 : (bytes > kBigMaxSpan ? kBigMaxSpan : bytes);
-  const uint64_t a = reinterpret_cast<uint64_t>(base);
-  return v4i{static_cast<int>(static_cast<uint32_t>(a)), static_cast<int>((a >> 32) & 0xFFFF),
-             static_cast<int>(n), 0x00020000};
-}
-
-// 16 bytes per lane from buffer offset `voff` into LDS at `lds` + 16 * lane
-// (`lds` wave-uniform).  No other code in these kernels reads m0.
-__device__ __forceinline__ void dma16(v4i rs, const bf16* lds, uint32_t voff) {
-  const uint32_t m = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(LD_LDS(const void, lds)));
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(m), "v"(voff),
-               "s"(rs));
-}
-
-// Waits until at most N of this wave's LDS loads are in flight and its LDS
-// reads are done, then meets the workgroup.  A compiler barrier for memory.
-template <int N>
-__device__ __forceinline__ void dma_barrier() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
 // Per-lane constants of one operand's tile loads and fragment reads.
@@ -429,12 +403,12 @@ template <bool KC>
 __device__ __forceinline__ void tile_part(bf16* lds, const OpLanes<KC>& o, const bf16* X, int64_t ld,
                                           int r0, int R, int k0, int K, int wave, int p) {
   if constexpr (KC) {
-    const v4i rs = make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
+    const v4i rs = dma_make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
     const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 64 * ld + k0) * 2);
     const uint32_t off = k0 + o.kchunk < K ? o.ld_off[0] + u : kOob;
     dma16(rs, lds + (p * 4 + wave) * 512, off);
   } else {
-    const v4i rs = make_rsrc(X + static_cast<int64_t>(k0) * ld, (static_cast<int64_t>(K) - k0) * ld * 2);
+    const v4i rs = dma_make_rsrc(X + static_cast<int64_t>(k0) * ld, (static_cast<int64_t>(K) - k0) * ld * 2);
     const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 8 * ld + r0) * 2);
     dma16(rs, lds + (p * 4 + wave) * 512, o.ld_off[p & 1] + u);
   }

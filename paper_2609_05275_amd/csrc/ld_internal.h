@@ -11,6 +11,54 @@ namespace ld {
 
 using bf16 = __bf16;
 
+// ------------------------------------------------ global-to-LDS loads
+// Buffer loads with an LDS destination: each lane's data goes to LDS at a
+// wave-uniform base plus (bytes per lane) * lane, so the layout in LDS is set
+// by which global address each lane fetches.  A raw buffer descriptor bounds
+// them: offsets at or past its size (kDmaOob is past every size used) return
+// zeros.  They are issued as inline assembly, so the compiler does not track
+// them: code that issues them waits itself (s_waitcnt vmcnt) before reading
+// what they wrote, and issues no compiler-visible global loads whose waits
+// would be miscounted meanwhile.  No other code in the kernels that use them
+// reads m0.
+
+typedef int dma_rsrc __attribute__((ext_vector_type(4)));
+constexpr uint32_t kDmaOob = 0x80000000u;
+constexpr int64_t kDmaMaxSpan = 0x7FFFFFFFll;  // bytes one descriptor may cover
+
+__device__ __forceinline__ dma_rsrc dma_make_rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0 ? 0 : (bytes > kDmaMaxSpan ? kDmaMaxSpan : bytes);
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return dma_rsrc{static_cast<int>(static_cast<uint32_t>(a)), static_cast<int>((a >> 32) & 0xFFFF),
+                  static_cast<int>(n), 0x00020000};
+}
+
+// LDS byte address of a pointer into __shared__ memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)(p)));
+}
+
+// 16 bytes per lane from buffer offset `voff` to LDS `lds` + 16 * lane.
+__device__ __forceinline__ void dma16(dma_rsrc rs, const void* lds, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_addr(lds)),
+               "v"(voff), "s"(rs));
+}
+
+// 4 bytes per lane from buffer offset `voff` to LDS `lds` + 4 * lane.
+__device__ __forceinline__ void dma4(dma_rsrc rs, const void* lds, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds" ::"s"(lds_addr(lds)),
+               "v"(voff), "s"(rs));
+}
+
+// Waits until at most N of this wave's vector memory operations are in
+// flight and its LDS accesses are done, then meets the workgroup.  A
+// compiler barrier for memory.
+template <int N>
+__device__ __forceinline__ void dma_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
 // ------------------------------------------------------------ kernel args
 
 // Rows of a compacted activation block.  When dev_count is set the row count
