@@ -36,6 +36,7 @@ class Shape:
     seq: int
     batch: int
     dtype: str  # "f32" or "bf16"
+    kind: int = 0  # block kind: 0 SwiGLU, 1 ALiBi + squared ReLU (W_up only)
 
     @property
     def torch_dtype(self):
@@ -49,6 +50,10 @@ SHAPES = {
     "1b": Shape(16, 2048, 16, 5504, 2048, 8, "bf16"),
     "7b": Shape(32, 4096, 32, 11008, 4096, 4, "bf16"),
     "1b_b32": Shape(16, 2048, 16, 5504, 2048, 32, "bf16"),
+    # the paper's 3.9B architecture (architecture table: d 2048, 40 layers,
+    # 16 heads of 128, FFN multiplier 8) with its block (ALiBi, squared ReLU);
+    # sequence length and batch as the 1B workload (the paper states neither)
+    "paper_3p9b": Shape(40, 2048, 16, 16384, 2048, 8, "bf16", 1),
 }
 
 
@@ -64,7 +69,7 @@ def _cast(a, dtype):
 def weight_shapes(sh):
     d, f = sh.d_model, sh.d_ff
     return dict(g_attn=(d,), w_qkv=(3 * d, d), w_o=(d, d), g_mlp=(d,),
-                w_gate_up=(2 * f, d), w_down=(d, f))
+                w_gate_up=((2 if sh.kind == 0 else 1) * f, d), w_down=(d, f))
 
 
 def layer_weights(sh, layer, seed=0, gain_jitter=False):

@@ -6,10 +6,13 @@ The block is f^l of the transformer form of the layer-dropout training
 equation (Preliminary section, "Layer Dropout for a Transformer"):
     Z  = X + r * f_attn(X)        f_attn(X) = MHA(RMSNorm(X; g_attn)) W_o^T
     X' = Z + r * f_ffn(Z)         f_ffn(Z)  = SwiGLU(RMSNorm(Z; g_mlp)) W_down^T
-with the sub-block choices of this hot path: RMSNorm, causal multi-head
-attention without positional bias, SwiGLU.  The paper's footnote on that
-equation states the formulation holds for any pre-norm attention/FFN variant
-with a residual connection.
+with the sub-block choices of this hot path (kind 0): RMSNorm, causal
+multi-head attention without positional bias, SwiGLU.  The paper's footnote
+on that equation states the formulation holds for any pre-norm attention/FFN
+variant with a residual connection.  Kind 1 is the block of the paper's
+experiments (Experimental Setup: ALiBi position embeddings, squared ReLU):
+the attention scores get the ALiBi bias, and f_ffn(Z) = relu(RMSNorm(Z) W_up^T)^2
+W_down^T with two matrices.
 
 Readings (the paper is silent on these):
   * RMSNorm(x; g) = x / sqrt(mean_d(x^2) + eps) * g, eps from the config;
@@ -18,7 +21,12 @@ Readings (the paper is silent on these):
   * w_qkv rows are [q | k | v], each d rows, head h owning rows h*dh..h*dh+dh
     of each part; w_gate_up rows [0, f) are the gate, [f, 2f) the up
     projection; SwiGLU(u, v) = silu(u) * v, silu(u) = u * sigmoid(u);
-  * weights are stored [out, in] and applied as x @ W^T.
+  * weights are stored [out, in] and applied as x @ W^T;
+  * kind 1: the normalisation stays RMSNorm with a gain and there are no
+    biases (the paper names a pre-norm parameter and a hidden-bias learning
+    rate in its parameterisation table but not which layers carry biases);
+    ALiBi is added to the scaled scores, s_ij = q_i.k_j / sqrt(dh) - m_h (i - j),
+    with the slopes of alibi_slopes; w_gate_up holds W_up [f, d].
 
 The backward is the chain rule of the forward written out by hand; it is
 pinned against finite differences and against torch float64 autograd.
@@ -40,17 +48,35 @@ def rmsnorm_bwd(x, g, rstd, gy):
     return dx, dg
 
 
-def causal_attention(q, k, v, n_heads):
-    """softmax(q k^T / sqrt(dh), causal j <= i) v per head.
+def alibi_slopes(n_heads):
+    """Head slopes of ALiBi (Press et al., ICLR 2022, section 3): for n heads
+    with n a power of two, the geometric sequence starting at 2^(-8/n) with
+    that ratio; for other head counts, the n' = largest power of two below
+    gets its own sequence and the remaining heads take every other slope of
+    the 2n'-head sequence, starting with its first."""
+    if n_heads < 1:
+        return np.zeros(0)
+    n = 1 << (int(n_heads).bit_length() - 1)
+    own = [2.0 ** (-8.0 * (i + 1) / n) for i in range(n)]
+    twice = [2.0 ** (-8.0 * (i + 1) / (2 * n)) for i in range(2 * n)]
+    return np.array(own + twice[0::2][:n_heads - n], dtype=np.float64)
+
+
+def causal_attention(q, k, v, n_heads, slopes=None):
+    """softmax(q k^T / sqrt(dh) + bias, causal j <= i) v per head, with the
+    ALiBi bias -m_h (i - j) when `slopes` is given (else no bias).
     q, k, v: [S, d].  Returns (out [S, d], probs [H, S, S])."""
     S, d = q.shape
     dh = d // n_heads
     out = np.zeros((S, d))
     probs = np.zeros((n_heads, S, S))
     future = np.triu(np.ones((S, S), dtype=bool), k=1)
+    dist = np.arange(S)[:, None] - np.arange(S)[None, :]   # i - j
     for h in range(n_heads):
         cols = slice(h * dh, (h + 1) * dh)
         s = q[:, cols] @ k[:, cols].T / np.sqrt(dh)
+        if slopes is not None:
+            s = s - slopes[h] * dist
         s[future] = -np.inf
         s = s - np.max(s, axis=-1, keepdims=True)
         e = np.exp(s)
@@ -77,6 +103,14 @@ def causal_attention_bwd(q, k, v, probs, gout, n_heads):
     return gq, gk, gv
 
 
+def relu2(u):
+    return np.maximum(u, 0.0) ** 2
+
+
+def relu2_grad(u):
+    return 2.0 * np.maximum(u, 0.0)
+
+
 def silu(u):
     return u / (1.0 + np.exp(-u))
 
@@ -86,26 +120,30 @@ def silu_grad(u):
     return sg * (1.0 + u * (1.0 - sg))
 
 
-def forward(x, w, r, n_heads, eps):
+def forward(x, w, r, n_heads, eps, kind=0):
     """Apply the block to one kept sequence x [S, d].
 
     w: dict with g_attn [d], w_qkv [3d, d], w_o [d, d], g_mlp [d],
-    w_gate_up [2f, d], w_down [d, f].  r is the residual-branch scale.
-    Returns (x_next, cache)."""
+    w_gate_up [2f, d] (kind 0) or [f, d] (kind 1), w_down [d, f].  r is the
+    residual-branch scale.  Returns (x_next, cache)."""
     d = x.shape[1]
     f = w["w_down"].shape[1]
     h1, rstd1 = rmsnorm(x, w["g_attn"], eps)
     qkv = h1 @ w["w_qkv"].T
     q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
-    a, probs = causal_attention(q, k, v, n_heads)
+    a, probs = causal_attention(q, k, v, n_heads, alibi_slopes(n_heads) if kind == 1 else None)
     z = x + r * (a @ w["w_o"].T)
     h2, rstd2 = rmsnorm(z, w["g_mlp"], eps)
     uv = h2 @ w["w_gate_up"].T
-    u, vv = uv[:, :f], uv[:, f:]
-    s = silu(u) * vv
+    if kind == 1:
+        u, vv = uv, None
+        s = relu2(u)
+    else:
+        u, vv = uv[:, :f], uv[:, f:]
+        s = silu(u) * vv
     x_next = z + r * (s @ w["w_down"].T)
     cache = dict(x=x, h1=h1, rstd1=rstd1, q=q, k=k, v=v, a=a, probs=probs,
-                 z=z, h2=h2, rstd2=rstd2, u=u, vv=vv, s=s)
+                 z=z, h2=h2, rstd2=rstd2, u=u, vv=vv, s=s, kind=kind)
     return x_next, cache
 
 
@@ -116,9 +154,12 @@ def backward(cache, g, w, r, n_heads):
     gy = r * g
     d_down = gy.T @ c["s"]
     gs = gy @ w["w_down"]
-    gu = gs * c["vv"] * silu_grad(c["u"])
-    gvv = gs * silu(c["u"])
-    guv = np.concatenate([gu, gvv], axis=1)
+    if c["kind"] == 1:
+        guv = gs * relu2_grad(c["u"])
+    else:
+        gu = gs * c["vv"] * silu_grad(c["u"])
+        gvv = gs * silu(c["u"])
+        guv = np.concatenate([gu, gvv], axis=1)
     d_gate_up = guv.T @ c["h2"]
     gh2 = guv @ w["w_gate_up"]
     gz_norm, d_g_mlp = rmsnorm_bwd(c["z"], w["g_mlp"], c["rstd2"], gh2)

@@ -34,6 +34,7 @@ class Config:
     rms_eps: float = 1e-5
     rescale: bool = True
     res_scale: float = 1.0
+    block_kind: int = 0     # 0: RMSNorm/MHA/SwiGLU; 1: ALiBi + squared ReLU (block.py)
 
 
 def residual_scale(p, cfg):
@@ -58,7 +59,7 @@ def layer_forward(X, w, keep_row, p, cfg):
             continue                      # dropped: H^{l+1}[b] = H^l[b]
         if r is None:
             r = residual_scale(p, cfg)
-        X_next[b], caches[b] = block.forward(X[b], w, r, cfg.n_heads, cfg.rms_eps)
+        X_next[b], caches[b] = block.forward(X[b], w, r, cfg.n_heads, cfg.rms_eps, cfg.block_kind)
     return X_next, dict(caches=caches, r=r, w=w)
 
 
