@@ -14,7 +14,12 @@ every iteration, so each iteration draws fresh masks.  A sweep over p_max in
 value = effective tokens/s = batch*seq / step time (every token of the
 batch, dropped or not, counts: the step trains the whole batch).
 Executed FLOPs per step = F_sl * sum_l kept_l with
-F_sl = 3 * [2*S*(4 d^2 + 3 d d_ff) + 2 d S (S+1)] per kept (sequence, layer).
+F_sl = 3 * [2*S*(4 d^2 + n_ffn d d_ff) + 2 d S (S+1)] per kept (sequence,
+layer), n_ffn = 3 (SwiGLU) or 2 (squared ReLU).
+
+--workload paper_3p9b runs the paper's own block (ALiBi attention, squared
+ReLU) at its 3.9B architecture (d 2048, 40 layers, 16 heads of 128, d_ff
+16384), same sequence length, batch and rates.
 """
 import argparse
 import json
@@ -42,10 +47,10 @@ KERNEL_SOURCES = {"ld_gemm": "paper_2609_05275_amd/csrc/k_gemm.hip",
                   "ld_attn": "paper_2609_05275_amd/csrc/k_attn.hip"}
 
 
-def traffic_record(kernel):
+def traffic_record(kernel, workload):
     """HBM bytes per launch of `kernel` from its committed counter summary,
     or None when there is none or the kernel's source changed since."""
-    rec = profsum.read_traffic(os.path.join(ROOT, "profiles", f"{kernel}_1b_traffic.md"))
+    rec = profsum.read_traffic(os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md"))
     if not rec or rec.get("kernel") != kernel:
         return None
     src = next((v for k, v in KERNEL_SOURCES.items() if kernel.startswith(k)), None)
@@ -71,13 +76,15 @@ def copy_calibration(mib):
 
 def f_sl(sh):
     S, d, f = sh.seq, sh.d_model, sh.d_ff
-    return 3.0 * (2.0 * S * (4 * d * d + 3 * d * f) + 2.0 * d * S * (S + 1))
+    n_ffn = 3 if sh.kind == 0 else 2
+    return 3.0 * (2.0 * S * (4 * d * d + n_ffn * d * f) + 2.0 * d * S * (S + 1))
 
 
 class Stack:
     def __init__(self, sh, dev):
         self.sh, self.dev = sh, dev
-        self.cfg = ld.config(sh.batch, sh.seq, sh.d_model, sh.n_heads, sh.d_ff, ld.LD_BF16)
+        self.cfg = ld.config(sh.batch, sh.seq, sh.d_model, sh.n_heads, sh.d_ff, ld.LD_BF16,
+                             block_kind=sh.kind)
         L = sh.n_layers
         self.W = [inp.device_layer_weights(sh, l, dev) for l in range(L)]
         self.dW = [{k: torch.empty(s, dtype=torch.float32, device=dev)
@@ -133,7 +140,7 @@ def cpu_baseline(sh, target_s=15.0):
     g = inp.device_upstream_grad(sh, "cuda:0")[0].to("cpu", _t.float64).numpy()
     n, t0 = 0, time.perf_counter()
     while True:
-        _, cache = block.forward(x, w, 1.0 / 0.9, sh.n_heads, 1e-5)
+        _, cache = block.forward(x, w, 1.0 / 0.9, sh.n_heads, 1e-5, sh.kind)
         block.backward(cache, g, w, 1.0 / 0.9, sh.n_heads)
         n += 1
         el = time.perf_counter() - t0
@@ -151,6 +158,7 @@ def main():
     ap.add_argument("--p-max", type=float, default=0.2)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--workload", default="1b", choices=["1b", "paper_3p9b"])
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run the traffic-counter calibration copy of this size first")
     ap.add_argument("--prof-kernel", default=None,
@@ -164,7 +172,7 @@ def main():
 
     if args.copy_calib_mib > 0:
         copy_calibration(args.copy_calib_mib)
-    sh = inp.SHAPES["1b"]
+    sh = inp.SHAPES[args.workload]
     dev = "cuda:0"
     st = Stack(sh, dev)
     fsl = f_sl(sh)
@@ -206,7 +214,7 @@ def main():
           flush=True)
     exec_tflops = fsl * np.mean(kept) / (ms * 1e-3) / 1e12
     achieved = pr["flops"] / (pr["ms"] * 1e-3) / 1e12 if pr["ms"] > 0 else 0.0
-    trec = traffic_record(prof_kernel)
+    trec = traffic_record(prof_kernel, args.workload)
 
     sweep = []
     if not args.no_sweep:
@@ -235,12 +243,21 @@ def main():
         cpu_step_s = t_unit * np.mean(kept)
         cpu = {"value": round(tokens / cpu_step_s, 3), "unit": "tokens/s", "cores": threads,
                "kind": "oracle",
-               "sample": f"{n} x one sequence through one 1B-shape layer forward+backward "
+               "sample": f"{n} x one sequence through one {args.workload} layer forward+backward "
                          f"(float64 numpy oracle, {t_unit:.2f} s each), scaled by the mean kept "
                          f"(sequence, layer) count per step {np.mean(kept):.1f}"}
 
+    if args.workload == "1b":
+        metric = "effective tokens/s per fwd+bwd step (1B-shape stack, ILD p_max 0.2)"
+        wdesc = ("1B-shape decoder stack: L=16, d_model=2048, heads=16x128, d_ff=5504 SwiGLU, "
+                 "seq=2048, batch=8; ILD p_max=0.2 at the end of a 0..1000 increasing ramp")
+    else:
+        metric = "effective tokens/s per fwd+bwd step (paper 3.9B-architecture stack, ILD p_max 0.2)"
+        wdesc = ("paper block (ALiBi, squared ReLU) at the 3.9B architecture: L=40, d_model=2048, "
+                 "heads=16x128, d_ff=16384, seq=2048, batch=8; ILD p_max=0.2 at the end of a "
+                 "0..1000 increasing ramp")
     out = {
-        "metric": "effective tokens/s per fwd+bwd step (1B-shape stack, ILD p_max 0.2)",
+        "metric": metric,
         "value": round(tokens / (ms * 1e-3), 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -252,9 +269,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "1B-shape decoder stack: L=16, d_model=2048, heads=16x128, "
-                               "d_ff=5504 SwiGLU, seq=2048, batch=8; ILD p_max=0.2 at the end "
-                               "of a 0..1000 increasing ramp",
+        "config": {"workload": wdesc,
                    "global_batch": sh.batch, "seq_len": sh.seq, "parallelism": "none (1 GPU)"},
         "executed_tflops": round(exec_tflops, 1),
         "mfma_frac_executed": round(exec_tflops / PEAK_BF16_TFLOPS, 4),

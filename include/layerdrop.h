@@ -67,18 +67,28 @@ typedef enum { LD_F32 = 0, LD_BF16 = 1 } ld_dtype;
  *   rms_eps: RMSNorm epsilon (the paper fixes none; 1e-5 is the default).
  *   rescale: 1 -> r = res_scale / (1 - p); 0 -> r = res_scale.
  *   res_scale: constant residual-branch multiplier (the depth multiplier of
- *   the paper's parameterisation table); 1 for plain layer dropout. */
+ *   the paper's parameterisation table); 1 for plain layer dropout.
+ *   block_kind: LD_BLOCK_SWIGLU (0): pre-norm RMSNorm, causal multi-head
+ *   attention, SwiGLU feed-forward.  LD_BLOCK_ALIBI_RELU2 (1): the block of
+ *   the paper's experiments (Experimental Setup: ALiBi position bias,
+ *   squared-ReLU activation): pre-norm RMSNorm, causal attention whose
+ *   scaled scores get the ALiBi bias -m_h (i - j) (query i, key j <= i, head
+ *   slope m_h of ld_alibi_slope), and the feed-forward relu(h W_up^T)^2 W_down^T. */
+typedef enum { LD_BLOCK_SWIGLU = 0, LD_BLOCK_ALIBI_RELU2 = 1 } ld_block_kind;
+
 typedef struct {
   int32_t batch, seq, d_model, n_heads, d_ff;
   int32_t dtype;
   float rms_eps;
   int32_t rescale;
   float res_scale;
+  int32_t block_kind;
 } ld_config;
 
 /* Device pointers to one layer's parameters (element type cfg->dtype):
- * g_attn [d], w_qkv [3d, d], w_o [d, d], g_mlp [d], w_gate_up [2f, d],
- * w_down [d, f].  Read only. */
+ * g_attn [d], w_qkv [3d, d], w_o [d, d], g_mlp [d], w_down [d, f], and
+ * w_gate_up [2f, d] (gate rows then up rows) for LD_BLOCK_SWIGLU or [f, d]
+ * (W_up) for LD_BLOCK_ALIBI_RELU2.  Read only. */
 typedef struct {
   const void *g_attn, *w_qkv, *w_o, *g_mlp, *w_gate_up, *w_down;
 } ld_weights;
@@ -208,6 +218,13 @@ int ld_rmsnorm_bwd(int32_t dtype, int32_t rows, int32_t d, const void* x, const 
                    const float* rstd, const void* gy, const void* gres, void* gx, float* dg,
                    void* ws, size_t ws_bytes, void* stream);
 
+/* s = relu(u)^2, u and s device [rows, f] (squared ReLU, cited in the
+ * paper's Experimental Setup). */
+int ld_relu2_fwd(int32_t dtype, int32_t rows, int32_t f, const void* u, void* s, void* stream);
+/* gu = gs * 2 relu(u), device [rows, f]. */
+int ld_relu2_bwd(int32_t dtype, int32_t rows, int32_t f, const void* u, const void* gs, void* gu,
+                 void* stream);
+
 /* s = silu(u) * v with uv = [u | v] device [rows, 2f], s device [rows, f]. */
 int ld_swiglu_fwd(int32_t dtype, int32_t rows, int32_t f, const void* uv, void* s, void* stream);
 /* guv = [gs * v * silu'(u) | gs * silu(u)], device [rows, 2f]. */
@@ -232,21 +249,30 @@ int ld_gemm(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int3
             int32_t c_f32, float alpha, const void* R, int32_t ldr, void* ws, size_t ws_bytes,
             void* stream);
 
+/* ALiBi slope of head h of n_heads (ALiBi paper, Press et al. 2022, §3):
+ * with n the largest power of two <= n_heads, m_h = 2^(-8(h+1)/n) for
+ * h < n, and m_h = 2^(-4(2(h-n)+1)/n) for the remaining heads (every other
+ * slope of the 2n-head sequence).  Host function; returns 0 for h outside
+ * [0, n_heads) or n_heads < 1. */
+float ld_alibi_slope(int32_t h, int32_t n_heads);
+
 /* Causal multi-head attention over n_seq independent sequences.
  *   qkv: device [n_seq*S, 3*H*dh] as produced by x W_qkv^T;
- *   o:   device [n_seq*S, H*dh]; o[s, h] = softmax_j<=s(q_s.k_j / sqrt(dh)) v
- *   lse: device float32 [n_seq, H, S], natural-log sum-exp of the scaled
- *        scores of each row (saved for the backward). */
+ *   o:   device [n_seq*S, H*dh]; o[s, h] = softmax_j<=s(q_s.k_j / sqrt(dh)
+ *        - alibi * m_h (s - j)) v
+ *   lse: device float32 [n_seq, H, S], natural-log sum-exp of the biased
+ *        scaled scores of each row (saved for the backward).
+ *   alibi: 0 or 1. */
 int ld_attn_fwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
-                const void* qkv, void* o, float* lse, void* stream);
+                int32_t alibi, const void* qkv, void* o, float* lse, void* stream);
 
 /* Backward of ld_attn_fwd: gqkv (device [n_seq*S, 3*H*dh]) from go
  * (device [n_seq*S, H*dh]); the probabilities are recomputed from lse.
  * ws: device scratch of ld_attn_bwd_ws_bytes(n_seq, seq, n_heads) bytes. */
 size_t ld_attn_bwd_ws_bytes(int32_t n_seq, int32_t seq, int32_t n_heads);
 int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
-                const void* qkv, const void* o, const float* lse, const void* go, void* gqkv,
-                void* ws, size_t ws_bytes, void* stream);
+                int32_t alibi, const void* qkv, const void* o, const float* lse, const void* go,
+                void* gqkv, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------- profiling
  * Per-kernel timing with HIP events recorded on the launch stream around

@@ -31,7 +31,8 @@ class LdError(RuntimeError):
 class ld_config(C.Structure):
     _fields_ = [("batch", C.c_int32), ("seq", C.c_int32), ("d_model", C.c_int32),
                 ("n_heads", C.c_int32), ("d_ff", C.c_int32), ("dtype", C.c_int32),
-                ("rms_eps", C.c_float), ("rescale", C.c_int32), ("res_scale", C.c_float)]
+                ("rms_eps", C.c_float), ("rescale", C.c_int32), ("res_scale", C.c_float),
+                ("block_kind", C.c_int32)]
 
 
 class ld_weights(C.Structure):
@@ -68,15 +69,18 @@ _SIGS = {
     "ld_rmsnorm_bwd_ws_bytes": (_sz, [_i32, _i32]),
     "ld_rmsnorm_bwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
                                  _vp]),
+    "ld_relu2_fwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp]),
+    "ld_relu2_bwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ld_alibi_slope": (C.c_float, [_i32, _i32]),
     "ld_swiglu_fwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp]),
     "ld_swiglu_bwd": (C.c_int, [_i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "ld_gemm_ws_bytes": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32]),
     "ld_gemm": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _i32, _vp, _i32, _vp, _i32,
                           _i32, _f32, _vp, _i32, _vp, _sz, _vp]),
-    "ld_attn_fwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ld_attn_fwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "ld_attn_bwd_ws_bytes": (_sz, [_i32, _i32, _i32]),
-    "ld_attn_bwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz,
-                              _vp]),
+    "ld_attn_bwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                              _sz, _vp]),
     "ld_prof_start": (C.c_int, [C.c_char_p]),
     "ld_prof_stop": (C.c_int, []),
     "ld_prof_result": (C.c_int, [C.POINTER(_i64), C.POINTER(C.c_double), C.POINTER(C.c_double),
@@ -128,9 +132,9 @@ def _dtype_code(t):
 
 
 def config(batch, seq, d_model, n_heads, d_ff, dtype=LD_BF16, rms_eps=1e-5, rescale=True,
-           res_scale=1.0):
+           res_scale=1.0, block_kind=0):
     return ld_config(batch, seq, d_model, n_heads, d_ff, dtype, rms_eps, int(bool(rescale)),
-                     res_scale)
+                     res_scale, block_kind)
 
 
 def weights(w):
@@ -220,6 +224,21 @@ def ld_rmsnorm_bwd(x, g, rstd, gy, gres, gx, dg, ws, stream=None):
                                ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def ld_relu2_fwd(u, s, stream=None):
+    rows, f = u.shape
+    _check(_lib.ld_relu2_fwd(_dtype_code(u), rows, f, _ptr(u), _ptr(s), _stream(stream)))
+
+
+def ld_relu2_bwd(u, gs, gu, stream=None):
+    rows, f = u.shape
+    _check(_lib.ld_relu2_bwd(_dtype_code(u), rows, f, _ptr(u), _ptr(gs), _ptr(gu),
+                             _stream(stream)))
+
+
+def ld_alibi_slope(h, n_heads):
+    return _lib.ld_alibi_slope(h, n_heads)
+
+
 def ld_swiglu_fwd(uv, s, stream=None):
     rows, f2 = uv.shape
     _check(_lib.ld_swiglu_fwd(_dtype_code(uv), rows, f2 // 2, _ptr(uv), _ptr(s), _stream(stream)))
@@ -244,18 +263,18 @@ def ld_gemm(a_kcontig, b_kcontig, M, N, K, A, lda, B, ldb, Cm, ldc, alpha=1.0, R
                         _stream(stream)))
 
 
-def ld_attn_fwd(n_seq, seq, n_heads, d_head, qkv, o, lse, stream=None):
-    _check(_lib.ld_attn_fwd(_dtype_code(qkv), n_seq, seq, n_heads, d_head, _ptr(qkv), _ptr(o),
-                            _ptr(lse), _stream(stream)))
+def ld_attn_fwd(n_seq, seq, n_heads, d_head, qkv, o, lse, stream=None, alibi=0):
+    _check(_lib.ld_attn_fwd(_dtype_code(qkv), n_seq, seq, n_heads, d_head, int(alibi), _ptr(qkv),
+                            _ptr(o), _ptr(lse), _stream(stream)))
 
 
 def ld_attn_bwd_ws_bytes(n_seq, seq, n_heads):
     return _lib.ld_attn_bwd_ws_bytes(n_seq, seq, n_heads)
 
 
-def ld_attn_bwd(n_seq, seq, n_heads, d_head, qkv, o, lse, go, gqkv, ws, stream=None):
-    _check(_lib.ld_attn_bwd(_dtype_code(qkv), n_seq, seq, n_heads, d_head, _ptr(qkv), _ptr(o),
-                            _ptr(lse), _ptr(go), _ptr(gqkv), _ptr(ws),
+def ld_attn_bwd(n_seq, seq, n_heads, d_head, qkv, o, lse, go, gqkv, ws, stream=None, alibi=0):
+    _check(_lib.ld_attn_bwd(_dtype_code(qkv), n_seq, seq, n_heads, d_head, int(alibi), _ptr(qkv),
+                            _ptr(o), _ptr(lse), _ptr(go), _ptr(gqkv), _ptr(ws),
                             ws.numel() * ws.element_size(), _stream(stream)))
 
 

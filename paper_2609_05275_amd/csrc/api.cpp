@@ -92,6 +92,8 @@ struct ProfScope {
 struct Dims {
   int64_t B, S, d, H, dh, f, T, es;
   int dtype;
+  int kind;    // ld_block_kind
+  int64_t fw;  // width of the gate_up GEMM output: 2f (SwiGLU) or f (squared ReLU)
 };
 
 int check_cfg(const ld_config* c, Dims* out) {
@@ -102,6 +104,8 @@ int check_cfg(const ld_config* c, Dims* out) {
   if (c->d_model % c->n_heads) return fail(LD_E_SHAPE, "d_model %% n_heads != 0");
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return fail(LD_E_INVALID, "rms_eps must be > 0");
   if (!std::isfinite(c->res_scale)) return fail(LD_E_INVALID, "res_scale must be finite");
+  if (c->block_kind != LD_BLOCK_SWIGLU && c->block_kind != LD_BLOCK_ALIBI_RELU2)
+    return fail(LD_E_INVALID, "unknown block_kind %d", c->block_kind);
   const int dh = c->d_model / c->n_heads;
   if (c->dtype == LD_BF16) {
     if (dh != 64 && dh != 128) return fail(LD_E_UNSUPPORTED, "bf16 needs d_head 64 or 128, got %d", dh);
@@ -127,6 +131,8 @@ int check_cfg(const ld_config* c, Dims* out) {
     out->T = T;
     out->es = c->dtype == LD_BF16 ? 2 : 4;
     out->dtype = c->dtype;
+    out->kind = c->block_kind;
+    out->fw = c->block_kind == LD_BLOCK_SWIGLU ? 2ll * c->d_ff : c->d_ff;
   }
   return LD_OK;
 }
@@ -184,7 +190,7 @@ ActLayout act_layout(const Dims& D) {
   L.zk = take(es * T * D.d);
   L.rstd2 = take(4 * T);
   L.h2 = take(es * T * D.d);
-  L.uv = take(es * T * 2 * D.f);
+  L.uv = take(es * T * D.fw);
   L.s = take(es * T * D.f);
   L.total = o;
   return L;
@@ -213,7 +219,7 @@ MaskLayout mask_layout(int64_t L, int64_t B) {
 // Split-K float32 scratch for the weight-gradient GEMMs (largest of the four).
 size_t splitk_bytes(const Dims& D) {
   if (D.dtype != LD_BF16) return 0;
-  const int64_t shapes[4][2] = {{D.d, D.f}, {2 * D.f, D.d}, {D.d, D.d}, {3 * D.d, D.d}};
+  const int64_t shapes[4][2] = {{D.d, D.f}, {D.fw, D.d}, {D.d, D.d}, {3 * D.d, D.d}};
   size_t best = 0;
   for (const auto& sh : shapes) {
     GemmArgs g;
@@ -244,7 +250,7 @@ BwdLayout bwd_layout(const Dims& D) {
   const size_t es = D.es, T = D.T;
   L.gk = take(es * T * D.d);
   L.gs = take(es * T * D.f);
-  L.guv = take(es * T * 2 * D.f);
+  L.guv = take(es * T * D.fw);
   L.gh = take(es * T * D.d);
   L.gz = take(es * T * D.d);
   L.ga = take(es * T * D.d);
@@ -375,6 +381,7 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
     a.H = static_cast<int32_t>(D.H);
     a.dh = static_cast<int32_t>(D.dh);
     a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.dh)));
+    a.alibi = D.kind == LD_BLOCK_ALIBI_RELU2;
     ProfScope ps(attn_fwd_kernel_name(dt), s);
     if ((e = launch_attn_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "attn_fwd: %s", hipGetErrorString(e));
     ps.end(2.0 * hc * D.d * D.S * (D.S + 1.0), D.es * hm * D.d * 4.0);
@@ -412,7 +419,7 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
     if ((e = launch_rmsnorm_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
     ps.end(0, D.es * hm * D.d * 2.0 + 4.0 * hm);
   }
-  // [u v] = h2 W_gate_up^T
+  // [u v] = h2 W_gate_up^T (SwiGLU), u = h2 W_up^T (squared ReLU)
   {
     GemmArgs g = gemm_args();
     g.A = act.at(act.L.h2);
@@ -420,23 +427,29 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
     g.B = w.w_gate_up;
     g.ldb = D.d;
     g.C = act.at(act.L.uv);
-    g.ldc = 2 * D.f;
-    g.N = static_cast<int32_t>(2 * D.f);
+    g.ldc = D.fw;
+    g.N = static_cast<int32_t>(D.fw);
     g.K = static_cast<int32_t>(D.d);
     g.dev_count = mv.count;
     g.count_mult = static_cast<int32_t>(D.S);
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
   }
-  // s = silu(u) * v
+  // s = silu(u) * v  or  s = relu(u)^2
   {
     EltArgs a{};
     a.a = act.at(act.L.uv);
     a.out = act.at(act.L.s);
     a.rc = {mv.count, static_cast<int32_t>(D.S), T};
     a.f = static_cast<int32_t>(D.f);
-    ProfScope ps("ld_swiglu_fwd_k", s);
-    if ((e = launch_swiglu_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "swiglu_fwd: %s", hipGetErrorString(e));
-    ps.end(0, D.es * hm * D.f * 3.0);
+    if (D.kind == LD_BLOCK_SWIGLU) {
+      ProfScope ps("ld_swiglu_fwd_k", s);
+      if ((e = launch_swiglu_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "swiglu_fwd: %s", hipGetErrorString(e));
+      ps.end(0, D.es * hm * D.f * 3.0);
+    } else {
+      ProfScope ps("ld_relu2_fwd_k", s);
+      if ((e = launch_relu2_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "relu2_fwd: %s", hipGetErrorString(e));
+      ps.end(0, D.es * hm * D.f * 2.0);
+    }
   }
   // X[kept rows] = zk + r * (s W_down^T)  (scatter into the residual stream)
   {
@@ -519,7 +532,7 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     g.count_dim = 1;
     if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s, SK, BL.splitk_bytes, T)) return rc;
   }
-  // guv = SwiGLU backward
+  // guv = SwiGLU backward, or gu = squared-ReLU backward
   {
     EltArgs a{};
     a.a = act.at(act.L.uv);
@@ -527,41 +540,47 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     a.out = W(BL.guv);
     a.rc = {mv.count, S, T};
     a.f = static_cast<int32_t>(D.f);
-    ProfScope ps("ld_swiglu_bwd_k", s);
-    if ((e = launch_swiglu_bwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "swiglu_bwd: %s", hipGetErrorString(e));
-    ps.end(0, D.es * hm * D.f * 5.0);
+    if (D.kind == LD_BLOCK_SWIGLU) {
+      ProfScope ps("ld_swiglu_bwd_k", s);
+      if ((e = launch_swiglu_bwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "swiglu_bwd: %s", hipGetErrorString(e));
+      ps.end(0, D.es * hm * D.f * 5.0);
+    } else {
+      ProfScope ps("ld_relu2_bwd_k", s);
+      if ((e = launch_relu2_bwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "relu2_bwd: %s", hipGetErrorString(e));
+      ps.end(0, D.es * hm * D.f * 3.0);
+    }
   }
   // gh2 = guv W_gate_up   [M, d]
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.guv);
-    g.lda = 2 * D.f;
+    g.lda = D.fw;
     g.B = w.w_gate_up;
     g.ldb = D.d;
     g.C = W(BL.gh);
     g.ldc = D.d;
     g.N = static_cast<int32_t>(D.d);
-    g.K = static_cast<int32_t>(2 * D.f);
+    g.K = static_cast<int32_t>(D.fw);
     g.dev_count = mv.count;
     g.count_mult = S;
-    if (int rc = run_gemm(dt, 1, 0, g, T, hm, 2 * D.f, s)) return rc;
+    if (int rc = run_gemm(dt, 1, 0, g, T, hm, D.fw, s)) return rc;
   }
-  // dW_gate_up = guv^T h2   [2f, d]
+  // dW_gate_up = guv^T h2   [fw, d]
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.guv);
-    g.lda = 2 * D.f;
+    g.lda = D.fw;
     g.B = act.at(act.L.h2);
     g.ldb = D.d;
     g.C = dw.w_gate_up;
     g.ldc = D.d;
     g.c_f32 = 1;
-    g.M = static_cast<int32_t>(2 * D.f);
+    g.M = static_cast<int32_t>(D.fw);
     g.N = static_cast<int32_t>(D.d);
     g.dev_count = mv.count;
     g.count_mult = S;
     g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, 2 * D.f, 2 * D.f, hm, s, SK, BL.splitk_bytes, T)) return rc;
+    if (int rc = run_gemm(dt, 0, 0, g, D.fw, D.fw, hm, s, SK, BL.splitk_bytes, T)) return rc;
   }
   // gz = gk + RMSNorm_bwd(zk, g_mlp, gh2); dg_mlp
   {
@@ -629,6 +648,7 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     a.H = static_cast<int32_t>(D.H);
     a.dh = static_cast<int32_t>(D.dh);
     a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.dh)));
+    a.alibi = D.kind == LD_BLOCK_ALIBI_RELU2;
     // algorithmic FLOPs of the backward (2x the forward), split over the two
     // MFMA kernels in proportion to the products each forms (4 and 3)
     const double fl_bwd = 4.0 * hc * D.d * D.S * (D.S + 1.0);
@@ -1035,6 +1055,42 @@ int ld_swiglu_bwd(int32_t dtype, int32_t rows, int32_t f, const void* uv, const 
   return LD_OK;
 }
 
+int ld_relu2_fwd(int32_t dtype, int32_t rows, int32_t f, const void* u, void* s, void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (rows < 0 || f < 1 || f % (dtype == LD_BF16 ? 8 : 4)) return fail(LD_E_SHAPE, "bad shape");
+  if (rows == 0) return LD_OK;
+  if (!u || !s) return fail(LD_E_INVALID, "NULL pointer");
+  EltArgs a{};
+  a.a = u;
+  a.out = s;
+  a.rc = {nullptr, 1, rows};
+  a.f = f;
+  hipError_t e = launch_relu2_fwd(dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "relu2_fwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+int ld_relu2_bwd(int32_t dtype, int32_t rows, int32_t f, const void* u, const void* gs, void* gu,
+                 void* stream) {
+  t_err.clear();
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (rows < 0 || f < 1 || f % (dtype == LD_BF16 ? 8 : 4)) return fail(LD_E_SHAPE, "bad shape");
+  if (rows == 0) return LD_OK;
+  if (!u || !gs || !gu) return fail(LD_E_INVALID, "NULL pointer");
+  EltArgs a{};
+  a.a = u;
+  a.b = gs;
+  a.out = gu;
+  a.rc = {nullptr, 1, rows};
+  a.f = f;
+  hipError_t e = launch_relu2_bwd(dtype, a, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "relu2_bwd: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+float ld_alibi_slope(int32_t h, int32_t n_heads) { return alibi_slope(h, n_heads); }
+
 size_t ld_gemm_ws_bytes(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int32_t N,
                         int32_t K, int32_t ldc, int32_t c_f32) {
   if (M < 1 || N < 1 || K < 0) return 0;
@@ -1090,13 +1146,14 @@ int ld_gemm(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int3
 }
 
 int ld_attn_fwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
-                const void* qkv, void* o, float* lse, void* stream) {
+                int32_t alibi, const void* qkv, void* o, float* lse, void* stream) {
   t_err.clear();
   if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
   if (n_seq < 0 || seq < 1 || n_heads < 1) return fail(LD_E_SHAPE, "bad shape");
   if (dtype == LD_BF16 ? (d_head != 64 && d_head != 128) || seq % 64
                        : (d_head != 16 && d_head != 32 && d_head != 64))
     return fail(LD_E_UNSUPPORTED, "unsupported d_head/seq");
+  if (alibi != 0 && alibi != 1) return fail(LD_E_INVALID, "alibi must be 0 or 1");
   if (n_seq == 0) return LD_OK;
   if (!qkv || !o || !lse) return fail(LD_E_INVALID, "NULL pointer");
   AttnArgs a{};
@@ -1108,6 +1165,7 @@ int ld_attn_fwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int3
   a.H = n_heads;
   a.dh = d_head;
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(d_head)));
+  a.alibi = alibi;
   hipError_t e = launch_attn_fwd(dtype, a, as_stream(stream));
   if (e != hipSuccess) return fail(LD_E_HIP, "attn_fwd: %s", hipGetErrorString(e));
   return LD_OK;
@@ -1119,14 +1177,15 @@ size_t ld_attn_bwd_ws_bytes(int32_t n_seq, int32_t seq, int32_t n_heads) {
 }
 
 int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
-                const void* qkv, const void* o, const float* lse, const void* go, void* gqkv,
-                void* ws, size_t ws_bytes, void* stream) {
+                int32_t alibi, const void* qkv, const void* o, const float* lse, const void* go,
+                void* gqkv, void* ws, size_t ws_bytes, void* stream) {
   t_err.clear();
   if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
   if (n_seq < 0 || seq < 1 || n_heads < 1) return fail(LD_E_SHAPE, "bad shape");
   if (dtype == LD_BF16 ? (d_head != 64 && d_head != 128) || seq % 64
                        : (d_head != 16 && d_head != 32 && d_head != 64))
     return fail(LD_E_UNSUPPORTED, "unsupported d_head/seq");
+  if (alibi != 0 && alibi != 1) return fail(LD_E_INVALID, "alibi must be 0 or 1");
   if (n_seq == 0) return LD_OK;
   if (!qkv || !o || !lse || !go || !gqkv || !ws) return fail(LD_E_INVALID, "NULL pointer");
   if (ws_bytes < ld_attn_bwd_ws_bytes(n_seq, seq, n_heads)) return fail(LD_E_WORKSPACE, "workspace too small");
@@ -1142,6 +1201,7 @@ int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int3
   a.H = n_heads;
   a.dh = d_head;
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(d_head)));
+  a.alibi = alibi;
   hipError_t e = launch_attn_bwd(dtype, a, as_stream(stream));
   if (e != hipSuccess) return fail(LD_E_HIP, "attn_bwd: %s", hipGetErrorString(e));
   return LD_OK;

@@ -179,7 +179,9 @@ __device__ __forceinline__ void kv_store(const KvRegs<DH, NT>& r, bf16* Ks, bf16
 // SIMD).  K/V blocks of 64 keys are double buffered in LDS and the next block
 // is fetched into registers while the current one is used, so there is one
 // barrier per block.
-template <int DH, int RPW>
+// AL: add the ALiBi bias to the scaled scores (in log2 units: slope * log2e
+// per position of distance).
+template <int DH, int RPW, bool AL>
 __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a) {
   constexpr int NSB = RPW / 32, NT = 64 * (FWQ / RPW);
   constexpr int KT = FKV * (DH + 8), VT = DH * FKV;
@@ -200,6 +202,7 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
   const bf16* Kp = base + static_cast<int64_t>(H) * DH + head * DH;
   const bf16* Vp = base + 2ll * H * DH + head * DH;
   const float sl2 = a.scale * kLog2e;
+  const float al2 = AL ? alibi_slope(head, H) * kLog2e : 0.f;
 
   bf16x8 qf[NSB][DH / 16];
   floatx16 o[NSB][DH / 32];
@@ -251,12 +254,14 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
 #pragma unroll
       for (int sb = 0; sb < NSB; ++sb) {
         const int qrow = qw + sb * 32 + cl;
+        const float ab = al2 * static_cast<float>(k0 + 4 * hf - qrow);  // bias of the lane's first key
         float mx = -INFINITY;
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             float x = sc[sb][kh][v] * sl2;
+            if constexpr (AL) x += fmaf(al2, static_cast<float>(kh * 32 + 8 * (v >> 2) + (v & 3)), ab);
             if (diag) {
               const int key = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
               if (key > qrow) x = -INFINITY;
@@ -458,7 +463,7 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 // after the other so only one half's scores are live.  Fragment addresses
 // are per-lane offsets computed once; the loop has no branch around its
 // MFMAs.
-template <int DH, int NW = dkdv_waves<DH>()>
+template <int DH, int NW, bool AL>
 __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   constexpr int BKEYS = 32 * NW, SB = dk_stage_bytes<DH>(), NL = dk_loads<DH, NW>();
   constexpr int RPI = 512 / DH, LPR = 64 / RPI;   // rows per 1 KB load, lanes per row
@@ -484,6 +489,7 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   const float* lse = a.lse + (static_cast<int64_t>(seq) * H + head) * S;
   const float* del = a.delta + (static_cast<int64_t>(seq) * H + head) * S;
   const float sl2 = a.scale * kLog2e;
+  const float al2 = AL ? alibi_slope(head, H) * kLog2e : 0.f;
 
   bf16x8 kf[DH / 16], vf[DH / 16];
 #pragma unroll
@@ -581,11 +587,14 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
         d4[g] = *reinterpret_cast<const float4*>(dl + qh * 32 + 8 * g + 4 * hf);
       }
       bf16x8 pb[2], dsb[2];
+      const float ab = al2 * static_cast<float>(key - qb - qh * 32 - 4 * hf);  // bias at the lane's first query
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int ql = qh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
         const float lv = (&l4[v >> 2].x)[v & 3], dv_ = (&d4[v >> 2].x)[v & 3];
-        float p = __builtin_amdgcn_exp2f(sc[v] * sl2 - lv * kLog2e);
+        float x = sc[v] * sl2 - lv * kLog2e;
+        if constexpr (AL) x += fmaf(-al2, static_cast<float>(8 * (v >> 2) + (v & 3)), ab);
+        float p = __builtin_amdgcn_exp2f(x);
         p = key > qb + ql ? 0.f : p;
         pb[v >> 3][v & 7] = static_cast<bf16>(p);
         dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dv_));
@@ -641,7 +650,7 @@ constexpr int DQ_ROWS = 256;  // query rows per dQ workgroup (8 waves x 32)
 // prefetched in registers.  Scores are formed transposed (S^T = K Q^T), so the
 // query's log-sum-exp and delta are per lane and dS^T feeds dQ^T += K^T dS^T
 // directly.
-template <int DH>
+template <int DH, bool AL>
 __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   constexpr int DT = FKV * (DH + 8), TT = DH * FKV;
   constexpr int STAGE = 2 * DT + TT;  // Ks, Vs, Kt
@@ -662,6 +671,7 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   const bf16* Vp = base + 2ll * H * DH + head * DH;
   const bf16* dOp = static_cast<const bf16*>(a.go) + static_cast<int64_t>(seq) * S * ldo + head * DH;
   const float sl2 = a.scale * kLog2e;
+  const float al2 = AL ? alibi_slope(head, H) * kLog2e : 0.f;
 
   const bool qok = qrow < S;
   const int64_t srow = (static_cast<int64_t>(seq) * H + head) * S + (qok ? qrow : 0);
@@ -713,9 +723,12 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
           dpt = mfma(load8(Vs + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), of[ks], dpt);
         }
         bf16x8 dsb[2];
+        const float ab = al2 * static_cast<float>(k0 + kh * 32 + 4 * hf - qrow);  // bias of the lane's first key
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float p = __builtin_amdgcn_exp2f(st[v] * sl2 - lse2);
+          float x = st[v] * sl2 - lse2;
+          if constexpr (AL) x += fmaf(al2, static_cast<float>(8 * (v >> 2) + (v & 3)), ab);
+          float p = __builtin_amdgcn_exp2f(x);
           if (diag) {
             const int keyi = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
             if (keyi > qrow) p = 0.f;
@@ -764,6 +777,7 @@ __global__ __launch_bounds__(64) void ld_attn_fwd_f32(AttnArgs a) {
   __shared__ float Ks[ST][DH], Vs[ST][DH];
   const int S = a.S, H = a.H;
   const int head = blockIdx.y, seq = blockIdx.z;
+  const float al = a.alibi ? alibi_slope(head, H) : 0.f;  // ALiBi slope (natural units)
   if (seq >= seq_count(a)) return;
   const int q0 = blockIdx.x * ST, q = q0 + threadIdx.x;
   const int64_t ldq = 3ll * H * DH;
@@ -788,7 +802,7 @@ __global__ __launch_bounds__(64) void ld_attn_fwd_f32(AttnArgs a) {
       if (key > q || key >= S) break;
       float s = 0.f;
       for (int i = 0; i < DH; ++i) s = __builtin_fmaf(qv[i], Ks[j][i], s);
-      s *= a.scale;
+      s = s * a.scale - al * static_cast<float>(q - key);
       const float m_new = fmaxf(m, s);
       const float alpha = expf(m - m_new), p = expf(s - m_new);
       l = l * alpha + p;
@@ -809,6 +823,7 @@ __global__ __launch_bounds__(64) void ld_attn_bwd_dq_f32(AttnArgs a) {
   __shared__ float Ks[ST][DH], Vs[ST][DH];
   const int S = a.S, H = a.H;
   const int head = blockIdx.y, seq = blockIdx.z;
+  const float al = a.alibi ? alibi_slope(head, H) : 0.f;  // ALiBi slope (natural units)
   if (seq >= seq_count(a)) return;
   const int q0 = blockIdx.x * ST, q = q0 + threadIdx.x;
   const int64_t ldq = 3ll * H * DH, ldo = static_cast<int64_t>(H) * DH;
@@ -839,7 +854,7 @@ __global__ __launch_bounds__(64) void ld_attn_bwd_dq_f32(AttnArgs a) {
         s = __builtin_fmaf(qv[i], Ks[j][i], s);
         dp = __builtin_fmaf(dov[i], Vs[j][i], dp);
       }
-      const float p = expf(s * a.scale - lse);
+      const float p = expf(s * a.scale - al * static_cast<float>(q - key) - lse);
       const float ds = p * (dp - dl);
       for (int i = 0; i < DH; ++i) dq[i] = __builtin_fmaf(ds, Ks[j][i], dq[i]);
     }
@@ -856,6 +871,7 @@ __global__ __launch_bounds__(64) void ld_attn_bwd_dkdv_f32(AttnArgs a) {
   __shared__ float Qs[ST][DH], Os[ST][DH], ls[ST], dls[ST];
   const int S = a.S, H = a.H;
   const int head = blockIdx.y, seq = blockIdx.z;
+  const float al = a.alibi ? alibi_slope(head, H) : 0.f;  // ALiBi slope (natural units)
   if (seq >= seq_count(a)) return;
   const int k0 = blockIdx.x * ST, key = k0 + threadIdx.x;
   const int64_t ldq = 3ll * H * DH, ldo = static_cast<int64_t>(H) * DH;
@@ -892,7 +908,7 @@ __global__ __launch_bounds__(64) void ld_attn_bwd_dkdv_f32(AttnArgs a) {
           s = __builtin_fmaf(Qs[j][i], kv[i], s);
           dp = __builtin_fmaf(Os[j][i], vv[i], dp);
         }
-        const float p = expf(s * a.scale - ls[j]);
+        const float p = expf(s * a.scale - al * static_cast<float>(q - key) - ls[j]);
         const float ds = p * (dp - dls[j]);
         for (int i = 0; i < DH; ++i) {
           dv[i] = __builtin_fmaf(p, Os[j][i], dv[i]);
@@ -917,7 +933,10 @@ hipError_t fwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
     if (dtype == LD_BF16) {
       const dim3 grid(a.H, a.n_seq, (a.S + FWQ - 1) / FWQ);
       constexpr int rpw = FWD_RPW;
-      hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw>), grid, dim3(64 * (FWQ / rpw)), 0, s, a);
+      if (a.alibi)
+        hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw, true>), grid, dim3(64 * (FWQ / rpw)), 0, s, a);
+      else
+        hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw, false>), grid, dim3(64 * (FWQ / rpw)), 0, s, a);
       return hipGetLastError();
     }
   }
@@ -938,11 +957,18 @@ hipError_t bwd_dh(int dtype, int part, const AttnArgs& a, hipStream_t s) {
         hipLaunchKernelGGL((ld_attn_delta<bf16, DH>), dgrid, dim3(256), 0, s, a);
       else if (part == 1) {
         constexpr int nw = dkdv_waves<DH>();
-        hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw>), dim3(a.H, a.n_seq, (a.S + 32 * nw - 1) / (32 * nw)),
-                           dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
-      } else
-        hipLaunchKernelGGL(ld_attn_bwd_dq_bf16<DH>, dim3(a.H, a.n_seq, (a.S + DQ_ROWS - 1) / DQ_ROWS),
-                           dim3(512), dq_lds_bytes<DH>(), s, a);
+        const dim3 grid(a.H, a.n_seq, (a.S + 32 * nw - 1) / (32 * nw));
+        if (a.alibi)
+          hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw, true>), grid, dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
+        else
+          hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw, false>), grid, dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
+      } else {
+        const dim3 grid(a.H, a.n_seq, (a.S + DQ_ROWS - 1) / DQ_ROWS);
+        if (a.alibi)
+          hipLaunchKernelGGL((ld_attn_bwd_dq_bf16<DH, true>), grid, dim3(512), dq_lds_bytes<DH>(), s, a);
+        else
+          hipLaunchKernelGGL((ld_attn_bwd_dq_bf16<DH, false>), grid, dim3(512), dq_lds_bytes<DH>(), s, a);
+      }
       return hipGetLastError();
     }
   }

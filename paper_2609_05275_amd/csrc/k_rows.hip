@@ -371,6 +371,47 @@ __global__ __launch_bounds__(256) void ld_swiglu_bwd_k(EltArgs a) {
   }
 }
 
+// Squared ReLU (the block of the paper's experiments): s = relu(u)^2 and its
+// backward gu = gs * 2 relu(u); u, s, gs, gu are [rows, f].
+template <typename T>
+__global__ __launch_bounds__(256) void ld_relu2_fwd_k(EltArgs a) {
+  constexpr int VN = Pack<T>::N;
+  const int64_t chunks = a.f / VN;
+  const int64_t total = row_count(a.rc) * chunks;
+  const T* u = static_cast<const T*>(a.a);
+  T* s = static_cast<T*>(a.out);
+  for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < total; id += gridDim.x * 256ll) {
+    const int64_t row = id / chunks, c = (id % chunks) * VN;
+    const Pack<T> x = load16(u + row * a.f + c);
+    Pack<T> o;
+#pragma unroll
+    for (int i = 0; i < VN; ++i) {
+      const float r = fmaxf(to_f(x.v[i]), 0.f);
+      o.v[i] = from_f<T>(r * r);
+    }
+    store16(s + row * a.f + c, o);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void ld_relu2_bwd_k(EltArgs a) {
+  constexpr int VN = Pack<T>::N;
+  const int64_t chunks = a.f / VN;
+  const int64_t total = row_count(a.rc) * chunks;
+  const T* u = static_cast<const T*>(a.a);
+  const T* gs = static_cast<const T*>(a.b);
+  T* gu = static_cast<T*>(a.out);
+  for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < total; id += gridDim.x * 256ll) {
+    const int64_t row = id / chunks, c = (id % chunks) * VN;
+    const Pack<T> x = load16(u + row * a.f + c);
+    const Pack<T> g = load16(gs + row * a.f + c);
+    Pack<T> o;
+#pragma unroll
+    for (int i = 0; i < VN; ++i) o.v[i] = from_f<T>(to_f(g.v[i]) * 2.f * fmaxf(to_f(x.v[i]), 0.f));
+    store16(gu + row * a.f + c, o);
+  }
+}
+
 int elt_grid(int64_t total_chunks) {
   int64_t g = (total_chunks + 255) / 256;
   if (g > 8192) g = 8192;
@@ -457,6 +498,26 @@ hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s) {
 
 hipError_t launch_rmsnorm_bwd(int dtype, const RmsBwdArgs& a, float* dg, hipStream_t s) {
   return dtype == LD_BF16 ? rms_bwd_t<bf16>(a, dg, s) : rms_bwd_t<float>(a, dg, s);
+}
+
+hipError_t launch_relu2_fwd(int dtype, const EltArgs& a, hipStream_t s) {
+  const int grid = elt_grid(a.rc.rows * (a.f / (dtype == LD_BF16 ? Pack<bf16>::N : Pack<float>::N)));
+  if (a.rc.rows == 0) return hipSuccess;
+  if (dtype == LD_BF16)
+    hipLaunchKernelGGL(ld_relu2_fwd_k<bf16>, dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ld_relu2_fwd_k<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_relu2_bwd(int dtype, const EltArgs& a, hipStream_t s) {
+  const int grid = elt_grid(a.rc.rows * (a.f / (dtype == LD_BF16 ? Pack<bf16>::N : Pack<float>::N)));
+  if (a.rc.rows == 0) return hipSuccess;
+  if (dtype == LD_BF16)
+    hipLaunchKernelGGL(ld_relu2_bwd_k<bf16>, dim3(grid), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(ld_relu2_bwd_k<float>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_swiglu_fwd(int dtype, const EltArgs& a, hipStream_t s) {

@@ -172,7 +172,20 @@ struct AttnArgs {
   int32_t n_seq;             // host count (upper bound when dev_count is set)
   int32_t S, H, dh;
   float scale;               // 1/sqrt(dh)
+  int32_t alibi;             // add the ALiBi bias -m_h (i - j) to the scaled scores
 };
+
+// ALiBi slope of head h of H heads (ALiBi paper, section 3): with n the
+// largest power of two <= H, 2^(-8(h+1)/n) for h < n, else every other slope
+// of the 2n-head sequence, 2^(-4(2(h-n)+1)/n).
+__host__ __device__ inline float alibi_slope(int h, int H) {
+  if (H < 1 || h < 0 || h >= H) return 0.f;
+  int n = 1;
+  while (2 * n <= H) n *= 2;
+  const float e = h < n ? -8.f * static_cast<float>(h + 1) / static_cast<float>(n)
+                        : -4.f * static_cast<float>(2 * (h - n) + 1) / static_cast<float>(n);
+  return exp2f(e);
+}
 
 // ------------------------------------------------------------- launchers
 // Each returns the HIP error of its launch(es).  Grids are sized for the
@@ -185,6 +198,8 @@ hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s);
 // Needs rmsnorm_bwd_blocks(max_rows) * d floats of dg_part.
 int64_t rmsnorm_bwd_blocks(int64_t max_rows);
 hipError_t launch_rmsnorm_bwd(int dtype, const RmsBwdArgs& a, float* dg, hipStream_t s);
+hipError_t launch_relu2_fwd(int dtype, const EltArgs& a, hipStream_t s);
+hipError_t launch_relu2_bwd(int dtype, const EltArgs& a, hipStream_t s);
 hipError_t launch_swiglu_fwd(int dtype, const EltArgs& a, hipStream_t s);
 hipError_t launch_swiglu_bwd(int dtype, const EltArgs& a, hipStream_t s);
 hipError_t launch_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,

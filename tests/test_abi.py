@@ -143,3 +143,23 @@ class _Fake:
 
     def numel(self):
         return int(np.prod(self.shape))
+
+
+def test_alibi_slope_host_function():
+    """ld_alibi_slope (host) against the ALiBi paper's stated slopes for 8
+    and 16 heads and the oracle's rule for other counts (float32)."""
+    import os
+    from oracle import block
+    gold = {}
+    for line in open(os.path.join(os.path.dirname(__file__), "golden", "alibi_slopes.txt")):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            h, rest = line.split(":")
+            gold[int(h)] = [2.0 ** -float(e) for e in rest.split()]
+    for h, want in gold.items():
+        got = [ld.ld_alibi_slope(i, h) for i in range(h)]
+        assert np.allclose(got, want, rtol=1e-6, atol=0), h
+    for h in (3, 6, 12, 21):
+        got = [ld.ld_alibi_slope(i, h) for i in range(h)]
+        assert np.allclose(got, block.alibi_slopes(h), rtol=1e-6, atol=0), h
+    assert ld.ld_alibi_slope(-1, 8) == 0.0 and ld.ld_alibi_slope(8, 8) == 0.0

@@ -4,7 +4,8 @@ The oracle cannot run whole steps of these shapes in seconds, so each test
 checks outputs it can compute one at a time, or properties that hold at any
 size, through the same entry points and kernel plans the benchmark drives:
 
-- 1B layer (batch 8, the real ILD mask): the first kept sequence's output,
+- 1B layer, and a layer of the paper's 3.9B architecture with its block
+  (ALiBi, squared ReLU; batch 8, the real ILD mask): the first kept sequence's output,
   input gradient and weight gradients against the float64 oracle; dropped
   sequences bitwise untouched; the weight gradients of the whole launch equal
   the sum of single-sequence launches (gradients are sums over kept
@@ -36,7 +37,8 @@ TOL_REORDER = 1e-4
 
 
 def _cfg(sh):
-    return ld.config(sh.batch, sh.seq, sh.d_model, sh.n_heads, sh.d_ff, ld.LD_BF16)
+    return ld.config(sh.batch, sh.seq, sh.d_model, sh.n_heads, sh.d_ff, ld.LD_BF16,
+                     block_kind=sh.kind)
 
 
 def _buf(nbytes):
@@ -71,8 +73,9 @@ def _layer_run(cfg, sh, wd, layer, p, step, x, gy, keep=None):
     return x1, gd, dw
 
 
-def test_1b_layer_sampled_and_additive():
-    sh = inp.SHAPES["1b"]
+@pytest.mark.parametrize("name", ["1b", "paper_3p9b"])
+def test_layer_sampled_and_additive(name):
+    sh = inp.SHAPES[name]
     cfg = _cfg(sh)
     layer = sh.n_layers - 1
     p = _ild(0.2, layer, sh.n_layers)
@@ -87,7 +90,7 @@ def test_1b_layer_sampled_and_additive():
             assert torch.equal(g0[b].cpu(), gy[b]), b
     # the first kept sequence against the oracle
     b0 = kept[0]
-    oc = stack.Config(n_heads=sh.n_heads)
+    oc = stack.Config(n_heads=sh.n_heads, block_kind=sh.kind)
     X1, octx = stack.layer_forward(inp.f64(x[b0:b0 + 1]), w64, np.ones(1, np.uint8), p, oc)
     G0, grads = stack.layer_backward(octx, inp.f64(gy[b0:b0 + 1]), oc)
     assert rel(f64(x1[b0]), X1[0]) < TOL_BF16

@@ -104,6 +104,26 @@ def test_rmsnorm_fwd_bwd(dt, d):
     assert rel(f64(dg), edg) < tol
 
 
+@pytest.mark.parametrize("dt,f", [("bf16", 16384), ("bf16", 2048), ("f32", 172)])
+def test_relu2_fwd_bwd(dt, f):
+    rows = 257
+    g = torch.Generator().manual_seed(6)
+    u = (2 * torch.randn(rows, f, generator=g)).to(TD[dt])
+    gs = torch.randn(rows, f, generator=g).to(TD[dt])
+    ud, gsd = u.to(DEV), gs.to(DEV)
+    s = torch.empty(rows, f, dtype=TD[dt], device=DEV)
+    gu = torch.empty(rows, f, dtype=TD[dt], device=DEV)
+    ld.ld_relu2_fwd(ud, s)
+    ld.ld_relu2_bwd(ud, gsd, gu)
+    torch.cuda.synchronize()
+    tol = TOL_BF16 if dt == "bf16" else TOL_F32
+    assert rel(f64(s), block.relu2(f64(u))) < tol
+    assert rel(f64(gu), f64(gs) * block.relu2_grad(f64(u))) < tol
+    # negative inputs give exactly zero
+    neg = f64(u) <= 0
+    assert not f64(s)[neg].any() and not f64(gu)[neg].any()
+
+
 @pytest.mark.parametrize("dt,f", [("bf16", 5504), ("bf16", 2048), ("f32", 172)])
 def test_swiglu_fwd_bwd(dt, f):
     rows = 257
@@ -208,21 +228,23 @@ def test_gemm_f32(layout):
     assert rel(f64(Cd), 2.0 * (f64(A) @ f64(B).T)) < TOL_F32
 
 
-def _attn_ref(qkv, n, S, H, dh):
+def _attn_ref(qkv, n, S, H, dh, alibi=0):
     d = H * dh
     q64 = f64(qkv).reshape(n, S, 3 * d)
     outs, probs = [], []
+    slopes = block.alibi_slopes(H) if alibi else None
     for b in range(n):
-        o, p = block.causal_attention(q64[b, :, :d], q64[b, :, d:2 * d], q64[b, :, 2 * d:], H)
+        o, p = block.causal_attention(q64[b, :, :d], q64[b, :, d:2 * d], q64[b, :, 2 * d:], H, slopes)
         outs.append(o)
         probs.append(p)
     return q64, outs, probs
 
 
+@pytest.mark.parametrize("alibi", [0, 1])
 @pytest.mark.parametrize("dt,n,S,H,dh", [("bf16", 2, 192, 2, 64), ("bf16", 2, 256, 2, 128),
-                                         ("bf16", 1, 1024, 1, 128), ("f32", 3, 32, 4, 16),
-                                         ("f32", 2, 100, 2, 64)])
-def test_attention_fwd_bwd(dt, n, S, H, dh):
+                                         ("bf16", 1, 1024, 1, 128), ("bf16", 1, 512, 6, 128),
+                                         ("f32", 3, 32, 4, 16), ("f32", 2, 100, 2, 64)])
+def test_attention_fwd_bwd(dt, n, S, H, dh, alibi):
     d = H * dh
     g = torch.Generator().manual_seed(5)
     qkv = torch.randn(n * S, 3 * d, generator=g).to(TD[dt])
@@ -230,12 +252,12 @@ def test_attention_fwd_bwd(dt, n, S, H, dh):
     qd, god = qkv.to(DEV), go.to(DEV)
     o = torch.empty(n * S, d, dtype=TD[dt], device=DEV)
     lse = torch.empty(n, H, S, dtype=torch.float32, device=DEV)
-    ld.ld_attn_fwd(n, S, H, dh, qd, o, lse)
+    ld.ld_attn_fwd(n, S, H, dh, qd, o, lse, alibi=alibi)
     gq = torch.empty(n * S, 3 * d, dtype=TD[dt], device=DEV)
     ws = torch.empty(ld.ld_attn_bwd_ws_bytes(n, S, H), dtype=torch.uint8, device=DEV)
-    ld.ld_attn_bwd(n, S, H, dh, qd, o, lse, god, gq, ws)
+    ld.ld_attn_bwd(n, S, H, dh, qd, o, lse, god, gq, ws, alibi=alibi)
     torch.cuda.synchronize()
-    q64, outs, probs = _attn_ref(qkv, n, S, H, dh)
+    q64, outs, probs = _attn_ref(qkv, n, S, H, dh, alibi)
     go64 = f64(go).reshape(n, S, d)
     tol = TOL_BF16 if dt == "bf16" else TOL_F32
     of, gf = f64(o).reshape(n, S, d), f64(gq).reshape(n, S, 3 * d)
@@ -247,10 +269,12 @@ def test_attention_fwd_bwd(dt, n, S, H, dh):
         assert rel(gf[b, :, :d], gq_) < tol, "dq"
         assert rel(gf[b, :, d:2 * d], gk_) < tol, "dk"
         assert rel(gf[b, :, 2 * d:], gv_) < tol, "dv"
-        # log-sum-exp of the scaled causal scores
+        # log-sum-exp of the scaled causal scores (with the ALiBi bias)
+        slopes = block.alibi_slopes(H) if alibi else np.zeros(H)
+        dist = np.arange(S)[:, None] - np.arange(S)[None, :]
         for h in range(H):
             cols = slice(h * dh, (h + 1) * dh)
-            s = q64[b, :, cols] @ q64[b, :, d:2 * d][:, cols].T / np.sqrt(dh)
+            s = q64[b, :, cols] @ q64[b, :, d:2 * d][:, cols].T / np.sqrt(dh) - slopes[h] * dist
             s[np.triu(np.ones((S, S), bool), 1)] = -np.inf
             m = s.max(axis=1)
             want = m + np.log(np.exp(s - m[:, None]).sum(axis=1))

@@ -2,6 +2,8 @@
 ld_layer_fwd / ld_layer_bwd / ld_stack_step through the C ABI, masks and
 kept lists bit-exact, dropped rows bitwise untouched, activations and
 gradients within the dtype's tolerance of the float64 oracle."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -17,15 +19,21 @@ SMALL_BF16 = inp.Shape(3, 256, 4, 704, 192, 5, "bf16")      # d_head 64, ragged 
 SMALL_BF16_128 = inp.Shape(2, 256, 2, 512, 128, 3, "bf16")  # d_head 128
 # large enough that every projection GEMM takes the 256x256 kernel path
 MID_BF16 = inp.Shape(2, 1024, 8, 2816, 512, 4, "bf16")
+# the block of the paper's experiments (ALiBi + squared ReLU, W_up only);
+# 6 heads: not a power of two, so both ALiBi slope rules are exercised
+TINY_P = dataclasses.replace(inp.SHAPES["tiny"], kind=1)
+SMALL_P = inp.Shape(3, 256, 4, 1024, 192, 5, "bf16", 1)
+SMALL_P_128 = inp.Shape(2, 768, 6, 2048, 256, 2, "bf16", 1)
+MID_P = inp.Shape(2, 1024, 8, 4096, 512, 4, "bf16", 1)
 
 
 def _cfg(sh, **kw):
     return ld.config(sh.batch, sh.seq, sh.d_model, sh.n_heads, sh.d_ff,
-                     ld.LD_BF16 if sh.dtype == "bf16" else ld.LD_F32, **kw)
+                     ld.LD_BF16 if sh.dtype == "bf16" else ld.LD_F32, block_kind=sh.kind, **kw)
 
 
 def _ocfg(sh, **kw):
-    return stack.Config(n_heads=sh.n_heads, **kw)
+    return stack.Config(n_heads=sh.n_heads, block_kind=sh.kind, **kw)
 
 
 def _buf(nbytes):
@@ -41,8 +49,11 @@ def _check_grads(got, want, t, where=""):
             assert rel(g, w) < t, (where, k, rel(g, w))
 
 
-@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16, SMALL_BF16_128, MID_BF16],
-                         ids=["tiny_f32", "small_bf16", "small_bf16_dh128", "mid_bf16"])
+@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16, SMALL_BF16_128, MID_BF16,
+                                TINY_P, SMALL_P, SMALL_P_128, MID_P],
+                         ids=["tiny_f32", "small_bf16", "small_bf16_dh128", "mid_bf16",
+                              "paper_tiny_f32", "paper_small_bf16", "paper_small_bf16_dh128_h6",
+                              "paper_mid_bf16"])
 @pytest.mark.parametrize("forced", [None, "none", "one", "ragged", "all"])
 def test_layer_fwd_bwd(sh, forced):
     cfg = _cfg(sh)
@@ -82,7 +93,8 @@ def test_layer_fwd_bwd(sh, forced):
     _check_grads(dw, grads, t, forced)
 
 
-@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16], ids=["tiny_f32", "small_bf16"])
+@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16, TINY_P, SMALL_P],
+                         ids=["tiny_f32", "small_bf16", "paper_tiny_f32", "paper_small_bf16"])
 @pytest.mark.parametrize("p_max", [0.0, 0.2, 0.6, 1.0])
 def test_stack_step(sh, p_max):
     cfg = _cfg(sh)
