@@ -43,8 +43,9 @@ T_RAMP = 1001               # steps 0..1000 of the p_max ramp
 
 
 # Kernel -> source file it is built from (for the traffic record's hash check).
-KERNEL_SOURCES = {"ld_gemm": "paper_2609_05275_amd/csrc/k_gemm.hip",
-                  "ld_attn": "paper_2609_05275_amd/csrc/k_attn.hip"}
+KERNEL_SOURCES = {
+    "ld_gemm": "paper_2609_05275_amd/csrc/k_gemm.hip+paper_2609_05275_amd/csrc/ld_internal.h",
+    "ld_attn": "paper_2609_05275_amd/csrc/k_attn.hip+paper_2609_05275_amd/csrc/ld_internal.h"}
 
 
 def traffic_record(kernel, workload):
@@ -56,7 +57,7 @@ def traffic_record(kernel, workload):
     src = next((v for k, v in KERNEL_SOURCES.items() if kernel.startswith(k)), None)
     if src is None or rec.get("source") != src:
         return None
-    if profsum.source_hash(os.path.join(ROOT, src)) != rec.get("source_sha256"):
+    if profsum.source_hash(src, ROOT) != rec.get("source_sha256"):
         return None
     return rec
 

@@ -8,9 +8,9 @@
       then WRITE_SIZE, each in KiB per dispatch), each scaled by what the same
       counter reads for the calibration copy that bench.py --copy-calib-mib
       runs (an elementwise y = 1 * x over float32 tensors of known size).
-      SOURCE is the kernel's source file; its SHA-256 goes into the summary so
-      that a reader can tell when the kernel has changed since the counters
-      were taken.
+      SOURCE lists the files the kernel is built from ('+'-separated); their
+      SHA-256 goes into the summary so that a reader can tell when the kernel
+      has changed since the counters were taken.
 
 Reads only rocprofv3 output; runs nothing on a GPU.
 """
@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import hashlib
 import json
+import os
 import re
 import sqlite3
 import sys
@@ -35,9 +36,14 @@ def short(name: str) -> str:
     return n[:70]
 
 
-def source_hash(path: str) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def source_hash(paths: str, root: str = "") -> str:
+    """SHA-256 over the files of a '+'-separated list (relative to root)."""
+    h = hashlib.sha256()
+    for p in paths.split("+"):
+        with open(os.path.join(root, p), "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    return h.hexdigest()
 
 
 def trace(db: str, title: str, cmd: str) -> str:
@@ -89,7 +95,10 @@ def traffic(fetch_db: str, write_db: str, kernel: str, source: str, cmd: str) ->
            "dispatches": len(kf), "fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
            "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4),
            "hbm_bytes_per_launch": round(bytes_per_launch)}
-    out = [f"# HBM traffic per dispatch: {kernel}, 1B-shape stack step", "",
+    wm = re.search(r"--workload (\S+)", cmd)
+    workload = wm.group(1) if wm else "1b"
+    rec["workload"] = workload
+    out = [f"# HBM traffic per dispatch: {kernel}, stack step of workload {workload}", "",
            "Commands (one counter pass each):", "", f"    {cmd}", "",
            f"- {kernel}: {len(kf)} dispatches, FETCH_SIZE {fk:.1f} KiB and WRITE_SIZE "
            f"{wk:.1f} KiB per dispatch (mean)",
