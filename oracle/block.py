@@ -120,19 +120,20 @@ def silu_grad(u):
     return sg * (1.0 + u * (1.0 - sg))
 
 
-def forward(x, w, r, n_heads, eps, kind=0):
-    """Apply the block to one kept sequence x [S, d].
-
-    w: dict with g_attn [d], w_qkv [3d, d], w_o [d, d], g_mlp [d],
-    w_gate_up [2f, d] (kind 0) or [f, d] (kind 1), w_down [d, f].  r is the
-    residual-branch scale.  Returns (x_next, cache)."""
+def attn_forward(x, w, r, n_heads, eps, kind=0):
+    """Attention residual sub-block on one sequence: z = x + r f_attn(x)."""
     d = x.shape[1]
-    f = w["w_down"].shape[1]
     h1, rstd1 = rmsnorm(x, w["g_attn"], eps)
     qkv = h1 @ w["w_qkv"].T
     q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
     a, probs = causal_attention(q, k, v, n_heads, alibi_slopes(n_heads) if kind == 1 else None)
     z = x + r * (a @ w["w_o"].T)
+    return z, dict(x=x, h1=h1, rstd1=rstd1, q=q, k=k, v=v, a=a, probs=probs)
+
+
+def ffn_forward(z, w, r, eps, kind=0):
+    """FFN residual sub-block on one sequence: x' = z + r f_ffn(z)."""
+    f = w["w_down"].shape[1]
     h2, rstd2 = rmsnorm(z, w["g_mlp"], eps)
     uv = h2 @ w["w_gate_up"].T
     if kind == 1:
@@ -142,14 +143,24 @@ def forward(x, w, r, n_heads, eps, kind=0):
         u, vv = uv[:, :f], uv[:, f:]
         s = silu(u) * vv
     x_next = z + r * (s @ w["w_down"].T)
-    cache = dict(x=x, h1=h1, rstd1=rstd1, q=q, k=k, v=v, a=a, probs=probs,
-                 z=z, h2=h2, rstd2=rstd2, u=u, vv=vv, s=s, kind=kind)
-    return x_next, cache
+    return x_next, dict(z=z, h2=h2, rstd2=rstd2, u=u, vv=vv, s=s, kind=kind)
 
 
-def backward(cache, g, w, r, n_heads):
-    """Backward of `forward` for one kept sequence given g = dL/dx_next.
-    Returns (dL/dx, grads dict with the same keys as w)."""
+def forward(x, w, r, n_heads, eps, kind=0):
+    """Apply the block to one kept sequence x [S, d]: the attention sub-block,
+    then the FFN sub-block on its output.
+
+    w: dict with g_attn [d], w_qkv [3d, d], w_o [d, d], g_mlp [d],
+    w_gate_up [2f, d] (kind 0) or [f, d] (kind 1), w_down [d, f].  r is the
+    residual-branch scale.  Returns (x_next, cache)."""
+    z, ca = attn_forward(x, w, r, n_heads, eps, kind)
+    x_next, cf = ffn_forward(z, w, r, eps, kind)
+    return x_next, dict(ca, **cf)
+
+
+def ffn_backward(cache, g, w, r):
+    """Backward of ffn_forward given g = dL/dx'.  Returns (dL/dz, grads of
+    g_mlp, w_gate_up, w_down)."""
     c = cache
     gy = r * g
     d_down = gy.T @ c["s"]
@@ -163,7 +174,13 @@ def backward(cache, g, w, r, n_heads):
     d_gate_up = guv.T @ c["h2"]
     gh2 = guv @ w["w_gate_up"]
     gz_norm, d_g_mlp = rmsnorm_bwd(c["z"], w["g_mlp"], c["rstd2"], gh2)
-    gz = g + gz_norm
+    return g + gz_norm, dict(g_mlp=d_g_mlp, w_gate_up=d_gate_up, w_down=d_down)
+
+
+def attn_backward(cache, gz, w, r, n_heads):
+    """Backward of attn_forward given gz = dL/dz.  Returns (dL/dx, grads of
+    g_attn, w_qkv, w_o)."""
+    c = cache
     go = r * gz
     d_o = go.T @ c["a"]
     ga = go @ w["w_o"]
@@ -172,7 +189,12 @@ def backward(cache, g, w, r, n_heads):
     d_qkv = gqkv.T @ c["h1"]
     gh1 = gqkv @ w["w_qkv"]
     gx_norm, d_g_attn = rmsnorm_bwd(c["x"], w["g_attn"], c["rstd1"], gh1)
-    gx = gz + gx_norm
-    grads = dict(g_attn=d_g_attn, w_qkv=d_qkv, w_o=d_o, g_mlp=d_g_mlp,
-                 w_gate_up=d_gate_up, w_down=d_down)
-    return gx, grads
+    return gz + gx_norm, dict(g_attn=d_g_attn, w_qkv=d_qkv, w_o=d_o)
+
+
+def backward(cache, g, w, r, n_heads):
+    """Backward of `forward` for one kept sequence given g = dL/dx_next.
+    Returns (dL/dx, grads dict with the same keys as w)."""
+    gz, gf = ffn_backward(cache, g, w, r)
+    gx, ga = attn_backward(cache, gz, w, r, n_heads)
+    return gx, dict(ga, **gf)

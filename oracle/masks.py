@@ -23,7 +23,7 @@ import math
 
 import numpy as np
 
-from .philox import mask_word
+from .philox import block_words, mask_word
 
 
 def threshold(p):
@@ -67,4 +67,59 @@ def masks(ps, seed, step, batch, first_layer=0):
     for i in range(L):
         keep[i] = keep_bits(ps[i], seed, step, first_layer + i, batch)
         idx[i], count[i] = compact(keep[i])
+    return keep, idx, count
+
+
+# ------------------------------------------------------------ granularity
+# Dropout Granularity section: model granularity (one mask per layer shared by
+# both sub-blocks, or independent attention and FFN masks: sub-layer dropout)
+# and tensor granularity (one draw per sequence, or one draw per layer and step
+# shared by the whole batch: per-batch dropout).  Encoded as two bits:
+LAYER_SEQ = 0        # layer granularity, per sequence (the paper's choice)
+SUBLAYER_SEQ = 1     # M_attn, M_ffn drawn independently, per sequence
+LAYER_BATCH = 2      # one draw per (layer, step) for all sequences
+SUBLAYER_BATCH = 3   # independent attention / FFN draws, per (layer, step)
+
+# Reading of the draws (the paper fixes no generator):
+#   per sequence: block (b, l, t, 0); per batch: block (0, l, t, 1); key (seed, 0)
+#   the attention mask (and the layer mask) takes word 0 of the block, the
+#   FFN mask of sub-layer dropout takes word 1.  So the attention mask of
+#   sub-layer dropout is the layer-dropout mask, and both sub-block masks are
+#   Bernoulli(1 - p^{l,t}) with the layer's rate.
+
+
+def n_masks(granularity):
+    """Masks per layer: 2 (attention, FFN) for sub-layer dropout, else 1."""
+    if granularity not in (LAYER_SEQ, SUBLAYER_SEQ, LAYER_BATCH, SUBLAYER_BATCH):
+        raise ValueError(f"unknown granularity {granularity}")
+    return 2 if granularity & 1 else 1
+
+
+def keep_bits_granular(p, seed, step, layer, batch, granularity):
+    """uint8[n_masks, batch]: row 0 the attention (or whole-layer) mask, row 1
+    the FFN mask of sub-layer dropout."""
+    nm = n_masks(granularity)
+    thr = threshold(p)
+    if thr is None:
+        return np.zeros((nm, batch), dtype=np.uint8)
+    if granularity & 2:
+        words = block_words(0, layer, step, seed, 1)
+        rows = [np.full(batch, words[m], dtype=np.uint64) for m in range(nm)]
+    else:
+        words = block_words(np.arange(batch, dtype=np.uint64), layer, step, seed, 0)
+        rows = [words[m] for m in range(nm)]
+    return np.stack([np.where(w < np.uint64(thr), 0, 1) for w in rows]).astype(np.uint8)
+
+
+def masks_granular(ps, seed, step, batch, granularity, first_layer=0):
+    """keep uint8[L, n_masks, B], idx int32[L, n_masks, B], count int32[L, n_masks]."""
+    ps = np.asarray(ps, dtype=np.float32)
+    L, nm = len(ps), n_masks(granularity)
+    keep = np.zeros((L, nm, batch), dtype=np.uint8)
+    idx = np.full((L, nm, batch), -1, dtype=np.int32)
+    count = np.zeros((L, nm), dtype=np.int32)
+    for i in range(L):
+        keep[i] = keep_bits_granular(ps[i], seed, step, first_layer + i, batch, granularity)
+        for m in range(nm):
+            idx[i, m], count[i, m] = compact(keep[i, m])
     return keep, idx, count

@@ -65,6 +65,13 @@ def philox4x64_10(c0, c1, c2, c3, k0, k1):
     return c0, c1, c2, c3
 
 
+def block_words(sample, layer, step, seed, c3=0):
+    """All four output words for counter (sample, layer, step, c3) and key
+    (seed, 0).  Sub-layer masks use words 0 and 1 of one block; per-batch
+    draws use c3 = 1 (so they never share a block with a per-sequence draw)."""
+    return philox4x64_10(sample, layer, step, c3, seed, 0)
+
+
 def mask_word(sample, layer, step, seed):
     """The 64-bit draw for one (sample, layer, step) under `seed`: word 0 of
     Philox4x64-10 with counter (sample, layer, step, 0) and key (seed, 0)."""

@@ -2,7 +2,8 @@
 torch float64 autograd built from library routines (rms_norm,
 scaled_dot_product_attention with is_causal or with an explicit float mask,
 silu, relu), applied to the whole batch and gated by the mask multiply of the
-layer-dropout training equation (H + r M f(H)).  Kind 1 adds the ALiBi bias
+layer-dropout training equation (H + r M f(H)), with one mask per layer or
+separate attention and FFN masks (sub-layer dropout).  Kind 1 adds the ALiBi bias
 through the attention mask and uses the squared-ReLU feed-forward.  Used only
 by the CPU pin tests of the oracle."""
 import numpy as np
@@ -45,12 +46,15 @@ def block_full_batch(X, w, n_heads, eps, kind=0):
 
 
 def layer_masked(X, w, keep, r, n_heads, eps, kind=0):
-    """X + r M f_attn, then + r M f_ffn, over the full batch (mask multiply)."""
+    """X + r M_attn f_attn, then + r M_ffn f_ffn, over the full batch (mask
+    multiply).  keep: [B] (one mask for both sub-blocks) or [2, B]."""
     B, S, d = X.shape
     f = w["w_down"].shape[1]
-    m = torch.as_tensor(keep, dtype=X.dtype).reshape(B, 1, 1)
+    k = np.asarray(keep).reshape(-1, B)
+    m_a = torch.as_tensor(k[0], dtype=X.dtype).reshape(B, 1, 1)
+    m = torch.as_tensor(k[-1], dtype=X.dtype).reshape(B, 1, 1)
     _, a = block_full_batch(X, w, n_heads, eps, kind)
-    Z = X + r * m * (a @ w["w_o"].T)
+    Z = X + r * m_a * (a @ w["w_o"].T)
     h2 = F.rms_norm(Z, (d,), w["g_mlp"], eps)
     uv = h2 @ w["w_gate_up"].T
     if kind == 1:
