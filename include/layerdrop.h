@@ -73,8 +73,29 @@ typedef enum { LD_F32 = 0, LD_BF16 = 1 } ld_dtype;
  *   the paper's experiments (Experimental Setup: ALiBi position bias,
  *   squared-ReLU activation): pre-norm RMSNorm, causal attention whose
  *   scaled scores get the ALiBi bias -m_h (i - j) (query i, key j <= i, head
- *   slope m_h of ld_alibi_slope), and the feed-forward relu(h W_up^T)^2 W_down^T. */
+ *   slope m_h of ld_alibi_slope), and the feed-forward relu(h W_up^T)^2 W_down^T.
+ *   granularity: which masks are drawn (Dropout Granularity section), two bits:
+ *   LD_GRAN_SUBLAYER: model granularity "sub-layer": the attention and FFN
+ *     sub-blocks get independent masks M_attn, M_ffn (both Bernoulli(1 - p)
+ *     with the layer's p, one r for both):
+ *       Z = X + r M_attn f_attn(X),  X^{l+1} = Z + r M_ffn f_ffn(Z);
+ *     without it one mask serves both (layer dropout, the paper's choice).
+ *   LD_GRAN_PER_BATCH: tensor granularity "per batch": one draw per
+ *     (layer, step) shared by every sequence, so a layer (or sub-block) is
+ *     kept or skipped for the whole batch; a skipped one reads no weights
+ *     and its weight gradients are zero-filled.  Without it the draws are per
+ *     sequence (the paper's choice).
+ *   Masks per layer: n_masks = 2 under LD_GRAN_SUBLAYER (attention, then
+ *   FFN), else 1. */
 typedef enum { LD_BLOCK_SWIGLU = 0, LD_BLOCK_ALIBI_RELU2 = 1 } ld_block_kind;
+typedef enum {
+  LD_GRAN_LAYER_SEQ = 0,
+  LD_GRAN_SUBLAYER = 1,
+  LD_GRAN_PER_BATCH = 2,
+  LD_GRAN_SUBLAYER_SEQ = 1,
+  LD_GRAN_LAYER_BATCH = 2,
+  LD_GRAN_SUBLAYER_BATCH = 3
+} ld_granularity;
 
 typedef struct {
   int32_t batch, seq, d_model, n_heads, d_ff;
@@ -83,6 +104,7 @@ typedef struct {
   int32_t rescale;
   float res_scale;
   int32_t block_kind;
+  int32_t granularity;
 } ld_config;
 
 /* Device pointers to one layer's parameters (element type cfg->dtype):
@@ -135,6 +157,19 @@ int ld_schedule_p(int32_t dist, int32_t sched, float p_max, int32_t layer, int32
 int ld_masks(int32_t n_layers, int32_t batch, const float* p, int32_t first_layer, uint64_t seed,
              uint64_t step, uint8_t* keep, int32_t* idx, int32_t* count, void* stream);
 
+/* ld_masks for any ld_granularity (Dropout Granularity section).  Per
+ * sequence, mask m of layer l uses word m of the Philox block with counter
+ * (b, l, t, 0); per batch, word m of the block (0, l, t, 1) decides every
+ * sample; key (seed, 0) and the threshold rule as in ld_masks.  Mask 0 is the
+ * attention (or whole-layer) mask, mask 1 the FFN mask of sub-layer dropout,
+ * so the attention mask of LD_GRAN_SUBLAYER_SEQ is the ld_masks mask.
+ *   keep, idx: device [n_layers][n_masks][batch]; count: device
+ *   [n_layers][n_masks].  Errors as ld_masks, plus LD_E_INVALID for an
+ *   unknown granularity. */
+int ld_masks_granular(int32_t granularity, int32_t n_layers, int32_t batch, const float* p,
+                      int32_t first_layer, uint64_t seed, uint64_t step, uint8_t* keep, int32_t* idx,
+                      int32_t* count, void* stream);
+
 /* Gather the rows of the kept sequences into a contiguous block:
  * xk[j*S + s, :] = x[idx[j]*S + s, :] for j < *count (bit copy).
  *   idx, count: device, as produced by ld_masks for one layer.
@@ -168,9 +203,11 @@ size_t ld_stack_ws_bytes(const ld_config* cfg, int32_t n_layers);
  *   ctx: device, ld_layer_ctx_bytes(cfg) bytes, written (mask, kept lists,
  *        saved activations); consumed by ld_layer_bwd.
  *   ws:  device scratch of ws_bytes >= ld_layer_ws_bytes(cfg).
- *   keep_override: NULL, or device uint8[B] used instead of the Philox mask
- *        (test hook for forcing kept counts 0, 1, all, ragged).
- * p in [0, 1]; with p = 1 (or no kept sample) x is left unchanged. */
+ *   keep_override: NULL, or device uint8[n_masks][B] used instead of the
+ *        Philox masks (test hook for forcing kept counts 0, 1, all, ragged).
+ * p in [0, 1]; with p = 1 (or no kept sample) x is left unchanged.  Under
+ * LD_GRAN_PER_BATCH without an override the host takes the draw itself and
+ * launches nothing for a dropped sub-block (the masks in ctx still say so). */
 int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float p, uint64_t seed,
                  uint64_t step, void* x, void* ctx, void* ws, size_t ws_bytes,
                  const uint8_t* keep_override, void* stream);
@@ -179,7 +216,8 @@ int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float
  *   dx: device [B, S, d], dL/dX^{l+1} in, dL/dX^l out, in place; rows of
  *       dropped sequences pass through untouched.
  *   dw: host struct of device float32 gradient pointers, overwritten with
- *       sums over kept rows (zero when no sequence is kept). */
+ *       sums over kept rows (zero when no sequence is kept).  The kept
+ *       counts are read on the device (every launch is made). */
 int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, void* dx,
                  const ld_grads* dw, void* ws, size_t ws_bytes, void* stream);
 
@@ -190,9 +228,12 @@ int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, voi
  *   x:     device [B, S, d], X^0 in, X^L out (in place).
  *   dx:    device [B, S, d], dL/dX^L in, dL/dX^0 out (in place).
  *   ws:    device, ws_bytes >= ld_stack_ws_bytes(cfg, n_layers).
- *   keep_override: NULL or device uint8[n_layers][B] (test hook).
+ *   keep_override: NULL or device uint8[n_layers][n_masks][B] (test hook).
  *   keep_out, idx_out, count_out: NULL or device buffers shaped as in
- *        ld_masks, receiving this step's masks (device-to-device copies).
+ *        ld_masks_granular, receiving this step's masks (device-to-device
+ *        copies).
+ * Under LD_GRAN_PER_BATCH without an override, a layer or sub-block whose
+ * draw drops it launches nothing but the zero fill of its weight gradients.
  * n_layers in [1, 1024]. */
 int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const float* p,
                   uint64_t seed, uint64_t step, void* x, void* dx, const ld_grads* dw, void* ws,

@@ -16,6 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblayerdrop.so")
 
 LD_F32, LD_BF16 = 0, 1
+LD_GRAN_LAYER_SEQ, LD_GRAN_SUBLAYER_SEQ, LD_GRAN_LAYER_BATCH, LD_GRAN_SUBLAYER_BATCH = 0, 1, 2, 3
 UNIFORM, ILD, ALD = 0, 1, 2
 CONSTANT, ITS, DTS = 0, 1, 2
 
@@ -32,7 +33,7 @@ class ld_config(C.Structure):
     _fields_ = [("batch", C.c_int32), ("seq", C.c_int32), ("d_model", C.c_int32),
                 ("n_heads", C.c_int32), ("d_ff", C.c_int32), ("dtype", C.c_int32),
                 ("rms_eps", C.c_float), ("rescale", C.c_int32), ("res_scale", C.c_float),
-                ("block_kind", C.c_int32)]
+                ("block_kind", C.c_int32), ("granularity", C.c_int32)]
 
 
 class ld_weights(C.Structure):
@@ -54,6 +55,8 @@ _SIGS = {
     "ld_last_error": (C.c_char_p, []),
     "ld_schedule_p": (C.c_int, [_i32, _i32, _f32, _i32, _i32, _i64, _i64, C.POINTER(_f32)]),
     "ld_masks": (C.c_int, [_i32, _i32, C.POINTER(_f32), _i32, _u64, _u64, _vp, _vp, _vp, _vp]),
+    "ld_masks_granular": (C.c_int, [_i32, _i32, _i32, C.POINTER(_f32), _i32, _u64, _u64, _vp, _vp,
+                                    _vp, _vp]),
     "ld_gather_rows": (C.c_int, [_PCFG, _vp, _vp, _vp, _vp, _vp]),
     "ld_scatter_add_rows": (C.c_int, [_PCFG, _vp, _vp, _f32, _vp, _vp, _vp]),
     "ld_layer_ctx_bytes": (_sz, [_PCFG]),
@@ -132,9 +135,9 @@ def _dtype_code(t):
 
 
 def config(batch, seq, d_model, n_heads, d_ff, dtype=LD_BF16, rms_eps=1e-5, rescale=True,
-           res_scale=1.0, block_kind=0):
+           res_scale=1.0, block_kind=0, granularity=0):
     return ld_config(batch, seq, d_model, n_heads, d_ff, dtype, rms_eps, int(bool(rescale)),
-                     res_scale, block_kind)
+                     res_scale, block_kind, granularity)
 
 
 def weights(w):
@@ -159,6 +162,13 @@ def ld_masks(p, seed, step, keep, idx, count, first_layer=0, stream=None):
     arr = (C.c_float * n)(*[float(v) for v in p])
     _check(_lib.ld_masks(n, keep.shape[-1], arr, first_layer, seed, step, _ptr(keep), _ptr(idx),
                          _ptr(count), _stream(stream)))
+
+
+def ld_masks_granular(granularity, p, seed, step, keep, idx, count, first_layer=0, stream=None):
+    n = len(p)
+    arr = (C.c_float * n)(*[float(v) for v in p])
+    _check(_lib.ld_masks_granular(granularity, n, keep.shape[-1], arr, first_layer, seed, step,
+                                  _ptr(keep), _ptr(idx), _ptr(count), _stream(stream)))
 
 
 def ld_gather_rows(cfg, idx, count, x, xk, stream=None):

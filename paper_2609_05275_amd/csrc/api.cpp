@@ -94,6 +94,9 @@ struct Dims {
   int dtype;
   int kind;    // ld_block_kind
   int64_t fw;  // width of the gate_up GEMM output: 2f (SwiGLU) or f (squared ReLU)
+  int sub;     // sub-layer granularity: independent attention / FFN masks
+  int per_batch;  // one draw per (layer, step) for the whole batch
+  int nm;      // masks per layer: 2 under sub-layer granularity, else 1
 };
 
 int check_cfg(const ld_config* c, Dims* out) {
@@ -106,6 +109,8 @@ int check_cfg(const ld_config* c, Dims* out) {
   if (!std::isfinite(c->res_scale)) return fail(LD_E_INVALID, "res_scale must be finite");
   if (c->block_kind != LD_BLOCK_SWIGLU && c->block_kind != LD_BLOCK_ALIBI_RELU2)
     return fail(LD_E_INVALID, "unknown block_kind %d", c->block_kind);
+  if (c->granularity < 0 || c->granularity > 3)
+    return fail(LD_E_INVALID, "unknown granularity %d", c->granularity);
   const int dh = c->d_model / c->n_heads;
   if (c->dtype == LD_BF16) {
     if (dh != 64 && dh != 128) return fail(LD_E_UNSUPPORTED, "bf16 needs d_head 64 or 128, got %d", dh);
@@ -133,6 +138,9 @@ int check_cfg(const ld_config* c, Dims* out) {
     out->dtype = c->dtype;
     out->kind = c->block_kind;
     out->fw = c->block_kind == LD_BLOCK_SWIGLU ? 2ll * c->d_ff : c->d_ff;
+    out->sub = c->granularity & LD_GRAN_SUBLAYER ? 1 : 0;
+    out->per_batch = c->granularity & LD_GRAN_PER_BATCH ? 1 : 0;
+    out->nm = out->sub ? 2 : 1;
   }
   return LD_OK;
 }
@@ -201,15 +209,17 @@ struct MaskLayout {
   size_t keep, idx, count, r, total;
 };
 
-MaskLayout mask_layout(int64_t L, int64_t B) {
+// nm masks per layer (attention, FFN under sub-layer granularity), stored
+// [layer][mask][batch].
+MaskLayout mask_layout(int64_t L, int64_t B, int64_t nm) {
   MaskLayout m{};
   size_t o = 0;
   m.keep = o;
-  o += up(L * B);
+  o += up(L * nm * B);
   m.idx = o;
-  o += up(4 * L * B);
+  o += up(4 * L * nm * B);
   m.count = o;
-  o += up(4 * L);
+  o += up(4 * L * nm);
   m.r = o;
   o += up(4 * L);
   m.total = o;
@@ -263,12 +273,22 @@ BwdLayout bwd_layout(const Dims& D) {
   return L;
 }
 
-// Pointers of one layer's mask data on the device.
+// Pointers of one sub-block's mask data on the device.
 struct MaskView {
   const uint8_t* keep;
   const int32_t* idx;
   const int32_t* count;
   const float* r;
+};
+
+// The masks of one layer: attention and FFN views (the same view under layer
+// granularity), what the host knows of them (-1: decided on the device;
+// 0: dropped for the whole batch; 1: kept for the whole batch, from the
+// per-batch draw), and the kept counts while profiling (-1 otherwise).
+struct LayerMasks {
+  MaskView a, f;
+  int host_a, host_f;
+  int64_t hc_a, hc_f;
 };
 
 struct ActPtrs {
@@ -330,9 +350,13 @@ int run_gemm(int dtype, int a_k, int b_k, GemmArgs g, int64_t max_m, int64_t hos
 
 // ------------------------------------------------------------ one layer
 
-// hc: the layer's kept count when profiling (read back by the caller), else -1.
-int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
-                  const ActPtrs& act, void* x, int64_t hc, hipStream_t s) {
+// Attention sub-block on the rows mv keeps.  hc: its kept count when
+// profiling (read back by the caller), else -1.  scatter = 0 leaves
+// Z = X + r f_attn(X) compacted in act (zk) for the FFN sub-block of the same
+// rows; scatter = 1 writes Z into the kept rows of x (sub-layer granularity,
+// where the FFN keeps its own rows).
+int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
+                      const ActPtrs& act, void* x, int64_t hc, bool scatter, hipStream_t s) {
   const int dt = D.dtype;
   const int64_t T = D.T;
   const int64_t hm = hc * D.S;
@@ -386,17 +410,21 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
     if ((e = launch_attn_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "attn_fwd: %s", hipGetErrorString(e));
     ps.end(2.0 * hc * D.d * D.S * (D.S + 1.0), D.es * hm * D.d * 4.0);
   }
-  // zk = xk + r * (att W_o^T)
+  // zk = xk + r * (att W_o^T), or x[kept rows] = the same
   {
     GemmArgs g = gemm_args();
     g.A = act.at(act.L.att);
     g.lda = D.d;
     g.B = w.w_o;
     g.ldb = D.d;
-    g.C = act.at(act.L.zk);
+    g.C = scatter ? x : act.at(act.L.zk);
     g.ldc = D.d;
     g.R = act.at(act.L.xk);
     g.ldr = D.d;
+    if (scatter) {
+      g.r_mapped = 0;
+      g.out_map = {mv.idx, static_cast<int32_t>(D.S)};
+    }
     g.alpha_dev = mv.r;
     g.N = static_cast<int32_t>(D.d);
     g.K = static_cast<int32_t>(D.d);
@@ -404,11 +432,29 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
     g.count_mult = static_cast<int32_t>(D.S);
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
   }
+  return LD_OK;
+}
+
+// FFN sub-block on the rows mv keeps, written into x.  gather = 0 reads Z from
+// act (zk, left there by attn_forward_part for the same rows); gather = 1
+// reads the kept rows of x (which then holds Z) and saves them to zk.
+int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
+                     const ActPtrs& act, void* x, int64_t hc, bool gather, hipStream_t s) {
+  const int dt = D.dtype;
+  const int64_t T = D.T;
+  const int64_t hm = hc * D.S;
+  hipError_t e;
   // RMSNorm (FFN input)
   {
     RmsFwdArgs a{};
-    a.x = act.at(act.L.zk);
-    a.src = {nullptr, 1};
+    if (gather) {
+      a.x = x;
+      a.src = {mv.idx, static_cast<int32_t>(D.S)};
+      a.xcopy = act.at(act.L.zk);
+    } else {
+      a.x = act.at(act.L.zk);
+      a.src = {nullptr, 1};
+    }
     a.g = w.g_mlp;
     a.y = act.at(act.L.h2);
     a.rstd = act.at<float>(act.L.rstd2);
@@ -417,7 +463,7 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
     a.eps = cfg->rms_eps;
     ProfScope ps("ld_rmsnorm_fwd_k", s);
     if ((e = launch_rmsnorm_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
-    ps.end(0, D.es * hm * D.d * 2.0 + 4.0 * hm);
+    ps.end(0, D.es * hm * D.d * (gather ? 3.0 : 2.0) + 4.0 * hm);
   }
   // [u v] = h2 W_gate_up^T (SwiGLU), u = h2 W_up^T (squared ReLU)
   {
@@ -474,9 +520,54 @@ int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, cons
   return LD_OK;
 }
 
-int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const ActPtrs& act,
-                   const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, int64_t hc,
-                   hipStream_t s) {
+// Weight gradients of a sub-block skipped for the whole batch: zeros.
+int zero_grads(const Dims& D, const ld_grads& dw, bool attn, bool ffn, hipStream_t s) {
+  ZeroArgs z{};
+  if (attn) {
+    z.p[z.count] = dw.g_attn, z.n[z.count++] = D.d;
+    z.p[z.count] = dw.w_qkv, z.n[z.count++] = 3 * D.d * D.d;
+    z.p[z.count] = dw.w_o, z.n[z.count++] = D.d * D.d;
+  }
+  if (ffn) {
+    z.p[z.count] = dw.g_mlp, z.n[z.count++] = D.d;
+    z.p[z.count] = dw.w_gate_up, z.n[z.count++] = D.fw * D.d;
+    z.p[z.count] = dw.w_down, z.n[z.count++] = D.d * D.f;
+  }
+  if (!z.count) return LD_OK;
+  ProfScope ps("ld_zero_f32_k", s);
+  hipError_t e = launch_zero_f32(z, s);
+  if (e != hipSuccess) return fail(LD_E_HIP, "zero fill: %s", hipGetErrorString(e));
+  double n = 0;
+  for (int i = 0; i < z.count; ++i) n += static_cast<double>(z.n[i]);
+  ps.end(0, 4.0 * n);
+  return LD_OK;
+}
+
+// One layer forward.  Layer granularity: both sub-blocks on the same rows, Z
+// kept compacted between them.  Sub-layer granularity: each sub-block on its
+// own rows, Z passed through x.  A sub-block the host knows to be dropped for
+// the whole batch launches nothing.
+int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, const LayerMasks& lm,
+                  const ActPtrs& act, void* x, hipStream_t s) {
+  if (!D.sub) {
+    if (lm.host_a == 0) return LD_OK;
+    if (int rc = attn_forward_part(cfg, D, w, lm.a, act, x, lm.hc_a, false, s)) return rc;
+    return ffn_forward_part(cfg, D, w, lm.a, act, x, lm.hc_a, false, s);
+  }
+  if (lm.host_a != 0)
+    if (int rc = attn_forward_part(cfg, D, w, lm.a, act, x, lm.hc_a, true, s)) return rc;
+  if (lm.host_f != 0)
+    if (int rc = ffn_forward_part(cfg, D, w, lm.f, act, x, lm.hc_f, true, s)) return rc;
+  return LD_OK;
+}
+
+// Backward of ffn_forward_part on the rows mv keeps, given dL/dX^{l+1} in
+// dx.  scatter = 0 leaves dL/dZ of those rows compacted in the scratch (gz)
+// for the attention sub-block of the same rows; scatter = 1 writes it into
+// the kept rows of dx (sub-layer granularity).
+int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, const ActPtrs& act,
+                      const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, int64_t hc,
+                      bool scatter, hipStream_t s) {
   const int dt = D.dtype;
   const int64_t T = D.T;
   const int64_t hm = hc * D.S;
@@ -590,14 +681,43 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
     a.rstd = act.at<float>(act.L.rstd2);
     a.gy = W(BL.gh);
     a.gres = W(BL.gk);
-    a.gx = W(BL.gz);
-    a.dst = {nullptr, 1};
+    a.gx = scatter ? dx : W(BL.gz);
+    a.dst = scatter ? RowMap{mv.idx, S} : RowMap{nullptr, 1};
     a.dg_part = reinterpret_cast<float*>(ws + BL.dg_part);
     a.rc = {mv.count, S, T};
     a.d = static_cast<int32_t>(D.d);
     ProfScope ps("ld_rmsnorm_bwd_k", s);
     if ((e = launch_rmsnorm_bwd(dt, a, dw.g_mlp, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_bwd: %s", hipGetErrorString(e));
     ps.end(0, D.es * hm * D.d * 4.0);
+  }
+  return LD_OK;
+}
+
+// Backward of attn_forward_part on the rows mv keeps; dL/dX^l of those rows
+// is written into dx.  gather = 0 takes dL/dZ from the scratch (gz, left by
+// ffn_backward_part for the same rows); gather = 1 reads the kept rows of dx,
+// which then holds dL/dZ.
+int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, const ActPtrs& act,
+                       const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, int64_t hc,
+                       bool gather, hipStream_t s) {
+  const int dt = D.dtype;
+  const int64_t T = D.T;
+  const int64_t hm = hc * D.S;
+  const int32_t S = static_cast<int32_t>(D.S);
+  auto W = [&](size_t off) { return static_cast<void*>(ws + off); };
+  float* SK = BL.splitk_bytes ? reinterpret_cast<float*>(ws + BL.splitk) : nullptr;
+  hipError_t e;
+  if (gather) {
+    RowsArgs a{};
+    a.src = dx;
+    a.dst = W(BL.gz);
+    a.src_map = {mv.idx, S};
+    a.dst_map = {nullptr, 1};
+    a.rc = {mv.count, S, T};
+    a.d = static_cast<int32_t>(D.d);
+    ProfScope ps("ld_gather_rows_k", s);
+    if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
+    ps.end(0, 2.0 * D.es * hm * D.d);
   }
   // ga = r * gz W_o   [M, d]
   {
@@ -712,6 +832,25 @@ int layer_backward(const Dims& D, const ld_weights& w, const MaskView& mv, const
   return LD_OK;
 }
 
+// One layer backward (FFN sub-block, then attention), mirroring layer_forward.
+// A sub-block the host knows to be dropped for the whole batch launches only
+// the zero fill of its weight gradients.
+int layer_backward(const Dims& D, const ld_weights& w, const LayerMasks& lm, const ActPtrs& act,
+                   const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, hipStream_t s) {
+  if (!D.sub) {
+    if (lm.host_a == 0) return zero_grads(D, dw, true, true, s);
+    if (int rc = ffn_backward_part(D, w, lm.a, act, BL, ws, dx, dw, lm.hc_a, false, s)) return rc;
+    return attn_backward_part(D, w, lm.a, act, BL, ws, dx, dw, lm.hc_a, false, s);
+  }
+  if (lm.host_f == 0) {
+    if (int rc = zero_grads(D, dw, false, true, s)) return rc;
+  } else if (int rc = ffn_backward_part(D, w, lm.f, act, BL, ws, dx, dw, lm.hc_f, true, s)) {
+    return rc;
+  }
+  if (lm.host_a == 0) return zero_grads(D, dw, true, false, s);
+  return attn_backward_part(D, w, lm.a, act, BL, ws, dx, dw, lm.hc_a, true, s);
+}
+
 int check_weights(const ld_weights* w) {
   if (!w || !w->g_attn || !w->w_qkv || !w->w_o || !w->g_mlp || !w->w_gate_up || !w->w_down)
     return fail(LD_E_INVALID, "weights pointer NULL");
@@ -723,9 +862,10 @@ int check_grads(const ld_grads* g) {
   return LD_OK;
 }
 
-int launch_mask_range(const ld_config* cfg, int32_t n, int32_t batch, const float* p, int32_t first,
-                      uint64_t seed, uint64_t step, const uint8_t* ovr, uint8_t* keep, int32_t* idx,
-                      int32_t* count, float* r_out, hipStream_t s) {
+// nm masks per layer, drawn per sequence or (per_batch) once per layer.
+int launch_mask_range(const ld_config* cfg, int32_t n, int32_t batch, int32_t nm, int32_t per_batch,
+                      const float* p, int32_t first, uint64_t seed, uint64_t step, const uint8_t* ovr,
+                      uint8_t* keep, int32_t* idx, int32_t* count, float* r_out, hipStream_t s) {
   for (int32_t l0 = 0; l0 < n; l0 += kMaxMaskLayers) {
     const int32_t nl = std::min<int32_t>(kMaxMaskLayers, n - l0);
     MaskArgs a;
@@ -737,19 +877,58 @@ int launch_mask_range(const ld_config* cfg, int32_t n, int32_t batch, const floa
     a.n_layers = nl;
     a.batch = batch;
     a.first_layer = first + l0;
+    a.n_masks = nm;
+    a.per_batch = per_batch;
     a.seed = seed;
     a.step = step;
-    a.keep_override = ovr ? ovr + static_cast<int64_t>(l0) * batch : nullptr;
-    a.keep = keep + static_cast<int64_t>(l0) * batch;
-    a.idx = idx + static_cast<int64_t>(l0) * batch;
-    a.count = count + l0;
+    const int64_t rows = static_cast<int64_t>(l0) * nm;
+    a.keep_override = ovr ? ovr + rows * batch : nullptr;
+    a.keep = keep + rows * batch;
+    a.idx = idx + rows * batch;
+    a.count = count + rows;
     a.r_out = r_out ? r_out + l0 : nullptr;
     ProfScope ps("ld_mask_compact", s);
     hipError_t e = launch_masks(a, s);
     if (e != hipSuccess) return fail(LD_E_HIP, "mask launch: %s", hipGetErrorString(e));
-    ps.end(0, 13.0 * nl * batch);
+    ps.end(0, 13.0 * nl * nm * batch);
   }
   return LD_OK;
+}
+
+// What the host knows of mask m of `layer` before any launch: under per-batch
+// granularity without an override the draw is taken here (the same Philox
+// block the mask kernel uses), so 0 = dropped for the whole batch and 1 =
+// kept; -1 otherwise (decided on the device).
+int host_mask_state(const Dims& D, float p, int64_t layer, uint64_t seed, uint64_t step,
+                    const uint8_t* ovr, int m) {
+  if (!D.per_batch || ovr) return -1;
+  uint64_t thr;
+  uint8_t drop_all;
+  threshold(p, &thr, &drop_all);
+  if (drop_all) return 0;
+  return mask_draw(0, static_cast<uint64_t>(layer), step, seed, 1, m) < thr ? 0 : 1;
+}
+
+// The masks of layer l of a block laid out by mask_layout (layer-major).
+LayerMasks layer_masks(const Dims& D, const MaskLayout& ml, char* base, int64_t l, int64_t layer_id,
+                       float p, uint64_t seed, uint64_t step, const uint8_t* ovr,
+                       const std::vector<int64_t>& hc) {
+  uint8_t* keep = reinterpret_cast<uint8_t*>(base + ml.keep);
+  int32_t* idx = reinterpret_cast<int32_t*>(base + ml.idx);
+  int32_t* count = reinterpret_cast<int32_t*>(base + ml.count);
+  float* r = reinterpret_cast<float*>(base + ml.r);
+  auto view = [&](int64_t m) {
+    const int64_t row = l * D.nm + m;
+    return MaskView{keep + row * D.B, idx + row * D.B, count + row, r + l};
+  };
+  LayerMasks lm{};
+  lm.a = view(0);
+  lm.f = view(D.nm - 1);
+  lm.host_a = host_mask_state(D, p, layer_id, seed, step, ovr, 0);
+  lm.host_f = host_mask_state(D, p, layer_id, seed, step, ovr, D.nm - 1);
+  lm.hc_a = hc[l * D.nm];
+  lm.hc_f = hc[l * D.nm + D.nm - 1];
+  return lm;
 }
 
 }  // namespace
@@ -801,15 +980,25 @@ int ld_schedule_p(int32_t dist, int32_t sched, float p_max, int32_t layer, int32
 
 int ld_masks(int32_t n_layers, int32_t batch, const float* p, int32_t first_layer, uint64_t seed,
              uint64_t step, uint8_t* keep, int32_t* idx, int32_t* count, void* stream) {
+  return ld_masks_granular(LD_GRAN_LAYER_SEQ, n_layers, batch, p, first_layer, seed, step, keep, idx,
+                           count, stream);
+}
+
+int ld_masks_granular(int32_t granularity, int32_t n_layers, int32_t batch, const float* p,
+                      int32_t first_layer, uint64_t seed, uint64_t step, uint8_t* keep, int32_t* idx,
+                      int32_t* count, void* stream) {
   t_err.clear();
+  if (granularity < 0 || granularity > 3) return fail(LD_E_INVALID, "unknown granularity %d", granularity);
   if (n_layers < 1 || n_layers > kMaxMaskLayers) return fail(LD_E_INVALID, "n_layers outside [1, %d]", kMaxMaskLayers);
   if (batch < 1) return fail(LD_E_INVALID, "batch < 1");
   if (first_layer < 0) return fail(LD_E_INVALID, "first_layer < 0");
   if (!p || !keep || !idx || !count) return fail(LD_E_INVALID, "NULL pointer");
   for (int32_t i = 0; i < n_layers; ++i)
     if (int rc = check_p(p[i])) return rc;
-  return launch_mask_range(nullptr, n_layers, batch, p, first_layer, seed, step, nullptr, keep, idx,
-                           count, nullptr, as_stream(stream));
+  const int32_t nm = granularity & LD_GRAN_SUBLAYER ? 2 : 1;
+  const int32_t pb = granularity & LD_GRAN_PER_BATCH ? 1 : 0;
+  return launch_mask_range(nullptr, n_layers, batch, nm, pb, p, first_layer, seed, step, nullptr, keep,
+                           idx, count, nullptr, as_stream(stream));
 }
 
 int ld_gather_rows(const ld_config* cfg, const int32_t* idx, const int32_t* count, const void* x,
@@ -853,7 +1042,7 @@ int ld_scatter_add_rows(const ld_config* cfg, const int32_t* idx, const int32_t*
 size_t ld_layer_ctx_bytes(const ld_config* cfg) {
   Dims D;
   if (check_cfg(cfg, &D)) return 0;
-  return mask_layout(1, D.B).total + act_layout(D).total;
+  return mask_layout(1, D.B, D.nm).total + act_layout(D).total;
 }
 
 size_t ld_layer_ws_bytes(const ld_config* cfg) {
@@ -865,7 +1054,7 @@ size_t ld_layer_ws_bytes(const ld_config* cfg) {
 size_t ld_stack_ws_bytes(const ld_config* cfg, int32_t n_layers) {
   Dims D;
   if (check_cfg(cfg, &D) || n_layers < 1) return 0;
-  return mask_layout(n_layers, D.B).total + static_cast<size_t>(n_layers) * act_layout(D).total +
+  return mask_layout(n_layers, D.B, D.nm).total + static_cast<size_t>(n_layers) * act_layout(D).total +
          bwd_layout(D).total;
 }
 
@@ -882,18 +1071,18 @@ int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float
   (void)ws;
   (void)ws_bytes;
   hipStream_t s = as_stream(stream);
-  const MaskLayout ml = mask_layout(1, D.B);
+  const MaskLayout ml = mask_layout(1, D.B, D.nm);
   char* c = static_cast<char*>(ctx);
-  uint8_t* keep = reinterpret_cast<uint8_t*>(c + ml.keep);
-  int32_t* idx = reinterpret_cast<int32_t*>(c + ml.idx);
   int32_t* count = reinterpret_cast<int32_t*>(c + ml.count);
-  float* r = reinterpret_cast<float*>(c + ml.r);
-  if (int rc = launch_mask_range(cfg, 1, static_cast<int32_t>(D.B), &p, layer, seed, step,
-                                 keep_override, keep, idx, count, r, s))
+  if (int rc = launch_mask_range(cfg, 1, static_cast<int32_t>(D.B), D.nm, D.per_batch, &p, layer, seed,
+                                 step, keep_override, reinterpret_cast<uint8_t*>(c + ml.keep),
+                                 reinterpret_cast<int32_t*>(c + ml.idx), count,
+                                 reinterpret_cast<float*>(c + ml.r), s))
     return rc;
   ActPtrs act{c + ml.total, act_layout(D)};
-  const int64_t hc = host_counts_if_profiling(count, 1, s)[0];
-  return layer_forward(cfg, D, *w, MaskView{keep, idx, count, r}, act, x, hc, s);
+  const std::vector<int64_t> hc = host_counts_if_profiling(count, D.nm, s);
+  const LayerMasks lm = layer_masks(D, ml, c, 0, layer, p, seed, step, keep_override, hc);
+  return layer_forward(cfg, D, *w, lm, act, x, s);
 }
 
 int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, void* dx,
@@ -906,14 +1095,16 @@ int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, voi
   if (!ctx || !dx || !ws) return fail(LD_E_INVALID, "NULL pointer");
   const BwdLayout BL = bwd_layout(D);
   if (ws_bytes < BL.total) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, BL.total);
-  const MaskLayout ml = mask_layout(1, D.B);
+  const MaskLayout ml = mask_layout(1, D.B, D.nm);
   char* c = const_cast<char*>(static_cast<const char*>(ctx));
-  MaskView mv{reinterpret_cast<uint8_t*>(c + ml.keep), reinterpret_cast<int32_t*>(c + ml.idx),
-              reinterpret_cast<int32_t*>(c + ml.count), reinterpret_cast<float*>(c + ml.r)};
   ActPtrs act{c + ml.total, act_layout(D)};
   hipStream_t s = as_stream(stream);
-  const int64_t hc = host_counts_if_profiling(mv.count, 1, s)[0];
-  return layer_backward(D, *w, mv, act, BL, static_cast<char*>(ws), dx, *dw, hc, s);
+  const std::vector<int64_t> hc =
+      host_counts_if_profiling(reinterpret_cast<int32_t*>(c + ml.count), D.nm, s);
+  // the ctx carries no p, seed or step: every decision is the device's
+  LayerMasks lm = layer_masks(D, ml, c, 0, 0, 0.f, 0, 0, nullptr, hc);
+  lm.host_a = lm.host_f = -1;
+  return layer_backward(D, *w, lm, act, BL, static_cast<char*>(ws), dx, *dw, s);
 }
 
 int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const float* p,
@@ -934,35 +1125,36 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
   if (ws_bytes < need) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   hipStream_t s = as_stream(stream);
   const int64_t L = n_layers, B = D.B;
-  const MaskLayout ml = mask_layout(L, B);
+  const int64_t nm = D.nm;
+  const MaskLayout ml = mask_layout(L, B, nm);
   const ActLayout al = act_layout(D);
   const BwdLayout BL = bwd_layout(D);
   char* base = static_cast<char*>(ws);
   uint8_t* keep = reinterpret_cast<uint8_t*>(base + ml.keep);
   int32_t* idx = reinterpret_cast<int32_t*>(base + ml.idx);
   int32_t* count = reinterpret_cast<int32_t*>(base + ml.count);
-  float* r = reinterpret_cast<float*>(base + ml.r);
   char* acts = base + ml.total;
   char* bws = acts + static_cast<size_t>(L) * al.total;
 
-  if (int rc = launch_mask_range(cfg, n_layers, static_cast<int32_t>(B), p, 0, seed, step,
-                                 keep_override, keep, idx, count, r, s))
+  if (int rc = launch_mask_range(cfg, n_layers, static_cast<int32_t>(B), D.nm, D.per_batch, p, 0, seed,
+                                 step, keep_override, keep, idx, count,
+                                 reinterpret_cast<float*>(base + ml.r), s))
     return rc;
-  auto view = [&](int64_t l) {
-    return MaskView{keep + l * B, idx + l * B, count + l, r + l};
-  };
-  const std::vector<int64_t> hc = host_counts_if_profiling(count, L, s);
+  const std::vector<int64_t> hc = host_counts_if_profiling(count, L * nm, s);
+  std::vector<LayerMasks> lms;
+  lms.reserve(L);
+  for (int64_t l = 0; l < L; ++l) lms.push_back(layer_masks(D, ml, base, l, l, p[l], seed, step, keep_override, hc));
   for (int64_t l = 0; l < L; ++l) {
     ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
-    if (int rc = layer_forward(cfg, D, w[l], view(l), act, x, hc[l], s)) return rc;
+    if (int rc = layer_forward(cfg, D, w[l], lms[l], act, x, s)) return rc;
   }
   for (int64_t l = L - 1; l >= 0; --l) {
     ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
-    if (int rc = layer_backward(D, w[l], view(l), act, BL, bws, dx, dw[l], hc[l], s)) return rc;
+    if (int rc = layer_backward(D, w[l], lms[l], act, BL, bws, dx, dw[l], s)) return rc;
   }
-  if (keep_out) LD_HIP(hipMemcpyAsync(keep_out, keep, L * B, hipMemcpyDeviceToDevice, s));
-  if (idx_out) LD_HIP(hipMemcpyAsync(idx_out, idx, 4 * L * B, hipMemcpyDeviceToDevice, s));
-  if (count_out) LD_HIP(hipMemcpyAsync(count_out, count, 4 * L, hipMemcpyDeviceToDevice, s));
+  if (keep_out) LD_HIP(hipMemcpyAsync(keep_out, keep, L * nm * B, hipMemcpyDeviceToDevice, s));
+  if (idx_out) LD_HIP(hipMemcpyAsync(idx_out, idx, 4 * L * nm * B, hipMemcpyDeviceToDevice, s));
+  if (count_out) LD_HIP(hipMemcpyAsync(count_out, count, 4 * L * nm, hipMemcpyDeviceToDevice, s));
   return LD_OK;
 }
 

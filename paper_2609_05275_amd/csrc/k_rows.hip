@@ -45,42 +45,18 @@ __device__ __forceinline__ int64_t map_row(const RowMap& m, int64_t row) {
   return static_cast<int64_t>(m.idx[row / m.S]) * m.S + row % m.S;
 }
 
-// ------------------------------------------------- Philox4x64-10 + masks
-// Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
-// (SC'11): 10 rounds of two 64x64->128 multiplies, the key bumped by the
-// Weyl constants between rounds.  Only word 0 of the output is used.
-__device__ __forceinline__ uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2,
-                                                 uint64_t c3, uint64_t k0, uint64_t k1) {
-  constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
-  constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
-#pragma unroll
-  for (int round = 0; round < 10; ++round) {
-    if (round) {
-      k0 += kW0;
-      k1 += kW1;
-    }
-    const uint64_t lo0 = kM0 * c0, hi0 = __umul64hi(kM0, c0);
-    const uint64_t lo1 = kM1 * c2, hi1 = __umul64hi(kM1, c2);
-    const uint64_t n0 = hi1 ^ c1 ^ k0;
-    const uint64_t n2 = hi0 ^ c3 ^ k1;
-    c0 = n0;
-    c1 = lo1;
-    c2 = n2;
-    c3 = lo0;
-  }
-  return c0;
-}
+// ------------------------------------------------------------- masks
 
-// One workgroup per layer.  Each chunk of blockDim samples draws its bits,
+// One workgroup per (layer, mask).  Each chunk of blockDim samples draws its bits,
 // a 64-wide ballot + popcount of the lower lanes gives each kept sample its
 // rank inside the wave, and a serial scan of the per-wave totals in LDS gives
 // the wave offsets, so the kept list comes out ascending.
 __global__ __launch_bounds__(1024) void ld_mask_compact(MaskArgs a) {
   __shared__ int wave_tot[16];
-  const int layer = blockIdx.x;
+  const int layer = blockIdx.x / a.n_masks, m = blockIdx.x % a.n_masks;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_waves = blockDim.x >> 6;
-  const int64_t row = static_cast<int64_t>(layer) * a.batch;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * a.batch;
   int base = 0;
   for (int b0 = 0; b0 < a.batch; b0 += blockDim.x) {
     const int b = b0 + tid;
@@ -89,9 +65,9 @@ __global__ __launch_bounds__(1024) void ld_mask_compact(MaskArgs a) {
       if (a.keep_override) {
         keep = a.keep_override[row + b] != 0;
       } else if (!a.drop_all[layer]) {
-        const uint64_t w = philox_word0(static_cast<uint64_t>(b),
-                                        static_cast<uint64_t>(a.first_layer + layer), a.step, 0,
-                                        a.seed, 0);
+        const uint64_t w = mask_draw(static_cast<uint64_t>(b),
+                                     static_cast<uint64_t>(a.first_layer + layer), a.step, a.seed,
+                                     a.per_batch, m);
         keep = !(w < a.thr[layer]);
       }
       a.keep[row + b] = static_cast<uint8_t>(keep);
@@ -111,8 +87,24 @@ __global__ __launch_bounds__(1024) void ld_mask_compact(MaskArgs a) {
   }
   for (int j = base + tid; j < a.batch; j += blockDim.x) a.idx[row + j] = -1;
   if (tid == 0) {
-    a.count[layer] = base;
-    if (a.r_out) a.r_out[layer] = a.r[layer];
+    a.count[blockIdx.x] = base;
+    if (a.r_out && m == 0) a.r_out[layer] = a.r[layer];
+  }
+}
+
+__global__ __launch_bounds__(256) void ld_zero_f32_k(ZeroArgs a) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  for (int i = 0; i < a.count; ++i) {
+    float* p = a.p[i];
+    const int64_t n = a.n[i];
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+      const int64_t n4 = n / 4;
+      for (int64_t j = t0; j < n4; j += stride) reinterpret_cast<float4*>(p)[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int64_t j = n4 * 4 + t0; j < n; j += stride) p[j] = 0.f;
+    } else {
+      for (int64_t j = t0; j < n; j += stride) p[j] = 0.f;
+    }
   }
 }
 
@@ -468,7 +460,15 @@ int64_t rmsnorm_bwd_blocks(int64_t max_rows) {
 hipError_t launch_masks(const MaskArgs& a, hipStream_t s) {
   int threads = ((a.batch + 63) / 64) * 64;
   if (threads > 1024) threads = 1024;
-  hipLaunchKernelGGL(ld_mask_compact, dim3(a.n_layers), dim3(threads), 0, s, a);
+  hipLaunchKernelGGL(ld_mask_compact, dim3(a.n_layers * a.n_masks), dim3(threads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_f32(const ZeroArgs& a, hipStream_t s) {
+  int64_t most = 0;
+  for (int i = 0; i < a.count; ++i) most = a.n[i] > most ? a.n[i] : most;
+  if (most == 0) return hipSuccess;
+  hipLaunchKernelGGL(ld_zero_f32_k, dim3(elt_grid(most / 4 + 1)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

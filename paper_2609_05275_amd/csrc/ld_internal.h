@@ -77,6 +77,50 @@ struct RowMap {
   int32_t S;
 };
 
+// ------------------------------------------------------ Philox4x64-10
+// Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
+// (SC'11): 10 rounds of two 64x64->128 multiplies, the key bumped by the
+// Weyl constants between rounds.  Host and device share this definition, so
+// the host can take the per-batch draws itself.
+struct Philox4 {
+  uint64_t w[4];
+};
+
+__host__ __device__ inline uint64_t mulhi64(uint64_t a, uint64_t b) {
+  return static_cast<uint64_t>((static_cast<unsigned __int128>(a) * b) >> 64);
+}
+
+__host__ __device__ inline Philox4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
+                                                 uint64_t k0, uint64_t k1) {
+  constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
+  constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    if (round) {
+      k0 += kW0;
+      k1 += kW1;
+    }
+    const uint64_t lo0 = kM0 * c0, hi0 = mulhi64(kM0, c0);
+    const uint64_t lo1 = kM1 * c2, hi1 = mulhi64(kM1, c2);
+    const uint64_t n0 = hi1 ^ c1 ^ k0;
+    const uint64_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  return Philox4{{c0, c1, c2, c3}};
+}
+
+// The Bernoulli draws of the masks.  Per sequence: block (b, l, t, 0); per
+// batch: block (0, l, t, 1); key (seed, 0).  Mask m of a layer (0: attention
+// or whole layer, 1: FFN under sub-layer granularity) takes word m.
+__host__ __device__ inline uint64_t mask_draw(uint64_t b, uint64_t layer, uint64_t step, uint64_t seed,
+                                              int per_batch, int m) {
+  const Philox4 r = philox4x64_10(per_batch ? 0 : b, layer, step, per_batch ? 1 : 0, seed, 0);
+  return r.w[m];
+}
+
 constexpr int kMaxMaskLayers = 128;
 
 struct MaskArgs {
@@ -84,12 +128,22 @@ struct MaskArgs {
   uint8_t drop_all[kMaxMaskLayers]; // p >= 1
   float r[kMaxMaskLayers];          // residual scale per layer (0 for p >= 1)
   int32_t n_layers, batch, first_layer;
+  int32_t n_masks;                  // 1, or 2 under sub-layer granularity
+  int32_t per_batch;                // one draw per (layer, step) for the batch
   uint64_t seed, step;
-  const uint8_t* keep_override;     // [n_layers][batch] or null
-  uint8_t* keep;                    // [n_layers][batch]
-  int32_t* idx;                     // [n_layers][batch]
-  int32_t* count;                   // [n_layers]
+  const uint8_t* keep_override;     // [n_layers][n_masks][batch] or null
+  uint8_t* keep;                    // [n_layers][n_masks][batch]
+  int32_t* idx;                     // [n_layers][n_masks][batch]
+  int32_t* count;                   // [n_layers][n_masks]
   float* r_out;                     // [n_layers] or null: copy of r for the layer
+};
+
+// Zero fill of up to 6 float32 arrays (the weight gradients of a layer or
+// sub-block that is skipped as a whole).
+struct ZeroArgs {
+  float* p[6];
+  int64_t n[6];
+  int32_t count;
 };
 
 struct RmsFwdArgs {
@@ -192,6 +246,7 @@ __host__ __device__ inline float alibi_slope(int h, int H) {
 // host upper bound; work past the device count exits early.
 
 hipError_t launch_masks(const MaskArgs& a, hipStream_t s);
+hipError_t launch_zero_f32(const ZeroArgs& a, hipStream_t s);
 hipError_t launch_gather(int dtype, const RowsArgs& a, hipStream_t s);
 hipError_t launch_scatter_add(int dtype, const RowsArgs& a, hipStream_t s);
 hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s);

@@ -84,6 +84,9 @@ def test_workspace_sizes():
     (dict(dtype=7), 1),
     (dict(rms_eps=0.0), 1),
     (dict(batch=0), 2),
+    (dict(block_kind=2), 1),
+    (dict(granularity=4), 1),
+    (dict(granularity=-1), 1),
 ])
 def test_invalid_configs_rejected(kw, code):
     c = _cfg(**kw)
@@ -112,6 +115,25 @@ def test_invalid_p_and_pointers_rejected():
     with pytest.raises(ld.LdError) as e:
         ld.ld_layer_fwd(c, w, 0, 0.1, 0, 0, 16, 16, stream=0)
     assert e.value.status == 1
+
+
+def test_granular_masks_reject_bad_arguments():
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_masks_granular(4, [0.1], 0, 0, _Fake((1, 8)), 8, 8, stream=0)
+    assert e.value.status == 1
+    with pytest.raises(ld.LdError) as e:
+        ld.ld_masks_granular(1, [0.1, -0.5], 0, 0, _Fake((2, 2, 8)), 8, 8, stream=0)
+    assert e.value.status == 1
+
+
+def test_sublayer_ctx_holds_two_masks():
+    small = dict(batch=1000, seq=64)   # mask arrays are padded to 256 bytes
+    one = ld.ld_layer_ctx_bytes(_cfg(**small))
+    two = ld.ld_layer_ctx_bytes(_cfg(granularity=ld.LD_GRAN_SUBLAYER_SEQ, **small))
+    assert two - one >= 1000 * 5      # a second keep row (1 B) and idx row (4 B) per sample
+    assert ld.ld_layer_ctx_bytes(_cfg(granularity=ld.LD_GRAN_LAYER_BATCH, **small)) == one
+    assert (ld.ld_stack_ws_bytes(_cfg(granularity=3, **small), 16)
+            > ld.ld_stack_ws_bytes(_cfg(**small), 16))
 
 
 def test_gemm_shape_checks():
