@@ -20,6 +20,13 @@ layer), n_ffn = 3 (SwiGLU) or 2 (squared ReLU).
 --workload paper_3p9b runs the paper's own block (ALiBi attention, squared
 ReLU) at its 3.9B architecture (d 2048, 40 layers, 16 heads of 128, d_ff
 16384), same sequence length, batch and rates.
+
+--granularity selects the masks (Dropout Granularity section): layer_seq
+(default: one mask per layer, drawn per sequence), sublayer_seq (independent
+attention and FFN masks), layer_batch (one draw per layer for the whole
+batch), sublayer_batch.  F_sl then splits into its attention part
+3 * [2 S 4 d^2 + 2 d S (S+1)] per kept attention (sequence, layer) and its
+FFN part 3 * 2 S n_ffn d d_ff per kept FFN (sequence, layer).
 """
 import argparse
 import json
@@ -75,17 +82,23 @@ def copy_calibration(mib):
     del x, y
 
 
-def f_sl(sh):
+GRANULARITIES = {"layer_seq": 0, "sublayer_seq": 1, "layer_batch": 2, "sublayer_batch": 3}
+
+
+def f_parts(sh):
+    """Executed FLOPs (forward + backward) per kept (sequence, layer) of the
+    attention and the FFN sub-block."""
     S, d, f = sh.seq, sh.d_model, sh.d_ff
     n_ffn = 3 if sh.kind == 0 else 2
-    return 3.0 * (2.0 * S * (4 * d * d + n_ffn * d * f) + 2.0 * d * S * (S + 1))
+    return 3.0 * (2.0 * S * 4 * d * d + 2.0 * d * S * (S + 1)), 3.0 * 2.0 * S * n_ffn * d * f
 
 
 class Stack:
-    def __init__(self, sh, dev):
-        self.sh, self.dev = sh, dev
+    def __init__(self, sh, dev, gran=0):
+        self.sh, self.dev, self.gran = sh, dev, gran
+        self.nm = 2 if gran & 1 else 1
         self.cfg = ld.config(sh.batch, sh.seq, sh.d_model, sh.n_heads, sh.d_ff, ld.LD_BF16,
-                             block_kind=sh.kind)
+                             block_kind=sh.kind, granularity=gran)
         L = sh.n_layers
         self.W = [inp.device_layer_weights(sh, l, dev) for l in range(L)]
         self.dW = [{k: torch.empty(s, dtype=torch.float32, device=dev)
@@ -108,13 +121,16 @@ class Stack:
                          count_out=count_out)
 
     def kept(self, ps, step):
-        """Sum of kept counts of one step (device mask kernel, outside timing)."""
-        L, B = self.sh.n_layers, self.sh.batch
-        keep = torch.empty(L, B, dtype=torch.uint8, device=self.dev)
-        idx = torch.empty(L, B, dtype=torch.int32, device=self.dev)
-        cnt = torch.empty(L, dtype=torch.int32, device=self.dev)
-        ld.ld_masks(ps, 0, step, keep, idx, cnt)
-        return int(cnt.sum().item())
+        """Kept (sequence, layer) counts of one step for the attention and the
+        FFN sub-block (equal under layer granularity); device mask kernel,
+        outside timing."""
+        L, B, nm = self.sh.n_layers, self.sh.batch, self.nm
+        keep = torch.empty(L, nm, B, dtype=torch.uint8, device=self.dev)
+        idx = torch.empty(L, nm, B, dtype=torch.int32, device=self.dev)
+        cnt = torch.empty(L, nm, dtype=torch.int32, device=self.dev)
+        ld.ld_masks_granular(self.gran, ps, 0, step, keep, idx, cnt)
+        c = cnt.sum(dim=0).cpu().numpy()
+        return int(c[0]), int(c[-1])
 
 
 def time_steps(st, ps, first_step, steps, warmup):
@@ -126,7 +142,7 @@ def time_steps(st, ps, first_step, steps, warmup):
         st.step(ps, first_step + i)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
-    kept = [st.kept(ps, first_step + i) for i in range(steps)]
+    kept = np.array([st.kept(ps, first_step + i) for i in range(steps)], dtype=np.float64)
     return ms, kept
 
 
@@ -160,6 +176,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--workload", default="1b", choices=["1b", "paper_3p9b"])
+    ap.add_argument("--granularity", default="layer_seq", choices=list(GRANULARITIES))
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run the traffic-counter calibration copy of this size first")
     ap.add_argument("--prof-kernel", default=None,
@@ -175,8 +192,16 @@ def main():
         copy_calibration(args.copy_calib_mib)
     sh = inp.SHAPES[args.workload]
     dev = "cuda:0"
-    st = Stack(sh, dev)
-    fsl = f_sl(sh)
+    gran = GRANULARITIES[args.granularity]
+    st = Stack(sh, dev, gran)
+    fa, ff = f_parts(sh)
+
+    def exec_flops(kept):          # kept: [steps, 2] attention / FFN counts
+        return float(np.mean(fa * kept[:, 0] + ff * kept[:, 1]))
+
+    def drop_frac(kept):
+        return 1.0 - float(np.mean(kept)) / (sh.n_layers * sh.batch)
+
     tokens = sh.batch * sh.seq
     ps = st.rates(args.p_max, T_RAMP - 1)
     first = T_RAMP - 1
@@ -210,10 +235,10 @@ def main():
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
     ld.ld_prof_stop()
     pr = ld.ld_prof_result()
-    kept = [st.kept(ps, first + i) for i in range(args.steps)]
-    print(f"# headline: {ms:.2f} ms/step, kept seq-layers mean {np.mean(kept):.1f}", file=sys.stderr,
-          flush=True)
-    exec_tflops = fsl * np.mean(kept) / (ms * 1e-3) / 1e12
+    kept = np.array([st.kept(ps, first + i) for i in range(args.steps)], dtype=np.float64)
+    print(f"# headline: {ms:.2f} ms/step, kept seq-layers mean {np.mean(kept, axis=0)}",
+          file=sys.stderr, flush=True)
+    exec_tflops = exec_flops(kept) / (ms * 1e-3) / 1e12
     achieved = pr["flops"] / (pr["ms"] * 1e-3) / 1e12 if pr["ms"] > 0 else 0.0
     trec = traffic_record(prof_kernel, args.workload)
 
@@ -223,10 +248,10 @@ def main():
             for t in (0, 500, 1000):
                 pp = st.rates(p_max, t)
                 sms, skept = time_steps(st, pp, 10_000 + t, 5, 1)
-                f = 1.0 - np.mean(skept) / (sh.n_layers * sh.batch)
-                sweep.append(dict(p_max=p_max, t=t, ms=round(sms, 3), drop_frac=round(f, 4),
+                sweep.append(dict(p_max=p_max, t=t, ms=round(sms, 3),
+                                  drop_frac=round(drop_frac(skept), 4),
                                   tokens_per_s=round(tokens / (sms * 1e-3), 1),
-                                  exec_tflops=round(fsl * np.mean(skept) / (sms * 1e-3) / 1e12, 1)))
+                                  exec_tflops=round(exec_flops(skept) / (sms * 1e-3) / 1e12, 1)))
                 print(f"# sweep {sweep[-1]}", file=sys.stderr, flush=True)
     fit = None
     if len(sweep) >= 3:
@@ -241,12 +266,13 @@ def main():
     cpu = None
     if not args.no_cpu:
         t_unit, n, threads = cpu_baseline(sh)
-        cpu_step_s = t_unit * np.mean(kept)
+        cpu_step_s = t_unit * exec_flops(kept) / (fa + ff)
         cpu = {"value": round(tokens / cpu_step_s, 3), "unit": "tokens/s", "cores": threads,
                "kind": "oracle",
                "sample": f"{n} x one sequence through one {args.workload} layer forward+backward "
                          f"(float64 numpy oracle, {t_unit:.2f} s each), scaled by the mean kept "
-                         f"(sequence, layer) count per step {np.mean(kept):.1f}"}
+                         f"(sequence, layer) work per step ({exec_flops(kept) / (fa + ff):.1f} "
+                         f"whole-layer equivalents)"}
 
     if args.workload == "1b":
         metric = "effective tokens/s per fwd+bwd step (1B-shape stack, ILD p_max 0.2)"
@@ -257,6 +283,9 @@ def main():
         wdesc = ("paper block (ALiBi, squared ReLU) at the 3.9B architecture: L=40, d_model=2048, "
                  "heads=16x128, d_ff=16384, seq=2048, batch=8; ILD p_max=0.2 at the end of a "
                  "0..1000 increasing ramp")
+    if gran:
+        metric = metric[:-1] + f", {args.granularity} masks)"
+        wdesc += f"; {args.granularity} masks"
     out = {
         "metric": metric,
         "value": round(tokens / (ms * 1e-3), 1),
@@ -270,11 +299,11 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": wdesc,
+        "config": {"workload": wdesc, "granularity": args.granularity,
                    "global_batch": sh.batch, "seq_len": sh.seq, "parallelism": "none (1 GPU)"},
         "executed_tflops": round(exec_tflops, 1),
         "mfma_frac_executed": round(exec_tflops / PEAK_BF16_TFLOPS, 4),
-        "drop_frac": round(1 - np.mean(kept) / (sh.n_layers * sh.batch), 4),
+        "drop_frac": round(drop_frac(kept), 4),
         "roofline": {"kernel": prof_kernel, "bound": "mfma", "achieved": round(achieved, 1),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
