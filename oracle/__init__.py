@@ -23,6 +23,8 @@ Modules
             hand-derived backward.
   stack     layer / stack forward+backward under layer dropout.
   rows      bit-level definitions of the isolated gather and scatter-add.
+  infer     evaluation form over a static active-layer set (early exit,
+            layer skipping) and KV-cached incremental decoding.
 
 Parity status: every function here is pinned by a CPU test against
 something other than itself (numpy's own Philox, closed forms printed in the
@@ -30,4 +32,4 @@ paper, torch float64 autograd of the dense block, finite differences,
 special cases p=0 and p=1).  No function is "parity unpinned".
 """
 
-from . import philox, schedule, masks, block, stack, rows  # noqa: F401
+from . import philox, schedule, masks, block, stack, rows, infer  # noqa: F401

@@ -76,3 +76,57 @@ def stack_step(X0, weights, keep, rs, G, n_heads, eps, kind=0):
     loss.backward()
     grads = [{k: w[k].grad.numpy().copy() for k in KEYS} for w in ws]
     return H.detach().numpy(), X.grad.numpy().copy(), grads
+
+
+def eval_stack(X0, weights, active, r_eval, n_heads, eps, kind=0):
+    """Evaluation form over an active set with torch library routines: an
+    active layer is layer_masked with every sequence kept and r = r_eval[l];
+    a skipped layer is the identity.  Returns X_L (numpy float64) and the
+    per-layer keys/values (k, v) [B, S, d] of active layers (None otherwise)."""
+    H = torch.tensor(np.asarray(X0, dtype=np.float64))
+    B, S, d = H.shape
+    kv = []
+    for l, w in enumerate(weights):
+        if not active[l]:
+            kv.append(None)
+            continue
+        wt = {k: torch.tensor(np.asarray(w[k], dtype=np.float64)) for k in KEYS}
+        h1 = F.rms_norm(H, (d,), wt["g_attn"], eps)
+        qkv = h1 @ wt["w_qkv"].T
+        kv.append((qkv[..., d:2 * d].numpy().copy(), qkv[..., 2 * d:].numpy().copy()))
+        H = layer_masked(H, wt, np.ones(B), float(r_eval[l]), n_heads, eps, kind)
+    return H.numpy(), kv
+
+
+def decode_layer(x_new, w, K, V, pos, r, n_heads, eps, kind=0):
+    """One active layer on rows x_new [B, n, d] at positions pos..pos+n-1,
+    attending to cached K, V [B, >= pos, d] plus their own keys/values:
+    scaled_dot_product_attention with an explicit [n, pos+n] mask (-inf past
+    each row's position, plus the ALiBi bias for kind 1)."""
+    X = torch.tensor(np.asarray(x_new, dtype=np.float64))
+    B, n, d = X.shape
+    dh = d // n_heads
+    wt = {k: torch.tensor(np.asarray(w[k], dtype=np.float64)) for k in KEYS}
+    f = wt["w_down"].shape[1]
+    h1 = F.rms_norm(X, (d,), wt["g_attn"], eps)
+    qkv = h1 @ wt["w_qkv"].T
+    Kc = torch.cat([torch.tensor(np.asarray(K, dtype=np.float64)[:, :pos]), qkv[..., d:2 * d]], 1)
+    Vc = torch.cat([torch.tensor(np.asarray(V, dtype=np.float64)[:, :pos]), qkv[..., 2 * d:]], 1)
+    P = pos + n
+    qpos = torch.arange(pos, P, dtype=torch.float64)[:, None]
+    kpos = torch.arange(P, dtype=torch.float64)[None, :]
+    mask = torch.zeros(n_heads, n, P, dtype=torch.float64)
+    if kind == 1:
+        full = alibi_mask(n_heads, P)            # [H, P, P], rows are query positions
+        mask = full[:, pos:P, :]
+    mask = mask.masked_fill((kpos > qpos)[None], float("-inf"))
+    q = qkv[..., :d].reshape(B, n, n_heads, dh).transpose(1, 2)
+    k = Kc.reshape(B, P, n_heads, dh).transpose(1, 2)
+    v = Vc.reshape(B, P, n_heads, dh).transpose(1, 2)
+    a = F.scaled_dot_product_attention(q, k, v, attn_mask=mask)
+    a = a.transpose(1, 2).reshape(B, n, d)
+    Z = X + r * (a @ wt["w_o"].T)
+    h2 = F.rms_norm(Z, (d,), wt["g_mlp"], eps)
+    uv = h2 @ wt["w_gate_up"].T
+    s = F.relu(uv) ** 2 if kind == 1 else F.silu(uv[..., :f]) * uv[..., f:]
+    return (Z + r * (s @ wt["w_down"].T)).numpy()
