@@ -240,6 +240,51 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
                   size_t ws_bytes, const uint8_t* keep_override, uint8_t* keep_out,
                   int32_t* idx_out, int32_t* count_out, void* stream);
 
+/* ------------------------------------------------ evaluation and decoding
+ * Depth-elastic inference (Preliminary section, evaluation equation;
+ * Inference Optimizations section).  An active layer applies
+ *   Z = X + r_eval f_attn(X),  X' = Z + r_eval f_ffn(Z)
+ * to every sequence (no masks); an inactive layer is skipped (identity).
+ * Static early exit at l' is active[l] = (l < l'); intermediate layer
+ * skipping is any active set; a self-speculative draft decodes with a subset
+ * of the layers over the caches the full model wrote.
+ *   active: host uint8[n_layers], NULL = every layer.
+ *   r_eval: host float[n_layers], NULL = 1 for every layer (the paper's
+ *           r_eval = 1, Hyperparameters section).
+ *   kv:     host array of n_layers device pointers, each a bf16 cache
+ *           [B, s_max, 2 d] holding per position the keys (columns 0..d-1,
+ *           head h at h*dh) then the values, as projected by that layer.
+ *           Only active layers' caches are read or written. */
+
+/* Bytes of scratch ld_stack_eval needs (one layer's activations). */
+size_t ld_eval_ws_bytes(const ld_config* cfg);
+
+/* Forward-only pass of the evaluation form over positions 0..S-1
+ * (cfg->seq = S) of every sequence, x [B, S, d] in place.  With kv non-NULL
+ * (bf16 only, s_max >= S) each active layer's keys and values of positions
+ * 0..S-1 are written to its cache.  fp32 and bf16 configurations. */
+int ld_stack_eval(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const uint8_t* active,
+                  const float* r_eval, void* x, void* const* kv, int32_t s_max, void* ws,
+                  size_t ws_bytes, void* stream);
+
+/* Bytes of scratch ld_stack_decode needs for n_new rows per sequence and
+ * caches of s_max positions (0 on invalid arguments). */
+size_t ld_decode_ws_bytes(const ld_config* cfg, int32_t n_new, int32_t s_max);
+
+/* Incremental decoding of n_new rows per sequence at positions
+ * pos..pos+n_new-1 (the same for every sequence): x [B, n_new, d] in place
+ * holds their layer-0 input and receives the output of the last layer.
+ * Each active layer first writes the rows' keys/values into its cache at
+ * those positions, then attends over positions 0..pos+n_new-1 (causal within
+ * the new rows; ALiBi for block kind 1), so positions 0..pos-1 of every
+ * active layer's cache must hold valid keys/values (from ld_stack_eval or
+ * earlier decoding steps).  The result equals the evaluation form's rows at
+ * those positions.  bf16 only; 1 <= n_new <= 8; pos + n_new <= s_max;
+ * cfg->seq is not used (it must still form a valid configuration). */
+int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const uint8_t* active,
+                    const float* r_eval, void* x, void* const* kv, int32_t s_max, int32_t pos,
+                    int32_t n_new, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------- kernel-level entry points
  * The single kernels the layer is built from, exposed for isolated parity
  * tests and roofline measurements.  dtype is an ld_dtype; all row counts are
@@ -296,6 +341,34 @@ int ld_gemm(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int3
  * slope of the 2n-head sequence).  Host function; returns 0 for h outside
  * [0, n_heads) or n_heads < 1. */
 float ld_alibi_slope(int32_t h, int32_t n_heads);
+
+/* Skinny GEMM of decoding, bf16: C[m, n] = (R ? R[m, n] : 0) + alpha *
+ * sum_k A[m, k] W[n, k] for 1 <= M <= 64 rows (A [M, K] and W [N, K] both
+ * k-contiguous, 16-byte aligned, lda and ldw multiples of 8, K % 8 == 0).
+ * ws: device scratch of ld_gemm_skinny_ws_bytes(M, N, K) bytes (may be 0,
+ * then ws may be NULL). */
+size_t ld_gemm_skinny_ws_bytes(int32_t M, int32_t N, int32_t K);
+int ld_gemm_skinny(int32_t M, int32_t N, int32_t K, const void* A, int32_t lda, const void* W, int32_t ldw,
+                   void* C, int32_t ldc, float alpha, const void* R, int32_t ldr, void* ws, size_t ws_bytes,
+                   void* stream);
+
+/* Keys and values of qkv rows (device bf16 [n_seq * n_new, 3 d], row
+ * b*n_new + j) into the cache kv (device bf16 [n_seq, s_max, 2 d]) at
+ * position pos + j of sequence b. */
+int ld_kv_store(int32_t n_seq, int32_t n_new, int32_t d_model, int32_t pos, const void* qkv, void* kv,
+                int32_t s_max, void* stream);
+
+/* Decode attention, bf16: the queries of qkv rows b*n_new + j (device
+ * [n_seq * n_new, 3 H dh], position pos + j) over positions 0..pos+j of the
+ * cache kv (device [n_seq, s_max, 2 H dh], which must already hold the new
+ * rows' keys/values), causal, with the ALiBi bias when alibi = 1.
+ *   o: device bf16 [n_seq * n_new, H dh].  d_head 64 or 128; n_new <= 8.
+ *   ws: device scratch of ld_attn_decode_ws_bytes(n_seq, n_heads, d_head,
+ *   s_max) bytes. */
+size_t ld_attn_decode_ws_bytes(int32_t n_seq, int32_t n_heads, int32_t d_head, int32_t s_max);
+int ld_attn_decode(int32_t n_seq, int32_t n_heads, int32_t d_head, int32_t alibi, int32_t pos, int32_t n_new,
+                   const void* qkv, const void* kv, int32_t s_max, void* o, void* ws, size_t ws_bytes,
+                   void* stream);
 
 /* Causal multi-head attention over n_seq independent sequences.
  *   qkv: device [n_seq*S, 3*H*dh] as produced by x W_qkv^T;

@@ -84,6 +84,19 @@ _SIGS = {
     "ld_attn_bwd_ws_bytes": (_sz, [_i32, _i32, _i32]),
     "ld_attn_bwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                               _sz, _vp]),
+    "ld_eval_ws_bytes": (_sz, [_PCFG]),
+    "ld_stack_eval": (C.c_int, [_PCFG, _i32, C.POINTER(ld_weights), _vp, _vp, _vp, _vp, _i32, _vp,
+                                _sz, _vp]),
+    "ld_decode_ws_bytes": (_sz, [_PCFG, _i32, _i32]),
+    "ld_stack_decode": (C.c_int, [_PCFG, _i32, C.POINTER(ld_weights), _vp, _vp, _vp, _vp, _i32,
+                                  _i32, _i32, _vp, _sz, _vp]),
+    "ld_gemm_skinny_ws_bytes": (_sz, [_i32, _i32, _i32]),
+    "ld_gemm_skinny": (C.c_int, [_i32, _i32, _i32, _vp, _i32, _vp, _i32, _vp, _i32, _f32, _vp, _i32,
+                                 _vp, _sz, _vp]),
+    "ld_kv_store": (C.c_int, [_i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp]),
+    "ld_attn_decode_ws_bytes": (_sz, [_i32, _i32, _i32, _i32]),
+    "ld_attn_decode": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _sz,
+                                 _vp]),
     "ld_prof_start": (C.c_int, [C.c_char_p]),
     "ld_prof_stop": (C.c_int, []),
     "ld_prof_result": (C.c_int, [C.POINTER(_i64), C.POINTER(C.c_double), C.POINTER(C.c_double),
@@ -215,6 +228,79 @@ def ld_stack_step(cfg, ws_list, p, seed, step, x, dx, dw_list, ws, keep_override
     _check(_lib.ld_stack_step(C.byref(cfg), L, wa, pa, seed, step, _ptr(x), _ptr(dx), ga, _ptr(ws),
                               ws.numel() * ws.element_size(), _ptr(keep_override), _ptr(keep_out),
                               _ptr(idx_out), _ptr(count_out), _stream(stream)))
+
+
+def _u8_array(v, n):
+    if v is None:
+        return None
+    return (C.c_uint8 * n)(*[1 if a else 0 for a in v])
+
+
+def _f32_array(v, n):
+    if v is None:
+        return None
+    if isinstance(v, (int, float)):
+        v = [v] * n
+    return (C.c_float * n)(*[float(a) for a in v])
+
+
+def _ptr_array(v, n):
+    if v is None:
+        return None
+    return (C.c_void_p * n)(*[_ptr(t) for t in v])
+
+
+def ld_eval_ws_bytes(cfg):
+    return _lib.ld_eval_ws_bytes(C.byref(cfg))
+
+
+def ld_stack_eval(cfg, ws_list, x, ws, active=None, r_eval=None, kv=None, s_max=0, stream=None):
+    """Forward-only evaluation form over the active layers; kv: list of
+    per-layer caches (None entries allowed for inactive layers)."""
+    L = len(ws_list)
+    wa = (ld_weights * L)(*[weights(w) for w in ws_list])
+    act, rr, kk = _u8_array(active, L), _f32_array(r_eval, L), _ptr_array(kv, L)
+    _check(_lib.ld_stack_eval(C.byref(cfg), L, wa, act, rr, _ptr(x), kk, s_max, _ptr(ws),
+                              ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ld_decode_ws_bytes(cfg, n_new, s_max):
+    return _lib.ld_decode_ws_bytes(C.byref(cfg), n_new, s_max)
+
+
+def ld_stack_decode(cfg, ws_list, x, kv, s_max, pos, n_new, ws, active=None, r_eval=None,
+                    stream=None):
+    L = len(ws_list)
+    wa = (ld_weights * L)(*[weights(w) for w in ws_list])
+    act, rr, kk = _u8_array(active, L), _f32_array(r_eval, L), _ptr_array(kv, L)
+    _check(_lib.ld_stack_decode(C.byref(cfg), L, wa, act, rr, _ptr(x), kk, s_max, pos, n_new,
+                                _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ld_gemm_skinny_ws_bytes(M, N, K):
+    return _lib.ld_gemm_skinny_ws_bytes(M, N, K)
+
+
+def ld_gemm_skinny(A, W, C_out, alpha=1.0, R=None, ws=None, stream=None):
+    M, K = A.shape
+    N = W.shape[0]
+    _check(_lib.ld_gemm_skinny(M, N, K, _ptr(A), A.stride(0), _ptr(W), W.stride(0), _ptr(C_out),
+                               C_out.stride(0), alpha, _ptr(R), 0 if R is None else R.stride(0),
+                               _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                               _stream(stream)))
+
+
+def ld_kv_store(n_seq, n_new, d_model, pos, qkv, kv, s_max, stream=None):
+    _check(_lib.ld_kv_store(n_seq, n_new, d_model, pos, _ptr(qkv), _ptr(kv), s_max, _stream(stream)))
+
+
+def ld_attn_decode_ws_bytes(n_seq, n_heads, d_head, s_max):
+    return _lib.ld_attn_decode_ws_bytes(n_seq, n_heads, d_head, s_max)
+
+
+def ld_attn_decode(n_seq, n_heads, d_head, pos, n_new, qkv, kv, s_max, o, ws, alibi=0, stream=None):
+    _check(_lib.ld_attn_decode(n_seq, n_heads, d_head, alibi, pos, n_new, _ptr(qkv), _ptr(kv), s_max,
+                               _ptr(o), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def ld_rmsnorm_fwd(x, g, y, rstd, eps=1e-5, stream=None):

@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "liblayerdrop.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["k_rows.hip", "k_gemm.hip", "k_attn.hip", "api.cpp"]
+SOURCES = ["k_rows.hip", "k_gemm.hip", "k_attn.hip", "k_decode.hip", "api.cpp"]
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     # packed fp32 instructions are kept out of every kernel

@@ -273,12 +273,15 @@ BwdLayout bwd_layout(const Dims& D) {
   return L;
 }
 
-// Pointers of one sub-block's mask data on the device.
+// Pointers of one sub-block's mask data on the device.  With count null
+// every row is processed (evaluation form: no masks), idx null is the
+// identity map, and r null means the host scale r_host.
 struct MaskView {
   const uint8_t* keep;
   const int32_t* idx;
   const int32_t* count;
   const float* r;
+  float r_host = 1.f;
 };
 
 // The masks of one layer: attention and FFN views (the same view under layer
@@ -355,8 +358,11 @@ int run_gemm(int dtype, int a_k, int b_k, GemmArgs g, int64_t max_m, int64_t hos
 // Z = X + r f_attn(X) compacted in act (zk) for the FFN sub-block of the same
 // rows; scatter = 1 writes Z into the kept rows of x (sub-layer granularity,
 // where the FFN keeps its own rows).
+// kv: null, or a cache [B, s_max, 2d] that receives the keys and values of
+// positions 0..S-1 (evaluation form only: every sequence processed).
 int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
-                      const ActPtrs& act, void* x, int64_t hc, bool scatter, hipStream_t s) {
+                      const ActPtrs& act, void* x, int64_t hc, bool scatter, hipStream_t s,
+                      void* kv = nullptr, int32_t s_max = 0) {
   const int dt = D.dtype;
   const int64_t T = D.T;
   const int64_t hm = hc * D.S;
@@ -389,9 +395,24 @@ int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, 
     g.ldc = 3 * D.d;
     g.N = static_cast<int32_t>(3 * D.d);
     g.K = static_cast<int32_t>(D.d);
+    g.M = static_cast<int32_t>(T);
     g.dev_count = mv.count;
     g.count_mult = static_cast<int32_t>(D.S);
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
+  }
+  if (kv) {
+    KvArgs k{};
+    k.qkv = act.at(act.L.qkv);
+    k.ld_qkv = 3 * D.d;
+    k.cache = kv;
+    k.s_max = s_max;
+    k.d = static_cast<int32_t>(D.d);
+    k.n = static_cast<int32_t>(D.S);
+    k.n_seq = static_cast<int32_t>(D.B);
+    k.pos = 0;
+    ProfScope ps("ld_kv_store_k", s);
+    if ((e = launch_kv_store(k, s)) != hipSuccess) return fail(LD_E_HIP, "kv store: %s", hipGetErrorString(e));
+    ps.end(0, 2.0 * D.es * hm * 2 * D.d);
   }
   // causal attention on the kept sequences
   {
@@ -426,8 +447,10 @@ int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, 
       g.out_map = {mv.idx, static_cast<int32_t>(D.S)};
     }
     g.alpha_dev = mv.r;
+    if (!mv.r) g.alpha = mv.r_host;
     g.N = static_cast<int32_t>(D.d);
     g.K = static_cast<int32_t>(D.d);
+    g.M = static_cast<int32_t>(T);
     g.dev_count = mv.count;
     g.count_mult = static_cast<int32_t>(D.S);
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
@@ -476,6 +499,7 @@ int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, c
     g.ldc = D.fw;
     g.N = static_cast<int32_t>(D.fw);
     g.K = static_cast<int32_t>(D.d);
+    g.M = static_cast<int32_t>(T);
     g.dev_count = mv.count;
     g.count_mult = static_cast<int32_t>(D.S);
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
@@ -511,8 +535,10 @@ int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, c
     g.r_mapped = 0;
     g.out_map = {mv.idx, static_cast<int32_t>(D.S)};
     g.alpha_dev = mv.r;
+    if (!mv.r) g.alpha = mv.r_host;
     g.N = static_cast<int32_t>(D.d);
     g.K = static_cast<int32_t>(D.f);
+    g.M = static_cast<int32_t>(T);
     g.dev_count = mv.count;
     g.count_mult = static_cast<int32_t>(D.S);
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.f, s)) return rc;
@@ -931,6 +957,94 @@ LayerMasks layer_masks(const Dims& D, const MaskLayout& ml, char* base, int64_t 
   return lm;
 }
 
+// ------------------------------------------------------ decoding helpers
+
+// Scratch of ld_stack_decode for n_new rows per sequence and caches of s_max
+// positions.
+struct DecLayout {
+  size_t h, rstd, qkv, att, z, uv, s, part_o, part_ml, skp, skp_bytes, total;
+};
+
+size_t skinny_part_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M > kSkinnyMaxM) return 0;
+  const int ks = skinny_ksplit(M, N, K);
+  return ks > 1 ? static_cast<size_t>(ks) * M * N * 4 : 0;
+}
+
+int64_t dec_chunks(int64_t keys) { return (keys + kDecKeys - 1) / kDecKeys; }
+
+DecLayout dec_layout(const Dims& D, int64_t n_new, int64_t s_max) {
+  DecLayout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += up(bytes);
+    return at;
+  };
+  const size_t es = D.es, M = D.B * n_new;
+  L.h = take(es * M * D.d);
+  L.rstd = take(4 * M);
+  L.qkv = take(es * M * 3 * D.d);
+  L.att = take(es * M * D.d);
+  L.z = take(es * M * D.d);
+  L.uv = take(es * M * D.fw);
+  L.s = take(es * M * D.f);
+  const size_t pc = static_cast<size_t>(D.B) * D.H * dec_chunks(s_max) * kDecMaxRows;
+  L.part_o = take(4 * pc * D.dh);
+  L.part_ml = take(4 * pc * 2);
+  const int64_t shapes[4][2] = {{3 * D.d, D.d}, {D.d, D.d}, {D.fw, D.d}, {D.d, D.f}};
+  for (const auto& sh : shapes) L.skp_bytes = std::max(L.skp_bytes, skinny_part_bytes(M, sh[0], sh[1]));
+  L.skp = take(L.skp_bytes);
+  L.total = o;
+  return L;
+}
+
+// C[M, N] = (R ? R : 0) + alpha * A W^T for the rows of a decoding step:
+// the skinny kernel for M <= kSkinnyMaxM, else the general GEMM.
+int dec_gemm(const void* A, int64_t lda, const void* W, int64_t ldw, void* C, int64_t ldc,
+             const void* R, int64_t ldr, int64_t M, int64_t N, int64_t K, float alpha, float* part,
+             size_t part_bytes, hipStream_t s) {
+  if (M > kSkinnyMaxM) {
+    GemmArgs g = gemm_args();
+    g.A = A;
+    g.lda = lda;
+    g.B = W;
+    g.ldb = ldw;
+    g.C = C;
+    g.ldc = ldc;
+    g.R = R;
+    g.ldr = ldr;
+    g.M = static_cast<int32_t>(M);
+    g.N = static_cast<int32_t>(N);
+    g.K = static_cast<int32_t>(K);
+    g.alpha = alpha;
+    return run_gemm(LD_BF16, 1, 1, g, M, M, K, s);
+  }
+  SkinnyArgs g{};
+  g.A = A;
+  g.lda = lda;
+  g.W = W;
+  g.ldw = ldw;
+  g.C = C;
+  g.ldc = ldc;
+  g.R = R;
+  g.ldr = ldr;
+  g.M = static_cast<int32_t>(M);
+  g.N = static_cast<int32_t>(N);
+  g.K = static_cast<int32_t>(K);
+  g.alpha = alpha;
+  const int ks = skinny_ksplit(M, N, K);
+  if (ks > 1) {
+    if (static_cast<size_t>(ks) * M * N * 4 > part_bytes) return fail(LD_E_WORKSPACE, "skinny GEMM scratch too small");
+    g.part = part;
+  }
+  ProfScope ps(M <= 32 ? "ld_gemm_bf16_skinny<1>" : "ld_gemm_bf16_skinny<2>", s);
+  hipError_t e = launch_gemm_skinny(g, ks, s);
+  if (e != hipSuccess) return fail(LD_E_HIP, "skinny GEMM: %s", hipGetErrorString(e));
+  ps.end(2.0 * M * N * K, 2.0 * (M * K + N * K + M * N) + (R ? 2.0 * M * N : 0.0));
+  return LD_OK;
+}
+
 }  // namespace
 
 // ====================================================================== ABI
@@ -1158,6 +1272,158 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
   return LD_OK;
 }
 
+// ------------------------------------------------ evaluation and decoding
+
+size_t ld_eval_ws_bytes(const ld_config* cfg) {
+  Dims D;
+  if (check_cfg(cfg, &D)) return 0;
+  return act_layout(D).total;
+}
+
+int ld_stack_eval(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const uint8_t* active,
+                  const float* r_eval, void* x, void* const* kv, int32_t s_max, void* ws,
+                  size_t ws_bytes, void* stream) {
+  t_err.clear();
+  Dims D;
+  if (int rc = check_cfg(cfg, &D)) return rc;
+  if (n_layers < 1 || n_layers > 1024) return fail(LD_E_INVALID, "n_layers outside [1, 1024]");
+  if (!w || !x || !ws) return fail(LD_E_INVALID, "NULL pointer");
+  if (kv && D.dtype != LD_BF16) return fail(LD_E_UNSUPPORTED, "KV caches are bf16 only");
+  if (kv && s_max < D.S) return fail(LD_E_SHAPE, "s_max %d < seq %lld", s_max, static_cast<long long>(D.S));
+  for (int32_t l = 0; l < n_layers; ++l) {
+    if (active && !active[l]) continue;
+    if (int rc = check_weights(&w[l])) return rc;
+    if (r_eval && !std::isfinite(r_eval[l])) return fail(LD_E_INVALID, "r_eval[%d] not finite", l);
+    if (kv && !kv[l]) return fail(LD_E_INVALID, "kv[%d] is NULL for an active layer", l);
+  }
+  const ActLayout al = act_layout(D);
+  if (ws_bytes < al.total) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, al.total);
+  hipStream_t s = as_stream(stream);
+  ActPtrs act{static_cast<char*>(ws), al};
+  for (int32_t l = 0; l < n_layers; ++l) {
+    if (active && !active[l]) continue;
+    MaskView mv{nullptr, nullptr, nullptr, nullptr, r_eval ? r_eval[l] : 1.f};
+    if (int rc = attn_forward_part(cfg, D, w[l], mv, act, x, D.B, false, s, kv ? kv[l] : nullptr, s_max))
+      return rc;
+    if (int rc = ffn_forward_part(cfg, D, w[l], mv, act, x, D.B, false, s)) return rc;
+  }
+  return LD_OK;
+}
+
+size_t ld_decode_ws_bytes(const ld_config* cfg, int32_t n_new, int32_t s_max) {
+  Dims D;
+  if (check_cfg(cfg, &D) || n_new < 1 || n_new > kDecMaxRows || s_max < 1) return 0;
+  return dec_layout(D, n_new, s_max).total;
+}
+
+int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const uint8_t* active,
+                    const float* r_eval, void* x, void* const* kv, int32_t s_max, int32_t pos,
+                    int32_t n_new, void* ws, size_t ws_bytes, void* stream) {
+  t_err.clear();
+  Dims D;
+  if (int rc = check_cfg(cfg, &D)) return rc;
+  if (D.dtype != LD_BF16) return fail(LD_E_UNSUPPORTED, "decoding is bf16 only");
+  if (n_layers < 1 || n_layers > 1024) return fail(LD_E_INVALID, "n_layers outside [1, 1024]");
+  if (!w || !x || !kv || !ws) return fail(LD_E_INVALID, "NULL pointer");
+  if (n_new < 1 || n_new > kDecMaxRows) return fail(LD_E_INVALID, "n_new outside [1, %d]", kDecMaxRows);
+  if (pos < 0 || s_max < 1 || static_cast<int64_t>(pos) + n_new > s_max)
+    return fail(LD_E_SHAPE, "positions %d..%d outside the cache of %d", pos, pos + n_new - 1, s_max);
+  for (int32_t l = 0; l < n_layers; ++l) {
+    if (active && !active[l]) continue;
+    if (int rc = check_weights(&w[l])) return rc;
+    if (r_eval && !std::isfinite(r_eval[l])) return fail(LD_E_INVALID, "r_eval[%d] not finite", l);
+    if (!kv[l]) return fail(LD_E_INVALID, "kv[%d] is NULL for an active layer", l);
+  }
+  const DecLayout L = dec_layout(D, n_new, s_max);
+  if (ws_bytes < L.total) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.total);
+  hipStream_t s = as_stream(stream);
+  char* base = static_cast<char*>(ws);
+  auto P = [&](size_t off) { return static_cast<void*>(base + off); };
+  float* skp = L.skp_bytes ? reinterpret_cast<float*>(base + L.skp) : nullptr;
+  const int64_t M = D.B * n_new, d = D.d;
+  hipError_t e;
+  auto norm = [&](const void* src, const void* gain) {
+    RmsFwdArgs a{};
+    a.x = src;
+    a.src = {nullptr, 1};
+    a.g = gain;
+    a.y = P(L.h);
+    a.rstd = reinterpret_cast<float*>(base + L.rstd);
+    a.rc = {nullptr, 1, M};
+    a.d = static_cast<int32_t>(d);
+    a.eps = cfg->rms_eps;
+    ProfScope ps("ld_rmsnorm_fwd_k", s);
+    if ((e = launch_rmsnorm_fwd(LD_BF16, a, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
+    ps.end(0, 4.0 * M * d);
+    return static_cast<int>(LD_OK);
+  };
+  for (int32_t l = 0; l < n_layers; ++l) {
+    if (active && !active[l]) continue;
+    const float r = r_eval ? r_eval[l] : 1.f;
+    const ld_weights& wl = w[l];
+    // h = RMSNorm(x); qkv = h W_qkv^T; new keys/values into the cache
+    if (int rc = norm(x, wl.g_attn)) return rc;
+    if (int rc = dec_gemm(P(L.h), d, wl.w_qkv, d, P(L.qkv), 3 * d, nullptr, 0, M, 3 * d, d, 1.f, skp,
+                          L.skp_bytes, s))
+      return rc;
+    KvArgs k{};
+    k.qkv = P(L.qkv);
+    k.ld_qkv = 3 * d;
+    k.cache = kv[l];
+    k.s_max = s_max;
+    k.d = static_cast<int32_t>(d);
+    k.n = n_new;
+    k.n_seq = static_cast<int32_t>(D.B);
+    k.pos = pos;
+    {
+      ProfScope ps("ld_kv_store_k", s);
+      if ((e = launch_kv_store(k, s)) != hipSuccess) return fail(LD_E_HIP, "kv store: %s", hipGetErrorString(e));
+      ps.end(0, 8.0 * M * d);
+    }
+    // attention of the new rows over positions 0..pos+n_new-1 of the cache
+    DecAttnArgs at{};
+    at.qkv = P(L.qkv);
+    at.ld_qkv = 3 * d;
+    at.cache = kv[l];
+    at.s_max = s_max;
+    at.out = P(L.att);
+    at.part_o = reinterpret_cast<float*>(base + L.part_o);
+    at.part_ml = reinterpret_cast<float*>(base + L.part_ml);
+    at.n_seq = static_cast<int32_t>(D.B);
+    at.H = static_cast<int32_t>(D.H);
+    at.dh = static_cast<int32_t>(D.dh);
+    at.n_new = n_new;
+    at.pos = pos;
+    at.n_chunks = static_cast<int32_t>(dec_chunks(static_cast<int64_t>(pos) + n_new));
+    at.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.dh)));
+    at.alibi = D.kind == LD_BLOCK_ALIBI_RELU2;
+    {
+      ProfScope ps("ld_attn_decode_bf16", s);
+      if ((e = launch_attn_decode(at, s)) != hipSuccess) return fail(LD_E_HIP, "attn decode: %s", hipGetErrorString(e));
+      const double keys = static_cast<double>(pos) + n_new;
+      ps.end(4.0 * M * d * keys, 2.0 * D.B * keys * 2 * d + 4.0 * M * d);
+    }
+    // z = x + r (att W_o^T); h = RMSNorm(z); uv = h W_gate_up^T; s = act(uv)
+    if (int rc = dec_gemm(P(L.att), d, wl.w_o, d, P(L.z), d, x, d, M, d, d, r, skp, L.skp_bytes, s))
+      return rc;
+    if (int rc = norm(P(L.z), wl.g_mlp)) return rc;
+    if (int rc = dec_gemm(P(L.h), d, wl.w_gate_up, d, P(L.uv), D.fw, nullptr, 0, M, D.fw, d, 1.f, skp,
+                          L.skp_bytes, s))
+      return rc;
+    EltArgs a{};
+    a.a = P(L.uv);
+    a.out = P(L.s);
+    a.rc = {nullptr, 1, M};
+    a.f = static_cast<int32_t>(D.f);
+    e = D.kind == LD_BLOCK_SWIGLU ? launch_swiglu_fwd(LD_BF16, a, s) : launch_relu2_fwd(LD_BF16, a, s);
+    if (e != hipSuccess) return fail(LD_E_HIP, "activation: %s", hipGetErrorString(e));
+    // x = z + r (s W_down^T)
+    if (int rc = dec_gemm(P(L.s), D.f, wl.w_down, D.f, x, d, P(L.z), d, M, d, D.f, r, skp, L.skp_bytes, s))
+      return rc;
+  }
+  return LD_OK;
+}
+
 // ------------------------------------------------------ kernel-level calls
 
 int ld_rmsnorm_fwd(int32_t dtype, int32_t rows, int32_t d, float eps, const void* x, const void* g,
@@ -1282,6 +1548,91 @@ int ld_relu2_bwd(int32_t dtype, int32_t rows, int32_t f, const void* u, const vo
 }
 
 float ld_alibi_slope(int32_t h, int32_t n_heads) { return alibi_slope(h, n_heads); }
+
+size_t ld_gemm_skinny_ws_bytes(int32_t M, int32_t N, int32_t K) {
+  if (M < 1 || M > kSkinnyMaxM || N < 1 || K < 0) return 0;
+  return skinny_part_bytes(M, N, K);
+}
+
+int ld_gemm_skinny(int32_t M, int32_t N, int32_t K, const void* A, int32_t lda, const void* W, int32_t ldw,
+                   void* C, int32_t ldc, float alpha, const void* R, int32_t ldr, void* ws, size_t ws_bytes,
+                   void* stream) {
+  t_err.clear();
+  if (M < 1 || M > kSkinnyMaxM) return fail(LD_E_SHAPE, "M outside [1, %d]", kSkinnyMaxM);
+  if (N < 1 || K < 0 || K % 8) return fail(LD_E_SHAPE, "need N >= 1, K >= 0, K %% 8 == 0");
+  if (lda < K || ldw < K || ldc < N || (R && ldr < N)) return fail(LD_E_SHAPE, "leading dimension too small");
+  if (lda % 8 || ldw % 8) return fail(LD_E_SHAPE, "lda, ldw must be multiples of 8");
+  if (!A || !W || !C) return fail(LD_E_INVALID, "NULL pointer");
+  if ((reinterpret_cast<uintptr_t>(A) | reinterpret_cast<uintptr_t>(W)) & 15)
+    return fail(LD_E_INVALID, "A and W must be 16-byte aligned");
+  if (!std::isfinite(alpha)) return fail(LD_E_INVALID, "alpha not finite");
+  return dec_gemm(A, lda, W, ldw, C, ldc, R, ldr, M, N, K, alpha, static_cast<float*>(ws), ws ? ws_bytes : 0,
+                  as_stream(stream));
+}
+
+int ld_kv_store(int32_t n_seq, int32_t n_new, int32_t d_model, int32_t pos, const void* qkv, void* kv,
+                int32_t s_max, void* stream) {
+  t_err.clear();
+  if (n_seq < 1 || n_new < 1 || d_model < 8 || d_model % 8) return fail(LD_E_SHAPE, "bad sizes");
+  if (pos < 0 || static_cast<int64_t>(pos) + n_new > s_max) return fail(LD_E_SHAPE, "positions outside the cache");
+  if (!qkv || !kv) return fail(LD_E_INVALID, "NULL pointer");
+  if ((reinterpret_cast<uintptr_t>(qkv) | reinterpret_cast<uintptr_t>(kv)) & 15)
+    return fail(LD_E_INVALID, "qkv and kv must be 16-byte aligned");
+  KvArgs k{};
+  k.qkv = qkv;
+  k.ld_qkv = 3ll * d_model;
+  k.cache = kv;
+  k.s_max = s_max;
+  k.d = d_model;
+  k.n = n_new;
+  k.n_seq = n_seq;
+  k.pos = pos;
+  hipError_t e = launch_kv_store(k, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "kv store: %s", hipGetErrorString(e));
+  return LD_OK;
+}
+
+size_t ld_attn_decode_ws_bytes(int32_t n_seq, int32_t n_heads, int32_t d_head, int32_t s_max) {
+  if (n_seq < 1 || n_heads < 1 || d_head < 1 || s_max < 1) return 0;
+  const size_t pc = static_cast<size_t>(n_seq) * n_heads * dec_chunks(s_max) * kDecMaxRows;
+  return up(4 * pc * d_head) + up(4 * pc * 2);
+}
+
+int ld_attn_decode(int32_t n_seq, int32_t n_heads, int32_t d_head, int32_t alibi, int32_t pos, int32_t n_new,
+                   const void* qkv, const void* kv, int32_t s_max, void* o, void* ws, size_t ws_bytes,
+                   void* stream) {
+  t_err.clear();
+  if (d_head != 64 && d_head != 128) return fail(LD_E_UNSUPPORTED, "d_head must be 64 or 128");
+  if (n_seq < 1 || n_heads < 1) return fail(LD_E_SHAPE, "n_seq, n_heads must be >= 1");
+  if (n_new < 1 || n_new > kDecMaxRows) return fail(LD_E_INVALID, "n_new outside [1, %d]", kDecMaxRows);
+  if (pos < 0 || static_cast<int64_t>(pos) + n_new > s_max) return fail(LD_E_SHAPE, "positions outside the cache");
+  if (alibi != 0 && alibi != 1) return fail(LD_E_INVALID, "alibi must be 0 or 1");
+  if (!qkv || !kv || !o || !ws) return fail(LD_E_INVALID, "NULL pointer");
+  if ((reinterpret_cast<uintptr_t>(qkv) | reinterpret_cast<uintptr_t>(kv)) & 15)
+    return fail(LD_E_INVALID, "qkv and kv must be 16-byte aligned");
+  const size_t need = ld_attn_decode_ws_bytes(n_seq, n_heads, d_head, s_max);
+  if (ws_bytes < need) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  const size_t pc = static_cast<size_t>(n_seq) * n_heads * dec_chunks(s_max) * kDecMaxRows;
+  DecAttnArgs at{};
+  at.qkv = qkv;
+  at.ld_qkv = 3ll * n_heads * d_head;
+  at.cache = kv;
+  at.s_max = s_max;
+  at.out = o;
+  at.part_o = static_cast<float*>(ws);
+  at.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + up(4 * pc * d_head));
+  at.n_seq = n_seq;
+  at.H = n_heads;
+  at.dh = d_head;
+  at.n_new = n_new;
+  at.pos = pos;
+  at.n_chunks = static_cast<int32_t>(dec_chunks(static_cast<int64_t>(pos) + n_new));
+  at.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(d_head)));
+  at.alibi = alibi;
+  hipError_t e = launch_attn_decode(at, as_stream(stream));
+  if (e != hipSuccess) return fail(LD_E_HIP, "attn decode: %s", hipGetErrorString(e));
+  return LD_OK;
+}
 
 size_t ld_gemm_ws_bytes(int32_t dtype, int32_t a_kcontig, int32_t b_kcontig, int32_t M, int32_t N,
                         int32_t K, int32_t ldc, int32_t c_f32) {

@@ -229,6 +229,48 @@ struct AttnArgs {
   int32_t alibi;             // add the ALiBi bias -m_h (i - j) to the scaled scores
 };
 
+// Skinny GEMM of incremental decoding: C[m, n] = (R ? R[m, n] : 0) + alpha *
+// sum_k A[m, k] W[n, k], bf16, both operands k-contiguous, M <= kSkinnyMaxM.
+struct SkinnyArgs {
+  const void* A;
+  const void* W;
+  void* C;
+  const void* R;
+  int64_t lda, ldw, ldc, ldr;
+  int32_t M, N, K;
+  float alpha;
+  float* part;  // float32 [ksplit][M][N] when ksplit > 1
+};
+constexpr int kSkinnyMaxM = 64;
+
+// Copy of the key/value columns of qkv rows into a cache [n_seq, s_max, 2d]
+// (keys, then values, of each position): row b*n + j goes to position pos + j
+// of sequence b.
+struct KvArgs {
+  const void* qkv;
+  int64_t ld_qkv;
+  void* cache;
+  int32_t s_max, d, n, n_seq, pos;
+};
+
+// Decode attention: queries (rows b*n_new + j of qkv, position pos + j) over
+// the cached keys/values of positions 0..pos+n_new-1, in chunks of kDecKeys
+// keys with float32 partials combined by a second kernel.
+struct DecAttnArgs {
+  const void* qkv;
+  int64_t ld_qkv;
+  const void* cache;
+  int32_t s_max;
+  void* out;        // [n_seq * n_new, H * dh]
+  float* part_o;    // [n_seq][H][n_chunks][kDecMaxRows][dh]
+  float* part_ml;   // [n_seq][H][n_chunks][kDecMaxRows][2]: base-2 max, sum
+  int32_t n_seq, H, dh, n_new, pos, n_chunks;
+  float scale;
+  int32_t alibi;
+};
+constexpr int kDecKeys = 256;
+constexpr int kDecMaxRows = 8;
+
 // ALiBi slope of head h of H heads (ALiBi paper, section 3): with n the
 // largest power of two <= H, 2^(-8(h+1)/n) for h < n, else every other slope
 // of the 2n-head sequence, 2^(-4(2(h-n)+1)/n).
@@ -247,6 +289,10 @@ __host__ __device__ inline float alibi_slope(int h, int H) {
 
 hipError_t launch_masks(const MaskArgs& a, hipStream_t s);
 hipError_t launch_zero_f32(const ZeroArgs& a, hipStream_t s);
+int skinny_ksplit(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_skinny(const SkinnyArgs& g, int ksplit, hipStream_t s);
+hipError_t launch_kv_store(const KvArgs& a, hipStream_t s);
+hipError_t launch_attn_decode(const DecAttnArgs& a, hipStream_t s);
 hipError_t launch_gather(int dtype, const RowsArgs& a, hipStream_t s);
 hipError_t launch_scatter_add(int dtype, const RowsArgs& a, hipStream_t s);
 hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s);
