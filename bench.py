@@ -27,6 +27,16 @@ attention and FFN masks), layer_batch (one draw per layer for the whole
 batch), sublayer_batch.  F_sl then splits into its attention part
 3 * [2 S 4 d^2 + 2 d S (S+1)] per kept attention (sequence, layer) and its
 FFN part 3 * 2 S n_ffn d d_ff per kept FFN (sequence, layer).
+
+--mode infer measures the depth-elastic inference path on the same stack
+instead (its own JSON line): the evaluation-form forward over S positions
+(prefill) with every layer, an early exit at 3/4 of the depth and every
+other layer, and, over the caches of those S positions, one decoding step of
+one row per sequence with the full model (target) and with every other
+layer (draft), and a verify step of 6 rows (a draft of 5, the paper's
+speculative-decoding setting).  The decoding steps are HBM-bound: their
+roofline is the weights of the active layers plus the cached keys/values
+they read, per step.
 """
 import argparse
 import json
@@ -167,6 +177,92 @@ def cpu_baseline(sh, target_s=15.0):
     return el / n, n, threads
 
 
+def _timed(fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def infer_main(args, sh):
+    dev = "cuda:0"
+    L, B, S, d = sh.n_layers, sh.batch, sh.seq, sh.d_model
+    cfg = ld.config(B, S, d, sh.n_heads, sh.d_ff, ld.LD_BF16, block_kind=sh.kind)
+    W = [inp.device_layer_weights(sh, l, dev) for l in range(L)]
+    x0 = inp.device_hidden(sh, dev)
+    x = torch.empty_like(x0)
+    s_max = S + 64
+    kv = [torch.zeros(B, s_max, 2 * d, dtype=torch.bfloat16, device=dev) for _ in range(L)]
+    ws = torch.empty(ld.ld_eval_ws_bytes(cfg), dtype=torch.uint8, device=dev)
+    sets = {"full": [1] * L, "exit_3/4": [1 if l < (3 * L) // 4 else 0 for l in range(L)],
+            "alternate": [1 if l % 2 == 0 else 0 for l in range(L)]}
+    prefill = {}
+    for name, act in sets.items():
+        def run(act=act):
+            x.copy_(x0)
+            ld.ld_stack_eval(cfg, W, x, ws, active=act, kv=kv if name == "full" else None,
+                             s_max=s_max)
+        ms = _timed(run, args.steps, args.warmup)
+        prefill[name] = {"layers": sum(act), "ms": round(ms, 3),
+                         "tokens_per_s": round(B * S / (ms * 1e-3), 1)}
+        print(f"# prefill {name}: {prefill[name]}", file=sys.stderr, flush=True)
+    # the caches hold positions 0..S-1 as the full model wrote them (only the
+    # "full" prefill writes caches)
+    dws = torch.empty(ld.ld_decode_ws_bytes(cfg, 8, s_max), dtype=torch.uint8, device=dev)
+    wbytes = 2.0 * sum(v.numel() for v in W[0].values())          # one layer's weights
+    dec = {}
+    cases = [("target", 1, sets["full"]), ("draft_alternate", 1, sets["alternate"]),
+             ("verify_6", 6, sets["full"])]
+    prof = {}
+    for name, n, act in cases:
+        xd = torch.randn(B, n, d, device=dev).to(torch.bfloat16)
+
+        def run(act=act, n=n, xd=xd):
+            ld.ld_stack_decode(cfg, W, xd, kv, s_max, S, n, dws, active=act)
+        ms = _timed(run, args.steps * 5, args.warmup)
+        nl = sum(act)
+        kv_bytes = 2.0 * B * (S + n) * 2 * d                         # keys + values read per layer
+        byts = nl * (wbytes + kv_bytes)
+        dec[name] = {"layers": nl, "rows_per_seq": n, "ms": round(ms, 4),
+                     "hbm_gbs": round(byts / (ms * 1e-3) / 1e9, 1),
+                     "hbm_frac": round(byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        print(f"# decode {name}: {dec[name]}", file=sys.stderr, flush=True)
+        if name == "target":
+            for k in ("ld_gemm_bf16_skinny<1>", "ld_attn_decode_bf16"):
+                ld.ld_prof_start(k)
+                run()
+                torch.cuda.synchronize()
+                ld.ld_prof_stop()
+                prof[k] = ld.ld_prof_result()
+    t = dec["target"]["ms"]
+    g = prof["ld_gemm_bf16_skinny<1>"]
+    out = {
+        "metric": f"decode ms per step (one row per sequence, {args.workload} stack, "
+                  f"{S}-position caches)",
+        "value": t, "unit": "ms", "higher_is_better": False, "n_gpus": 1,
+        "steps": args.steps * 5, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{args.workload}: L={L}, d_model={d}, heads={sh.n_heads}, "
+                               f"d_ff={sh.d_ff}, batch={B}, prefill {S} positions",
+                   "parallelism": "none (1 GPU)"},
+        "decode": dec,
+        "draft_over_target": round(dec["draft_alternate"]["ms"] / t, 4),
+        "prefill": prefill,
+        "roofline": {"kernel": "decode step (all kernels)", "bound": "hbm",
+                     "achieved": dec["target"]["hbm_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": dec["target"]["hbm_frac"], "traffic": None},
+        "kernels": {k: {"launches": v["launches"],
+                        "avg_us": round(v["ms"] * 1e3 / max(v["launches"], 1), 2),
+                        "gbs": round(v["bytes"] / max(v["ms"] * 1e-3, 1e-12) / 1e9, 1)}
+                    for k, v in prof.items()},
+        "skinny_gemm_weight_gbs": round(g["bytes"] / max(g["ms"] * 1e-3, 1e-12) / 1e9, 1),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,6 +273,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--workload", default="1b", choices=["1b", "paper_3p9b"])
     ap.add_argument("--granularity", default="layer_seq", choices=list(GRANULARITIES))
+    ap.add_argument("--mode", default="train", choices=["train", "infer"])
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run the traffic-counter calibration copy of this size first")
     ap.add_argument("--prof-kernel", default=None,
@@ -191,6 +288,9 @@ def main():
     if args.copy_calib_mib > 0:
         copy_calibration(args.copy_calib_mib)
     sh = inp.SHAPES[args.workload]
+    if args.mode == "infer":
+        infer_main(args, sh)
+        return
     dev = "cuda:0"
     gran = GRANULARITIES[args.granularity]
     st = Stack(sh, dev, gran)
