@@ -971,6 +971,7 @@ size_t skinny_part_bytes(int64_t M, int64_t N, int64_t K) {
   return ks > 1 ? static_cast<size_t>(ks) * M * N * 4 : 0;
 }
 
+
 int64_t dec_chunks(int64_t keys) { return (keys + kDecKeys - 1) / kDecKeys; }
 
 DecLayout dec_layout(const Dims& D, int64_t n_new, int64_t s_max) {
@@ -999,11 +1000,20 @@ DecLayout dec_layout(const Dims& D, int64_t n_new, int64_t s_max) {
   return L;
 }
 
+// Where a qkv projection's keys/values also go (see SkinnyArgs).
+struct KvOut {
+  void* kv;
+  int32_t d, n, s_max, pos;
+};
+
 // C[M, N] = (R ? R : 0) + alpha * A W^T for the rows of a decoding step:
-// the skinny kernel for M <= kSkinnyMaxM, else the general GEMM.
+// the skinny kernel for M <= kSkinnyMaxM, else the general GEMM.  kv: the
+// columns from kv.d on also go to that cache (skinny kernel), or the caller
+// stores them (general GEMM: returns with *kv_done = false).
 int dec_gemm(const void* A, int64_t lda, const void* W, int64_t ldw, void* C, int64_t ldc,
              const void* R, int64_t ldr, int64_t M, int64_t N, int64_t K, float alpha, float* part,
-             size_t part_bytes, hipStream_t s) {
+             size_t part_bytes, hipStream_t s, const KvOut* kv = nullptr, bool* kv_done = nullptr) {
+  if (kv_done) *kv_done = false;
   if (M > kSkinnyMaxM) {
     GemmArgs g = gemm_args();
     g.A = A;
@@ -1037,6 +1047,14 @@ int dec_gemm(const void* A, int64_t lda, const void* W, int64_t ldw, void* C, in
   if (ks > 1) {
     if (static_cast<size_t>(ks) * M * N * 4 > part_bytes) return fail(LD_E_WORKSPACE, "skinny GEMM scratch too small");
     g.part = part;
+  }
+  if (kv) {
+    g.kv = kv->kv;
+    g.kv_d = kv->d;
+    g.kv_n = kv->n;
+    g.kv_s_max = kv->s_max;
+    g.kv_pos = kv->pos;
+    if (kv_done) *kv_done = true;
   }
   ProfScope ps(M <= 32 ? "ld_gemm_bf16_skinny<1>" : "ld_gemm_bf16_skinny<2>", s);
   hipError_t e = launch_gemm_skinny(g, ks, s);
@@ -1363,19 +1381,21 @@ int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w,
     const ld_weights& wl = w[l];
     // h = RMSNorm(x); qkv = h W_qkv^T; new keys/values into the cache
     if (int rc = norm(x, wl.g_attn)) return rc;
+    const KvOut ko{kv[l], static_cast<int32_t>(d), n_new, s_max, pos};
+    bool kv_done = false;
     if (int rc = dec_gemm(P(L.h), d, wl.w_qkv, d, P(L.qkv), 3 * d, nullptr, 0, M, 3 * d, d, 1.f, skp,
-                          L.skp_bytes, s))
+                          L.skp_bytes, s, &ko, &kv_done))
       return rc;
-    KvArgs k{};
-    k.qkv = P(L.qkv);
-    k.ld_qkv = 3 * d;
-    k.cache = kv[l];
-    k.s_max = s_max;
-    k.d = static_cast<int32_t>(d);
-    k.n = n_new;
-    k.n_seq = static_cast<int32_t>(D.B);
-    k.pos = pos;
-    {
+    if (!kv_done) {
+      KvArgs k{};
+      k.qkv = P(L.qkv);
+      k.ld_qkv = 3 * d;
+      k.cache = kv[l];
+      k.s_max = s_max;
+      k.d = static_cast<int32_t>(d);
+      k.n = n_new;
+      k.n_seq = static_cast<int32_t>(D.B);
+      k.pos = pos;
       ProfScope ps("ld_kv_store_k", s);
       if ((e = launch_kv_store(k, s)) != hipSuccess) return fail(LD_E_HIP, "kv store: %s", hipGetErrorString(e));
       ps.end(0, 8.0 * M * d);
@@ -1566,6 +1586,8 @@ int ld_gemm_skinny(int32_t M, int32_t N, int32_t K, const void* A, int32_t lda, 
   if ((reinterpret_cast<uintptr_t>(A) | reinterpret_cast<uintptr_t>(W)) & 15)
     return fail(LD_E_INVALID, "A and W must be 16-byte aligned");
   if (!std::isfinite(alpha)) return fail(LD_E_INVALID, "alpha not finite");
+  const size_t need = ld_gemm_skinny_ws_bytes(M, N, K);
+  if (need && (!ws || ws_bytes < need)) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   return dec_gemm(A, lda, W, ldw, C, ldc, R, ldr, M, N, K, alpha, static_cast<float*>(ws), ws ? ws_bytes : 0,
                   as_stream(stream));
 }

@@ -11,7 +11,10 @@
 // k = 64c + 32h + 8s + e (e < 8), in A and W alike, which leaves the
 // contraction unchanged.  The waves' accumulators are summed in LDS in wave
 // order; split workgroups write float32 partials summed in split order by a
-// second kernel, so results do not depend on timing.
+// second kernel, so results do not depend on timing.  (A last-arriving
+// workgroup doing that sum needs device-scope fences, which on this chip
+// write back and invalidate the per-XCD L2 and cost far more than the
+// second launch.)
 //
 // Decode attention: one workgroup per (256-key chunk, head, sequence).
 // Scores: eight lanes per key, each holding an eighth of the head's
@@ -46,7 +49,12 @@ __device__ __forceinline__ bf16x8 load8(const bf16* p) { return *reinterpret_cas
 __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int m, int n, float sum) {
   float v = g.alpha * sum;
   if (g.R) v += static_cast<float>(static_cast<const bf16*>(g.R)[static_cast<int64_t>(m) * g.ldr + n]);
-  static_cast<bf16*>(g.C)[static_cast<int64_t>(m) * g.ldc + n] = static_cast<bf16>(v);
+  const bf16 o = static_cast<bf16>(v);
+  static_cast<bf16*>(g.C)[static_cast<int64_t>(m) * g.ldc + n] = o;
+  if (g.kv && n >= g.kv_d) {
+    const int64_t b = m / g.kv_n, j = m % g.kv_n;
+    static_cast<bf16*>(g.kv)[(b * g.kv_s_max + g.kv_pos + j) * 2 * g.kv_d + (n - g.kv_d)] = o;
+  }
 }
 
 template <int MB>
@@ -74,22 +82,30 @@ __global__ __launch_bounds__(256) void ld_gemm_bf16_skinny(SkinnyArgs g) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[mb][v] = 0.f;
 
-  for (int c = blockIdx.y * kSkWaves + wave; c < nchunks; c += workers) {
-    const int kc = c * kSkChunk;
-    bf16x8 b[4], a[MB][4];
+  // U chunks per pass, all loaded before their MFMAs (chunks past the end
+  // load zeros, so the MFMAs need no branch)
+  constexpr int U = MB == 1 ? 4 : 2;
+  for (int c0 = blockIdx.y * kSkWaves + wave; c0 < nchunks; c0 += U * workers) {
+    bf16x8 b[U][4], a[U][MB][4];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const bool kv = kc + 32 * h + 8 * s < g.K;   // K % 8 == 0: the whole 8 are in range
-      b[s] = (nvalid && kv) ? load8(wrow + kc + 8 * s) : zero8();
+    for (int u = 0; u < U; ++u) {
+      const int kc = (c0 + u * workers) * kSkChunk;
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        a[mb][s] = (mvalid[mb] && kv) ? load8(arow[mb] + kc + 8 * s) : zero8();
+      for (int s = 0; s < 4; ++s) {
+        const bool kv = kc + 32 * h + 8 * s < g.K;   // K % 8 == 0: the whole 8 are in range
+        b[u][s] = (nvalid && kv) ? load8(wrow + kc + 8 * s) : zero8();
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+          a[u][mb][s] = (mvalid[mb] && kv) ? load8(arow[mb] + kc + 8 * s) : zero8();
+      }
     }
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mb][s], b[s], acc[mb], 0, 0, 0);
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+          acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[u][mb][s], b[u][s], acc[mb], 0, 0, 0);
   }
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -115,10 +131,9 @@ __global__ __launch_bounds__(256) void ld_gemm_bf16_skinny(SkinnyArgs g) {
 
 __global__ __launch_bounds__(256) void ld_skinny_reduce_k(SkinnyArgs g, int ksplit) {
   const int64_t total = static_cast<int64_t>(g.M) * g.N;
-  const int64_t plane = total;
   for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < total; i += gridDim.x * 256ll) {
     float sum = g.part[i];
-    for (int s = 1; s < ksplit; ++s) sum += g.part[s * plane + i];
+    for (int s = 1; s < ksplit; ++s) sum += g.part[s * total + i];
     skinny_store(g, static_cast<int>(i / g.N), static_cast<int>(i % g.N), sum);
   }
 }
@@ -140,65 +155,81 @@ __global__ __launch_bounds__(256) void ld_kv_store_k(KvArgs a) {
 
 // ------------------------------------------------------ decode attention
 
-template <int DH>
+// NQ >= n_new query rows per sequence (1, 2, 4 or 8).  A wave covers 64 keys
+// of the chunk: DH/8 lanes per key row, 8 dimensions (16 bytes) each, so a
+// pass covers 64/(DH/8) keys and all passes' loads are issued before any
+// arithmetic.
+template <int DH, int NQ>
 __global__ __launch_bounds__(256) void ld_attn_decode_bf16(DecAttnArgs a) {
-  constexpr int NQ = kDecMaxRows;
-  constexpr int EL = DH / 8;   // dimensions per lane of a key row
-  constexpr int CL = DH / 64;  // value columns per lane
+  constexpr int LPK = DH / 8;    // lanes per key row
+  constexpr int KPP = 64 / LPK;  // keys per pass
+  constexpr int NP = 64 / KPP;   // passes per wave
   __shared__ float sc[NQ][kDecKeys];
   __shared__ float red[4][NQ][DH];
   const int c = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kg = lane / LPK, sl = lane % LPK;
   const int d = a.H * DH;
   const int64_t row2 = 2ll * d;
   const int nk = a.pos + a.n_new;
-  const int k0 = c * kDecKeys;
+  const int k0 = c * kDecKeys + wave * 64;
   const float al2 = a.alibi ? alibi_slope(h, a.H) * kLog2e : 0.f;
-  const int grp = lane >> 3, sl = lane & 7;
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
   const bf16* cache = static_cast<const bf16*>(a.cache) + static_cast<int64_t>(b) * a.s_max * row2;
 
-  float q[NQ][EL];
+  // keys of this wave's 64 positions (rows past the last position read row 0)
+  bf16x8 kr[NP];
 #pragma unroll
-  for (int j = 0; j < NQ; ++j) {
-    const bool jv = j < a.n_new;
-    const bf16* qp = qkv + (static_cast<int64_t>(b) * a.n_new + (jv ? j : 0)) * a.ld_qkv + h * DH + sl * EL;
-#pragma unroll
-    for (int e8 = 0; e8 < EL / 8; ++e8) {
-      const bf16x8 v = jv ? load8(qp + 8 * e8) : zero8();
-#pragma unroll
-      for (int e = 0; e < 8; ++e) q[j][8 * e8 + e] = static_cast<float>(v[e]) * (a.scale * kLog2e);
-    }
+  for (int p = 0; p < NP; ++p) {
+    const int kk = k0 + p * KPP + kg;
+    kr[p] = load8(cache + static_cast<int64_t>(kk < nk ? kk : 0) * row2 + h * DH + sl * 8);
   }
-
-  // scores: each wave 64 keys of the chunk, 8 keys per pass
-  const bf16* kbase = cache + h * DH + sl * EL;
-  for (int it = 0; it < 8; ++it) {
-    const int kl = wave * 64 + it * 8 + grp;
-    const int kk = k0 + kl;
-    const bool valid = kk < nk;
-    float kv[EL];
+  // scores in base 2 (causal cut at each row's position, ALiBi bias), in
+  // groups of at most four rows to bound the registers held
+  // (the group loop stays rolled: unrolled, the key conversions to float
+  // would be shared across groups and held in registers)
+  constexpr int JG = NQ < 4 ? NQ : 4;
+#pragma unroll 1
+  for (int j0 = 0; j0 < NQ; j0 += JG) {
+    float q[JG][8];
 #pragma unroll
-    for (int e8 = 0; e8 < EL / 8; ++e8) {
-      const bf16x8 v = load8(kbase + static_cast<int64_t>(valid ? kk : 0) * row2 + 8 * e8);
+    for (int j = 0; j < JG; ++j) {
+      const bool jv = j0 + j < a.n_new;
+      const bf16x8 v = jv ? load8(qkv + (static_cast<int64_t>(b) * a.n_new + j0 + j) * a.ld_qkv + h * DH +
+                                  sl * 8)
+                          : zero8();
 #pragma unroll
-      for (int e = 0; e < 8; ++e) kv[8 * e8 + e] = static_cast<float>(v[e]);
+      for (int e = 0; e < 8; ++e) q[j][e] = static_cast<float>(v[e]) * (a.scale * kLog2e);
     }
 #pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-      if (j < a.n_new) {
+    for (int p = 0; p < NP; ++p) {
+      const int kl = wave * 64 + p * KPP + kg;
+      const int kk = k0 + p * KPP + kg;
+#pragma unroll
+      for (int j = 0; j < JG; ++j) {
         float s = 0.f;
 #pragma unroll
-        for (int e = 0; e < EL; ++e) s = __builtin_fmaf(q[j][e], kv[e], s);
-        s += __shfl_xor(s, 1, 64);
-        s += __shfl_xor(s, 2, 64);
-        s += __shfl_xor(s, 4, 64);
-        const int qpos = a.pos + j;
-        if (sl == 0)
-          sc[j][kl] = (valid && kk <= qpos) ? s - al2 * static_cast<float>(qpos - kk) : -INFINITY;
+        for (int e = 0; e < 8; ++e) s = __builtin_fmaf(q[j][e], static_cast<float>(kr[p][e]), s);
+#pragma unroll
+        for (int o = LPK / 2; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+        const int qpos = a.pos + j0 + j;
+        if (sl == 0 && j0 + j < a.n_new)
+          sc[j0 + j][kl] = (kk < nk && kk <= qpos) ? s - al2 * static_cast<float>(qpos - kk) : -INFINITY;
       }
     }
   }
+  // values of the same positions; with few rows they are in flight during
+  // the softmax, with more rows they are loaded after it (registers)
+  constexpr bool kEarlyV = NQ <= 4;
+  bf16x8 vr[NP];
+  auto load_v = [&]() {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int kk = k0 + p * KPP + kg;
+      vr[p] = load8(cache + static_cast<int64_t>(kk < nk ? kk : 0) * row2 + d + h * DH + sl * 8);
+    }
+  };
+  if constexpr (kEarlyV) load_v();
   __syncthreads();
 
   // per query row: chunk maximum, probabilities, sum
@@ -210,66 +241,64 @@ __global__ __launch_bounds__(256) void ld_attn_decode_bf16(DecAttnArgs a) {
     for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
     float l = 0.f;
     for (int i = lane; i < kDecKeys; i += 64) {
-      const float p = m == -INFINITY ? 0.f : exp2f(sc[j][i] - m);
-      sc[j][i] = p;
-      l += p;
+      const float pr = m == -INFINITY ? 0.f : exp2f(sc[j][i] - m);
+      sc[j][i] = pr;
+      l += pr;
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o, 64);
     if (lane == 0) {
-      a.part_ml[(prow * NQ + j) * 2] = m;
-      a.part_ml[(prow * NQ + j) * 2 + 1] = l;
+      a.part_ml[(prow * kDecMaxRows + j) * 2] = m;
+      a.part_ml[(prow * kDecMaxRows + j) * 2 + 1] = l;
     }
   }
   __syncthreads();
 
-  // P V over this wave's 64 keys
-  float o[NQ][CL];
+  if constexpr (!kEarlyV) load_v();
+  // P V in groups of at most four rows: each lane its key's 8 dimensions,
+  // then a sum over the wave's key groups (lane exchanges) and over the four
+  // waves (LDS, in wave order)
+#pragma unroll 1
+  for (int j0 = 0; j0 < NQ; j0 += JG) {
+    float o[JG][8];
 #pragma unroll
-  for (int j = 0; j < NQ; ++j)
+    for (int j = 0; j < JG; ++j)
 #pragma unroll
-    for (int cc = 0; cc < CL; ++cc) o[j][cc] = 0.f;
-  int kn = nk - (k0 + wave * 64);
-  kn = kn < 0 ? 0 : (kn > 64 ? 64 : kn);
-  const bf16* vbase = cache + d + h * DH + lane * CL;
-#pragma unroll 4
-  for (int i = 0; i < kn; ++i) {
-    const int kl = wave * 64 + i;
-    const bf16* vp = vbase + static_cast<int64_t>(k0 + kl) * row2;
-    float v[CL];
-    if constexpr (CL == 2) {
-      const bf16x2 pr = *reinterpret_cast<const bf16x2*>(vp);
-      v[0] = static_cast<float>(pr[0]);
-      v[1] = static_cast<float>(pr[CL - 1]);
-    } else {
-      v[0] = static_cast<float>(vp[0]);
-    }
+      for (int e = 0; e < 8; ++e) o[j][e] = 0.f;
 #pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-      if (j < a.n_new) {
-        const float p = sc[j][kl];
+    for (int p = 0; p < NP; ++p) {
+      const int kl = wave * 64 + p * KPP + kg;
 #pragma unroll
-        for (int cc = 0; cc < CL; ++cc) o[j][cc] = __builtin_fmaf(p, v[cc], o[j][cc]);
+      for (int j = 0; j < JG; ++j) {
+        const float pr = j0 + j < a.n_new ? sc[j0 + j][kl] : 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[j][e] = __builtin_fmaf(pr, static_cast<float>(vr[p][e]), o[j][e]);
       }
     }
+#pragma unroll
+    for (int j = 0; j < JG; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int off = LPK; off < 64; off <<= 1) o[j][e] += __shfl_xor(o[j][e], off, 64);
+    if (kg == 0)
+#pragma unroll
+      for (int j = 0; j < JG; ++j)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[wave][j0 + j][sl * 8 + e] = o[j][e];
   }
-#pragma unroll
-  for (int j = 0; j < NQ; ++j)
-    if (j < a.n_new)
-#pragma unroll
-      for (int cc = 0; cc < CL; ++cc) red[wave][j][lane * CL + cc] = o[j][cc];
   __syncthreads();
   for (int e = tid; e < a.n_new * DH; e += 256) {
     const int j = e / DH, col = e % DH;
     const float s = red[0][j][col] + red[1][j][col] + red[2][j][col] + red[3][j][col];
-    a.part_o[(prow * NQ + j) * DH + col] = s;
+    a.part_o[(prow * kDecMaxRows + j) * DH + col] = s;
   }
 }
 
 // One wave per (sequence, head, query row): merge the chunks.
 template <int DH>
 __global__ __launch_bounds__(256) void ld_attn_decode_combine(DecAttnArgs a) {
-  constexpr int NQ = kDecMaxRows;
+  constexpr int NQ = kDecMaxRows;   // row stride of the partials
   constexpr int CL = DH / 64;
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -337,22 +366,27 @@ hipError_t launch_kv_store(const KvArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attn_decode(const DecAttnArgs& a, hipStream_t s) {
+template <int DH, int NQ>
+hipError_t attn_decode_t(const DecAttnArgs& a, hipStream_t s) {
   const dim3 grid(a.n_chunks, a.H, a.n_seq);
+  hipLaunchKernelGGL((ld_attn_decode_bf16<DH, NQ>), grid, dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int rows = a.n_seq * a.H * a.n_new;
-  const dim3 cgrid((rows + 3) / 4);
-  if (a.dh == 128) {
-    hipLaunchKernelGGL(ld_attn_decode_bf16<128>, grid, dim3(256), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(ld_attn_decode_combine<128>, cgrid, dim3(256), 0, s, a);
-  } else {
-    hipLaunchKernelGGL(ld_attn_decode_bf16<64>, grid, dim3(256), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(ld_attn_decode_combine<64>, cgrid, dim3(256), 0, s, a);
-  }
+  hipLaunchKernelGGL(ld_attn_decode_combine<DH>, dim3((rows + 3) / 4), dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+template <int DH>
+hipError_t attn_decode_dh(const DecAttnArgs& a, hipStream_t s) {
+  if (a.n_new <= 1) return attn_decode_t<DH, 1>(a, s);
+  if (a.n_new <= 2) return attn_decode_t<DH, 2>(a, s);
+  if (a.n_new <= 4) return attn_decode_t<DH, 4>(a, s);
+  return attn_decode_t<DH, 8>(a, s);
+}
+
+hipError_t launch_attn_decode(const DecAttnArgs& a, hipStream_t s) {
+  return a.dh == 128 ? attn_decode_dh<128>(a, s) : attn_decode_dh<64>(a, s);
 }
 
 }  // namespace ld

@@ -239,7 +239,12 @@ struct SkinnyArgs {
   int64_t lda, ldw, ldc, ldr;
   int32_t M, N, K;
   float alpha;
-  float* part;  // float32 [ksplit][M][N] when ksplit > 1
+  float* part;        // float32 [ksplit][M][N] when ksplit > 1
+  // optional: columns kv_d.. of row m also go to the cache kv [*, s_max, 2 kv_d]
+  // at position kv_pos + m % kv_n of sequence m / kv_n (the keys/values of a
+  // qkv projection)
+  void* kv;
+  int32_t kv_d, kv_n, kv_s_max, kv_pos;
 };
 constexpr int kSkinnyMaxM = 64;
 
