@@ -30,9 +30,9 @@ CALIB_DISPATCHES = 3  # bench.py runs it 3 times before any other GPU work
 
 def short(name: str) -> str:
     n = re.sub(r"\(anonymous namespace\)::", "", name)
-    m = re.search(r"(ld_[a-z0-9_]+)", n)
+    m = re.search(r"(ld_[a-z0-9_]+(<[^>]*>)?)", n)
     if m:
-        return m.group(1)
+        return m.group(1).replace(" ", "")
     return n[:70]
 
 
