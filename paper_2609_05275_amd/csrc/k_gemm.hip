@@ -431,16 +431,140 @@ __device__ __forceinline__ bf16x8 frag(const bf16* t, const OpLanes<KC>& o, int 
   }
 }
 
-__device__ __forceinline__ void tile_coords(int pid, int n_wg, int tiles_m, int tiles_n, int& tm,
-                                            int& tn) {
-  if ((n_wg & 7) == 0) pid = (pid & 7) * (n_wg >> 3) + (pid >> 3);
+// Tile of workgroup `pid` among the n_valid = tiles_m * tiles_n tiles that
+// hold rows (tiles_m counts only tile rows below the kept count), or false
+// when the workgroup has none.  Workgroup ids are dealt to the 8 XCDs in
+// turn (id % 8), so XCD x is given its own contiguous, balanced range of
+// n_valid / 8 (+1) tiles: the tiles of rows past the kept count are not
+// piled onto the last XCDs, and consecutive tiles share an XCD's L2.  Within
+// a range, tiles go in groups of 8 tile rows, column by column.  The grid has
+// at least as many ids per XCD as the largest range (it is sized for every
+// row), so every tile is taken.
+__device__ __forceinline__ bool tile_coords(int pid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int n_valid = tiles_m * tiles_n;
+  const int x = pid & 7, li = pid >> 3;
+  const int base = n_valid >> 3, rem = n_valid & 7;
+  if (li >= base + (x < rem ? 1 : 0)) return false;
+  const int t = x * base + min(x, rem) + li;
   constexpr int G = 8;
   const int group = G * tiles_n;
-  const int first_m = (pid / group) * G;
+  const int first_m = (t / group) * G;
   const int gsz = min(tiles_m - first_m, G);
-  const int in = pid % group;
+  const int in = t % group;
   tm = first_m + in % gsz;
   tn = in / gsz;
+  return true;
+}
+
+// Epilogue of one staged 32-row block row: the lane's rows are r0 + 2 it
+// (it = 0..15), its 4 columns n..n+3; the staged values (alpha applied) sit
+// at stage[(2 it + half) * kStagePitch + c].
+//
+// Full block row (every row < M, every column < N): all staged values, row
+// map entries and residual values are requested before the first store, so
+// their latencies overlap, and no branch splits the rows.
+__device__ __forceinline__ void epilogue_rows_full(const GemmArgs& g, float* part, const float* stage,
+                                                   int r0, int half, int c, int n, int q_last) {
+  float4 v[16];
+#pragma unroll
+  for (int it = 0; it < 16; ++it)
+    v[it] = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
+  if (part) {
+#pragma unroll
+    for (int it = 0; it < 16; ++it)
+      *reinterpret_cast<float4*>(part + static_cast<int64_t>(r0 + 2 * it) * g.N + n) = v[it];
+    return;
+  }
+  int32_t orow[16];
+  if (g.out_map.idx) {
+    // output row = idx[r / S] * S + r % S
+    const int S = g.out_map.S;
+    const int q0 = r0 / S, rem0 = r0 - q0 * S;
+    if (S >= 32) {
+      // the 32 rows span at most two sequences
+      const int s0 = g.out_map.idx[q0], s1 = g.out_map.idx[min(q0 + 1, q_last)];
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const int rr = rem0 + 2 * it;
+        orow[it] = rr >= S ? s1 * S + (rr - S) : s0 * S + rr;
+      }
+    } else {
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const int r = r0 + 2 * it, q = r / S;
+        orow[it] = g.out_map.idx[q] * S + (r - q * S);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int it = 0; it < 16; ++it) orow[it] = r0 + 2 * it;
+  }
+  if (g.R) {  // bf16 residual (a float32 one takes the edge path)
+    uint2 rv[16];
+    const bf16* R = static_cast<const bf16*>(g.R);
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int64_t rrow = g.r_mapped ? orow[it] : r0 + 2 * it;
+      rv[it] = *reinterpret_cast<const uint2*>(R + rrow * g.ldr + n);
+    }
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const bf16* rb = reinterpret_cast<const bf16*>(&rv[it]);
+      v[it].x += static_cast<float>(rb[0]);
+      v[it].y += static_cast<float>(rb[1]);
+      v[it].z += static_cast<float>(rb[2]);
+      v[it].w += static_cast<float>(rb[3]);
+    }
+  }
+  if (g.c_f32) {
+#pragma unroll
+    for (int it = 0; it < 16; ++it)
+      *reinterpret_cast<float4*>(static_cast<float*>(g.C) + static_cast<int64_t>(orow[it]) * g.ldc + n) = v[it];
+  } else {
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      __attribute__((aligned(8))) bf16 o[4] = {static_cast<bf16>(v[it].x), static_cast<bf16>(v[it].y),
+                                               static_cast<bf16>(v[it].z), static_cast<bf16>(v[it].w)};
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + static_cast<int64_t>(orow[it]) * g.ldc + n) =
+          *reinterpret_cast<const uint2*>(o);
+    }
+  }
+}
+
+// Block row with rows past M or columns past N (or a float32 residual): one
+// row at a time, each checked.
+__device__ __forceinline__ void epilogue_rows_edge(const GemmArgs& g, float* part, const float* stage,
+                                                   int r0, int half, int c, int n, int M) {
+#pragma unroll 1
+  for (int it = 0; it < 16; ++it) {
+    const int m = r0 + 2 * it;
+    if (m >= M || n >= g.N) continue;
+    float4 v = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
+    if (part) {
+      *reinterpret_cast<float4*>(part + static_cast<int64_t>(m) * g.N + n) = v;
+      continue;
+    }
+    const int64_t orow = map_row(g.out_map, m);
+    if (g.R) {
+      const int64_t rrow = g.r_mapped ? orow : m;
+      if (g.c_f32) {
+        const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(g.R) + rrow * g.ldr + n);
+        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+      } else {
+        const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(g.R) + rrow * g.ldr + n);
+        const bf16* rb = reinterpret_cast<const bf16*>(&r);
+        v.x += static_cast<float>(rb[0]); v.y += static_cast<float>(rb[1]);
+        v.z += static_cast<float>(rb[2]); v.w += static_cast<float>(rb[3]);
+      }
+    }
+    if (g.c_f32) {
+      *reinterpret_cast<float4*>(static_cast<float*>(g.C) + orow * g.ldc + n) = v;
+    } else {
+      __attribute__((aligned(8))) bf16 o[4] = {static_cast<bf16>(v.x), static_cast<bf16>(v.y),
+                                               static_cast<bf16>(v.z), static_cast<bf16>(v.w)};
+      *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + orow * g.ldc + n) = *reinterpret_cast<const uint2*>(o);
+    }
+  }
 }
 
 template <bool AK, bool BKC>
@@ -449,11 +573,10 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
   int M, K;
   resolve_counts(g, M, K);
   const int tiles_n = (g.N + GB - 1) / GB;
-  const int tiles_m = static_cast<int>(gridDim.x) / tiles_n;
+  const int tiles_m = min(static_cast<int>(gridDim.x) / tiles_n, (M + GB - 1) / GB);
   int tm, tn;
-  tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  if (!tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn)) return;
   const int m0 = tm * GB, n0 = tn * GB;
-  if (m0 >= M) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -548,6 +671,13 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
   const int half = lane >> 5, lm = lane & 31;
   float* part = g.part ? g.part + static_cast<int64_t>(sp) * g.M * g.N : nullptr;
   float* stage = reinterpret_cast<float*>(ring) + wave * (32 * kStagePitch);
+  const int c = lm * 4;
+  const int n = n0 + wn * 128 + c;
+  // A block row takes the branch-free path when all its 32 rows and 128
+  // columns are in range (and the residual, if any, is bf16).
+  const bool full_cols = n0 + wn * 128 + 128 <= g.N && !(g.R && g.c_f32);
+  // Largest kept sequence index, for the row map (rows < M only).
+  const int q_last = g.out_map.idx && M > 0 ? (M - 1) / g.out_map.S : 0;
   dma_barrier<0>();  // the loop's last loads (zeros) land before the ring is reused
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -560,39 +690,11 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
             make_float4(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
       }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // staged values visible to the wave
-    const int c = (lane & 31) * 4;
-    const int n = n0 + wn * 128 + c;
-#pragma unroll 4
-    for (int it = 0; it < 16; ++it) {
-      const int rl = 2 * it + half;
-      const int m = m0 + wm * 128 + i * 32 + rl;
-      if (m >= M || n >= g.N) continue;
-      float4 v = *reinterpret_cast<const float4*>(stage + rl * kStagePitch + c);
-      if (part) {
-        *reinterpret_cast<float4*>(part + static_cast<int64_t>(m) * g.N + n) = v;
-        continue;
-      }
-      const int64_t orow = map_row(g.out_map, m);
-      if (g.R) {
-        const int64_t rrow = g.r_mapped ? orow : m;
-        if (g.c_f32) {
-          const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(g.R) + rrow * g.ldr + n);
-          v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
-        } else {
-          const uint2 r = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(g.R) + rrow * g.ldr + n);
-          const bf16* rb = reinterpret_cast<const bf16*>(&r);
-          v.x += static_cast<float>(rb[0]); v.y += static_cast<float>(rb[1]);
-          v.z += static_cast<float>(rb[2]); v.w += static_cast<float>(rb[3]);
-        }
-      }
-      if (g.c_f32) {
-        *reinterpret_cast<float4*>(static_cast<float*>(g.C) + orow * g.ldc + n) = v;
-      } else {
-        __attribute__((aligned(8))) bf16 o[4] = {static_cast<bf16>(v.x), static_cast<bf16>(v.y),
-                                                 static_cast<bf16>(v.z), static_cast<bf16>(v.w)};
-        *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + orow * g.ldc + n) = *reinterpret_cast<const uint2*>(o);
-      }
-    }
+    const int mb = m0 + wm * 128 + i * 32;             // first row of the block row
+    if (full_cols && mb + 32 <= M)
+      epilogue_rows_full(g, part, stage, mb + half, half, c, n, q_last);
+    else
+      epilogue_rows_edge(g, part, stage, mb + half, half, c, n, M);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // reads done before the block is rewritten
   }
 }
