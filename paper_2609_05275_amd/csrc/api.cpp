@@ -351,6 +351,36 @@ int run_gemm(int dtype, int a_k, int b_k, GemmArgs g, int64_t max_m, int64_t hos
   return LD_OK;
 }
 
+// A weight-gradient GEMM (g1: both operands mn-contiguous, float32 out, its
+// reduction length the kept rows) and the input-gradient GEMM that reads the
+// same upstream gradient (g2: A k-contiguous, B mn-contiguous) in one launch
+// when both take the 256x256 kernel; otherwise one after the other.
+int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmArgs g2, int64_t max_m2,
+                  int64_t host_m2, int64_t host_k2, hipStream_t s, float* part, size_t part_bytes) {
+  const GemmPlan p1 = plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, part != nullptr);
+  const GemmPlan p2 = plan_gemm(dtype, 1, 0, g2, max_m2, 0, false);
+  if (dtype != LD_BF16 || !p1.big || !p2.big) {
+    if (int rc = run_gemm(dtype, 1, 0, g2, max_m2, host_m2, host_k2, s)) return rc;
+    return run_gemm(dtype, 0, 0, g1, g1.M, g1.M, host_k1, s, part, part_bytes, max_k1);
+  }
+  // at most the split count the standalone plan (and the scratch) allows
+  const PairPlan pp = plan_gemm_pair(g1.M, g1.N, max_k1, max_m2, g2.N, g2.K, p1.splits);
+  if (pp.splits1 > 1) {
+    GemmPlan q = p1;
+    q.splits = pp.splits1;
+    if (gemm_part_bytes(q, g1.M, g1.N) > part_bytes) return fail(LD_E_WORKSPACE, "split-K scratch too small");
+    g1.part = part;
+  }
+  ProfScope ps("ld_gemm_bf16_tn_nn_256", s);
+  const hipError_t e = launch_gemm_pair(g1, pp, g2, max_m2, s);
+  if (e != hipSuccess) return fail(LD_E_HIP, "ld_gemm_bf16_tn_nn_256 launch: %s", hipGetErrorString(e));
+  const double M1 = g1.M, N1 = g1.N, K1 = static_cast<double>(host_k1);
+  const double M2 = static_cast<double>(host_m2), N2 = g2.N, K2 = static_cast<double>(host_k2);
+  ps.end(2.0 * (M1 * N1 * K1 + M2 * N2 * K2),
+         2.0 * (M1 * K1 + N1 * K1) + 4.0 * M1 * N1 + 2.0 * (M2 * K2 + N2 * K2 + M2 * N2));
+  return LD_OK;
+}
+
 // ------------------------------------------------------------ one layer
 
 // Attention sub-block on the rows mv keeps.  hc: its kept count when
@@ -615,7 +645,7 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
     ps.end(0, 2.0 * D.es * hm * D.d);
   }
-  // gs = r * gk W_down   [M, f]
+  // gs = r * gk W_down [M, f] and dW_down = r * gk^T s [d, f], one launch
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.gk);
@@ -629,25 +659,21 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     g.K = static_cast<int32_t>(D.d);
     g.dev_count = mv.count;
     g.count_mult = S;
-    if (int rc = run_gemm(dt, 1, 0, g, T, hm, D.d, s)) return rc;
-  }
-  // dW_down = r * gk^T s   [d, f]
-  {
-    GemmArgs g = gemm_args();
-    g.A = W(BL.gk);
-    g.lda = D.d;
-    g.B = act.at(act.L.s);
-    g.ldb = D.f;
-    g.C = dw.w_down;
-    g.ldc = D.f;
-    g.c_f32 = 1;
-    g.alpha_dev = mv.r;
-    g.M = static_cast<int32_t>(D.d);
-    g.N = static_cast<int32_t>(D.f);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s, SK, BL.splitk_bytes, T)) return rc;
+    GemmArgs g1 = gemm_args();
+    g1.A = W(BL.gk);
+    g1.lda = D.d;
+    g1.B = act.at(act.L.s);
+    g1.ldb = D.f;
+    g1.C = dw.w_down;
+    g1.ldc = D.f;
+    g1.c_f32 = 1;
+    g1.alpha_dev = mv.r;
+    g1.M = static_cast<int32_t>(D.d);
+    g1.N = static_cast<int32_t>(D.f);
+    g1.dev_count = mv.count;
+    g1.count_mult = S;
+    g1.count_dim = 1;
+    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
   }
   // guv = SwiGLU backward, or gu = squared-ReLU backward
   {
@@ -667,7 +693,7 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
       ps.end(0, D.es * hm * D.f * 3.0);
     }
   }
-  // gh2 = guv W_gate_up   [M, d]
+  // gh2 = guv W_gate_up [M, d] and dW_gate_up = guv^T h2 [fw, d], one launch
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.guv);
@@ -680,24 +706,20 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     g.K = static_cast<int32_t>(D.fw);
     g.dev_count = mv.count;
     g.count_mult = S;
-    if (int rc = run_gemm(dt, 1, 0, g, T, hm, D.fw, s)) return rc;
-  }
-  // dW_gate_up = guv^T h2   [fw, d]
-  {
-    GemmArgs g = gemm_args();
-    g.A = W(BL.guv);
-    g.lda = D.fw;
-    g.B = act.at(act.L.h2);
-    g.ldb = D.d;
-    g.C = dw.w_gate_up;
-    g.ldc = D.d;
-    g.c_f32 = 1;
-    g.M = static_cast<int32_t>(D.fw);
-    g.N = static_cast<int32_t>(D.d);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, D.fw, D.fw, hm, s, SK, BL.splitk_bytes, T)) return rc;
+    GemmArgs g1 = gemm_args();
+    g1.A = W(BL.guv);
+    g1.lda = D.fw;
+    g1.B = act.at(act.L.h2);
+    g1.ldb = D.d;
+    g1.C = dw.w_gate_up;
+    g1.ldc = D.d;
+    g1.c_f32 = 1;
+    g1.M = static_cast<int32_t>(D.fw);
+    g1.N = static_cast<int32_t>(D.d);
+    g1.dev_count = mv.count;
+    g1.count_mult = S;
+    g1.count_dim = 1;
+    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.fw, s, SK, BL.splitk_bytes)) return rc;
   }
   // gz = gk + RMSNorm_bwd(zk, g_mlp, gh2); dg_mlp
   {
@@ -745,7 +767,7 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
     if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
     ps.end(0, 2.0 * D.es * hm * D.d);
   }
-  // ga = r * gz W_o   [M, d]
+  // ga = r * gz W_o [M, d] and dW_o = r * gz^T att [d, d], one launch
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.gz);
@@ -759,25 +781,21 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
     g.K = static_cast<int32_t>(D.d);
     g.dev_count = mv.count;
     g.count_mult = S;
-    if (int rc = run_gemm(dt, 1, 0, g, T, hm, D.d, s)) return rc;
-  }
-  // dW_o = r * gz^T att   [d, d]
-  {
-    GemmArgs g = gemm_args();
-    g.A = W(BL.gz);
-    g.lda = D.d;
-    g.B = act.at(act.L.att);
-    g.ldb = D.d;
-    g.C = dw.w_o;
-    g.ldc = D.d;
-    g.c_f32 = 1;
-    g.alpha_dev = mv.r;
-    g.M = static_cast<int32_t>(D.d);
-    g.N = static_cast<int32_t>(D.d);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, D.d, D.d, hm, s, SK, BL.splitk_bytes, T)) return rc;
+    GemmArgs g1 = gemm_args();
+    g1.A = W(BL.gz);
+    g1.lda = D.d;
+    g1.B = act.at(act.L.att);
+    g1.ldb = D.d;
+    g1.C = dw.w_o;
+    g1.ldc = D.d;
+    g1.c_f32 = 1;
+    g1.alpha_dev = mv.r;
+    g1.M = static_cast<int32_t>(D.d);
+    g1.N = static_cast<int32_t>(D.d);
+    g1.dev_count = mv.count;
+    g1.count_mult = S;
+    g1.count_dim = 1;
+    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
   }
   // attention backward -> gqkv
   {
@@ -806,7 +824,7 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
       ps.end(parts_fl[part], D.es * hm * D.d * (part == 0 ? 2.0 : 5.0));
     }
   }
-  // gh1 = gqkv W_qkv   [M, d]
+  // gh1 = gqkv W_qkv [M, d] and dW_qkv = gqkv^T h1 [3d, d], one launch
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.gqkv);
@@ -819,24 +837,20 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
     g.K = static_cast<int32_t>(3 * D.d);
     g.dev_count = mv.count;
     g.count_mult = S;
-    if (int rc = run_gemm(dt, 1, 0, g, T, hm, 3 * D.d, s)) return rc;
-  }
-  // dW_qkv = gqkv^T h1   [3d, d]
-  {
-    GemmArgs g = gemm_args();
-    g.A = W(BL.gqkv);
-    g.lda = 3 * D.d;
-    g.B = act.at(act.L.h1);
-    g.ldb = D.d;
-    g.C = dw.w_qkv;
-    g.ldc = D.d;
-    g.c_f32 = 1;
-    g.M = static_cast<int32_t>(3 * D.d);
-    g.N = static_cast<int32_t>(D.d);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    g.count_dim = 1;
-    if (int rc = run_gemm(dt, 0, 0, g, 3 * D.d, 3 * D.d, hm, s, SK, BL.splitk_bytes, T)) return rc;
+    GemmArgs g1 = gemm_args();
+    g1.A = W(BL.gqkv);
+    g1.lda = 3 * D.d;
+    g1.B = act.at(act.L.h1);
+    g1.ldb = D.d;
+    g1.C = dw.w_qkv;
+    g1.ldc = D.d;
+    g1.c_f32 = 1;
+    g1.M = static_cast<int32_t>(3 * D.d);
+    g1.N = static_cast<int32_t>(D.d);
+    g1.dev_count = mv.count;
+    g1.count_mult = S;
+    g1.count_dim = 1;
+    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, 3 * D.d, s, SK, BL.splitk_bytes)) return rc;
   }
   // dL/dX^l[kept rows] = gz + RMSNorm_bwd(xk, g_attn, gh1); dg_attn
   {

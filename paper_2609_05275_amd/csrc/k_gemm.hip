@@ -17,7 +17,10 @@
 // fp32: a plain SIMT kernel (64x64 tiles, 4x4 per thread) used by the fp32
 // configuration only.
 #include <algorithm>
+#include <functional>
+#include <queue>
 #include <type_traits>
+#include <vector>
 
 #include "ld_internal.h"
 
@@ -567,15 +570,18 @@ __device__ __forceinline__ void epilogue_rows_edge(const GemmArgs& g, float* par
   }
 }
 
+// One workgroup's tile of a GEMM: `pid` in [0, n_tiles) picks the tile
+// (n_tiles covers every row the grid was sized for), `sp` of `splits` the
+// k range; `ring` is the workgroup's LDS.
 template <bool AK, bool BKC>
-__device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
-  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
+__device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int pid, int n_tiles, int sp,
+                                              int splits) {
   int M, K;
   resolve_counts(g, M, K);
   const int tiles_n = (g.N + GB - 1) / GB;
-  const int tiles_m = min(static_cast<int>(gridDim.x) / tiles_n, (M + GB - 1) / GB);
+  const int tiles_m = min(n_tiles / tiles_n, (M + GB - 1) / GB);
   int tm, tn;
-  if (!tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn)) return;
+  if (!tile_coords(pid, tiles_m, tiles_n, tm, tn)) return;
   const int m0 = tm * GB, n0 = tn * GB;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -585,7 +591,6 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
 
   // k range of this split
   const int nkt_all = (K + GK - 1) / GK;
-  const int splits = gridDim.y, sp = blockIdx.y;
   const int kt0 = static_cast<int>((static_cast<int64_t>(nkt_all) * sp) / splits);
   const int kt1 = static_cast<int>((static_cast<int64_t>(nkt_all) * (sp + 1)) / splits);
   const int nk = kt1 - kt0;
@@ -700,22 +705,59 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g) {
 }
 
 #define LD_BIG_ATTRS __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
-LD_BIG_ATTRS void ld_gemm_bf16_nt_256(GemmArgs g) { gemm_big_body<true, true>(g); }
-LD_BIG_ATTRS void ld_gemm_bf16_nn_256(GemmArgs g) { gemm_big_body<true, false>(g); }
-LD_BIG_ATTRS void ld_gemm_bf16_tn_256(GemmArgs g) { gemm_big_body<false, false>(g); }
-LD_BIG_ATTRS void ld_gemm_bf16_tt_256(GemmArgs g) { gemm_big_body<false, true>(g); }
+#define LD_BIG_KERNEL(name, ak, bk)                                                    \
+  LD_BIG_ATTRS void name(GemmArgs g) {                                                 \
+    __shared__ __align__(16) bf16 ring[NSTAGE * kStage];                               \
+    gemm_big_body<ak, bk>(g, ring, blockIdx.x, gridDim.x, blockIdx.y, gridDim.y);      \
+  }
+LD_BIG_KERNEL(ld_gemm_bf16_nt_256, true, true)
+LD_BIG_KERNEL(ld_gemm_bf16_nn_256, true, false)
+LD_BIG_KERNEL(ld_gemm_bf16_tn_256, false, false)
+LD_BIG_KERNEL(ld_gemm_bf16_tt_256, false, true)
 
-// C[i] = R[i] + sum over splits of part[s][i], float32, in split order.
+// Two GEMMs in one launch: a weight-gradient GEMM g1 (both operands
+// mn-contiguous, tiles1 tiles, each split into splits1 k ranges) and an
+// input-gradient GEMM g2 (A k-contiguous, B mn-contiguous, tiles2 tiles) that
+// read the same upstream gradient.  The workgroups of one GEMM come first
+// (g2's when g2_first); the other's then fill the CUs the first leaves idle,
+// so neither GEMM's last partial round of tiles runs on a part-empty chip.
+LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
+                                         int g2_first) {
+  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
+  const int n1 = tiles1 * splits1;
+  int id = blockIdx.x;
+  bool first = true;
+  if (g2_first) {
+    first = id >= tiles2;
+    id = first ? id - tiles2 : id;
+  } else if (id >= n1) {
+    first = false;
+    id -= n1;
+  }
+  if (first)
+    gemm_big_body<false, false>(g1, ring, id % tiles1, tiles1, id / tiles1, splits1);
+  else
+    gemm_big_body<true, false>(g2, ring, id, tiles2, 0, 1);
+}
+
+// C[i] = sum over splits of part[s][i], float32, in split order.  Every
+// split's value is requested before the first add (splits <= kMaxSplits).
+constexpr int kMaxSplits = 8;
 __global__ __launch_bounds__(256) void ld_splitk_reduce(const float* part, int splits, int64_t mn,
                                                         const int32_t* dev_m_unused, float* C) {
   (void)dev_m_unused;
   for (int64_t i4 = blockIdx.x * 256ll + threadIdx.x; i4 < mn / 4; i4 += gridDim.x * 256ll) {
-    float4 s = reinterpret_cast<const float4*>(part)[i4];
-    for (int k = 1; k < splits; ++k) {
-      const float4 t = reinterpret_cast<const float4*>(part + static_cast<int64_t>(k) * mn)[i4];
-      s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
-    }
-    reinterpret_cast<float4*>(C)[i4] = s;
+    float4 t[kMaxSplits];
+#pragma unroll
+    for (int k = 0; k < kMaxSplits; ++k)
+      if (k < splits) t[k] = reinterpret_cast<const float4*>(part + static_cast<int64_t>(k) * mn)[i4];
+    float4 sum = t[0];
+#pragma unroll
+    for (int k = 1; k < kMaxSplits; ++k)
+      if (k < splits) {
+        sum.x += t[k].x; sum.y += t[k].y; sum.z += t[k].z; sum.w += t[k].w;
+      }
+    reinterpret_cast<float4*>(C)[i4] = sum;
   }
 }
 
@@ -750,7 +792,7 @@ GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, i
     // split-K only for float32 outputs without a residual (weight gradients)
     if (allow_split && g.c_f32 && !g.R && !g.out_map.idx && g.ldc == g.N && max_k >= 16 * GK) {
       double best = 0;
-      for (int s = 1; s <= 8; ++s) {
+      for (int s = 1; s <= kMaxSplits; ++s) {
         const int64_t wg = big_tiles * s;
         const double eff = static_cast<double>(wg) / (256.0 * ((wg + 255) / 256)) - 0.02 * (s - 1);
         if (eff > best + 1e-9 && max_k / s >= 8 * GK) {
@@ -816,6 +858,87 @@ hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmP
     return hipGetLastError();
   }
   return launch_gemm(dtype, a_kcontig, b_kcontig, g, max_m, 0, s);
+}
+
+// Estimated finish time, in k tiles of 32 (~1 us each at these shapes), of
+// n1 workgroups of cost c1 followed by n2 of cost c2 dealt in launch order to
+// n_cu CUs, one workgroup per CU, each CU taking the next when it frees.
+static double list_schedule(int64_t n1, double c1, int64_t n2, double c2, int n_cu) {
+  std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
+  for (int i = 0; i < n_cu; ++i) cu.push(0.0);
+  double end = 0.0;
+  for (int64_t w = 0; w < n1 + n2; ++w) {
+    const double t = cu.top() + (w < n1 ? c1 : c2);
+    cu.pop();
+    cu.push(t);
+    end = std::max(end, t);
+  }
+  return end;
+}
+
+PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m2, int64_t n2, int64_t k2,
+                         int max_splits) {
+  int dev = 0, n_cu = 256;
+  if (hipGetDevice(&dev) == hipSuccess)
+    (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (n_cu <= 0) n_cu = 256;
+  struct Entry {
+    int64_t key[7];
+    PairPlan plan;
+  };
+  thread_local Entry cache[8];
+  thread_local int next = 0;
+  const int64_t key[7] = {m1, n1, k1, m2, n2, k2, max_splits * 4096ll + n_cu};
+  for (const Entry& e : cache)
+    if (std::equal(key, key + 7, e.key)) return e.plan;
+  constexpr double kEpi = 8.0;       // epilogue of one tile, in k-tile times
+  constexpr double kLaunch = 4.0;    // a second (reduction) launch
+  constexpr double kTileUs = 0.95;   // one k tile of 32 on one CU
+  const int64_t tiles1 = ((m1 + GB - 1) / GB) * ((n1 + GB - 1) / GB);
+  const int64_t tiles2 = ((m2 + GB - 1) / GB) * ((n2 + GB - 1) / GB);
+  const double c2 = static_cast<double>((k2 + GK - 1) / GK) + kEpi;
+  PairPlan best{1, 0};
+  double best_t = 0.0;
+  for (int sp = 1; sp <= max_splits; ++sp) {
+    const double c1 = static_cast<double>(((k1 + GK - 1) / GK + sp - 1) / sp) + kEpi;
+    for (int order = 0; order < 2; ++order) {
+      double t = order ? list_schedule(tiles2, c2, tiles1 * sp, c1, n_cu)
+                       : list_schedule(tiles1 * sp, c1, tiles2, c2, n_cu);
+      if (sp > 1)  // partials written and read back at ~5 TB/s, plus a launch
+        t += kLaunch + (sp + 1.0) * 4.0 * m1 * n1 / 5e12 / (kTileUs * 1e-6);
+      if ((sp == 1 && order == 0) || t < best_t - 1e-9) {
+        best_t = t;
+        best = PairPlan{sp, order};
+      }
+    }
+  }
+  Entry& e = cache[next];
+  next = (next + 1) % 8;
+  std::copy(key, key + 7, e.key);
+  e.plan = best;
+  return best;
+}
+
+hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s) {
+  const int splits1 = p.splits1;
+  const int64_t tiles1 = ((static_cast<int64_t>(g1.M) + GB - 1) / GB) * ((g1.N + GB - 1) / GB);
+  const int64_t tiles2 = ((max_m2 + GB - 1) / GB) * ((g2.N + GB - 1) / GB);
+  if (splits1 > 1) {
+    if (!g1.part) return hipErrorInvalidValue;
+  } else {
+    g1.part = nullptr;
+  }
+  const int64_t wg = tiles1 * splits1 + tiles2;
+  if (wg <= 0) return hipSuccess;
+  hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
+                     static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits1 == 1) return e;
+  const int64_t mn = static_cast<int64_t>(g1.M) * g1.N;
+  const int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 4096));
+  hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, g1.part, splits1, mn, nullptr,
+                     static_cast<float*>(g1.C));
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,

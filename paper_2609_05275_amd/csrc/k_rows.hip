@@ -297,19 +297,33 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
   for (int col = threadIdx.x; col < a.d; col += 256) part[col] = dg_lds[col];
 }
 
-// dg[c] = sum over blocks of part[b][c] in a fixed order: four row-strided
-// partial sums per column (b = r, r+4, ...), then those four in order.
-__global__ __launch_bounds__(256) void ld_dg_reduce_k(const float* part, int64_t n_blocks, int d,
-                                                      float* dg) {
-  __shared__ float acc[4][64];
-  const int c = threadIdx.x & 63, r = threadIdx.x >> 6;
-  const int col = blockIdx.x * 64 + c;
-  float s = 0.f;
-  if (col < d)
-    for (int64_t b = r; b < n_blocks; b += 4) s += part[b * d + col];
-  acc[r][c] = s;
+// dg[c] = sum over blocks of part[b][c] in a fixed order: 32 row-strided
+// partial sums per column (b = r, r+32, ...), then those 32 in order.  A
+// workgroup covers 32 columns with 32 row groups, so the d / 32 workgroups
+// keep many loads in flight.
+constexpr int kDgCols = 32, kDgGroups = 32;
+__global__ __launch_bounds__(1024) void ld_dg_reduce_k(const float* part, int64_t n_blocks, int d,
+                                                       float* dg) {
+  __shared__ float acc[kDgGroups][kDgCols + 1];
+  const int c = threadIdx.x % kDgCols, r = threadIdx.x / kDgCols;
+  const int col = blockIdx.x * kDgCols + c;
+  float sum = 0.f;
+  if (col < d) {
+    int64_t b = r;
+    for (; b + 3 * kDgGroups < n_blocks; b += 4 * kDgGroups) {
+      const float v0 = part[b * d + col], v1 = part[(b + kDgGroups) * d + col];
+      const float v2 = part[(b + 2 * kDgGroups) * d + col], v3 = part[(b + 3 * kDgGroups) * d + col];
+      sum = (((sum + v0) + v1) + v2) + v3;
+    }
+    for (; b < n_blocks; b += kDgGroups) sum += part[b * d + col];
+  }
+  acc[r][c] = sum;
   __syncthreads();
-  if (r == 0 && col < d) dg[col] = ((acc[0][c] + acc[1][c]) + acc[2][c]) + acc[3][c];
+  if (r == 0 && col < d) {
+    float t = 0.f;
+    for (int k = 0; k < kDgGroups; ++k) t += acc[k][c];
+    dg[col] = t;
+  }
 }
 
 // ----------------------------------------------------------------- SwiGLU
@@ -445,7 +459,7 @@ hipError_t rms_bwd_t(const RmsBwdArgs& a, float* dg, hipStream_t s) {
 #undef LD_RB
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(ld_dg_reduce_k, dim3((a.d + 63) / 64), dim3(256), 0, s, a.dg_part, nblk,
+  hipLaunchKernelGGL(ld_dg_reduce_k, dim3((a.d + kDgCols - 1) / kDgCols), dim3(kDgCols * kDgGroups), 0, s, a.dg_part, nblk,
                      a.d, dg);
   return hipGetLastError();
 }

@@ -316,6 +316,19 @@ const char* gemm_kernel_name(int dtype, int a_kcontig, int b_kcontig);
 GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,
                    int64_t max_k, bool allow_split);
 size_t gemm_part_bytes(const GemmPlan& p, int64_t M, int64_t N);
+// A weight-gradient GEMM g1 (both operands mn-contiguous, float32 out) and an
+// input-gradient GEMM g2 (A k-contiguous, B mn-contiguous) in one launch,
+// both of whose plans are the 256x256 kernel.  plan_gemm_pair picks g1's
+// split count (at most max_splits) and which GEMM's workgroups go first from
+// an estimate of the pair's finish time; g1.part must hold
+// splits1 * M1 * N1 floats when splits1 > 1.
+struct PairPlan {
+  int splits1;
+  int g2_first;
+};
+PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m2, int64_t n2, int64_t k2,
+                        int max_splits);
+hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s);
 hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmPlan& p, GemmArgs g,
                             int64_t max_m, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
