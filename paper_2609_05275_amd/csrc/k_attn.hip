@@ -19,6 +19,8 @@
 //   diagonal.  Heavy (late) query tiles are scheduled first.
 // fp32 path: plain SIMT kernels, one thread per query (or key) row, used by
 // the fp32 configuration only.
+#include <type_traits>
+
 #include "ld_internal.h"
 
 namespace ld {
@@ -415,13 +417,11 @@ __device__ __forceinline__ void rgn_store(const RowGroupsN<DH, NT>& t, bf16* dir
 }
 
 constexpr int BQ = 64;       // query rows per step of the dK/dV kernel
-constexpr int DK_NST = 3;    // dK/dV ring stages (query blocks in LDS)
+constexpr int DK_NST = 4;    // dK/dV ring stages (query blocks in LDS)
 
-// Waves per dK/dV workgroup: 8 (two per SIMD) where the per-wave state fits
-// in 256 registers (d_head 64); 4 for d_head 128, whose K/V fragments and
-// dK/dV accumulators need the whole register file of a SIMD.
+// Waves per dK/dV workgroup: four, one per SIMD.
 template <int DH>
-constexpr int dkdv_waves() { return DH <= 64 ? 8 : 4; }
+constexpr int dkdv_waves() { return 4; }
 
 // Q and dO blocks in the dK/dV ring are [64 q][DH] without padding, the
 // 16-byte chunks of a row XOR-swizzled by row bits 0-3: 16 lanes reading one
@@ -449,25 +449,49 @@ constexpr int dk_loads() { return 2 * (BQ * DH * 2 / 1024) / NW + 2; }
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 
+// LDS reads at a byte address (an LDS pointer as a 32-bit integer); constant
+// parts of the address become instruction immediates.
+typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8_t;
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) const floatx4 lds_float4_t;
+typedef __attribute__((address_space(3))) v4s lds_v4s_t;
+__device__ __forceinline__ bf16x8 lds_frag(uint32_t addr) {
+  return *reinterpret_cast<lds_bf16x8_t*>(static_cast<uintptr_t>(addr));
+}
+__device__ __forceinline__ floatx4 lds_f4(uint32_t addr) {
+  return *reinterpret_cast<lds_float4_t*>(static_cast<uintptr_t>(addr));
+}
+__device__ __forceinline__ v4s lds_tr(uint32_t addr) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4s_t*>(static_cast<uintptr_t>(addr)));
+}
+
 // dK, dV.  A workgroup of NW waves owns 32 NW keys (32 per wave, K and V
 // fragments in registers) and walks the 64-row query blocks from the diagonal
 // to the end.  Q, dO, log-sum-exp and delta of each block go from global
-// memory straight into a three-stage LDS ring (buffer loads with an LDS
+// memory straight into a four-stage LDS ring (buffer loads with an LDS
 // destination, see ld_internal.h), so a block's loads have two block-times to
-// land; one barrier per block.  P = 2^(s*scale*log2e - lse*log2e) is
-// recomputed, dS = P (dP - delta); dV^T += dO^T P and dK^T += Q^T dS take P
-// and dS straight from the score accumulators (their rows are a fixed
-// permutation of the MFMA k index), and dO^T, Q^T come from the same [q][d]
-// blocks through transposing reads (ds_read_b64_tr_b16) in that
-// permutation.  The two 32-row halves of a query block are processed one
-// after the other so only one half's scores are live.  Fragment addresses
-// are per-lane offsets computed once; the loop has no branch around its
-// MFMAs.
+// land.  P = 2^(s*scale*log2e - lse*log2e) is recomputed, dS = P (dP - delta);
+// dV^T += dO^T P and dK^T += Q^T dS take P and dS straight from the score
+// accumulators (their rows are a fixed permutation of the MFMA k index), and
+// dO^T, Q^T come from the same [q][d] blocks through transposing reads
+// (ds_read_b64_tr_b16) in that permutation.
+//
+// Work goes in 32-row halves of a block, three steps each: A (scores S and
+// dP, 16 MFMAs), B (softmax, vector ALU only) and C (dV and dK, 16 MFMAs).
+// They are software-pipelined: while B of half u runs, the MFMAs of A(u+1)
+// and C(u-1) run beside it, so the softmax hides under matrix work instead
+// of stalling it.  Each block is one loop iteration of two half-steps with
+// the ring's barrier between them.  Fragment addresses are per-lane offsets
+// moved by one stage per block; the loop has no branch around its MFMAs
+// (query rows before a wave's keys are computed and masked to P = 0, a
+// phantom block past the end multiplies zeros, and waves past the end
+// compute on zero K/V and store nothing).
 template <int DH, int NW, bool AL>
 __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   constexpr int BKEYS = 32 * NW, SB = dk_stage_bytes<DH>(), NL = dk_loads<DH, NW>();
   constexpr int RPI = 512 / DH, LPR = 64 / RPI;   // rows per 1 KB load, lanes per row
   constexpr int NPW = (BQ * DH * 2 / 1024) / NW;  // 1 KB loads per wave per tile
+  static_assert(DK_NST == 4, "stage arithmetic assumes a ring of four");
   extern __shared__ __align__(16) char ring[];
   const int S = a.S, H = a.H;
   // grid (head, sequence, tile), tile slowest: early key tiles see the most
@@ -479,6 +503,7 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hf = lane >> 5, cl = lane & 31;
   const int k0 = kt * BKEYS, kw = k0 + wave * 32, key = kw + cl;
+  if (k0 >= S) return;  // the whole workgroup is past the end
   const bool active = kw < S;
   const int64_t ldq = 3ll * H * DH, ldo = static_cast<int64_t>(H) * DH;
   const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
@@ -532,90 +557,187 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     dma4(rd, sb + 4 * BQ * DH + 4 * BQ, in ? static_cast<uint32_t>((qb + lane) * 4) : kDmaOob);
   };
 
-  // Per-lane fragment offsets within a block; the row offsets of the halves
-  // and 16-row groups are instruction immediates.
-  int po[DH / 16];            // plain reads: row cl, 16-byte chunk 2ks + hf
-  int to0[DH / 32], to1[DH / 32];  // transposing reads, rows tr_r and tr_r + 8
+  // Per-lane LDS byte addresses of the fragments, each set pointing into the
+  // stage of the block it serves: plain reads of Q (row cl, 16-byte chunk
+  // 2ks + hf) for step A, transposing reads (rows tr_r and tr_r + 8) for
+  // step C, and the log-sum-exp of the lane's first query for step B.  The
+  // dO block, the half, the 16-row groups and delta are immediates.
+  uint32_t aq[DH / 16], at0[DH / 32], at1[DH / 32], al;
   {
+    const uint32_t r0 = lds_addr(ring);
     const int sw_c = qd_swz<DH>(cl);
 #pragma unroll
-    for (int ks = 0; ks < DH / 16; ++ks) po[ks] = cl * DH + (((2 * ks + hf) ^ sw_c) << 3);
+    for (int ks = 0; ks < DH / 16; ++ks) aq[ks] = r0 + 2u * (cl * DH + (((2 * ks + hf) ^ sw_c) << 3));
     const int tr_r = 4 * hf + ((lane & 15) >> 2);
     const int tr_d = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
     const int sw0 = qd_swz<DH>(tr_r), sw1 = qd_swz<DH>(tr_r + 8);
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db) {
       const int d0 = db * 32 + tr_d;
-      to0[db] = tr_r * DH + (((d0 >> 3) ^ sw0) << 3) + (d0 & 7);
-      to1[db] = (tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7);
+      at0[db] = r0 + 2u * (tr_r * DH + (((d0 >> 3) ^ sw0) << 3) + (d0 & 7));
+      at1[db] = r0 + 2u * ((tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7));
     }
+    al = r0 + 4u * BQ * DH + 16u * hf;
   }
+  constexpr uint32_t kOb = 2u * BQ * DH;  // dO block after the Q block (bytes)
+  constexpr uint32_t kDl = 4u * BQ;       // delta after the log-sum-exp (bytes)
+  // moving a set from the stage of block b to that of block b + 1
+  auto adv = [](int b) { return (b & 3) == 3 ? static_cast<uint32_t>(-3 * SB) : static_cast<uint32_t>(SB); };
 
-  const int q_first = k0;  // the first query that can see key k0
-  const int nqb = q_first < S ? (S - q_first) / BQ : 0;
-  load_block(0, q_first);
-  load_block(1, q_first + BQ);
-  // No branch around the MFMAs (a branch would merge the dK/dV accumulators
-  // across register files): query rows before a wave's keys are computed and
-  // masked to P = 0, and waves past the end compute on zero K/V and store
-  // nothing.
-  for (int ib = 0; ib < nqb; ++ib) {
-    const int qb = q_first + ib * BQ, st = ib % DK_NST;
-    // block ib has landed (block ib+1 may be in flight); the stage of block
-    // ib-1 is no longer read and takes block ib+2
-    dma_barrier<NL>();
-    load_block((ib + 2) % DK_NST, qb + 2 * BQ);
-    const char* sb = ring + st * SB;
-    const bf16* Qs = reinterpret_cast<const bf16*>(sb);
-    const bf16* Os = Qs + BQ * DH;
-    const float* ls = reinterpret_cast<const float*>(sb + 4 * BQ * DH);
-    const float* dl = ls + BQ;
+  // A: scores S = Q K^T and dP = dO V^T of half qh of the block aq points at.
+  auto step_a = [&](int qh, floatx16& sc, floatx16& dp) {
+    const uint32_t hq = 2u * qh * 32 * DH;
+    sc = mfma(lds_frag(aq[0] + hq), kf[0], floatx16{});
+    dp = mfma(lds_frag(aq[0] + hq + kOb), vf[0], floatx16{});
 #pragma unroll
-    for (int qh = 0; qh < 2; ++qh) {
-      floatx16 sc, dp;
+    for (int ks = 1; ks < DH / 16; ++ks) {
+      sc = mfma(lds_frag(aq[ks] + hq), kf[ks], sc);
+      dp = mfma(lds_frag(aq[ks] + hq + kOb), vf[ks], dp);
+    }
+  };
+  // B: P and dS of half qh of query block qb (the block al points at), as
+  // bf16 MFMA operands.
+  auto step_b = [&](const floatx16& sc, const floatx16& dp, int qb, int qh, bf16x8 (&pb)[2],
+                    bf16x8 (&dsb)[2]) {
+    floatx4 l4[4], d4[4];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) sc[v] = dp[v] = 0.f;
+    for (int g = 0; g < 4; ++g) {
+      l4[g] = lds_f4(al + 4u * (qh * 32 + 8 * g));
+      d4[g] = lds_f4(al + kDl + 4u * (qh * 32 + 8 * g));
+    }
+    const int t = key - (qb + qh * 32 + 4 * hf);  // key minus the lane's first query
+    const float ab = al2 * static_cast<float>(t);  // ALiBi bias at that query
 #pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks) {
-        sc = mfma(load8(Qs + qh * 32 * DH + po[ks]), kf[ks], sc);
-        dp = mfma(load8(Os + qh * 32 * DH + po[ks]), vf[ks], dp);
-      }
-      float4 l4[4], d4[4];
+    for (int v = 0; v < 16; ++v) {
+      const int c = 8 * (v >> 2) + (v & 3);  // the element's query after the first
+      float x = fmaf(sc[v], sl2, -l4[v >> 2][v & 3] * kLog2e);
+      if constexpr (AL) x += fmaf(-al2, static_cast<float>(c), ab);
+      float p = __builtin_amdgcn_exp2f(x);
+      p = t > c ? 0.f : p;  // causal: keys after the query
+      pb[v >> 3][v & 7] = static_cast<bf16>(p);
+      dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - d4[v >> 2][v & 3]));
+    }
+  };
+  // C: dV^T += dO^T P, dK^T += Q^T dS for half qh of the block at0/at1 point at.
+  auto step_c = [&](const bf16x8 (&pb)[2], const bf16x8 (&dsb)[2], int qh) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        l4[g] = *reinterpret_cast<const float4*>(ls + qh * 32 + 8 * g + 4 * hf);
-        d4[g] = *reinterpret_cast<const float4*>(dl + qh * 32 + 8 * g + 4 * hf);
-      }
-      bf16x8 pb[2], dsb[2];
-      const float ab = al2 * static_cast<float>(key - qb - qh * 32 - 4 * hf);  // bias at the lane's first query
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int ql = qh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-        const float lv = (&l4[v >> 2].x)[v & 3], dv_ = (&d4[v >> 2].x)[v & 3];
-        float x = sc[v] * sl2 - lv * kLog2e;
-        if constexpr (AL) x += fmaf(-al2, static_cast<float>(8 * (v >> 2) + (v & 3)), ab);
-        float p = __builtin_amdgcn_exp2f(x);
-        p = key > qb + ql ? 0.f : p;
-        pb[v >> 3][v & 7] = static_cast<bf16>(p);
-        dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - dv_));
-      }
+    for (int c = 0; c < 2; ++c) {
 #pragma unroll
       for (int db = 0; db < DH / 32; ++db) {
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int rr = (qh * 32 + 16 * c) * DH;
-          typedef __attribute__((address_space(3))) v4s lds_v4s;
-          const v4s ol = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Os + rr + to0[db]));
-          const v4s oh = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Os + rr + to1[db]));
-          const v4s ql_ = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Qs + rr + to0[db]));
-          const v4s qh_ = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(Qs + rr + to1[db]));
-          dv[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ol, oh, 0, 1, 2, 3, 4, 5, 6, 7)), pb[c], dv[db]);
-          dk[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ql_, qh_, 0, 1, 2, 3, 4, 5, 6, 7)), dsb[c], dk[db]);
-        }
+        const uint32_t rr = 2u * (qh * 32 + 16 * c) * DH;
+        const v4s ol = lds_tr(at0[db] + rr + kOb), oh = lds_tr(at1[db] + rr + kOb);
+        const v4s ql_ = lds_tr(at0[db] + rr), qh_ = lds_tr(at1[db] + rr);
+        dv[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ol, oh, 0, 1, 2, 3, 4, 5, 6, 7)), pb[c], dv[db]);
+        dk[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ql_, qh_, 0, 1, 2, 3, 4, 5, 6, 7)), dsb[c], dk[db]);
       }
-      __builtin_amdgcn_sched_barrier(0);  // keep the two halves' live ranges apart
     }
+  };
+  // One half-step of the pipeline, ordered by hand: C of half qh_c (the
+  // block at0/at1 point at), A of half qh_a (the block aq points at) and B of
+  // the half whose scores are scb/dpb.  Iteration i issues, in this order,
+  // the S MFMA of k step i, the dV MFMA of C pair i, the dP MFMA and the dK
+  // MFMA ((db, c) = (i % (DH/32), i / (DH/32)); both steps have DH/16
+  // iterations), so an accumulator's consecutive MFMAs are at least four
+  // apart and none waits on the one before it.  The softmax elements of B
+  // go between the MFMAs, the fragments of iteration i+2 are read during
+  // iteration i, and scheduling barriers keep the compiler to this order.
+  auto half_step = [&](const bf16x8 (&pbc)[2], const bf16x8 (&dsbc)[2], int qh_c, int qh_a, floatx16& sc,
+                       floatx16& dp, const floatx16& scb, const floatx16& dpb, int qb_b, int qh_b,
+                       bf16x8 (&pbo)[2], bf16x8 (&dsbo)[2]) {
+    constexpr int N = DH / 16, NDB = DH / 32, EPI = 16 / N;  // softmax elements per iteration
+    const uint32_t hq = 2u * qh_a * 32 * DH;
+    struct Frags {
+      v4s ol, oh, ql, qh;
+      bf16x8 qf, of;
+    };
+    auto load = [&](Frags& f, int i) {
+      const int db = i % NDB, c = i / NDB;
+      const uint32_t rr = 2u * (qh_c * 32 + 16 * c) * DH;
+      f.ol = lds_tr(at0[db] + rr + kOb);
+      f.oh = lds_tr(at1[db] + rr + kOb);
+      f.ql = lds_tr(at0[db] + rr);
+      f.qh = lds_tr(at1[db] + rr);
+      f.qf = lds_frag(aq[i] + hq);
+      f.of = lds_frag(aq[i] + hq + kOb);
+    };
+    Frags fr[3];
+    load(fr[0], 0);
+    load(fr[1], 1);
+    floatx4 l4[4], d4[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      l4[g] = lds_f4(al + 4u * (qh_b * 32 + 8 * g));
+      d4[g] = lds_f4(al + kDl + 4u * (qh_b * 32 + 8 * g));
+    }
+    const int t = key - (qb_b + qh_b * 32 + 4 * hf);  // key minus the lane's first query
+    const float ab = al2 * static_cast<float>(t);      // ALiBi bias at that query
+    auto softmax = [&](int v) {
+      const int c = 8 * (v >> 2) + (v & 3);  // the element's query after the first
+      float x = fmaf(scb[v], sl2, -l4[v >> 2][v & 3] * kLog2e);
+      if constexpr (AL) x += fmaf(-al2, static_cast<float>(c), ab);
+      float p = __builtin_amdgcn_exp2f(x);
+      p = t > c ? 0.f : p;  // causal: keys after the query
+      pbo[v >> 3][v & 7] = static_cast<bf16>(p);
+      dsbo[v >> 3][v & 7] = static_cast<bf16>(p * (dpb[v] - d4[v >> 2][v & 3]));
+    };
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if (i + 2 < N) load(fr[(i + 2) % 3], i + 2);
+      const Frags& f = fr[i % 3];
+      const int db = i % NDB, c = i / NDB;
+      sc = mfma(f.qf, kf[i], i == 0 ? floatx16{} : sc);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = 0; e < EPI / 2; ++e) softmax(EPI * i + e);
+      dv[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(f.ol, f.oh, 0, 1, 2, 3, 4, 5, 6, 7)), pbc[c], dv[db]);
+      __builtin_amdgcn_sched_barrier(0);
+      dp = mfma(f.of, vf[i], i == 0 ? floatx16{} : dp);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = EPI / 2; e < EPI; ++e) softmax(EPI * i + e);
+      dk[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(f.ql, f.qh, 0, 1, 2, 3, 4, 5, 6, 7)), dsbc[c], dk[db]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto move = [](auto& set, uint32_t d) {
+#pragma unroll
+    for (auto& x : set) x += d;
+  };
+
+  const int q_first = k0;  // the first query that can see key k0
+  const int nqb = (S - q_first) / BQ;
+  floatx16 scx, dpx, scy, dpy;  // scores of two halves in flight
+  bf16x8 pbx[2], dsbx[2], pby[2], dsby[2];
+
+  // Block 0: A(0); then A(1) next to B(0); the ring's barrier; then C(0)
+  // and A(2) (block 1) next to B(1).
+  load_block(0, q_first);
+  load_block(1, q_first + BQ);
+  load_block(2, q_first + 2 * BQ);
+  dma_barrier<2 * NL>();  // block 0 has landed
+  step_a(0, scx, dpx);
+  step_a(1, scy, dpy);
+  step_b(scx, dpx, q_first, 0, pbx, dsbx);
+  dma_barrier<NL>();  // block 1 has landed; block 3 goes to the fourth stage
+  load_block(3, q_first + 3 * BQ);
+  move(aq, adv(0));
+  half_step(pbx, dsbx, 0, 0, scx, dpx, scy, dpy, q_first, 1, pby, dsby);
+  al += adv(0);
+  // Block j: C(2j-1) (block j-1) and A(2j+1) next to B(2j); barrier (block
+  // j+1 has landed, block j+3 goes to the stage block j-1 left); C(2j) and
+  // A(2j+2) (block j+1) next to B(2j+1).
+  for (int j = 1; j < nqb; ++j) {
+    const int qb = q_first + j * BQ;
+    half_step(pby, dsby, 1, 1, scy, dpy, scx, dpx, qb, 0, pbx, dsbx);
+    dma_barrier<NL>();
+    load_block((j + 3) & 3, qb + 3 * BQ);
+    move(aq, adv(j));
+    move(at0, adv(j - 1));
+    move(at1, adv(j - 1));
+    half_step(pbx, dsbx, 0, 0, scx, dpx, scy, dpy, qb, 1, pby, dsby);
+    al += adv(j);
   }
+  step_c(pby, dsby, 1);  // C of the last half
   dma_barrier<0>();  // no load may still write LDS when the workgroup ends
   if (active && key < S) {
     bf16* G = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + key) * ldq + head * DH;
