@@ -264,13 +264,20 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
           for (int v = 0; v < 16; ++v) {
             float x = sc[sb][kh][v] * sl2;
             if constexpr (AL) x += fmaf(al2, static_cast<float>(kh * 32 + 8 * (v >> 2) + (v & 3)), ab);
-            if (diag) {
-              const int key = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-              if (key > qrow) x = -INFINITY;
-            }
             sc[sb][kh][v] = x;
-            mx = fmaxf(mx, x);
           }
+        if (diag) {  // causal mask, only on blocks that reach past a row (wave-uniform)
+          const int t = qrow - k0 - 4 * hf;  // the row minus the lane's first key
+#pragma unroll
+          for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+              if (kh * 32 + 8 * (v >> 2) + (v & 3) > t) sc[sb][kh][v] = -INFINITY;
+        }
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[sb][kh][v]);
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
         // Lazy rescaling: the running maximum only moves (and O, l are only
         // rescaled) when a row's maximum grows by more than 8 in log2 units;
@@ -298,20 +305,21 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
           }
         l[sb] += ls;
       }
-      // O^T += V^T P^T for both blocks: each V fragment feeds two chains
+      // O^T += V^T P^T; consecutive MFMAs go to different accumulators (the
+      // d blocks innermost), so none waits on the one before it
 #pragma unroll
-      for (int db = 0; db < DH / 32; ++db) {
-        const int vr = db * 32 + cl;
+      for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
+        for (int c = 0; c < 2; ++c) {
+          const int kbb = kh * 32 + 16 * c + 4 * hf;
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int kbb = kh * 32 + 16 * c + 4 * hf;
+          for (int db = 0; db < DH / 32; ++db) {
+            const int vr = db * 32 + cl;
             const bf16x8 vf = load4x2(Vt + tr_off(vr, kbb), Vt + tr_off(vr, kbb + 8));
 #pragma unroll
             for (int sb = 0; sb < NSB; ++sb) o[sb][db] = mfma(vf, pb[sb][kh][c], o[sb][db]);
           }
-      }
+        }
     }
     if (kb + 1 < nkb) {
       bf16* Kn = lds + ((kb + 1) & 1) * (KT + VT);
