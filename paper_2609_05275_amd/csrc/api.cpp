@@ -355,11 +355,19 @@ int run_gemm(int dtype, int a_k, int b_k, GemmArgs g, int64_t max_m, int64_t hos
 // reduction length the kept rows) and the input-gradient GEMM that reads the
 // same upstream gradient (g2: A k-contiguous, B mn-contiguous) in one launch
 // when both take the 256x256 kernel; otherwise one after the other.
+bool gemm_pair_ok(int dtype, const GemmArgs& g1, int64_t max_k1, const GemmArgs& g2, int64_t max_m2) {
+  return dtype == LD_BF16 && plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, true).big &&
+         plan_gemm(dtype, 1, 0, g2, max_m2, 0, false).big;
+}
+
+// g2.glu_f > 0 (only when gemm_pair_ok): the SwiGLU backward is fused into
+// g2's epilogue (see GemmArgs).
 int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmArgs g2, int64_t max_m2,
                   int64_t host_m2, int64_t host_k2, hipStream_t s, float* part, size_t part_bytes) {
   const GemmPlan p1 = plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, part != nullptr);
   const GemmPlan p2 = plan_gemm(dtype, 1, 0, g2, max_m2, 0, false);
   if (dtype != LD_BF16 || !p1.big || !p2.big) {
+    if (g2.glu_f > 0) return fail(LD_E_INVALID, "fused SwiGLU backward needs the paired 256x256 kernels");
     if (int rc = run_gemm(dtype, 1, 0, g2, max_m2, host_m2, host_k2, s)) return rc;
     return run_gemm(dtype, 0, 0, g1, g1.M, g1.M, host_k1, s, part, part_bytes, max_k1);
   }
@@ -371,13 +379,16 @@ int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmA
     if (gemm_part_bytes(q, g1.M, g1.N) > part_bytes) return fail(LD_E_WORKSPACE, "split-K scratch too small");
     g1.part = part;
   }
-  ProfScope ps("ld_gemm_bf16_tn_nn_256", s);
+  const char* name = g2.glu_f > 0 ? "ld_gemm_bf16_tn_nn_glu_256" : "ld_gemm_bf16_tn_nn_256";
+  ProfScope ps(name, s);
   const hipError_t e = launch_gemm_pair(g1, pp, g2, max_m2, s);
-  if (e != hipSuccess) return fail(LD_E_HIP, "ld_gemm_bf16_tn_nn_256 launch: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return fail(LD_E_HIP, "%s launch: %s", name, hipGetErrorString(e));
   const double M1 = g1.M, N1 = g1.N, K1 = static_cast<double>(host_k1);
   const double M2 = static_cast<double>(host_m2), N2 = g2.N, K2 = static_cast<double>(host_k2);
+  // the fused epilogue reads [u v] and writes [gu gv] instead of writing gs
+  const double out2 = g2.glu_f > 0 ? 4.0 * M2 * N2 : 1.0 * M2 * N2;
   ps.end(2.0 * (M1 * N1 * K1 + M2 * N2 * K2),
-         2.0 * (M1 * K1 + N1 * K1) + 4.0 * M1 * N1 + 2.0 * (M2 * K2 + N2 * K2 + M2 * N2));
+         2.0 * (M1 * K1 + N1 * K1) + 4.0 * M1 * N1 + 2.0 * (M2 * K2 + N2 * K2 + out2));
   return LD_OK;
 }
 
@@ -532,6 +543,17 @@ int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, c
     g.M = static_cast<int32_t>(T);
     g.dev_count = mv.count;
     g.count_mult = static_cast<int32_t>(D.S);
+    // SwiGLU fused into the projection's epilogue where the 256x256 kernel
+    // applies and d_ff is a multiple of 128
+    if (D.kind == LD_BLOCK_SWIGLU && dt == LD_BF16 && D.f % 128 == 0 && plan_gemm(dt, 1, 1, g, T, 0, false).big) {
+      g.aux = act.at(act.L.s);
+      g.glu_f = static_cast<int32_t>(D.f);
+      ProfScope ps("ld_gemm_bf16_nt_glu_256", s);
+      if ((e = launch_gemm_glu_fwd(g, T, s)) != hipSuccess)
+        return fail(LD_E_HIP, "ld_gemm_bf16_nt_glu_256 launch: %s", hipGetErrorString(e));
+      ps.end(2.0 * hm * D.fw * D.d, D.es * (hm * D.d + D.fw * D.d + hm * D.fw + hm * D.f));
+      goto down_projection;
+    }
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
   }
   // s = silu(u) * v  or  s = relu(u)^2
@@ -551,6 +573,7 @@ int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, c
       ps.end(0, D.es * hm * D.f * 2.0);
     }
   }
+down_projection:
   // X[kept rows] = zk + r * (s W_down^T)  (scatter into the residual stream)
   {
     GemmArgs g = gemm_args();
@@ -645,7 +668,10 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
     ps.end(0, 2.0 * D.es * hm * D.d);
   }
-  // gs = r * gk W_down [M, f] and dW_down = r * gk^T s [d, f], one launch
+  // gs = r * gk W_down [M, f] and dW_down = r * gk^T s [d, f], one launch;
+  // for SwiGLU in the paired kernels, the SwiGLU backward is fused into the
+  // first product's epilogue (guv from gs without storing gs)
+  bool glu_fused = false;
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.gk);
@@ -673,10 +699,17 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     g1.dev_count = mv.count;
     g1.count_mult = S;
     g1.count_dim = 1;
+    if (D.kind == LD_BLOCK_SWIGLU && gemm_pair_ok(dt, g1, T, g, T)) {
+      glu_fused = true;
+      g.C = W(BL.guv);
+      g.ldc = D.fw;
+      g.aux = act.at(act.L.uv);
+      g.glu_f = static_cast<int32_t>(D.f);
+    }
     if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
   }
   // guv = SwiGLU backward, or gu = squared-ReLU backward
-  {
+  if (!glu_fused) {
     EltArgs a{};
     a.a = act.at(act.L.uv);
     a.b = W(BL.gs);

@@ -418,6 +418,19 @@ __device__ __forceinline__ void tile_part(bf16* lds, const OpLanes<KC>& o, const
   (void)R;
 }
 
+// B tile of the fused SwiGLU forward: load instruction p fills the tile's
+// 64-row block p with gate rows (p even) or up rows (p odd)
+// tn*128 + (p/2)*64 .. +63 of W_gate_up [2f, K], so the tile holds
+// [gate 0-63 | up 0-63 | gate 64-127 | up 64-127] of its 128 d_ff columns and
+// each wave's 128 rows pair every gate row with its up row 64 further on.
+__device__ __forceinline__ void tile_part_glu(bf16* lds, const OpLanes<true>& o, const bf16* W, int64_t ld,
+                                              int tn, int f, int k0, int K, int wave, int p) {
+  const int64_t rbase = ((p & 1) ? f : 0) + static_cast<int64_t>(tn) * 128 + (p >> 1) * 64;
+  const v4i rs = dma_make_rsrc(W + rbase * ld, 64 * ld * 2);
+  const uint32_t off = k0 + o.kchunk < K ? o.ld_off[0] + static_cast<uint32_t>(k0 * 2) : kOob;
+  dma16(rs, lds + (p * 4 + wave) * 512, off);
+}
+
 // Fragment of block i of the wave's 128 rows for k-substep ks: the lane's
 // MFMA row is r + 32 i + lane % 32 (r as given to op_lanes), its 8 k values
 // start at ks*16 + (lane/32)*8.  Only the per-lane offset is a register; the
@@ -570,10 +583,120 @@ __device__ __forceinline__ void epilogue_rows_edge(const GemmArgs& g, float* par
   }
 }
 
+constexpr int kEpiPlain = 0, kEpiGluFwd = 1, kEpiGluBwd = 2;
+
+__device__ __forceinline__ float bf16r(float x) { return static_cast<float>(static_cast<bf16>(x)); }
+
+__device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) {
+  __attribute__((aligned(8))) bf16 o[4] = {static_cast<bf16>(a), static_cast<bf16>(b), static_cast<bf16>(c),
+                                           static_cast<bf16>(d)};
+  return *reinterpret_cast<const uint2*>(o);
+}
+
+__device__ __forceinline__ float4 unpack4_bf16(uint2 r) {
+  const bf16* b = reinterpret_cast<const bf16*>(&r);
+  return make_float4(static_cast<float>(b[0]), static_cast<float>(b[1]), static_cast<float>(b[2]),
+                     static_cast<float>(b[3]));
+}
+
+// Fused SwiGLU forward, [u v] part: the staged block row (lane rows
+// r0 + 2 it, 4 columns at stage column c) goes to C column gc.  `full`: all
+// 32 rows are below M (loads of the block issued before any store).
+__device__ __forceinline__ void glu_fwd_uv_rows(const GemmArgs& g, const float* stage, int r0, int half, int c,
+                                                int gc, int M, bool full) {
+  bf16* C = static_cast<bf16*>(g.C);
+  if (full) {
+    float4 v[16];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) v[it] = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
+#pragma unroll
+    for (int it = 0; it < 16; ++it)
+      *reinterpret_cast<uint2*>(C + static_cast<int64_t>(r0 + 2 * it) * g.ldc + gc) =
+          pack4_bf16(v[it].x, v[it].y, v[it].z, v[it].w);
+  } else {
+#pragma unroll 1
+    for (int it = 0; it < 16; ++it) {
+      if (r0 + 2 * it >= M) break;
+      const float4 v = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
+      *reinterpret_cast<uint2*>(C + static_cast<int64_t>(r0 + 2 * it) * g.ldc + gc) = pack4_bf16(v.x, v.y, v.z, v.w);
+    }
+  }
+}
+
+// Fused SwiGLU forward, s part: 32 staged rows of 64 columns (stage columns
+// 0-63) to aux columns sc0..sc0+63; lane: row 4 it + lane/16, 4 columns at
+// 4 (lane % 16).
+__device__ __forceinline__ void glu_fwd_s_rows(const GemmArgs& g, const float* stage, int mb, int lane, int sc0,
+                                               int M, bool full) {
+  bf16* Sp = static_cast<bf16*>(g.aux);
+  const int rl = lane >> 4, cc = (lane & 15) * 4;
+  if (full) {
+    float4 v[8];
+#pragma unroll
+    for (int it = 0; it < 8; ++it) v[it] = *reinterpret_cast<const float4*>(stage + (4 * it + rl) * kStagePitch + cc);
+#pragma unroll
+    for (int it = 0; it < 8; ++it)
+      *reinterpret_cast<uint2*>(Sp + static_cast<int64_t>(mb + 4 * it + rl) * g.glu_f + sc0 + cc) =
+          pack4_bf16(v[it].x, v[it].y, v[it].z, v[it].w);
+  } else {
+#pragma unroll 1
+    for (int it = 0; it < 8; ++it) {
+      const int m = mb + 4 * it + rl;
+      if (m >= M) continue;
+      const float4 v = *reinterpret_cast<const float4*>(stage + (4 * it + rl) * kStagePitch + cc);
+      *reinterpret_cast<uint2*>(Sp + static_cast<int64_t>(m) * g.glu_f + sc0 + cc) = pack4_bf16(v.x, v.y, v.z, v.w);
+    }
+  }
+}
+
+// Fused SwiGLU backward: the staged gs values (alpha applied; rows r0 + 2 it,
+// columns n..n+3 < N = f), rounded to bf16 as a stored gs would be, with u
+// and v read from aux, give gu and gv in C columns n and f + n.
+__device__ __forceinline__ void glu_bwd_one(const GemmArgs& g, float4 gs, uint2 ur, uint2 vr, int64_t m, int n) {
+  const float4 u = unpack4_bf16(ur), v = unpack4_bf16(vr);
+  float gu[4], gv[4];
+  swiglu_bwd_f(u.x, v.x, bf16r(gs.x), gu[0], gv[0]);
+  swiglu_bwd_f(u.y, v.y, bf16r(gs.y), gu[1], gv[1]);
+  swiglu_bwd_f(u.z, v.z, bf16r(gs.z), gu[2], gv[2]);
+  swiglu_bwd_f(u.w, v.w, bf16r(gs.w), gu[3], gv[3]);
+  bf16* C = static_cast<bf16*>(g.C) + m * g.ldc;
+  *reinterpret_cast<uint2*>(C + n) = pack4_bf16(gu[0], gu[1], gu[2], gu[3]);
+  *reinterpret_cast<uint2*>(C + g.glu_f + n) = pack4_bf16(gv[0], gv[1], gv[2], gv[3]);
+}
+
+__device__ __forceinline__ void glu_bwd_rows(const GemmArgs& g, const float* stage, int r0, int half, int c, int n,
+                                             int M, bool full) {
+  const bf16* U = static_cast<const bf16*>(g.aux);
+  const int64_t ldu = 2ll * g.glu_f;
+  if (full) {
+    uint2 ur[16], vr[16];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int64_t m = r0 + 2 * it;
+      ur[it] = *reinterpret_cast<const uint2*>(U + m * ldu + n);
+      vr[it] = *reinterpret_cast<const uint2*>(U + m * ldu + g.glu_f + n);
+    }
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const float4 gs = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
+      glu_bwd_one(g, gs, ur[it], vr[it], r0 + 2 * it, n);
+    }
+  } else {
+#pragma unroll 1
+    for (int it = 0; it < 16; ++it) {
+      const int64_t m = r0 + 2 * it;
+      if (m >= M || n >= g.N) continue;
+      const float4 gs = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
+      glu_bwd_one(g, gs, *reinterpret_cast<const uint2*>(U + m * ldu + n),
+                  *reinterpret_cast<const uint2*>(U + m * ldu + g.glu_f + n), m, n);
+    }
+  }
+}
+
 // One workgroup's tile of a GEMM: `pid` in [0, n_tiles) picks the tile
 // (n_tiles covers every row the grid was sized for), `sp` of `splits` the
 // k range; `ring` is the workgroup's LDS.
-template <bool AK, bool BKC>
+template <bool AK, bool BKC, int EPI = kEpiPlain>
 __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int pid, int n_tiles, int sp,
                                               int splits) {
   int M, K;
@@ -612,6 +735,8 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
     const int k0 = (kt0 + kt) * GK;
     if (q < kLoads)
       tile_part<AK>(sa, oa, A, g.lda, m0, M, k0, kend, wave, q);
+    else if constexpr (EPI == kEpiGluFwd)
+      tile_part_glu(sa + kBigTile, ob, B, g.ldb, tn, g.glu_f, k0, kend, wave, q - kLoads);
     else
       tile_part<BKC>(sa + kBigTile, ob, B, g.ldb, n0, g.N, k0, kend, wave, q - kLoads);
   };
@@ -696,10 +821,34 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
       }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // staged values visible to the wave
     const int mb = m0 + wm * 128 + i * 32;             // first row of the block row
-    if (full_cols && mb + 32 <= M)
-      epilogue_rows_full(g, part, stage, mb + half, half, c, n, q_last);
-    else
-      epilogue_rows_edge(g, part, stage, mb + half, half, c, n, M);
+    if constexpr (EPI == kEpiGluFwd) {
+      // [u v] rows: the wave's columns c < 64 are gate columns, the rest up
+      const int gc = tn * 128 + wn * 64 + (c & 63) + (c >= 64 ? g.glu_f : 0);
+      glu_fwd_uv_rows(g, stage, mb + half, half, c, gc, M, mb + 32 <= M);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // s = silu(u) v from the pairs of accumulators, staged over the gate
+      // columns and stored as 64-column rows
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float sv[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            sv[e] = swiglu_fwd_f(bf16r(alpha * acc[i][j][4 * q + e]), bf16r(alpha * acc[i][j + 2][4 * q + e]));
+          *reinterpret_cast<float4*>(stage + lm * kStagePitch + j * 32 + 8 * q + 4 * half) =
+              make_float4(sv[0], sv[1], sv[2], sv[3]);
+        }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      glu_fwd_s_rows(g, stage, mb, lane, tn * 128 + wn * 64, M, mb + 32 <= M);
+    } else if constexpr (EPI == kEpiGluBwd) {
+      glu_bwd_rows(g, stage, mb + half, half, c, n, M, n0 + wn * 128 + 128 <= g.N && mb + 32 <= M);
+    } else {
+      if (full_cols && mb + 32 <= M)
+        epilogue_rows_full(g, part, stage, mb + half, half, c, n, q_last);
+      else
+        epilogue_rows_edge(g, part, stage, mb + half, half, c, n, M);
+    }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // reads done before the block is rewritten
   }
 }
@@ -715,14 +864,21 @@ LD_BIG_KERNEL(ld_gemm_bf16_nn_256, true, false)
 LD_BIG_KERNEL(ld_gemm_bf16_tn_256, false, false)
 LD_BIG_KERNEL(ld_gemm_bf16_tt_256, false, true)
 
+// C = [u v] rows and aux = silu(u) v rows of the SwiGLU projection (see GemmArgs).
+LD_BIG_ATTRS void ld_gemm_bf16_nt_glu_256(GemmArgs g) {
+  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
+  gemm_big_body<true, true, kEpiGluFwd>(g, ring, blockIdx.x, gridDim.x, 0, 1);
+}
+
 // Two GEMMs in one launch: a weight-gradient GEMM g1 (both operands
 // mn-contiguous, tiles1 tiles, each split into splits1 k ranges) and an
 // input-gradient GEMM g2 (A k-contiguous, B mn-contiguous, tiles2 tiles) that
 // read the same upstream gradient.  The workgroups of one GEMM come first
 // (g2's when g2_first); the other's then fill the CUs the first leaves idle,
 // so neither GEMM's last partial round of tiles runs on a part-empty chip.
-LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
-                                         int g2_first) {
+template <int EPI2>
+__device__ __forceinline__ void gemm_pair_body(const GemmArgs& g1, const GemmArgs& g2, int tiles1, int splits1,
+                                               int tiles2, int g2_first) {
   __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
   const int n1 = tiles1 * splits1;
   int id = blockIdx.x;
@@ -737,7 +893,16 @@ LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_256(GemmArgs g1, GemmArgs g2, int tiles1, i
   if (first)
     gemm_big_body<false, false>(g1, ring, id % tiles1, tiles1, id / tiles1, splits1);
   else
-    gemm_big_body<true, false>(g2, ring, id, tiles2, 0, 1);
+    gemm_big_body<true, false, EPI2>(g2, ring, id, tiles2, 0, 1);
+}
+LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
+                                         int g2_first) {
+  gemm_pair_body<kEpiPlain>(g1, g2, tiles1, splits1, tiles2, g2_first);
+}
+// The same with the SwiGLU backward fused into g2's epilogue (see GemmArgs).
+LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_glu_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
+                                             int g2_first) {
+  gemm_pair_body<kEpiGluBwd>(g1, g2, tiles1, splits1, tiles2, g2_first);
 }
 
 // C[i] = sum over splits of part[s][i], float32, in split order.  Every
@@ -919,6 +1084,13 @@ PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m2, int64_t 
   return best;
 }
 
+hipError_t launch_gemm_glu_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s) {
+  if (max_m <= 0 || g.N <= 0) return hipSuccess;
+  const int64_t tiles = ((max_m + GB - 1) / GB) * (g.N / GB);
+  hipLaunchKernelGGL(ld_gemm_bf16_nt_glu_256, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s) {
   const int splits1 = p.splits1;
   const int64_t tiles1 = ((static_cast<int64_t>(g1.M) + GB - 1) / GB) * ((g1.N + GB - 1) / GB);
@@ -930,8 +1102,12 @@ hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, 
   }
   const int64_t wg = tiles1 * splits1 + tiles2;
   if (wg <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
-                     static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
+  if (g2.glu_f > 0)
+    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_glu_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
+                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
+  else
+    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
+                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits1 == 1) return e;
   const int64_t mn = static_cast<int64_t>(g1.M) * g1.N;

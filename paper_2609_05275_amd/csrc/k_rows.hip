@@ -328,8 +328,6 @@ __global__ __launch_bounds__(1024) void ld_dg_reduce_k(const float* part, int64_
 
 // ----------------------------------------------------------------- SwiGLU
 
-__device__ __forceinline__ float sigmoidf_(float u) { return 1.f / (1.f + expf(-u)); }
-
 template <typename T>
 __global__ __launch_bounds__(256) void ld_swiglu_fwd_k(EltArgs a) {
   constexpr int VN = Pack<T>::N;
@@ -345,7 +343,7 @@ __global__ __launch_bounds__(256) void ld_swiglu_fwd_k(EltArgs a) {
 #pragma unroll
     for (int i = 0; i < VN; ++i) {
       const float uf = to_f(u.v[i]);
-      o.v[i] = from_f<T>(uf * sigmoidf_(uf) * to_f(v.v[i]));
+      o.v[i] = from_f<T>(swiglu_fwd_f(uf, to_f(v.v[i])));
     }
     store16(s + row * a.f + c, o);
   }
@@ -368,9 +366,10 @@ __global__ __launch_bounds__(256) void ld_swiglu_bwd_k(EltArgs a) {
 #pragma unroll
     for (int i = 0; i < VN; ++i) {
       const float uf = to_f(u.v[i]), vf = to_f(v.v[i]), gf = to_f(g.v[i]);
-      const float sg = sigmoidf_(uf);
-      gu.v[i] = from_f<T>(gf * vf * sg * (1.f + uf * (1.f - sg)));
-      gv.v[i] = from_f<T>(gf * uf * sg);
+      float guf, gvf;
+      swiglu_bwd_f(uf, vf, gf, guf, gvf);
+      gu.v[i] = from_f<T>(guf);
+      gv.v[i] = from_f<T>(gvf);
     }
     store16(guv + row * 2 * a.f + c, gu);
     store16(guv + row * 2 * a.f + a.f + c, gv);

@@ -59,6 +59,20 @@ __device__ __forceinline__ void dma_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
+// ---------------------------------------------------------------- SwiGLU
+// SwiGLU on float inputs (the gate u and up v as stored): s = silu(u) v, and
+// the gradients gu = g v silu'(u), gv = g silu(u) with
+// silu'(u) = sigmoid(u) (1 + u (1 - sigmoid(u))).  One definition for the
+// elementwise kernels and the GEMM epilogues that fuse them, so both give
+// the same bits.
+__device__ __forceinline__ float swiglu_sigmoid(float u) { return 1.f / (1.f + expf(-u)); }
+__device__ __forceinline__ float swiglu_fwd_f(float u, float v) { return u * swiglu_sigmoid(u) * v; }
+__device__ __forceinline__ void swiglu_bwd_f(float u, float v, float g, float& gu, float& gv) {
+  const float sg = swiglu_sigmoid(u);
+  gu = g * v * sg * (1.f + u * (1.f - sg));
+  gv = g * u * sg;
+}
+
 // ------------------------------------------------------------ kernel args
 
 // Rows of a compacted activation block.  When dev_count is set the row count
@@ -205,6 +219,15 @@ struct GemmArgs {
   const float* alpha_dev;    // when set, alpha is multiplied by *alpha_dev
   int32_t c_f32;
   float* part;               // split-K float32 partials [splits][M][N] (plan.splits > 1)
+  // SwiGLU epilogues (256x256 kernels only), d_ff = glu_f:
+  //   forward (ld_gemm_bf16_nt_glu_256): B is W_gate_up [2 glu_f, K], N = 2 glu_f;
+  //     C receives [u v] rows (ldc = 2 glu_f) and aux the rows of
+  //     s = silu(u) v (ld glu_f);
+  //   backward (NN part of ld_gemm_bf16_tn_nn_glu_256): N = glu_f; the
+  //     product (gs, rounded to bf16) is not stored: aux holds the [u v] rows
+  //     (ld 2 glu_f) and C receives [gu gv] rows (ldc = 2 glu_f).
+  void* aux;
+  int32_t glu_f;
 };
 
 // Kernel choice for one GEMM: the 256x256 MFMA kernel (optionally split
@@ -329,6 +352,10 @@ struct PairPlan {
 PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m2, int64_t n2, int64_t k2,
                         int max_splits);
 hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s);
+// The SwiGLU projection with its activation fused (GemmArgs glu_f, aux):
+// ld_gemm_bf16_nt_glu_256 over max_m rows, for bf16 with glu_f % 128 == 0
+// and N = 2 glu_f, both operands k-contiguous.
+hipError_t launch_gemm_glu_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s);
 hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmPlan& p, GemmArgs g,
                             int64_t max_m, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
