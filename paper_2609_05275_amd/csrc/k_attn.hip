@@ -350,30 +350,37 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
 
 // --------------------------------------------------------------- backward
 
-// delta[seq, head, q] = sum_d dO * O (float32), one thread per (token, head).
+// delta[seq, head, q] = sum_d dO * O (float32).  One wave per token row of
+// H*DH values: each pass reads 16 contiguous bytes per lane of O and dO (the
+// row in 64*16-byte pieces), the DH/VN lanes of a head sum their products
+// with butterfly shuffles, and the first lane of each head writes it.
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
-  constexpr int VN = 16 / sizeof(T);
-  const int64_t rows = static_cast<int64_t>(seq_count(a)) * a.S * a.H;
-  const int64_t id = blockIdx.x * 256ll + threadIdx.x;
-  if (id >= rows) return;
-  const int64_t tok = id / a.H;
-  const int head = static_cast<int>(id % a.H);
-  const int64_t ld = static_cast<int64_t>(a.H) * DH;
-  const T* o = static_cast<const T*>(a.o) + tok * ld + head * DH;
-  const T* go = static_cast<const T*>(a.go) + tok * ld + head * DH;
-  float s = 0.f;
-#pragma unroll
-  for (int c = 0; c < DH; c += VN) {
-    const uint4 ov = *reinterpret_cast<const uint4*>(o + c);
-    const uint4 gv = *reinterpret_cast<const uint4*>(go + c);
-    const T* op = reinterpret_cast<const T*>(&ov);
-    const T* gp = reinterpret_cast<const T*>(&gv);
-#pragma unroll
-    for (int i = 0; i < VN; ++i) s = __builtin_fmaf(static_cast<float>(op[i]), static_cast<float>(gp[i]), s);
-  }
+  constexpr int VN = 16 / sizeof(T), G = DH / VN;  // elements per lane per pass, lanes per head
+  static_assert(G >= 1 && 64 % G == 0, "a head spans whole lanes of a pass");
+  const int64_t tokens = static_cast<int64_t>(seq_count(a)) * a.S;
+  const int64_t tok = blockIdx.x * 4ll + (threadIdx.x >> 6);
+  if (tok >= tokens) return;
+  const int lane = threadIdx.x & 63;
+  const int W = a.H * DH;
   const int64_t seq = tok / a.S, q = tok % a.S;
-  a.delta[(seq * a.H + head) * a.S + q] = s;
+  const T* o = static_cast<const T*>(a.o) + tok * W;
+  const T* go = static_cast<const T*>(a.go) + tok * W;
+  for (int e0 = 0; e0 < W; e0 += 64 * VN) {
+    const int e = e0 + lane * VN;
+    float s = 0.f;
+    if (e < W) {
+      const uint4 ov = *reinterpret_cast<const uint4*>(o + e);
+      const uint4 gv = *reinterpret_cast<const uint4*>(go + e);
+      const T* op = reinterpret_cast<const T*>(&ov);
+      const T* gp = reinterpret_cast<const T*>(&gv);
+#pragma unroll
+      for (int i = 0; i < VN; ++i) s = __builtin_fmaf(static_cast<float>(op[i]), static_cast<float>(gp[i]), s);
+    }
+#pragma unroll
+    for (int off = G / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (e < W && lane % G == 0) a.delta[(seq * a.H + e / DH) * a.S + q] = s;
+  }
 }
 
 // Registers holding 64 rows x DH of one operand as groups of 4 rows x 8
@@ -1079,8 +1086,8 @@ hipError_t fwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
 
 template <int DH>
 hipError_t bwd_dh(int dtype, int part, const AttnArgs& a, hipStream_t s) {
-  const int64_t rows = static_cast<int64_t>(a.n_seq) * a.S * a.H;
-  const dim3 dgrid(static_cast<unsigned>((rows + 255) / 256));
+  const int64_t tokens = static_cast<int64_t>(a.n_seq) * a.S;  // one wave per token
+  const dim3 dgrid(static_cast<unsigned>((tokens + 3) / 4));
   if constexpr (DH >= 64) {
     if (dtype == LD_BF16) {
       if (part == 0)

@@ -1017,7 +1017,7 @@ hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmP
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t mn = static_cast<int64_t>(g.M) * g.N;
-    int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 4096));
+    int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 1 << 20));
     hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, g.part, p.splits, mn,
                        nullptr, C);
     return hipGetLastError();
@@ -1111,7 +1111,7 @@ hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits1 == 1) return e;
   const int64_t mn = static_cast<int64_t>(g1.M) * g1.N;
-  const int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 4096));
+  const int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 1 << 20));
   hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, g1.part, splits1, mn, nullptr,
                      static_cast<float*>(g1.C));
   return hipGetLastError();
