@@ -388,7 +388,14 @@ int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmA
   // the fused epilogue reads [u v] and writes [gu gv] instead of writing gs
   const double out2 = g2.glu_f > 0 ? 4.0 * M2 * N2 : 1.0 * M2 * N2;
   ps.end(2.0 * (M1 * N1 * K1 + M2 * N2 * K2),
-         2.0 * (M1 * K1 + N1 * K1) + 4.0 * M1 * N1 + 2.0 * (M2 * K2 + N2 * K2 + out2));
+         2.0 * (M1 * K1 + N1 * K1) + 4.0 * M1 * N1 * pp.splits1 + 2.0 * (M2 * K2 + N2 * K2 + out2));
+  if (pp.splits1 > 1) {
+    const int64_t mn = static_cast<int64_t>(g1.M) * g1.N;
+    ProfScope pr("ld_splitk_reduce", s);
+    const hipError_t er = launch_splitk_reduce(g1.part, pp.splits1, mn, static_cast<float*>(g1.C), s);
+    if (er != hipSuccess) return fail(LD_E_HIP, "ld_splitk_reduce launch: %s", hipGetErrorString(er));
+    pr.end(0, 4.0 * mn * (pp.splits1 + 1.0));
+  }
   return LD_OK;
 }
 

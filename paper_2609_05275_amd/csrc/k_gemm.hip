@@ -1108,12 +1108,13 @@ hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, 
   else
     hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
                        static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || splits1 == 1) return e;
-  const int64_t mn = static_cast<int64_t>(g1.M) * g1.N;
+  return hipGetLastError();
+}
+
+hipError_t launch_splitk_reduce(const float* part, int splits, int64_t mn, float* C, hipStream_t s) {
+  if (splits <= 1 || mn <= 0) return hipSuccess;
   const int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 1 << 20));
-  hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, g1.part, splits1, mn, nullptr,
-                     static_cast<float*>(g1.C));
+  hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, splits, mn, nullptr, C);
   return hipGetLastError();
 }
 

@@ -351,7 +351,11 @@ struct PairPlan {
 };
 PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m2, int64_t n2, int64_t k2,
                         int max_splits);
+// Launches the pair kernel only; with p.splits1 > 1 the caller then sums the
+// partials with launch_splitk_reduce.
 hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s);
+// C[i] = sum over splits of part[s * mn + i] (float32, split order).
+hipError_t launch_splitk_reduce(const float* part, int splits, int64_t mn, float* C, hipStream_t s);
 // The SwiGLU projection with its activation fused (GemmArgs glu_f, aux):
 // ld_gemm_bf16_nt_glu_256 over max_m rows, for bf16 with glu_f % 128 == 0
 // and N = 2 glu_f, both operands k-contiguous.
