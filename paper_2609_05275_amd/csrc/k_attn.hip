@@ -782,23 +782,35 @@ constexpr size_t dkdv_lds_bytes() {
 constexpr int DQ_ROWS = 256;  // query rows per dQ workgroup (8 waves x 32)
 
 // dQ.  A workgroup of 8 waves owns 256 query rows (32 per wave, two waves per
-// SIMD) and walks the 64-key blocks up to the diagonal; K ([key][d] and
-// transposed [d][key]) and V are double buffered in LDS with the next block
-// prefetched in registers.  Scores are formed transposed (S^T = K Q^T), so the
-// query's log-sum-exp and delta are per lane and dS^T feeds dQ^T += K^T dS^T
-// directly.
+// SIMD) and walks the 64-key blocks up to the diagonal.  K and V blocks go
+// from global memory straight into a four-stage LDS ring ([key][d] without
+// padding, 16-byte chunks XOR-swizzled by the key as in the dK/dV ring), so a
+// block's loads have two block-times to land.  Scores are formed transposed
+// (S^T = K Q^T), so the query's log-sum-exp and delta are per lane, and
+// dS^T feeds dQ^T += K^T dS^T directly, K^T coming from the same [key][d]
+// block through transposing reads in the accumulator's key permutation.
+// Fragment addresses are per-lane offsets moved by one stage per block; the
+// causal mask is applied on diagonal blocks only.
+constexpr int DQ_NST = 4;
+template <int DH>
+constexpr int dq_stage_bytes() { return 4 * FKV * DH; }  // K block, then V block
+
 template <int DH, bool AL>
 __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
-  constexpr int DT = FKV * (DH + 8), TT = DH * FKV;
-  constexpr int STAGE = 2 * DT + TT;  // Ks, Vs, Kt
-  extern __shared__ __align__(16) bf16 lds[];
+  constexpr int NW = 8, SB = dq_stage_bytes<DH>();
+  constexpr int RPI = 512 / DH, LPR = 64 / RPI;   // rows per 1 KB load, lanes per row
+  constexpr int NPW = (FKV * DH * 2 / 1024) / NW;  // 1 KB loads per wave per tensor and block
+  constexpr int NL = 2 * NPW;                      // loads per wave per block
+  static_assert(NPW >= 1, "every wave loads part of each block");
+  extern __shared__ __align__(16) char ring[];
   const int S = a.S, H = a.H;
   const int n_qt = (S + DQ_ROWS - 1) / DQ_ROWS;
   // grid (head, sequence, tile), tile slowest: heavy (late) query tiles first
   const int qt = n_qt - 1 - static_cast<int>(blockIdx.z);
   const int head = blockIdx.x, seq = blockIdx.y;
   if (seq >= seq_count(a)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hf = lane >> 5, cl = lane & 31;
   const int q0 = qt * DQ_ROWS, qw = q0 + wave * 32, qrow = qw + cl;
   const int64_t ldq = 3ll * H * DH, ldo = static_cast<int64_t>(H) * DH;
@@ -820,72 +832,119 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
     qf[ks] = qok ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
     of[ks] = qok ? load8(dOp + static_cast<int64_t>(qrow) * ldo + ks * 16 + hf * 8) : zero8();
   }
+  // The fragments must have arrived before the first LDS load is issued
+  // (the compiler does not see those loads).
+#pragma unroll
+  for (int ks = 0; ks < DH / 16; ++ks) asm volatile("" ::"v"(qf[ks]), "v"(of[ks]));
+  asm volatile("" ::"v"(lse2), "v"(dl));
   floatx16 dq[DH / 32];
 #pragma unroll
   for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) dq[db][v] = 0.f;
 
+  // Loads of key block k0 into stage st; blocks at or past the end read zeros.
+  const dma_rsrc rk = dma_make_rsrc(Kp, static_cast<int64_t>(S) * ldq * 2);
+  const dma_rsrc rv = dma_make_rsrc(Vp, static_cast<int64_t>(S) * ldq * 2);
+  const int lrow = wave * RPI + lane / LPR;
+  const int lchk = ((lane % LPR) ^ qd_swz<DH>(lrow)) << 3;
+  const uint32_t lk = static_cast<uint32_t>((lrow * ldq + lchk) * 2);
+  auto load_block = [&](int st, int k0) {
+    char* sb = ring + st * SB;
+    const bool in = k0 < S;
+#pragma unroll
+    for (int i = 0; i < NPW; ++i) {
+      const int p = wave + NW * i;
+      const uint32_t r = static_cast<uint32_t>((static_cast<int64_t>(k0) + NW * i * RPI) * ldq * 2);
+      dma16(rk, sb + p * 1024, in ? lk + r : kDmaOob);
+      dma16(rv, sb + FKV * DH * 2 + p * 1024, in ? lk + r : kDmaOob);
+    }
+  };
+  // Per-lane LDS byte addresses in the stage of the current block: plain
+  // reads of K (row cl, 16-byte chunk 2ks + hf; V one block further) and the
+  // transposing reads of K (rows tr_r and tr_r + 8).
+  uint32_t ak[DH / 16], at0[DH / 32], at1[DH / 32];
+  {
+    const uint32_t r0 = lds_addr(ring);
+    const int sw_c = qd_swz<DH>(cl);
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) ak[ks] = r0 + 2u * (cl * DH + (((2 * ks + hf) ^ sw_c) << 3));
+    const int tr_r = 4 * hf + ((lane & 15) >> 2);
+    const int tr_d = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+    const int sw0 = qd_swz<DH>(tr_r), sw1 = qd_swz<DH>(tr_r + 8);
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) {
+      const int d0 = db * 32 + tr_d;
+      at0[db] = r0 + 2u * (tr_r * DH + (((d0 >> 3) ^ sw0) << 3) + (d0 & 7));
+      at1[db] = r0 + 2u * ((tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7));
+    }
+  }
+  constexpr uint32_t kVb = 2u * FKV * DH;  // V block after the K block (bytes)
+
   const int kv_end = min(S, q0 + DQ_ROWS);
   const int nkb = kv_end / FKV;
-  RowGroupsN<DH, 512> rk, rv;
-  auto put = [&](int buf) {
-    bf16* st = lds + buf * STAGE;
-    rgn_store<DH, 512>(rk, st, st + 2 * DT, tid);
-    rgn_store<DH, 512>(rv, st + DT, nullptr, tid);
-  };
-  rgn_load<DH, 512>(rk, Kp, ldq, 0, tid);
-  rgn_load<DH, 512>(rv, Vp, ldq, 0, tid);
-  put(0);
-  __syncthreads();
+  load_block(0, 0);
+  load_block(1, FKV);
+  load_block(2, 2 * FKV);
   for (int kb = 0; kb < nkb; ++kb) {
-    const int k0 = kb * FKV, buf = kb & 1;
-    if (kb + 1 < nkb) {
-      rgn_load<DH, 512>(rk, Kp, ldq, k0 + FKV, tid);
-      rgn_load<DH, 512>(rv, Vp, ldq, k0 + FKV, tid);
-    }
-    const bf16* Ks = lds + buf * STAGE;
-    const bf16* Vs = Ks + DT;
-    const bf16* Kt = Ks + 2 * DT;
+    const int k0 = kb * FKV, st = kb & (DQ_NST - 1);
+    // block kb has landed (blocks kb+1, kb+2 may be in flight); the stage of
+    // block kb-1 is no longer read and takes block kb+3
+    dma_barrier<2 * NL>();
+    load_block((kb + 3) & (DQ_NST - 1), k0 + 3 * FKV);
     if (qw < S && k0 <= qw + 31) {
-      const bool diag = k0 + FKV - 1 > qw;
+      const bool diag = k0 + FKV - 1 > qw;  // some key of the block is past some row
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
-        floatx16 st, dpt;
+        const uint32_t hk = 2u * kh * 32 * DH;
+        floatx16 st_ = mfma(lds_frag(ak[0] + hk), qf[0], floatx16{});
+        floatx16 dpt = mfma(lds_frag(ak[0] + hk + kVb), of[0], floatx16{});
 #pragma unroll
-        for (int v = 0; v < 16; ++v) st[v] = dpt[v] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < DH / 16; ++ks) {
-          st = mfma(load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), qf[ks], st);
-          dpt = mfma(load8(Vs + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8), of[ks], dpt);
+        for (int ks = 1; ks < DH / 16; ++ks) {
+          st_ = mfma(lds_frag(ak[ks] + hk), qf[ks], st_);
+          dpt = mfma(lds_frag(ak[ks] + hk + kVb), of[ks], dpt);
         }
         bf16x8 dsb[2];
         const float ab = al2 * static_cast<float>(k0 + kh * 32 + 4 * hf - qrow);  // bias of the lane's first key
+        float pv[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float x = st[v] * sl2 - lse2;
+          float x = fmaf(st_[v], sl2, -lse2);
           if constexpr (AL) x += fmaf(al2, static_cast<float>(8 * (v >> 2) + (v & 3)), ab);
-          float p = __builtin_amdgcn_exp2f(x);
-          if (diag) {
-            const int keyi = k0 + kh * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-            if (keyi > qrow) p = 0.f;
-          }
-          dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dpt[v] - dl));
+          pv[v] = __builtin_amdgcn_exp2f(x);
+        }
+        if (diag) {  // causal mask (wave-uniform branch): keys after the row
+          const int t = qrow - (k0 + kh * 32 + 4 * hf);  // the row minus the lane's first key
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (8 * (v >> 2) + (v & 3) > t) pv[v] = 0.f;
         }
 #pragma unroll
-        for (int db = 0; db < DH / 32; ++db) {
-          const int dr = db * 32 + cl;
+        for (int v = 0; v < 16; ++v) dsb[v >> 3][v & 7] = static_cast<bf16>(pv[v] * (dpt[v] - dl));
+        // dQ^T += K^T dS^T, the d blocks innermost (consecutive MFMAs use
+        // different accumulators)
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int kk = kh * 32 + 16 * c + 4 * hf;
-            dq[db] = mfma(load4x2(Kt + tr_off(dr, kk), Kt + tr_off(dr, kk + 8)), dsb[c], dq[db]);
+        for (int c = 0; c < 2; ++c) {
+          const uint32_t rr = hk + 2u * 16 * c * DH;
+#pragma unroll
+          for (int db = 0; db < DH / 32; ++db) {
+            const v4s lo = lds_tr(at0[db] + rr), hi = lds_tr(at1[db] + rr);
+            dq[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7)), dsb[c], dq[db]);
           }
         }
       }
     }
-    if (kb + 1 < nkb) put(buf ^ 1);
-    __syncthreads();
+    // next block: one stage on (wrapping around the ring)
+    const uint32_t adv = st == DQ_NST - 1 ? static_cast<uint32_t>(-(DQ_NST - 1) * SB) : static_cast<uint32_t>(SB);
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) ak[ks] += adv;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) {
+      at0[db] += adv;
+      at1[db] += adv;
+    }
   }
+  dma_barrier<0>();  // no load may still write LDS when the workgroup ends
   if (qok) {
     bf16* G = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * ldq + head * DH;
 #pragma unroll
@@ -902,7 +961,7 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
 
 template <int DH>
 constexpr size_t dq_lds_bytes() {
-  return 2ull * (2 * FKV * (DH + 8) + DH * FKV) * sizeof(bf16);
+  return static_cast<size_t>(DQ_NST) * dq_stage_bytes<DH>();
 }
 
 // ------------------------------------------------------------ fp32 (SIMT)
