@@ -1,22 +1,24 @@
 // Causal multi-head attention, forward and backward, on kept sequences only.
 //
-// bf16 path (d_head 64 or 128), gfx950 MFMA v_mfma_f32_32x32x16_bf16:
-//   Forward: one workgroup per (128-row query tile, head, kept sequence), four
-//   waves of 32 query rows.  Scores are formed transposed, S^T = K Q^T, so a
-//   lane owns one query row (its column of the 32x32 accumulator) and holds
-//   16 of the block's keys; the softmax statistics are per lane, with one
-//   exchange between the two half-waves for the running maximum.  The
-//   accumulator layout (row 8*(v/4) + 4*(lane/32) + v%4) is reused directly as
-//   the B operand of O^T += V^T P^T: the keys a lane holds are a permutation of
-//   the MFMA k index, and V^T is read from LDS in the same permutation (two
-//   8-byte reads per fragment).  K is staged [key][d], V transposed [d][key].
-//   Online softmax in base 2, fp32; O normalised at the end and the natural
-//   log-sum-exp saved per row.
+// bf16 path (d_head 64 or 128), gfx950 MFMA v_mfma_f32_32x32x16_bf16.  Every
+// kernel streams 64-row blocks of [row][d] bf16 (keys and values, or queries
+// and output gradients) from global memory straight into a four-stage LDS
+// ring with buffer loads that have an LDS destination; the 16-byte chunks of
+// a row are XOR-swizzled by the row so that plain fragment reads and the
+// transposing reads (ds_read_b64_tr_b16) are bank-conflict free.  Scores are
+// formed with the streamed rows as the MFMA A operand, so a lane owns one
+// column (the wave's fixed query or key) and 16 streamed rows; that
+// accumulator layout (row 8*(v/4) + 4*(lane/32) + v%4) is reused directly as
+// the B operand of the next product, whose A operand (V^T, K^T, dO^T, Q^T) is
+// read transposed from the same [row][d] block in the same row permutation.
+//   Forward: one workgroup per (256-row query tile, head, kept sequence),
+//   eight waves of 32 query rows; online softmax in base 2 with lazy
+//   rescaling, O normalised at the end and the natural log-sum-exp saved.
 //   Backward (no float atomics): delta = rowsum(dO * O); a dK/dV kernel per
 //   (128-key tile, head, sequence) walks the query blocks at and after the
 //   diagonal recomputing P from the saved log-sum-exp; a dQ kernel per
-//   (128-row query tile, head, sequence) walks the key blocks up to the
-//   diagonal.  Heavy (late) query tiles are scheduled first.
+//   (256-row query tile, head, sequence) walks the key blocks up to the
+//   diagonal.  Heavy causal tiles are scheduled first.
 // fp32 path: plain SIMT kernels, one thread per query (or key) row, used by
 // the fp32 configuration only.
 #include <type_traits>
@@ -49,304 +51,11 @@ __device__ __forceinline__ bf16x8 zero8() {
   return z;
 }
 
-// Transposed LDS tiles ([d][key] or [d][query], 64 columns) are unpadded
-// 128-byte rows whose 16-byte chunks are XOR-swizzled by the row, so that 32
-// consecutive rows read at one column and 16 rows written 8 apart both spread
-// over the banks.
-__device__ __forceinline__ int tr_off(int row, int col) {
-  const int chunk = (col >> 3) ^ ((row & 7) ^ ((row >> 3) & 7));
-  return row * 64 + (chunk << 3) + (col & 7);
-}
-
-// Two 4-element pieces of an LDS row -> one 8-element fragment.
-__device__ __forceinline__ bf16x8 load4x2(const bf16* lo, const bf16* hi) {
-  const uint2 a = *reinterpret_cast<const uint2*>(lo);
-  const uint2 b = *reinterpret_cast<const uint2*>(hi);
-  uint4 u = make_uint4(a.x, a.y, b.x, b.y);
-  return *reinterpret_cast<const bf16x8*>(&u);
-}
-
-__device__ __forceinline__ uint32_t half_of(const uint4& v, int i) {
-  const uint32_t w = (i >> 1) == 0 ? v.x : (i >> 1) == 1 ? v.y : (i >> 1) == 2 ? v.z : v.w;
-  return (i & 1) ? (w >> 16) : (w & 0xffffu);
-}
-
-// Stage rows [r0, r0+ROWS) x DH of a strided bf16 matrix into LDS, both as
-// [row][d] (pitch DH+8) when `direct` is set and transposed as [d][row]
-// (pitch ROWS+8) when `trans` is set.  Rows at or past `limit` are zero.
-template <int ROWS, int DH>
-__device__ __forceinline__ void stage_rows(const bf16* src, int64_t ld, int r0, int limit,
-                                           bf16* direct, bf16* trans, int tid) {
-  if (direct) {
-    for (int c = tid; c < ROWS * DH / 8; c += 256) {
-      const int r = c / (DH / 8), dc = (c % (DH / 8)) * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (r0 + r < limit) v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r0 + r) * ld + dc);
-      *reinterpret_cast<uint4*>(direct + r * (DH + 8) + dc) = v;
-    }
-  }
-  if (trans) {
-    for (int c = tid; c < (ROWS / 4) * (DH / 8); c += 256) {
-      const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
-      uint4 v[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        v[k] = make_uint4(0, 0, 0, 0);
-        if (r0 + rg + k < limit)
-          v[k] = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r0 + rg + k) * ld + dc);
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        uint2 o;
-        o.x = half_of(v[0], i) | (half_of(v[1], i) << 16);
-        o.y = half_of(v[2], i) | (half_of(v[3], i) << 16);
-        *reinterpret_cast<uint2*>(trans + (dc + i) * (ROWS + 8) + rg) = o;
-      }
-    }
-  }
-}
-
 // ---------------------------------------------------------------- forward
 
-constexpr int FQ = 128, FKV = 64;   // dQ kernel tiles
+constexpr int FKV = 64;   // keys per streamed block
 constexpr int FWQ = 256;            // forward: query rows per workgroup
-#ifndef FWD_RPW
-#define FWD_RPW 32                  // forward: query rows per wave (8 waves)
-#endif
-
-// Registers holding one K/V block (64 keys x DH) on its way to LDS, split
-// over NT threads.
-template <int DH, int NT>
-struct KvRegs {
-  static constexpr int NKC = 64 * DH / 8;            // 16-byte K chunks
-  static constexpr int NK = (NKC + NT - 1) / NT;     // per thread
-  static constexpr int NV = (64 / 4) * (DH / 8);     // V groups of 4 keys x 8 d
-  static constexpr int NVT = (NV + NT - 1) / NT;     // per thread
-  uint4 k[NK];
-  uint4 v[NVT][4];
-};
-
-// The block [k0, k0+64) must lie inside the sequence (S % 64 == 0).
-template <int DH, int NT>
-__device__ __forceinline__ void kv_load(KvRegs<DH, NT>& r, const bf16* Kp, const bf16* Vp, int64_t ld,
-                                        int k0, int tid) {
-#pragma unroll
-  for (int p = 0; p < KvRegs<DH, NT>::NK; ++p) {
-    const int c = p * NT + tid;
-    const int row = c / (DH / 8), dc = (c % (DH / 8)) * 8;
-    r.k[p] = c < KvRegs<DH, NT>::NKC
-                 ? *reinterpret_cast<const uint4*>(Kp + static_cast<int64_t>(k0 + row) * ld + dc)
-                 : make_uint4(0, 0, 0, 0);
-  }
-#pragma unroll
-  for (int p = 0; p < KvRegs<DH, NT>::NVT; ++p) {
-    const int c = p * NT + tid;
-    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      r.v[p][k] = c < KvRegs<DH, NT>::NV
-                      ? *reinterpret_cast<const uint4*>(Vp + static_cast<int64_t>(k0 + rg + k) * ld + dc)
-                      : make_uint4(0, 0, 0, 0);
-  }
-}
-
-// K as [key][d] (pitch DH+8), V transposed as [d][key] (swizzled, tr_off).
-template <int DH, int NT>
-__device__ __forceinline__ void kv_store(const KvRegs<DH, NT>& r, bf16* Ks, bf16* Vt, int tid) {
-#pragma unroll
-  for (int p = 0; p < KvRegs<DH, NT>::NK; ++p) {
-    const int c = p * NT + tid;
-    if (c >= KvRegs<DH, NT>::NKC) continue;
-    const int row = c / (DH / 8), dc = (c % (DH / 8)) * 8;
-    *reinterpret_cast<uint4*>(Ks + row * (DH + 8) + dc) = r.k[p];
-  }
-#pragma unroll
-  for (int p = 0; p < KvRegs<DH, NT>::NVT; ++p) {
-    const int c = p * NT + tid;
-    if (c >= KvRegs<DH, NT>::NV) continue;
-    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      uint2 o;
-      o.x = half_of(r.v[p][0], i) | (half_of(r.v[p][1], i) << 16);
-      o.y = half_of(r.v[p][2], i) | (half_of(r.v[p][3], i) << 16);
-      *reinterpret_cast<uint2*>(Vt + tr_off(dc + i, rg)) = o;
-    }
-  }
-}
-
-// Forward.  A workgroup owns 256 query rows; each wave owns RPW of them as
-// RPW/32 MFMA blocks that share every K and V fragment it reads from LDS
-// (64 rows: 4 waves, fewer LDS reads per FLOP; 32 rows: 8 waves, two per
-// SIMD).  K/V blocks of 64 keys are double buffered in LDS and the next block
-// is fetched into registers while the current one is used, so there is one
-// barrier per block.
-// AL: add the ALiBi bias to the scaled scores (in log2 units: slope * log2e
-// per position of distance).
-template <int DH, int RPW, bool AL>
-__global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a) {
-  constexpr int NSB = RPW / 32, NT = 64 * (FWQ / RPW);
-  constexpr int KT = FKV * (DH + 8), VT = DH * FKV;
-  __shared__ __align__(16) bf16 lds[2 * (KT + VT)];
-  const int S = a.S, H = a.H;
-  const int n_qt = (S + FWQ - 1) / FWQ;
-  // grid (head, sequence, tile): the tile index varies slowest, so every
-  // (heaviest) last query tile is dispatched before any lighter one
-  const int qt = n_qt - 1 - static_cast<int>(blockIdx.z);
-  const int head = blockIdx.x, seq = blockIdx.y;
-  if (seq >= seq_count(a)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int hf = lane >> 5, cl = lane & 31;
-  const int q0 = qt * FWQ, qw = q0 + wave * RPW;
-  const int64_t ldq = 3ll * H * DH;
-  const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
-  const bf16* Qp = base + head * DH;
-  const bf16* Kp = base + static_cast<int64_t>(H) * DH + head * DH;
-  const bf16* Vp = base + 2ll * H * DH + head * DH;
-  const float sl2 = a.scale * kLog2e;
-  const float al2 = AL ? alibi_slope(head, H) * kLog2e : 0.f;
-
-  bf16x8 qf[NSB][DH / 16];
-  floatx16 o[NSB][DH / 32];
-  float m[NSB], l[NSB];
-#pragma unroll
-  for (int sb = 0; sb < NSB; ++sb) {
-    const int qrow = qw + sb * 32 + cl;
-#pragma unroll
-    for (int ks = 0; ks < DH / 16; ++ks)
-      qf[sb][ks] = qrow < S ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
-#pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) o[sb][db][v] = 0.f;
-    m[sb] = -INFINITY;
-    l[sb] = 0.f;
-  }
-
-  const int kv_end = min(S, q0 + FWQ);
-  const int nkb = (kv_end + FKV - 1) / FKV;
-  KvRegs<DH, NT> kr;
-  kv_load<DH, NT>(kr, Kp, Vp, ldq, 0, tid);
-  kv_store<DH, NT>(kr, lds, lds + KT, tid);
-  __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
-    const int k0 = kb * FKV;
-    bf16* Ks = lds + (kb & 1) * (KT + VT);
-    bf16* Vt = Ks + KT;
-    if (kb + 1 < nkb) kv_load<DH, NT>(kr, Kp, Vp, ldq, k0 + FKV, tid);
-    if (qw < S && k0 <= qw + RPW - 1) {
-      const bool diag = k0 + FKV - 1 > qw;  // some key of the block is past some row
-      // scores of every 32-row block: each K fragment feeds NSB MFMA chains
-      floatx16 sc[NSB][2];
-#pragma unroll
-      for (int sb = 0; sb < NSB; ++sb)
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) sc[sb][kh][v] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks)
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh) {
-          const bf16x8 kf = load8(Ks + (kh * 32 + cl) * (DH + 8) + ks * 16 + hf * 8);
-#pragma unroll
-          for (int sb = 0; sb < NSB; ++sb) sc[sb][kh] = mfma(kf, qf[sb][ks], sc[sb][kh]);
-        }
-      bf16x8 pb[NSB][2][2];
-#pragma unroll
-      for (int sb = 0; sb < NSB; ++sb) {
-        const int qrow = qw + sb * 32 + cl;
-        const float ab = al2 * static_cast<float>(k0 + 4 * hf - qrow);  // bias of the lane's first key
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float x = sc[sb][kh][v] * sl2;
-            if constexpr (AL) x += fmaf(al2, static_cast<float>(kh * 32 + 8 * (v >> 2) + (v & 3)), ab);
-            sc[sb][kh][v] = x;
-          }
-        if (diag) {  // causal mask, only on blocks that reach past a row (wave-uniform)
-          const int t = qrow - k0 - 4 * hf;  // the row minus the lane's first key
-#pragma unroll
-          for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-            for (int v = 0; v < 16; ++v)
-              if (kh * 32 + 8 * (v >> 2) + (v & 3) > t) sc[sb][kh][v] = -INFINITY;
-        }
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[sb][kh][v]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        // Lazy rescaling: the running maximum only moves (and O, l are only
-        // rescaled) when a row's maximum grows by more than 8 in log2 units;
-        // otherwise p = 2^(s - m) stays below 2^8, exact enough in bf16 and
-        // far from float overflow, and the result O / l is unchanged.
-        const bool grow = mx > m[sb] + 8.f;
-        if (__builtin_amdgcn_read_exec() & __ballot(grow)) {
-          const float m_new = grow ? mx : m[sb];
-          const float alpha = __builtin_amdgcn_exp2f(m[sb] - m_new);
-          m[sb] = m_new;
-          l[sb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) o[sb][db][v] *= alpha;
-        }
-        float ls = 0.f;
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float p = __builtin_amdgcn_exp2f(sc[sb][kh][v] - m[sb]);
-            ls += p;
-            pb[sb][kh][v >> 3][v & 7] = static_cast<bf16>(p);
-          }
-        l[sb] += ls;
-      }
-      // O^T += V^T P^T; consecutive MFMAs go to different accumulators (the
-      // d blocks innermost), so none waits on the one before it
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int kbb = kh * 32 + 16 * c + 4 * hf;
-#pragma unroll
-          for (int db = 0; db < DH / 32; ++db) {
-            const int vr = db * 32 + cl;
-            const bf16x8 vf = load4x2(Vt + tr_off(vr, kbb), Vt + tr_off(vr, kbb + 8));
-#pragma unroll
-            for (int sb = 0; sb < NSB; ++sb) o[sb][db] = mfma(vf, pb[sb][kh][c], o[sb][db]);
-          }
-        }
-    }
-    if (kb + 1 < nkb) {
-      bf16* Kn = lds + ((kb + 1) & 1) * (KT + VT);
-      kv_store<DH, NT>(kr, Kn, Kn + KT, tid);
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int sb = 0; sb < NSB; ++sb) {
-    const int qrow = qw + sb * 32 + cl;
-    const float lt = l[sb] + __shfl_xor(l[sb], 32, 64);
-    if (qrow < S) {
-      const float inv = 1.f / lt;
-      bf16* Op = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * (static_cast<int64_t>(H) * DH) + head * DH;
-#pragma unroll
-      for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          __attribute__((aligned(8))) bf16 t[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(o[sb][db][4 * g + i] * inv);
-          *reinterpret_cast<uint2*>(Op + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(t);
-        }
-      if (hf == 0) a.lse[(static_cast<int64_t>(seq) * H + head) * S + qrow] = (m[sb] + log2f(lt)) * kLn2;
-    }
-  }
-}
+constexpr int kFwdRowsPerWave = 32;  // forward: query rows per wave (8 waves)
 
 // --------------------------------------------------------------- backward
 
@@ -380,54 +89,6 @@ __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
 #pragma unroll
     for (int off = G / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
     if (e < W && lane % G == 0) a.delta[(seq * a.H + e / DH) * a.S + q] = s;
-  }
-}
-
-// Registers holding 64 rows x DH of one operand as groups of 4 rows x 8
-// columns, split over NT threads, from which both the [row][d] and the
-// transposed [d][row] LDS copies are written.  Rows [r0, r0+64) must lie
-// inside the sequence (S % 64 == 0).
-template <int DH, int NT>
-struct RowGroupsN {
-  static constexpr int NG = (64 / 4) * (DH / 8);
-  static constexpr int NGT = (NG + NT - 1) / NT;
-  uint4 v[NGT][4];
-};
-
-template <int DH, int NT>
-__device__ __forceinline__ void rgn_load(RowGroupsN<DH, NT>& t, const bf16* src, int64_t ld, int r0,
-                                         int tid) {
-#pragma unroll
-  for (int p = 0; p < RowGroupsN<DH, NT>::NGT; ++p) {
-    const int c = p * NT + tid;
-    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      t.v[p][k] = c < RowGroupsN<DH, NT>::NG
-                      ? *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r0 + rg + k) * ld + dc)
-                      : make_uint4(0, 0, 0, 0);
-  }
-}
-
-template <int DH, int NT>
-__device__ __forceinline__ void rgn_store(const RowGroupsN<DH, NT>& t, bf16* direct, bf16* trans,
-                                          int tid) {
-#pragma unroll
-  for (int p = 0; p < RowGroupsN<DH, NT>::NGT; ++p) {
-    const int c = p * NT + tid;
-    if (c >= RowGroupsN<DH, NT>::NG) continue;
-    const int rg = (c / (DH / 8)) * 4, dc = (c % (DH / 8)) * 8;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) *reinterpret_cast<uint4*>(direct + (rg + k) * (DH + 8) + dc) = t.v[p][k];
-    if (trans) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        uint2 o;
-        o.x = half_of(t.v[p][0], i) | (half_of(t.v[p][1], i) << 16);
-        o.y = half_of(t.v[p][2], i) | (half_of(t.v[p][3], i) << 16);
-        *reinterpret_cast<uint2*>(trans + tr_off(dc + i, rg)) = o;
-      }
-    }
   }
 }
 
@@ -771,6 +432,230 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
         *reinterpret_cast<uint2*>(Gk + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(tk);
         *reinterpret_cast<uint2*>(Gv + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(tv);
       }
+  }
+}
+
+// Forward.  A workgroup owns 256 query rows; each wave owns RPW of them as
+// RPW/32 MFMA blocks that share every K and V fragment it reads from LDS.
+// K/V blocks of 64 keys go from global memory straight into a four-stage LDS
+// ring ([key][d], as in the dQ kernel), so a block's loads have two
+// block-times to land; V^T comes from transposing reads of the [key][d]
+// block in the accumulator's key permutation.  Online softmax in base 2 with
+// lazy rescaling; causal mask on diagonal blocks only.
+// AL: add the ALiBi bias to the scaled scores (in log2 units: slope * log2e
+// per position of distance).
+template <int DH>
+constexpr int fwd_stage_bytes() { return 4 * FKV * DH; }  // K block, then V block
+constexpr int FWD_NST = 4;
+
+template <int DH, int RPW, bool AL>
+__global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a) {
+  constexpr int NSB = RPW / 32, NW = FWQ / RPW, SB = fwd_stage_bytes<DH>();
+  constexpr int RPI = 512 / DH, LPR = 64 / RPI;   // rows per 1 KB load, lanes per row
+  constexpr int NPW = (FKV * DH * 2 / 1024) / NW;  // 1 KB loads per wave per tensor and block
+  constexpr int NL = 2 * NPW;
+  static_assert(NPW >= 1, "every wave loads part of each block");
+  extern __shared__ __align__(16) char ring[];
+  const int S = a.S, H = a.H;
+  const int n_qt = (S + FWQ - 1) / FWQ;
+  // grid (head, sequence, tile): the tile index varies slowest, so every
+  // (heaviest) last query tile is dispatched before any lighter one
+  const int qt = n_qt - 1 - static_cast<int>(blockIdx.z);
+  const int head = blockIdx.x, seq = blockIdx.y;
+  if (seq >= seq_count(a)) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int hf = lane >> 5, cl = lane & 31;
+  const int q0 = qt * FWQ, qw = q0 + wave * RPW;
+  const int64_t ldq = 3ll * H * DH;
+  const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
+  const bf16* Qp = base + head * DH;
+  const bf16* Kp = base + static_cast<int64_t>(H) * DH + head * DH;
+  const bf16* Vp = base + 2ll * H * DH + head * DH;
+  const float sl2 = a.scale * kLog2e;
+  const float al2 = AL ? alibi_slope(head, H) * kLog2e : 0.f;
+
+  bf16x8 qf[NSB][DH / 16];
+  floatx16 o[NSB][DH / 32];
+  float m[NSB], l[NSB];
+#pragma unroll
+  for (int sb = 0; sb < NSB; ++sb) {
+    const int qrow = qw + sb * 32 + cl;
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks)
+      qf[sb][ks] = qrow < S ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[sb][db][v] = 0.f;
+    m[sb] = -INFINITY;
+    l[sb] = 0.f;
+  }
+  // The fragments must have arrived before the first LDS load is issued
+  // (the compiler does not see those loads).
+#pragma unroll
+  for (int sb = 0; sb < NSB; ++sb)
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) asm volatile("" ::"v"(qf[sb][ks]));
+
+  // Loads of key block k0 into stage st; blocks at or past the end read zeros.
+  const dma_rsrc rk = dma_make_rsrc(Kp, static_cast<int64_t>(S) * ldq * 2);
+  const dma_rsrc rv = dma_make_rsrc(Vp, static_cast<int64_t>(S) * ldq * 2);
+  const int lrow = wave * RPI + lane / LPR;
+  const int lchk = ((lane % LPR) ^ qd_swz<DH>(lrow)) << 3;
+  const uint32_t lk = static_cast<uint32_t>((lrow * ldq + lchk) * 2);
+  auto load_block = [&](int st, int k0) {
+    char* sbp = ring + st * SB;
+    const bool in = k0 < S;
+#pragma unroll
+    for (int i = 0; i < NPW; ++i) {
+      const int p = wave + NW * i;
+      const uint32_t r = static_cast<uint32_t>((static_cast<int64_t>(k0) + NW * i * RPI) * ldq * 2);
+      dma16(rk, sbp + p * 1024, in ? lk + r : kDmaOob);
+      dma16(rv, sbp + FKV * DH * 2 + p * 1024, in ? lk + r : kDmaOob);
+    }
+  };
+  // Per-lane LDS byte addresses in the stage of the current block: plain
+  // reads of K (row cl, 16-byte chunk 2ks + hf) and transposing reads of V
+  // (rows tr_r and tr_r + 8).
+  uint32_t ak[DH / 16], at0[DH / 32], at1[DH / 32];
+  {
+    const uint32_t r0 = lds_addr(ring);
+    const int sw_c = qd_swz<DH>(cl);
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) ak[ks] = r0 + 2u * (cl * DH + (((2 * ks + hf) ^ sw_c) << 3));
+    const int tr_r = 4 * hf + ((lane & 15) >> 2);
+    const int tr_d = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+    const int sw0 = qd_swz<DH>(tr_r), sw1 = qd_swz<DH>(tr_r + 8);
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) {
+      const int d0 = db * 32 + tr_d;
+      at0[db] = r0 + 2u * FKV * DH + 2u * (tr_r * DH + (((d0 >> 3) ^ sw0) << 3) + (d0 & 7));
+      at1[db] = r0 + 2u * FKV * DH + 2u * ((tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7));
+    }
+  }
+
+  const int kv_end = min(S, q0 + FWQ);
+  const int nkb = (kv_end + FKV - 1) / FKV;
+  load_block(0, 0);
+  load_block(1, FKV);
+  load_block(2, 2 * FKV);
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int k0 = kb * FKV, st = kb & (FWD_NST - 1);
+    // block kb has landed (blocks kb+1, kb+2 may be in flight); the stage of
+    // block kb-1 is no longer read and takes block kb+3
+    dma_barrier<2 * NL>();
+    load_block((kb + 3) & (FWD_NST - 1), k0 + 3 * FKV);
+    if (qw < S && k0 <= qw + RPW - 1) {
+      const bool diag = k0 + FKV - 1 > qw;  // some key of the block is past some row
+      // scores of every 32-row block: each K fragment feeds NSB MFMA chains
+      floatx16 sc[NSB][2];
+#pragma unroll
+      for (int ks = 0; ks < DH / 16; ++ks)
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh) {
+          const bf16x8 kf = lds_frag(ak[ks] + 2u * kh * 32 * DH);
+#pragma unroll
+          for (int sb = 0; sb < NSB; ++sb) sc[sb][kh] = mfma(kf, qf[sb][ks], ks == 0 ? floatx16{} : sc[sb][kh]);
+        }
+      bf16x8 pb[NSB][2][2];
+#pragma unroll
+      for (int sb = 0; sb < NSB; ++sb) {
+        const int qrow = qw + sb * 32 + cl;
+        const float ab = al2 * static_cast<float>(k0 + 4 * hf - qrow);  // bias of the lane's first key
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            float x = sc[sb][kh][v] * sl2;
+            if constexpr (AL) x += fmaf(al2, static_cast<float>(kh * 32 + 8 * (v >> 2) + (v & 3)), ab);
+            sc[sb][kh][v] = x;
+          }
+        if (diag) {  // causal mask, only on blocks that reach past a row (wave-uniform)
+          const int t = qrow - k0 - 4 * hf;  // the row minus the lane's first key
+#pragma unroll
+          for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+              if (kh * 32 + 8 * (v >> 2) + (v & 3) > t) sc[sb][kh][v] = -INFINITY;
+        }
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[sb][kh][v]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        // Lazy rescaling: the running maximum only moves (and O, l are only
+        // rescaled) when a row's maximum grows by more than 8 in log2 units;
+        // otherwise p = 2^(s - m) stays below 2^8, exact enough in bf16 and
+        // far from float overflow, and the result O / l is unchanged.
+        const bool grow = mx > m[sb] + 8.f;
+        if (__builtin_amdgcn_read_exec() & __ballot(grow)) {
+          const float m_new = grow ? mx : m[sb];
+          const float alpha = __builtin_amdgcn_exp2f(m[sb] - m_new);
+          m[sb] = m_new;
+          l[sb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) o[sb][db][v] *= alpha;
+        }
+        float ls = 0.f;
+#pragma unroll
+        for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float p = __builtin_amdgcn_exp2f(sc[sb][kh][v] - m[sb]);
+            ls += p;
+            pb[sb][kh][v >> 3][v & 7] = static_cast<bf16>(p);
+          }
+        l[sb] += ls;
+      }
+      // O^T += V^T P^T; consecutive MFMAs go to different accumulators (the
+      // d blocks innermost), so none waits on the one before it
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint32_t rr = 2u * (kh * 32 + 16 * c) * DH;
+#pragma unroll
+          for (int db = 0; db < DH / 32; ++db) {
+            const v4s lo = lds_tr(at0[db] + rr), hi = lds_tr(at1[db] + rr);
+            const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+            for (int sb = 0; sb < NSB; ++sb) o[sb][db] = mfma(vf, pb[sb][kh][c], o[sb][db]);
+          }
+        }
+    }
+    // next block: one stage on (wrapping around the ring)
+    const uint32_t adv = st == FWD_NST - 1 ? static_cast<uint32_t>(-(FWD_NST - 1) * SB) : static_cast<uint32_t>(SB);
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) ak[ks] += adv;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) {
+      at0[db] += adv;
+      at1[db] += adv;
+    }
+  }
+  dma_barrier<0>();  // no load may still write LDS when the workgroup ends
+#pragma unroll
+  for (int sb = 0; sb < NSB; ++sb) {
+    const int qrow = qw + sb * 32 + cl;
+    const float lt = l[sb] + __shfl_xor(l[sb], 32, 64);
+    if (qrow < S) {
+      const float inv = 1.f / lt;
+      bf16* Op = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * (static_cast<int64_t>(H) * DH) + head * DH;
+#pragma unroll
+      for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          __attribute__((aligned(8))) bf16 t[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(o[sb][db][4 * g + i] * inv);
+          *reinterpret_cast<uint2*>(Op + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(t);
+        }
+      if (hf == 0) a.lse[(static_cast<int64_t>(seq) * H + head) * S + qrow] = (m[sb] + log2f(lt)) * kLn2;
+    }
   }
 }
 
@@ -1128,11 +1013,13 @@ hipError_t fwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
   if constexpr (DH >= 64) {
     if (dtype == LD_BF16) {
       const dim3 grid(a.H, a.n_seq, (a.S + FWQ - 1) / FWQ);
-      constexpr int rpw = FWD_RPW;
+      constexpr int rpw = kFwdRowsPerWave;
       if (a.alibi)
-        hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw, true>), grid, dim3(64 * (FWQ / rpw)), 0, s, a);
+        hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw, true>), grid, dim3(64 * (FWQ / rpw)),
+                           FWD_NST * fwd_stage_bytes<DH>(), s, a);
       else
-        hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw, false>), grid, dim3(64 * (FWQ / rpw)), 0, s, a);
+        hipLaunchKernelGGL((ld_attn_fwd_bf16<DH, rpw, false>), grid, dim3(64 * (FWQ / rpw)),
+                           FWD_NST * fwd_stage_bytes<DH>(), s, a);
       return hipGetLastError();
     }
   }
