@@ -177,6 +177,54 @@ def cpu_baseline(sh, target_s=15.0):
     return el / n, n, threads
 
 
+# HBM-bound kernels of the step, with the algorithmic bytes each launch moves
+# (the library's profiling hook records them per launch).
+HBM_KERNELS = ["ld_mask_compact", "ld_rmsnorm_fwd_k", "ld_rmsnorm_bwd_k", "ld_gather_rows_k",
+               "ld_attn_delta", "ld_splitk_reduce"]
+
+
+def hbm_kernels(st, ps, step):
+    """One profiled step per kernel: launches, average duration (HIP events on
+    the library's stream), algorithmic bytes and the rate they imply."""
+    out = {}
+    for k in HBM_KERNELS:
+        ld.ld_prof_start(k)
+        st.step(ps, step)
+        torch.cuda.synchronize()
+        ld.ld_prof_stop()
+        r = ld.ld_prof_result()
+        if r["launches"] == 0:
+            continue
+        gbs = r["bytes"] / max(r["ms"] * 1e-3, 1e-12) / 1e9
+        out[k] = {"launches_per_step": r["launches"],
+                  "avg_us": round(r["ms"] * 1e3 / r["launches"], 2),
+                  "bytes_per_launch": round(r["bytes"] / r["launches"]),
+                  "gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return out
+
+
+def mask_microbench(dev, layers=128, batch=1 << 17, iters=5):
+    """Mask + compaction over 2^24 draws (128 layers x 2^17 samples, one
+    workgroup per layer): 13 algorithmic bytes per draw (8-byte draw, 4-byte
+    index, 1-byte mask)."""
+    p = [0.5] * layers
+    keep = torch.empty(layers, batch, dtype=torch.uint8, device=dev)
+    idx = torch.empty(layers, batch, dtype=torch.int32, device=dev)
+    cnt = torch.empty(layers, dtype=torch.int32, device=dev)
+    ld.ld_masks(p, 0, 0, keep, idx, cnt)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(iters):
+        ld.ld_masks(p, 0, i, keep, idx, cnt)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    gbs = 13.0 * layers * batch / (ms * 1e-3) / 1e9
+    return {"draws": layers * batch, "ms": round(ms, 3), "gbs": round(gbs, 1),
+            "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
 def _timed(fn, steps, warmup):
     for _ in range(warmup):
         fn()
@@ -341,6 +389,10 @@ def main():
           file=sys.stderr, flush=True)
     exec_tflops = exec_flops(kept) / (ms * 1e-3) / 1e12
     achieved = pr["flops"] / (pr["ms"] * 1e-3) / 1e12 if pr["ms"] > 0 else 0.0
+    hbm = hbm_kernels(st, ps, first)
+    print(f"# hbm kernels: {json.dumps(hbm)}", file=sys.stderr, flush=True)
+    maskb = mask_microbench(dev)
+    print(f"# mask microbench: {json.dumps(maskb)}", file=sys.stderr, flush=True)
     trec = traffic_record(prof_kernel, args.workload)
 
     sweep = []
@@ -413,6 +465,8 @@ def main():
                      "algorithmic_bytes": round(pr["bytes"] / max(pr["launches"], 1)),
                      "launches": pr["launches"],
                      "avg_launch_us": round(pr["ms"] * 1e3 / max(pr["launches"], 1), 2)},
+        "hbm_kernels": hbm,
+        "mask_microbench": maskb,
         "cpu_baseline": cpu,
         "sweep": sweep,
         "sweep_fit": fit,
