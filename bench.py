@@ -280,14 +280,14 @@ def infer_main(args, sh):
                      "hbm_frac": round(byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
         print(f"# decode {name}: {dec[name]}", file=sys.stderr, flush=True)
         if name == "target":
-            for k in ("ld_gemm_bf16_skinny<1>", "ld_attn_decode_bf16"):
+            for k in ("ld_gemm_bf16_dec", "ld_attn_decode_bf16"):
                 ld.ld_prof_start(k)
                 run()
                 torch.cuda.synchronize()
                 ld.ld_prof_stop()
                 prof[k] = ld.ld_prof_result()
     t = dec["target"]["ms"]
-    g = prof["ld_gemm_bf16_skinny<1>"]
+    g = prof["ld_gemm_bf16_dec"]
     out = {
         "metric": f"decode ms per step (one row per sequence, {args.workload} stack, "
                   f"{S}-position caches)",
@@ -306,7 +306,7 @@ def infer_main(args, sh):
                         "avg_us": round(v["ms"] * 1e3 / max(v["launches"], 1), 2),
                         "gbs": round(v["bytes"] / max(v["ms"] * 1e-3, 1e-12) / 1e9, 1)}
                     for k, v in prof.items()},
-        "skinny_gemm_weight_gbs": round(g["bytes"] / max(g["ms"] * 1e-3, 1e-12) / 1e9, 1),
+        "projection_gbs": round(g["bytes"] / max(g["ms"] * 1e-3, 1e-12) / 1e9, 1),
     }
     print(json.dumps(out), flush=True)
 

@@ -352,6 +352,26 @@ int ld_gemm_skinny(int32_t M, int32_t N, int32_t K, const void* A, int32_t lda, 
                    void* C, int32_t ldc, float alpha, const void* R, int32_t ldr, void* ws, size_t ws_bytes,
                    void* stream);
 
+/* Fused projection of a decoding step, bf16, for 1 <= M <= 8 rows (one new
+ * row per sequence): the pre-norm, the projection and the feed-forward
+ * activation of an active layer of the evaluation form (Preliminary section,
+ * evaluation equation; Inference Optimizations section) in one launch,
+ *   C[m, n] = act(R[m, n] + alpha * sum_k A'[m, k] W[n, k]),
+ * A' = A when g is NULL, else the RMSNorm of A's rows with gain g [K]:
+ * A'[m, k] = bf16(A[m, k] * rstd_m * g[k]), rstd_m = 1/sqrt(mean_k A[m, k]^2 + eps).
+ *   act 0: none (R optional, [M, N] with leading dimension ldr);
+ *   act 1: SwiGLU; W holds 2N rows (gate rows 0..N-1, then up rows N..2N-1)
+ *          and C = silu(u) v for u, v = bf16(alpha * A' W_gate^T), likewise
+ *          with W_up (R must be NULL);
+ *   act 2: squared ReLU, C = relu(bf16(alpha * A' W^T))^2 (R must be NULL).
+ * A [M, K], W and C (bf16 [M, N], leading dimension ldc) are device
+ * pointers; A, W (and g) 16-byte aligned, lda and ldw multiples of 8,
+ * K % 8 == 0.  The rows of A are staged in LDS: K <= 4096 with g, K <= 9664
+ * without; LD_E_UNSUPPORTED beyond.  No workspace; deterministic. */
+int ld_gemm_dec(int32_t M, int32_t N, int32_t K, const void* A, int32_t lda, const void* g, float eps,
+                const void* W, int32_t ldw, void* C, int32_t ldc, float alpha, const void* R, int32_t ldr,
+                int32_t act, void* stream);
+
 /* Keys and values of qkv rows (device bf16 [n_seq * n_new, 3 d], row
  * b*n_new + j) into the cache kv (device bf16 [n_seq, s_max, 2 d]) at
  * position pos + j of sequence b. */

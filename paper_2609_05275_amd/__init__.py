@@ -93,6 +93,8 @@ _SIGS = {
     "ld_gemm_skinny_ws_bytes": (_sz, [_i32, _i32, _i32]),
     "ld_gemm_skinny": (C.c_int, [_i32, _i32, _i32, _vp, _i32, _vp, _i32, _vp, _i32, _f32, _vp, _i32,
                                  _vp, _sz, _vp]),
+    "ld_gemm_dec": (C.c_int, [_i32, _i32, _i32, _vp, _i32, _vp, _f32, _vp, _i32, _vp, _i32, _f32, _vp, _i32,
+                              _i32, _vp]),
     "ld_kv_store": (C.c_int, [_i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp]),
     "ld_attn_decode_ws_bytes": (_sz, [_i32, _i32, _i32, _i32]),
     "ld_attn_decode": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _sz,
@@ -288,6 +290,20 @@ def ld_gemm_skinny(A, W, C_out, alpha=1.0, R=None, ws=None, stream=None):
                                C_out.stride(0), alpha, _ptr(R), 0 if R is None else R.stride(0),
                                _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                                _stream(stream)))
+
+
+DEC_ACT_NONE, DEC_ACT_SWIGLU, DEC_ACT_RELU2 = 0, 1, 2
+
+
+def ld_gemm_dec(A, W, C_out, g=None, eps=1e-5, alpha=1.0, R=None, act=DEC_ACT_NONE, stream=None):
+    """Fused decoding projection (M <= 8 rows): C = act(R + alpha A' W^T), A'
+    the RMSNorm of A's rows with gain g when g is given; with SwiGLU W holds
+    the gate rows then the up rows and C has half as many columns."""
+    M, K = A.shape
+    N = C_out.shape[1]
+    _check(_lib.ld_gemm_dec(M, N, K, _ptr(A), A.stride(0), _ptr(g), eps, _ptr(W), W.stride(0), _ptr(C_out),
+                            C_out.stride(0), alpha, _ptr(R), 0 if R is None else R.stride(0), act,
+                            _stream(stream)))
 
 
 def ld_kv_store(n_seq, n_new, d_model, pos, qkv, kv, s_max, stream=None):

@@ -1117,6 +1117,42 @@ int dec_gemm(const void* A, int64_t lda, const void* W, int64_t ldw, void* C, in
   return LD_OK;
 }
 
+// Fused decode projection (at most 8 rows; see launch_gemm_dec): C = act(R +
+// alpha * A' W^T) with A' the RMSNorm of A's rows when g is set.
+int dec_proj(const void* A, int64_t lda, const void* g, float eps, const void* W, int64_t ldw, void* C,
+             int64_t ldc, const void* R, int64_t ldr, int64_t M, int64_t N, int64_t K, float alpha, int act,
+             hipStream_t s, const KvOut* kv = nullptr) {
+  SkinnyArgs a{};
+  a.A = A;
+  a.lda = lda;
+  a.W = W;
+  a.ldw = ldw;
+  a.C = C;
+  a.ldc = ldc;
+  a.R = R;
+  a.ldr = ldr;
+  a.M = static_cast<int32_t>(M);
+  a.N = static_cast<int32_t>(N);
+  a.K = static_cast<int32_t>(K);
+  a.alpha = alpha;
+  a.g = g;
+  a.eps = eps;
+  a.act = act;
+  if (kv) {
+    a.kv = kv->kv;
+    a.kv_d = kv->d;
+    a.kv_n = kv->n;
+    a.kv_s_max = kv->s_max;
+    a.kv_pos = kv->pos;
+  }
+  ProfScope ps("ld_gemm_bf16_dec", s);
+  hipError_t e = launch_gemm_dec(a, s);
+  if (e != hipSuccess) return fail(LD_E_HIP, "decode projection: %s", hipGetErrorString(e));
+  const double wrows = act == kDecActSwiglu ? 2.0 * N : static_cast<double>(N);
+  ps.end(2.0 * M * wrows * K, 2.0 * (M * K + wrows * K + M * N) + (R ? 2.0 * M * N : 0.0));
+  return LD_OK;
+}
+
 }  // namespace
 
 // ====================================================================== ABI
@@ -1429,17 +1465,29 @@ int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w,
     ps.end(0, 4.0 * M * d);
     return static_cast<int>(LD_OK);
   };
+  // At most 8 rows (one new row per sequence of a batch of 8): each
+  // projection is one fused launch that normalises its input rows and
+  // applies the FFN activation itself.
+  const bool fused = dec_gemm_ok(M, d, true) && dec_gemm_ok(M, D.f, false);
+  const int act = D.kind == LD_BLOCK_SWIGLU ? kDecActSwiglu : kDecActRelu2;
   for (int32_t l = 0; l < n_layers; ++l) {
     if (active && !active[l]) continue;
     const float r = r_eval ? r_eval[l] : 1.f;
     const ld_weights& wl = w[l];
     // h = RMSNorm(x); qkv = h W_qkv^T; new keys/values into the cache
-    if (int rc = norm(x, wl.g_attn)) return rc;
     const KvOut ko{kv[l], static_cast<int32_t>(d), n_new, s_max, pos};
     bool kv_done = false;
-    if (int rc = dec_gemm(P(L.h), d, wl.w_qkv, d, P(L.qkv), 3 * d, nullptr, 0, M, 3 * d, d, 1.f, skp,
-                          L.skp_bytes, s, &ko, &kv_done))
-      return rc;
+    if (fused) {
+      if (int rc = dec_proj(x, d, wl.g_attn, cfg->rms_eps, wl.w_qkv, d, P(L.qkv), 3 * d, nullptr, 0, M, 3 * d, d,
+                            1.f, kDecActNone, s, &ko))
+        return rc;
+      kv_done = true;
+    } else {
+      if (int rc = norm(x, wl.g_attn)) return rc;
+      if (int rc = dec_gemm(P(L.h), d, wl.w_qkv, d, P(L.qkv), 3 * d, nullptr, 0, M, 3 * d, d, 1.f, skp,
+                            L.skp_bytes, s, &ko, &kv_done))
+        return rc;
+    }
     if (!kv_done) {
       KvArgs k{};
       k.qkv = P(L.qkv);
@@ -1478,6 +1526,18 @@ int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w,
       ps.end(4.0 * M * d * keys, 2.0 * D.B * keys * 2 * d + 4.0 * M * d);
     }
     // z = x + r (att W_o^T); h = RMSNorm(z); uv = h W_gate_up^T; s = act(uv)
+    if (fused) {
+      if (int rc = dec_proj(P(L.att), d, nullptr, 0.f, wl.w_o, d, P(L.z), d, x, d, M, d, d, r, kDecActNone, s))
+        return rc;
+      if (int rc = dec_proj(P(L.z), d, wl.g_mlp, cfg->rms_eps, wl.w_gate_up, d, P(L.s), D.f, nullptr, 0, M, D.f,
+                            d, 1.f, act, s))
+        return rc;
+      // x = z + r (s W_down^T)
+      if (int rc = dec_proj(P(L.s), D.f, nullptr, 0.f, wl.w_down, D.f, x, d, P(L.z), d, M, d, D.f, r,
+                            kDecActNone, s))
+        return rc;
+      continue;
+    }
     if (int rc = dec_gemm(P(L.att), d, wl.w_o, d, P(L.z), d, x, d, M, d, d, r, skp, L.skp_bytes, s))
       return rc;
     if (int rc = norm(P(L.z), wl.g_mlp)) return rc;
@@ -1644,6 +1704,25 @@ int ld_gemm_skinny(int32_t M, int32_t N, int32_t K, const void* A, int32_t lda, 
   if (need && (!ws || ws_bytes < need)) return fail(LD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   return dec_gemm(A, lda, W, ldw, C, ldc, R, ldr, M, N, K, alpha, static_cast<float*>(ws), ws ? ws_bytes : 0,
                   as_stream(stream));
+}
+
+int ld_gemm_dec(int32_t M, int32_t N, int32_t K, const void* A, int32_t lda, const void* g, float eps,
+                const void* W, int32_t ldw, void* C, int32_t ldc, float alpha, const void* R, int32_t ldr,
+                int32_t act, void* stream) {
+  t_err.clear();
+  if (M < 1 || M > kDecGemmMaxM) return fail(LD_E_SHAPE, "M outside [1, %d]", kDecGemmMaxM);
+  if (N < 1 || K < 8 || K % 8) return fail(LD_E_SHAPE, "need N >= 1, K >= 8, K %% 8 == 0");
+  if (act != kDecActNone && act != kDecActSwiglu && act != kDecActRelu2) return fail(LD_E_INVALID, "unknown act");
+  if (act != kDecActNone && R) return fail(LD_E_INVALID, "a residual only without activation");
+  if (!dec_gemm_ok(M, K, g != nullptr)) return fail(LD_E_UNSUPPORTED, "K = %d does not fit the staged rows", K);
+  if (lda < K || ldw < K || ldc < N || (R && ldr < N)) return fail(LD_E_SHAPE, "leading dimension too small");
+  if (lda % 8 || ldw % 8) return fail(LD_E_SHAPE, "lda, ldw must be multiples of 8");
+  if (!A || !W || !C) return fail(LD_E_INVALID, "NULL pointer");
+  if ((reinterpret_cast<uintptr_t>(A) | reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(g)) & 15)
+    return fail(LD_E_INVALID, "A, W and g must be 16-byte aligned");
+  if (!std::isfinite(alpha)) return fail(LD_E_INVALID, "alpha not finite");
+  if (g && !(eps > 0.f)) return fail(LD_E_INVALID, "eps must be > 0");
+  return dec_proj(A, lda, g, eps, W, ldw, C, ldc, R, ldr, M, N, K, alpha, act, as_stream(stream));
 }
 
 int ld_kv_store(int32_t n_seq, int32_t n_new, int32_t d_model, int32_t pos, const void* qkv, void* kv,

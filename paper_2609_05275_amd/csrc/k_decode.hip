@@ -138,6 +138,208 @@ __global__ __launch_bounds__(256) void ld_skinny_reduce_k(SkinnyArgs g, int kspl
   }
 }
 
+// ------------------------------------------------ fused decode projection
+// At most 8 rows, so the product is a few dot products per weight: vector
+// ALU work (v_dot2 on bf16 pairs), not MFMA tiles, and the layout is chosen
+// for the weight stream.  A tile is 8 output columns (8 rows of W; with
+// SwiGLU the 8 gate rows and the 8 up rows of those columns) over the whole
+// k range, so every column is finished in one workgroup (no split-K
+// partials) and N = 2048 still spreads over 256 workgroups.  Lane 8r + t
+// reads 16 bytes at k = 64c + 8t of row r: each load instruction takes 8
+// whole 128-byte lines.  The NW waves take interleaved chunks c, four per
+// pass, the next pass's loads in flight while one is summed (a workgroup
+// may also walk several tiles in turn; the launch gives each one tile, as
+// timing favoured more resident waves over fewer rounds).  The rows of A are
+// staged in LDS once per workgroup (zero rows past M), normalised on the way
+// when a gain is given:
+// one wave per row, sum of squares in lane order, rstd = 1/sqrt(mean + eps),
+// A' = bf16(A rstd g), as the row-wise RMSNorm kernel computes it.  Partial
+// sums are reduced over the 8 lanes of a row, then over the waves in wave
+// order through LDS; the epilogue applies alpha and the residual (and copies
+// key/value columns to the cache) or the activation, rounding u and v to
+// bf16 first as the unfused path stores them.
+
+constexpr int kDecCols = 8;   // output columns per workgroup
+constexpr int kDecU = 4;      // chunks per pass
+constexpr int kDecCus = 256;  // compute units
+
+__host__ __device__ inline int dec_pitch(int64_t K) { return static_cast<int>((K + 63) & ~63ll); }
+
+__device__ __forceinline__ float bf16r(float x) { return static_cast<float>(static_cast<bf16>(x)); }
+
+__device__ __forceinline__ float dot8(const bf16x8& w, const bf16x8& a, float c) {
+#pragma unroll
+  for (int e = 0; e < 8; e += 2)
+    c = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{w[e], w[e + 1]}, bf16x2{a[e], a[e + 1]}, c, false);
+  return c;
+}
+
+template <int NW, int ACT, bool NORM>
+__global__ __launch_bounds__(NW * 64) void ld_gemm_bf16_dec(SkinnyArgs g) {
+  constexpr int NR = ACT == kDecActSwiglu ? 2 : 1;  // W rows per lane
+  extern __shared__ __align__(16) unsigned char dsm[];
+  const int M = g.M, N = g.N, K = g.K;
+  const int pitch = dec_pitch(K);
+  bf16* as = reinterpret_cast<bf16*>(dsm);
+  float* red = reinterpret_cast<float*>(dsm + static_cast<size_t>(kDecGemmMaxM) * pitch * 2);
+  float* fin = red + NW * NR * kDecCols * kDecGemmMaxM;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane >> 3, t = lane & 7;
+  const int nchunks = (K + 63) >> 6;
+  const bf16* A = static_cast<const bf16*>(g.A);
+  const bf16* W = static_cast<const bf16*>(g.W);
+
+  // This workgroup's tile: columns col of its lanes' rows; the k range in
+  // npass passes of kDecU chunks per wave.
+  const int col = blockIdx.x * kDecCols + r;
+  const bool nvalid = col < N;
+  const int npass = (nchunks + kDecU * NW - 1) / (kDecU * NW);
+  const bf16* wrow[NR];
+#pragma unroll
+  for (int j = 0; j < NR; ++j) wrow[j] = W + static_cast<int64_t>(nvalid ? col + j * N : 0) * g.ldw + 8 * t;
+
+  typedef bf16x8 WBuf[kDecU][NR];
+  auto load_w = [&](WBuf& wb, int p) {
+#pragma unroll
+    for (int u = 0; u < kDecU; ++u) {
+      const int kc = (wave + NW * (kDecU * p + u)) * 64;
+#pragma unroll
+      for (int j = 0; j < NR; ++j) wb[u][j] = (nvalid && kc + 8 * t < K) ? load8(wrow[j] + kc) : zero8();
+    }
+  };
+  // the first two passes' loads and the epilogue's residual go out before
+  // the staging below waits on its own loads
+  WBuf w0, w1;
+  load_w(w0, 0);
+  if (npass > 1) load_w(w1, 1);
+  const int em = tid / kDecCols, en = blockIdx.x * kDecCols + tid % kDecCols;  // epilogue element
+  const bool eval = tid < M * kDecCols && en < N;
+  float resid = 0.f;
+  if (ACT == kDecActNone && g.R && eval)
+    resid = static_cast<float>(static_cast<const bf16*>(g.R)[static_cast<int64_t>(em) * g.ldr + en]);
+
+  // stage the rows of A (normalised when a gain is given), zero rows past M
+  const int k8n = K >> 3, p8 = pitch >> 3;
+  for (int m = wave; m < kDecGemmMaxM; m += NW) {
+    bf16* dst = as + m * pitch;
+    if (m >= M) {
+      for (int k8 = lane; k8 < p8; k8 += 64) *reinterpret_cast<bf16x8*>(dst + 8 * k8) = zero8();
+      continue;
+    }
+    const bf16* x = A + static_cast<int64_t>(m) * g.lda;
+    if constexpr (NORM) {
+      constexpr int NCH = kDecGemmMaxKNorm / 512;
+      bf16x8 xv[NCH];
+      float ss = 0.f;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const int k8 = c * 64 + lane;
+        if (k8 < k8n) {
+          xv[c] = load8(x + 8 * k8);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float f = static_cast<float>(xv[c][e]);
+            ss = __builtin_fmaf(f, f, ss);
+          }
+        }
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+      const float rstd = rsqrtf(ss / static_cast<float>(K) + g.eps);
+      const bf16* gain = static_cast<const bf16*>(g.g);
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const int k8 = c * 64 + lane;
+        if (k8 < k8n) {
+          const bf16x8 gv = load8(gain + 8 * k8);
+          bf16x8 o;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            o[e] = static_cast<bf16>(static_cast<float>(xv[c][e]) * rstd * static_cast<float>(gv[e]));
+          *reinterpret_cast<bf16x8*>(dst + 8 * k8) = o;
+        }
+      }
+    } else {
+      for (int k8 = lane; k8 < k8n; k8 += 64) *reinterpret_cast<bf16x8*>(dst + 8 * k8) = load8(x + 8 * k8);
+    }
+    for (int k8 = k8n + lane; k8 < p8; k8 += 64) *reinterpret_cast<bf16x8*>(dst + 8 * k8) = zero8();
+  }
+  __syncthreads();
+
+  float acc[NR][kDecGemmMaxM];
+#pragma unroll
+  for (int j = 0; j < NR; ++j)
+#pragma unroll
+    for (int m = 0; m < kDecGemmMaxM; ++m) acc[j][m] = 0.f;
+  auto dots = [&](const WBuf& wb, int p) {
+#pragma unroll
+    for (int u = 0; u < kDecU; ++u) {
+      const int c = wave + NW * (kDecU * p + u);
+      if (c < nchunks) {  // wave-uniform
+        const bf16* ak = as + c * 64 + 8 * t;
+#pragma unroll
+        for (int m = 0; m < kDecGemmMaxM; ++m) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(ak + m * pitch);
+#pragma unroll
+          for (int j = 0; j < NR; ++j) acc[j][m] = dot8(wb[u][j], a, acc[j][m]);
+        }
+      }
+    }
+  };
+  for (int p = 0; p < npass; p += 2) {
+    dots(w0, p);
+    if (p + 2 < npass) load_w(w0, p + 2);
+    if (p + 1 < npass) {
+      dots(w1, p + 1);
+      if (p + 3 < npass) load_w(w1, p + 3);
+    }
+  }
+
+  // sums over the 8 lanes of a row, then over the waves in wave order
+#pragma unroll
+  for (int j = 0; j < NR; ++j)
+#pragma unroll
+    for (int m = 0; m < kDecGemmMaxM; ++m) {
+      float v = acc[j][m];
+      v += __shfl_xor(v, 1, 8);
+      v += __shfl_xor(v, 2, 8);
+      v += __shfl_xor(v, 4, 8);
+      acc[j][m] = v;
+    }
+  if (t == 0)
+#pragma unroll
+    for (int j = 0; j < NR; ++j)
+#pragma unroll
+      for (int m = 0; m < kDecGemmMaxM; ++m) red[((wave * NR + j) * kDecCols + r) * kDecGemmMaxM + m] = acc[j][m];
+  __syncthreads();
+  constexpr int kVals = NR * kDecCols * kDecGemmMaxM;
+  if (tid < kVals) {
+    float sum = 0.f;
+    for (int w = 0; w < NW; ++w) sum += red[w * kVals + tid];
+    fin[tid] = sum;  // [j][column][row]
+  }
+  __syncthreads();
+  if (eval) {
+    const int c = tid % kDecCols;
+    bf16* C = static_cast<bf16*>(g.C) + static_cast<int64_t>(em) * g.ldc + en;
+    const float s0 = fin[c * kDecGemmMaxM + em];
+    if constexpr (ACT == kDecActSwiglu) {
+      const float u = bf16r(g.alpha * s0), v = bf16r(g.alpha * fin[(kDecCols + c) * kDecGemmMaxM + em]);
+      *C = static_cast<bf16>(swiglu_fwd_f(u, v));
+    } else if constexpr (ACT == kDecActRelu2) {
+      const float z = fmaxf(bf16r(g.alpha * s0), 0.f);
+      *C = static_cast<bf16>(z * z);
+    } else {
+      const bf16 o = static_cast<bf16>(g.alpha * s0 + resid);
+      *C = o;
+      if (g.kv && en >= g.kv_d) {
+        const int64_t b = em / g.kv_n, jj = em % g.kv_n;
+        static_cast<bf16*>(g.kv)[(b * g.kv_s_max + g.kv_pos + jj) * 2 * g.kv_d + (en - g.kv_d)] = o;
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------ KV store
 
 __global__ __launch_bounds__(256) void ld_kv_store_k(KvArgs a) {
@@ -357,6 +559,41 @@ hipError_t launch_gemm_skinny(const SkinnyArgs& g, int ksplit, hipStream_t s) {
   hipLaunchKernelGGL(ld_skinny_reduce_k, dim3(grid_for(static_cast<int64_t>(g.M) * g.N)), dim3(256), 0,
                      s, g, ksplit);
   return hipGetLastError();
+}
+
+size_t dec_gemm_lds_bytes(int64_t K, int nw) {
+  return static_cast<size_t>(kDecGemmMaxM) * dec_pitch(K) * 2 +
+         static_cast<size_t>(nw + 1) * 2 * kDecCols * kDecGemmMaxM * 4;
+}
+
+bool dec_gemm_ok(int64_t M, int64_t K, bool norm) {
+  return M >= 1 && M <= kDecGemmMaxM && K >= 8 && K % 8 == 0 && (!norm || K <= kDecGemmMaxKNorm) &&
+         dec_gemm_lds_bytes(K, 16) <= 160 * 1024;
+}
+
+template <int NW, int ACT>
+hipError_t gemm_dec_t(const SkinnyArgs& g, int tiles, hipStream_t s) {
+  const size_t lds = dec_gemm_lds_bytes(g.K, NW);
+  if (g.g)
+    hipLaunchKernelGGL((ld_gemm_bf16_dec<NW, ACT, true>), dim3(tiles), dim3(NW * 64), lds, s, g);
+  else
+    hipLaunchKernelGGL((ld_gemm_bf16_dec<NW, ACT, false>), dim3(tiles), dim3(NW * 64), lds, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_dec(const SkinnyArgs& g, hipStream_t s) {
+  if (g.N <= 0) return hipSuccess;
+  if (!dec_gemm_ok(g.M, g.K, g.g != nullptr)) return hipErrorInvalidValue;
+  const int tiles = (g.N + kDecCols - 1) / kDecCols;
+  // One workgroup per tile, all resident at once: while the tiles fit one
+  // per CU, 16 waves (8 with SwiGLU, whose two rows per lane need more than
+  // the 128 registers of 16 waves), else 4 (up to four workgroups per CU);
+  // either way every wave's loads are issued up front.
+  if (g.act == kDecActSwiglu)
+    return tiles <= kDecCus ? gemm_dec_t<8, kDecActSwiglu>(g, tiles, s) : gemm_dec_t<4, kDecActSwiglu>(g, tiles, s);
+  if (g.act == kDecActRelu2)
+    return tiles <= kDecCus ? gemm_dec_t<16, kDecActRelu2>(g, tiles, s) : gemm_dec_t<4, kDecActRelu2>(g, tiles, s);
+  return tiles <= kDecCus ? gemm_dec_t<16, kDecActNone>(g, tiles, s) : gemm_dec_t<4, kDecActNone>(g, tiles, s);
 }
 
 hipError_t launch_kv_store(const KvArgs& a, hipStream_t s) {

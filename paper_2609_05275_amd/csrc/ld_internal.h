@@ -268,8 +268,26 @@ struct SkinnyArgs {
   // qkv projection)
   void* kv;
   int32_t kv_d, kv_n, kv_s_max, kv_pos;
+  // fused decode projection only (launch_gemm_dec): RMSNorm gain applied to
+  // the rows of A on load (NULL: A as given), and the activation of the
+  // output (kDecAct*; SwiGLU reads gate rows 0..N-1 and up rows N..2N-1 of W)
+  const void* g;
+  float eps;
+  int32_t act;
 };
 constexpr int kSkinnyMaxM = 64;
+
+// Fused decode projection (at most 8 rows): one workgroup per 8 output
+// columns and the whole k range, A rows staged in LDS (normalised on the
+// way when g is set); no split-K partials and no separate norm or
+// activation launch.
+constexpr int kDecGemmMaxM = 8;
+constexpr int kDecGemmMaxKNorm = 4096;
+constexpr int kDecActNone = 0, kDecActSwiglu = 1, kDecActRelu2 = 2;
+// LDS bytes the fused projection needs for K (0 when it does not fit).
+size_t dec_gemm_lds_bytes(int64_t K, int nw);
+bool dec_gemm_ok(int64_t M, int64_t K, bool norm);
+hipError_t launch_gemm_dec(const SkinnyArgs& g, hipStream_t s);
 
 // Copy of the key/value columns of qkv rows into a cache [n_seq, s_max, 2d]
 // (keys, then values, of each position): row b*n + j goes to position pos + j

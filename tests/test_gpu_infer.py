@@ -64,6 +64,69 @@ def test_gemm_skinny_rejects():
         ld.ld_gemm_skinny(A, W, C)
 
 
+DEC_MODES = ["plain", "resid", "norm", "norm_resid", "swiglu", "norm_swiglu", "norm_relu2"]
+
+
+@pytest.mark.parametrize("M", [1, 3, 8])
+@pytest.mark.parametrize("N,K", [(96, 64), (130, 200), (2048, 2048), (704, 5504), (11008, 2048)])
+@pytest.mark.parametrize("mode", DEC_MODES)
+def test_gemm_dec(M, N, K, mode):
+    """Fused decoding projection: RMSNorm of the input rows, projection,
+    residual or activation in one launch, against the oracle's RMSNorm and
+    activations in float64 on the same bf16 inputs (16 waves per workgroup
+    for N = 2048, 8 for the 11008-column SwiGLU, ragged column tiles for
+    N = 130 and 704, a ragged k chunk for K = 200)."""
+    norm = mode.startswith("norm")
+    if norm and K > 4096:
+        pytest.skip("the fused RMSNorm stages at most 4096 columns")
+    act = ld.DEC_ACT_SWIGLU if "swiglu" in mode else ld.DEC_ACT_RELU2 if "relu2" in mode else ld.DEC_ACT_NONE
+    rng = np.random.default_rng(M * 131 + N * 7 + K + len(mode))
+    wrows = 2 * N if act == ld.DEC_ACT_SWIGLU else N
+    A = _rng_bf16(rng, (M, K))
+    W = _rng_bf16(rng, (wrows, K), 0.05)
+    G = _bf16(1.0 + 0.2 * rng.standard_normal(K)) if norm else None
+    R = _rng_bf16(rng, (M, N)) if "resid" in mode else None
+    alpha = 0.75
+    eps = 1e-5
+    Ad, Wd = A.to(DEV), W.to(DEV)
+    Gd = None if G is None else G.to(DEV)
+    Rd = None if R is None else R.to(DEV)
+    outs = []
+    for _ in range(2):
+        C = torch.full((M, N), 3.0, dtype=torch.bfloat16, device=DEV)
+        ld.ld_gemm_dec(Ad, Wd, C, g=Gd, eps=eps, alpha=alpha, R=Rd, act=act)
+        torch.cuda.synchronize()
+        outs.append(C.cpu())
+    assert torch.equal(outs[0], outs[1])
+    a = f64(A)
+    if norm:
+        a, _ = block.rmsnorm(a, f64(G), eps)
+    y = alpha * (a @ f64(W).T)
+    if act == ld.DEC_ACT_SWIGLU:
+        want = block.silu(y[:, :N]) * y[:, N:]
+    elif act == ld.DEC_ACT_RELU2:
+        want = block.relu2(y)
+    else:
+        want = y + (f64(R) if R is not None else 0.0)
+    assert rel(f64(outs[0]), want) < 1e-2
+
+
+def test_gemm_dec_rejects():
+    A = torch.zeros(9, 64, dtype=torch.bfloat16, device=DEV)
+    W = torch.zeros(32, 64, dtype=torch.bfloat16, device=DEV)
+    C = torch.zeros(9, 32, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(ld.LdError):
+        ld.ld_gemm_dec(A, W, C)                                       # 9 rows
+    A8, C8 = A[:8], C[:8]
+    with pytest.raises(ld.LdError):
+        ld.ld_gemm_dec(A8, W, C8, R=C8, act=ld.DEC_ACT_RELU2)       # residual with an activation
+    Ak = torch.zeros(8, 4104, dtype=torch.bfloat16, device=DEV)
+    Wk = torch.zeros(32, 4104, dtype=torch.bfloat16, device=DEV)
+    g = torch.ones(4104, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(ld.LdError):
+        ld.ld_gemm_dec(Ak, Wk, C8, g=g)                               # norm over more than 4096 columns
+
+
 @pytest.mark.parametrize("pos,n", [(0, 1), (5, 3), (248, 8)])
 def test_kv_store_bit_exact(pos, n):
     rng = np.random.default_rng(pos + n)
