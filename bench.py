@@ -221,8 +221,10 @@ def mask_microbench(dev, layers=128, batch=1 << 17, iters=5):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / iters
     gbs = 13.0 * layers * batch / (ms * 1e-3) / 1e9
-    return {"draws": layers * batch, "ms": round(ms, 3), "gbs": round(gbs, 1),
-            "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    # bound by the vector ALU, not HBM: one Philox4x64-10 block per draw is
+    # 20 64x64->128-bit products (~360 vector instructions in the kernel)
+    return {"draws": layers * batch, "ms": round(ms, 3), "draws_per_s": round(layers * batch / (ms * 1e-3), 1),
+            "bound": "alu", "gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 def _timed(fn, steps, warmup):
