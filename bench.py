@@ -357,8 +357,8 @@ def main():
     first = T_RAMP - 1
 
     # pick the dominant kernel: one profiled step per candidate (untimed)
-    cands = ["ld_gemm_bf16_nt_256", "ld_gemm_bf16_nt_glu_256", "ld_gemm_bf16_tn_nn_256",
-             "ld_gemm_bf16_tn_nn_glu_256",
+    cands = ["ld_gemm_bf16_nt_256", "ld_gemm_bf16_nt_glu_256", "ld_gemm_bf16_nt_relu2_256",
+             "ld_gemm_bf16_tn_nn_256", "ld_gemm_bf16_tn_nn_glu_256", "ld_gemm_bf16_tn_nn_relu2_256",
              "ld_attn_fwd_bf16", "ld_attn_bwd_dkdv_bf16", "ld_attn_bwd_dq_bf16"]
     prof_kernel = args.prof_kernel
     st.step(ps, first - 1)

@@ -367,7 +367,7 @@ int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmA
   const GemmPlan p1 = plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, part != nullptr);
   const GemmPlan p2 = plan_gemm(dtype, 1, 0, g2, max_m2, 0, false);
   if (dtype != LD_BF16 || !p1.big || !p2.big) {
-    if (g2.glu_f > 0) return fail(LD_E_INVALID, "fused SwiGLU backward needs the paired 256x256 kernels");
+    if (g2.glu_f > 0 || g2.relu2) return fail(LD_E_INVALID, "a fused activation backward needs the paired 256x256 kernels");
     if (int rc = run_gemm(dtype, 1, 0, g2, max_m2, host_m2, host_k2, s)) return rc;
     return run_gemm(dtype, 0, 0, g1, g1.M, g1.M, host_k1, s, part, part_bytes, max_k1);
   }
@@ -379,14 +379,16 @@ int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmA
     if (gemm_part_bytes(q, g1.M, g1.N) > part_bytes) return fail(LD_E_WORKSPACE, "split-K scratch too small");
     g1.part = part;
   }
-  const char* name = g2.glu_f > 0 ? "ld_gemm_bf16_tn_nn_glu_256" : "ld_gemm_bf16_tn_nn_256";
+  const char* name = g2.relu2 ? "ld_gemm_bf16_tn_nn_relu2_256"
+                    : g2.glu_f > 0 ? "ld_gemm_bf16_tn_nn_glu_256" : "ld_gemm_bf16_tn_nn_256";
   ProfScope ps(name, s);
   const hipError_t e = launch_gemm_pair(g1, pp, g2, max_m2, s);
   if (e != hipSuccess) return fail(LD_E_HIP, "%s launch: %s", name, hipGetErrorString(e));
   const double M1 = g1.M, N1 = g1.N, K1 = static_cast<double>(host_k1);
   const double M2 = static_cast<double>(host_m2), N2 = g2.N, K2 = static_cast<double>(host_k2);
-  // the fused epilogue reads [u v] and writes [gu gv] instead of writing gs
-  const double out2 = g2.glu_f > 0 ? 4.0 * M2 * N2 : 1.0 * M2 * N2;
+  // a fused epilogue reads [u v] and writes [gu gv] (u and gu with squared
+  // ReLU) instead of writing gs
+  const double out2 = g2.relu2 ? 2.0 * M2 * N2 : g2.glu_f > 0 ? 4.0 * M2 * N2 : 1.0 * M2 * N2;
   ps.end(2.0 * (M1 * N1 * K1 + M2 * N2 * K2),
          2.0 * (M1 * K1 + N1 * K1) + 4.0 * M1 * N1 * pp.splits1 + 2.0 * (M2 * K2 + N2 * K2 + out2));
   if (pp.splits1 > 1) {
@@ -561,6 +563,17 @@ int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, c
       ps.end(2.0 * hm * D.fw * D.d, D.es * (hm * D.d + D.fw * D.d + hm * D.fw + hm * D.f));
       goto down_projection;
     }
+    // squared ReLU likewise (u and s from one epilogue)
+    if (D.kind == LD_BLOCK_ALIBI_RELU2 && dt == LD_BF16 && plan_gemm(dt, 1, 1, g, T, 0, false).big) {
+      g.aux = act.at(act.L.s);
+      g.glu_f = static_cast<int32_t>(D.f);
+      g.relu2 = 1;
+      ProfScope ps("ld_gemm_bf16_nt_relu2_256", s);
+      if ((e = launch_gemm_relu2_fwd(g, T, s)) != hipSuccess)
+        return fail(LD_E_HIP, "ld_gemm_bf16_nt_relu2_256 launch: %s", hipGetErrorString(e));
+      ps.end(2.0 * hm * D.fw * D.d, D.es * (hm * D.d + D.fw * D.d + 2.0 * hm * D.f));
+      goto down_projection;
+    }
     if (int rc = run_gemm(dt, 1, 1, g, T, hm, D.d, s)) return rc;
   }
   // s = silu(u) * v  or  s = relu(u)^2
@@ -676,9 +689,9 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     ps.end(0, 2.0 * D.es * hm * D.d);
   }
   // gs = r * gk W_down [M, f] and dW_down = r * gk^T s [d, f], one launch;
-  // for SwiGLU in the paired kernels, the SwiGLU backward is fused into the
-  // first product's epilogue (guv from gs without storing gs)
-  bool glu_fused = false;
+  // in the paired kernels the activation's backward is fused into the first
+  // product's epilogue (guv from gs without storing gs)
+  bool act_fused = false;
   {
     GemmArgs g = gemm_args();
     g.A = W(BL.gk);
@@ -706,17 +719,18 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     g1.dev_count = mv.count;
     g1.count_mult = S;
     g1.count_dim = 1;
-    if (D.kind == LD_BLOCK_SWIGLU && gemm_pair_ok(dt, g1, T, g, T)) {
-      glu_fused = true;
+    if (gemm_pair_ok(dt, g1, T, g, T)) {
+      act_fused = true;
       g.C = W(BL.guv);
       g.ldc = D.fw;
       g.aux = act.at(act.L.uv);
       g.glu_f = static_cast<int32_t>(D.f);
+      g.relu2 = D.kind == LD_BLOCK_ALIBI_RELU2;
     }
     if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
   }
   // guv = SwiGLU backward, or gu = squared-ReLU backward
-  if (!glu_fused) {
+  if (!act_fused) {
     EltArgs a{};
     a.a = act.at(act.L.uv);
     a.b = W(BL.gs);

@@ -583,7 +583,7 @@ __device__ __forceinline__ void epilogue_rows_edge(const GemmArgs& g, float* par
   }
 }
 
-constexpr int kEpiPlain = 0, kEpiGluFwd = 1, kEpiGluBwd = 2;
+constexpr int kEpiPlain = 0, kEpiGluFwd = 1, kEpiGluBwd = 2, kEpiRelu2Fwd = 3, kEpiRelu2Bwd = 4;
 
 __device__ __forceinline__ float bf16r(float x) { return static_cast<float>(static_cast<bf16>(x)); }
 
@@ -689,6 +689,70 @@ __device__ __forceinline__ void glu_bwd_rows(const GemmArgs& g, const float* sta
       const float4 gs = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
       glu_bwd_one(g, gs, *reinterpret_cast<const uint2*>(U + m * ldu + n),
                   *reinterpret_cast<const uint2*>(U + m * ldu + g.glu_f + n), m, n);
+    }
+  }
+}
+
+// Fused squared-ReLU forward: staged values (alpha applied) of rows r0 + 2 it,
+// columns n..n+3, go to C as u (bf16) and to aux as s = relu(u)^2 of the
+// bf16 u, as the elementwise kernel computes it from a stored u.
+__device__ __forceinline__ void relu2_fwd_one(const GemmArgs& g, float4 v, int64_t m, int n) {
+  const float u[4] = {bf16r(v.x), bf16r(v.y), bf16r(v.z), bf16r(v.w)};
+  float q[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float z = fmaxf(u[e], 0.f);
+    q[e] = z * z;
+  }
+  *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + m * g.ldc + n) = pack4_bf16(u[0], u[1], u[2], u[3]);
+  *reinterpret_cast<uint2*>(static_cast<bf16*>(g.aux) + m * g.glu_f + n) = pack4_bf16(q[0], q[1], q[2], q[3]);
+}
+
+__device__ __forceinline__ void relu2_fwd_rows(const GemmArgs& g, const float* stage, int r0, int half, int c,
+                                               int n, int M, bool full) {
+  if (full) {
+    float4 v[16];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) v[it] = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
+#pragma unroll
+    for (int it = 0; it < 16; ++it) relu2_fwd_one(g, v[it], r0 + 2 * it, n);
+  } else {
+#pragma unroll 1
+    for (int it = 0; it < 16; ++it) {
+      const int64_t m = r0 + 2 * it;
+      if (m >= M || n >= g.N) continue;
+      relu2_fwd_one(g, *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c), m, n);
+    }
+  }
+}
+
+// Fused squared-ReLU backward: the staged gs values, rounded to bf16 as a
+// stored gs would be, with u read from aux, give gu = gs 2 relu(u) in C.
+__device__ __forceinline__ void relu2_bwd_one(const GemmArgs& g, float4 gs, uint2 ur, int64_t m, int n) {
+  const float4 u = unpack4_bf16(ur);
+  *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + m * g.ldc + n) =
+      pack4_bf16(bf16r(gs.x) * 2.f * fmaxf(u.x, 0.f), bf16r(gs.y) * 2.f * fmaxf(u.y, 0.f),
+                 bf16r(gs.z) * 2.f * fmaxf(u.z, 0.f), bf16r(gs.w) * 2.f * fmaxf(u.w, 0.f));
+}
+
+__device__ __forceinline__ void relu2_bwd_rows(const GemmArgs& g, const float* stage, int r0, int half, int c,
+                                               int n, int M, bool full) {
+  const bf16* U = static_cast<const bf16*>(g.aux);
+  if (full) {
+    uint2 ur[16];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) ur[it] = *reinterpret_cast<const uint2*>(U + static_cast<int64_t>(r0 + 2 * it) * g.glu_f + n);
+#pragma unroll
+    for (int it = 0; it < 16; ++it)
+      relu2_bwd_one(g, *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c), ur[it],
+                    r0 + 2 * it, n);
+  } else {
+#pragma unroll 1
+    for (int it = 0; it < 16; ++it) {
+      const int64_t m = r0 + 2 * it;
+      if (m >= M || n >= g.N) continue;
+      relu2_bwd_one(g, *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c),
+                    *reinterpret_cast<const uint2*>(U + m * g.glu_f + n), m, n);
     }
   }
 }
@@ -843,6 +907,10 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
       glu_fwd_s_rows(g, stage, mb, lane, tn * 128 + wn * 64, M, mb + 32 <= M);
     } else if constexpr (EPI == kEpiGluBwd) {
       glu_bwd_rows(g, stage, mb + half, half, c, n, M, n0 + wn * 128 + 128 <= g.N && mb + 32 <= M);
+    } else if constexpr (EPI == kEpiRelu2Fwd) {
+      relu2_fwd_rows(g, stage, mb + half, half, c, n, M, n0 + wn * 128 + 128 <= g.N && mb + 32 <= M);
+    } else if constexpr (EPI == kEpiRelu2Bwd) {
+      relu2_bwd_rows(g, stage, mb + half, half, c, n, M, n0 + wn * 128 + 128 <= g.N && mb + 32 <= M);
     } else {
       if (full_cols && mb + 32 <= M)
         epilogue_rows_full(g, part, stage, mb + half, half, c, n, q_last);
@@ -868,6 +936,12 @@ LD_BIG_KERNEL(ld_gemm_bf16_tt_256, false, true)
 LD_BIG_ATTRS void ld_gemm_bf16_nt_glu_256(GemmArgs g) {
   __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
   gemm_big_body<true, true, kEpiGluFwd>(g, ring, blockIdx.x, gridDim.x, 0, 1);
+}
+
+// C = u rows and aux = relu(u)^2 rows of the squared-ReLU projection (see GemmArgs).
+LD_BIG_ATTRS void ld_gemm_bf16_nt_relu2_256(GemmArgs g) {
+  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
+  gemm_big_body<true, true, kEpiRelu2Fwd>(g, ring, blockIdx.x, gridDim.x, 0, 1);
 }
 
 // Two GEMMs in one launch: a weight-gradient GEMM g1 (both operands
@@ -903,6 +977,11 @@ LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_256(GemmArgs g1, GemmArgs g2, int tiles1, i
 LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_glu_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
                                              int g2_first) {
   gemm_pair_body<kEpiGluBwd>(g1, g2, tiles1, splits1, tiles2, g2_first);
+}
+// The same with the squared-ReLU backward fused into g2's epilogue.
+LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_relu2_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
+                                               int g2_first) {
+  gemm_pair_body<kEpiRelu2Bwd>(g1, g2, tiles1, splits1, tiles2, g2_first);
 }
 
 // C[i] = sum over splits of part[s][i], float32, in split order.  Every
@@ -1091,6 +1170,13 @@ hipError_t launch_gemm_glu_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s) 
   return hipGetLastError();
 }
 
+hipError_t launch_gemm_relu2_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s) {
+  if (max_m <= 0 || g.N <= 0) return hipSuccess;
+  const int64_t tiles = ((max_m + GB - 1) / GB) * ((g.N + GB - 1) / GB);
+  hipLaunchKernelGGL(ld_gemm_bf16_nt_relu2_256, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s) {
   const int splits1 = p.splits1;
   const int64_t tiles1 = ((static_cast<int64_t>(g1.M) + GB - 1) / GB) * ((g1.N + GB - 1) / GB);
@@ -1102,7 +1188,10 @@ hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, 
   }
   const int64_t wg = tiles1 * splits1 + tiles2;
   if (wg <= 0) return hipSuccess;
-  if (g2.glu_f > 0)
+  if (g2.relu2)
+    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_relu2_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
+                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
+  else if (g2.glu_f > 0)
     hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_glu_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
                        static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
   else

@@ -228,6 +228,14 @@ struct GemmArgs {
   //     (ld 2 glu_f) and C receives [gu gv] rows (ldc = 2 glu_f).
   void* aux;
   int32_t glu_f;
+  // Squared-ReLU epilogues (256x256 kernels only) when relu2 is set; aux
+  // has leading dimension glu_f (= d_ff):
+  //   forward (ld_gemm_bf16_nt_relu2_256): C receives u and aux the rows of
+  //     s = relu(u)^2 of the bf16 u;
+  //   backward (NN part of ld_gemm_bf16_tn_nn_relu2_256): the product (gs,
+  //     rounded to bf16) is not stored: aux holds the u rows and C receives
+  //     gu = gs 2 relu(u).
+  int32_t relu2;
 };
 
 // Kernel choice for one GEMM: the 256x256 MFMA kernel (optionally split
@@ -378,6 +386,8 @@ hipError_t launch_splitk_reduce(const float* part, int splits, int64_t mn, float
 // ld_gemm_bf16_nt_glu_256 over max_m rows, for bf16 with glu_f % 128 == 0
 // and N = 2 glu_f, both operands k-contiguous.
 hipError_t launch_gemm_glu_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s);
+// ld_gemm_bf16_nt_relu2_256 over max_m rows (see GemmArgs.relu2)
+hipError_t launch_gemm_relu2_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s);
 hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmPlan& p, GemmArgs g,
                             int64_t max_m, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
