@@ -19,7 +19,9 @@ layer), n_ffn = 3 (SwiGLU) or 2 (squared ReLU).
 
 --workload paper_3p9b runs the paper's own block (ALiBi attention, squared
 ReLU) at its 3.9B architecture (d 2048, 40 layers, 16 heads of 128, d_ff
-16384), same sequence length, batch and rates.
+16384), same sequence length, batch and rates.  --workload 125m and 7b run
+the 125M-shape (12 x 768, seq 1024, batch 8) and 7B-shape (32 x 4096, d_ff
+11008, seq 4096, batch 4) SwiGLU stacks with the same rates.
 
 --granularity selects the masks (Dropout Granularity section): layer_seq
 (default: one mask per layer, drawn per sequence), sublayer_seq (independent
@@ -321,7 +323,7 @@ def main():
     ap.add_argument("--p-max", type=float, default=0.2)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--workload", default="1b", choices=["1b", "paper_3p9b"])
+    ap.add_argument("--workload", default="1b", choices=["1b", "paper_3p9b", "125m", "7b"])
     ap.add_argument("--granularity", default="layer_seq", choices=list(GRANULARITIES))
     ap.add_argument("--mode", default="train", choices=["train", "infer"])
     ap.add_argument("--copy-calib-mib", type=int, default=0,
@@ -433,6 +435,12 @@ def main():
         metric = "effective tokens/s per fwd+bwd step (1B-shape stack, ILD p_max 0.2)"
         wdesc = ("1B-shape decoder stack: L=16, d_model=2048, heads=16x128, d_ff=5504 SwiGLU, "
                  "seq=2048, batch=8; ILD p_max=0.2 at the end of a 0..1000 increasing ramp")
+    elif args.workload in ("125m", "7b"):
+        name = {"125m": "125M", "7b": "7B"}[args.workload]
+        metric = f"effective tokens/s per fwd+bwd step ({name}-shape stack, ILD p_max 0.2)"
+        wdesc = (f"{name}-shape decoder stack: L={sh.n_layers}, d_model={sh.d_model}, "
+                 f"heads={sh.n_heads}x{sh.d_model // sh.n_heads}, d_ff={sh.d_ff} SwiGLU, seq={sh.seq}, "
+                 f"batch={sh.batch}; ILD p_max=0.2 at the end of a 0..1000 increasing ramp")
     else:
         metric = "effective tokens/s per fwd+bwd step (paper 3.9B-architecture stack, ILD p_max 0.2)"
         wdesc = ("paper block (ALiBi, squared ReLU) at the 3.9B architecture: L=40, d_model=2048, "

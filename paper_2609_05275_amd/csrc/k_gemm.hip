@@ -1030,11 +1030,14 @@ GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, i
   // each operand is addressed through one buffer descriptor: spans < 2 GiB
   const int64_t a_span = 2 * g.lda * (a_kcontig ? max_m : max_k);
   const int64_t b_span = 2 * g.ldb * (b_kcontig ? static_cast<int64_t>(g.N) : max_k);
-  p.big = (g.N % 4 == 0) && (g.ldc % 4 == 0) && (!g.R || g.ldr % 4 == 0) && max_m >= 512 &&
-          g.N >= 512 && big_tiles >= 32 && a_span < kBigMaxSpan && b_span < kBigMaxSpan;
+  // split-K only for float32 outputs without a residual (weight gradients);
+  // such a GEMM fills the CUs through its splits even with few tiles
+  const bool splittable = allow_split && g.c_f32 && !g.R && !g.out_map.idx && g.ldc == g.N && max_k >= 16 * GK;
+  p.big = (g.N % 4 == 0) && (g.ldc % 4 == 0) && (!g.R || g.ldr % 4 == 0) && max_m >= 512 && g.N >= 512 &&
+          (big_tiles >= 32 || (splittable && big_tiles * kMaxSplits >= 32)) && a_span < kBigMaxSpan &&
+          b_span < kBigMaxSpan;
   if (p.big) {
-    // split-K only for float32 outputs without a residual (weight gradients)
-    if (allow_split && g.c_f32 && !g.R && !g.out_map.idx && g.ldc == g.N && max_k >= 16 * GK) {
+    if (splittable) {
       double best = 0;
       for (int s = 1; s <= kMaxSplits; ++s) {
         const int64_t wg = big_tiles * s;
