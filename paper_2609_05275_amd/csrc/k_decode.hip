@@ -16,14 +16,15 @@
 // write back and invalidate the per-XCD L2 and cost far more than the
 // second launch.)
 //
-// Decode attention: one workgroup per (256-key chunk, head, sequence).
-// Scores: eight lanes per key, each holding an eighth of the head's
-// dimensions of every query row, reduced by three lane exchanges; scores in
-// base 2 with the causal cut (key <= query position) and the ALiBi bias.
-// Softmax statistics per query row over the chunk, then P V with a lane per
-// head dimension (coalesced value reads), the four waves' key ranges summed
-// in LDS.  A combine kernel merges the chunks with the usual max/sum
-// rescaling and writes bf16.
+// Decode attention: one workgroup per (256-key chunk, head, sequence), a
+// wave per 64 keys.  Scores in base 2 with the causal cut (key <= query
+// position) and the ALiBi bias: for one query row, dh/8 lanes per key, each
+// with 8 of the head's dimensions, summed by lane exchanges; for several
+// rows, S^T = K Q^T on the matrix cores (the rows padded to 32 columns).
+// Softmax statistics per query row over the chunk, then P V with dh/8 lanes
+// per key (16-byte coalesced value reads), summed over the wave's keys by
+// lane exchanges and over the four waves in LDS.  A combine kernel merges
+// the chunks with the usual max/sum rescaling and writes bf16.
 #include "ld_internal.h"
 
 namespace ld {
@@ -366,7 +367,7 @@ __global__ __launch_bounds__(256) void ld_attn_decode_bf16(DecAttnArgs a) {
   constexpr int LPK = DH / 8;    // lanes per key row
   constexpr int KPP = 64 / LPK;  // keys per pass
   constexpr int NP = 64 / KPP;   // passes per wave
-  __shared__ float sc[NQ][kDecKeys];
+  __shared__ float sc[NQ][kDecKeys + 1];  // + 1: the MFMA path's rows in different banks
   __shared__ float red[4][NQ][DH];
   const int c = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -379,59 +380,81 @@ __global__ __launch_bounds__(256) void ld_attn_decode_bf16(DecAttnArgs a) {
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
   const bf16* cache = static_cast<const bf16*>(a.cache) + static_cast<int64_t>(b) * a.s_max * row2;
 
-  // keys of this wave's 64 positions (rows past the last position read row 0)
-  bf16x8 kr[NP];
+  if constexpr (NQ == 1) {
+    // one query row: each lane's 8 dimensions of a key, dot products summed
+    // over the key's lanes (keys of rows past the last position read row 0)
+    bf16x8 kr[NP];
 #pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const int kk = k0 + p * KPP + kg;
-    kr[p] = load8(cache + static_cast<int64_t>(kk < nk ? kk : 0) * row2 + h * DH + sl * 8);
-  }
-  // scores in base 2 (causal cut at each row's position, ALiBi bias), in
-  // groups of at most four rows to bound the registers held
-  // (the group loop stays rolled: unrolled, the key conversions to float
-  // would be shared across groups and held in registers)
-  constexpr int JG = NQ < 4 ? NQ : 4;
-#pragma unroll 1
-  for (int j0 = 0; j0 < NQ; j0 += JG) {
-    float q[JG][8];
+    for (int p = 0; p < NP; ++p) {
+      const int kk = k0 + p * KPP + kg;
+      kr[p] = load8(cache + static_cast<int64_t>(kk < nk ? kk : 0) * row2 + h * DH + sl * 8);
+    }
+    float q[8];
+    {
+      const bf16x8 v = load8(qkv + static_cast<int64_t>(b) * a.ld_qkv + h * DH + sl * 8);
 #pragma unroll
-    for (int j = 0; j < JG; ++j) {
-      const bool jv = j0 + j < a.n_new;
-      const bf16x8 v = jv ? load8(qkv + (static_cast<int64_t>(b) * a.n_new + j0 + j) * a.ld_qkv + h * DH +
-                                  sl * 8)
-                          : zero8();
-#pragma unroll
-      for (int e = 0; e < 8; ++e) q[j][e] = static_cast<float>(v[e]) * (a.scale * kLog2e);
+      for (int e = 0; e < 8; ++e) q[e] = static_cast<float>(v[e]) * (a.scale * kLog2e);
     }
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       const int kl = wave * 64 + p * KPP + kg;
       const int kk = k0 + p * KPP + kg;
+      float s = 0.f;
 #pragma unroll
-      for (int j = 0; j < JG; ++j) {
-        float s = 0.f;
+      for (int e = 0; e < 8; ++e) s = __builtin_fmaf(q[e], static_cast<float>(kr[p][e]), s);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s = __builtin_fmaf(q[j][e], static_cast<float>(kr[p][e]), s);
+      for (int o = LPK / 2; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+      if (sl == 0) sc[0][kl] = (kk < nk && kk <= a.pos) ? s - al2 * static_cast<float>(a.pos - kk) : -INFINITY;
+    }
+  } else {
+    // several query rows: S^T = K Q^T on the matrix cores, the wave's 64 keys
+    // in two 32-key blocks (A operand: lane l holds key l % 32, dimensions
+    // 16 ks + 8 (l / 32) .. +7), the query rows as the 32 columns (B operand;
+    // rows past n_new are zero).  Lane l, register v of block kb then holds
+    // key 32 kb + 8 (v / 4) + 4 (l / 32) + v % 4 of query row l % 32.
+    const int ql = lane & 31, hf = lane >> 5;
+    bf16x8 qf[DH / 16], kf[2][DH / 16];
 #pragma unroll
-        for (int o = LPK / 2; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
-        const int qpos = a.pos + j0 + j;
-        if (sl == 0 && j0 + j < a.n_new)
-          sc[j0 + j][kl] = (kk < nk && kk <= qpos) ? s - al2 * static_cast<float>(qpos - kk) : -INFINITY;
-      }
+    for (int ks = 0; ks < DH / 16; ++ks)
+      qf[ks] = ql < a.n_new ? load8(qkv + (static_cast<int64_t>(b) * a.n_new + ql) * a.ld_qkv + h * DH + 16 * ks + 8 * hf)
+                            : zero8();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int kk = k0 + kb * 32 + ql;
+      const bf16* kp = cache + static_cast<int64_t>(kk < nk ? kk : 0) * row2 + h * DH + 8 * hf;
+#pragma unroll
+      for (int ks = 0; ks < DH / 16; ++ks) kf[kb][ks] = load8(kp + 16 * ks);
+    }
+    floatx16 acc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[kb][v] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < DH / 16; ++ks)
+        acc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb][ks], qf[ks], acc[kb], 0, 0, 0);
+    }
+    if (ql < a.n_new) {
+      const int qpos = a.pos + ql;
+      const float sl2 = a.scale * kLog2e;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int kl = 32 * kb + 8 * (v >> 2) + 4 * hf + (v & 3);
+          const int kk = k0 + kl;
+          sc[ql][wave * 64 + kl] =
+              (kk < nk && kk <= qpos) ? acc[kb][v] * sl2 - al2 * static_cast<float>(qpos - kk) : -INFINITY;
+        }
     }
   }
-  // values of the same positions; with few rows they are in flight during
-  // the softmax, with more rows they are loaded after it (registers)
-  constexpr bool kEarlyV = NQ <= 4;
+  // values of the same positions, in flight during the softmax
   bf16x8 vr[NP];
-  auto load_v = [&]() {
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const int kk = k0 + p * KPP + kg;
-      vr[p] = load8(cache + static_cast<int64_t>(kk < nk ? kk : 0) * row2 + d + h * DH + sl * 8);
-    }
-  };
-  if constexpr (kEarlyV) load_v();
+  for (int p = 0; p < NP; ++p) {
+    const int kk = k0 + p * KPP + kg;
+    vr[p] = load8(cache + static_cast<int64_t>(kk < nk ? kk : 0) * row2 + d + h * DH + sl * 8);
+  }
   __syncthreads();
 
   // per query row: chunk maximum, probabilities, sum
@@ -456,10 +479,10 @@ __global__ __launch_bounds__(256) void ld_attn_decode_bf16(DecAttnArgs a) {
   }
   __syncthreads();
 
-  if constexpr (!kEarlyV) load_v();
   // P V in groups of at most four rows: each lane its key's 8 dimensions,
   // then a sum over the wave's key groups (lane exchanges) and over the four
   // waves (LDS, in wave order)
+  constexpr int JG = NQ < 4 ? NQ : 4;
 #pragma unroll 1
   for (int j0 = 0; j0 < NQ; j0 += JG) {
     float o[JG][8];
