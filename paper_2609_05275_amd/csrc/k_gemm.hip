@@ -987,9 +987,7 @@ LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_relu2_256(GemmArgs g1, GemmArgs g2, int til
 // C[i] = sum over splits of part[s][i], float32, in split order.  Every
 // split's value is requested before the first add (splits <= kMaxSplits).
 constexpr int kMaxSplits = 8;
-__global__ __launch_bounds__(256) void ld_splitk_reduce(const float* part, int splits, int64_t mn,
-                                                        const int32_t* dev_m_unused, float* C) {
-  (void)dev_m_unused;
+__global__ __launch_bounds__(256) void ld_splitk_reduce(const float* part, int splits, int64_t mn, float* C) {
   for (int64_t i4 = blockIdx.x * 256ll + threadIdx.x; i4 < mn / 4; i4 += gridDim.x * 256ll) {
     float4 t[kMaxSplits];
 #pragma unroll
@@ -1005,14 +1003,18 @@ __global__ __launch_bounds__(256) void ld_splitk_reduce(const float* part, int s
   }
 }
 
-bool g_attr_done = false;
-
+// Dynamic LDS limit of the 128x128 kernels, raised once per process (a
+// function-local static: its initialisation is thread-safe).
 void set_attrs() {
-  if (g_attr_done) return;
-  const void* small[] = {reinterpret_cast<const void*>(ld_gemm_bf16_nt), reinterpret_cast<const void*>(ld_gemm_bf16_nn),
-                         reinterpret_cast<const void*>(ld_gemm_bf16_tn), reinterpret_cast<const void*>(ld_gemm_bf16_tt)};
-  for (const void* f : small) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
-  g_attr_done = true;
+  static const bool done = [] {
+    const void* small[] = {reinterpret_cast<const void*>(ld_gemm_bf16_nt),
+                           reinterpret_cast<const void*>(ld_gemm_bf16_nn),
+                           reinterpret_cast<const void*>(ld_gemm_bf16_tn),
+                           reinterpret_cast<const void*>(ld_gemm_bf16_tt)};
+    for (const void* f : small) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+    return true;
+  }();
+  (void)done;
 }
 
 }  // namespace
@@ -1100,8 +1102,7 @@ hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmP
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t mn = static_cast<int64_t>(g.M) * g.N;
     int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 1 << 20));
-    hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, g.part, p.splits, mn,
-                       nullptr, C);
+    hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, g.part, p.splits, mn, C);
     return hipGetLastError();
   }
   return launch_gemm(dtype, a_kcontig, b_kcontig, g, max_m, 0, s);
@@ -1206,7 +1207,7 @@ hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, 
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t mn, float* C, hipStream_t s) {
   if (splits <= 1 || mn <= 0) return hipSuccess;
   const int blocks = static_cast<int>(std::min<int64_t>((mn / 4 + 255) / 256, 1 << 20));
-  hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, splits, mn, nullptr, C);
+  hipLaunchKernelGGL(ld_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, splits, mn, C);
   return hipGetLastError();
 }
 
