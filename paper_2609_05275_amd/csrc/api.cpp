@@ -1039,6 +1039,13 @@ size_t skinny_part_bytes(int64_t M, int64_t N, int64_t K) {
   return ks > 1 ? static_cast<size_t>(ks) * M * N * 4 : 0;
 }
 
+// Partials of a skinny GEMM whose reduction is fused with what follows it
+// (written even with one split).
+size_t skinny_fused_part_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M > kSkinnyMaxM) return 0;
+  return static_cast<size_t>(skinny_ksplit(M, N, K)) * M * N * 4;
+}
+
 
 int64_t dec_chunks(int64_t keys) { return (keys + kDecKeys - 1) / kDecKeys; }
 
@@ -1062,7 +1069,7 @@ DecLayout dec_layout(const Dims& D, int64_t n_new, int64_t s_max) {
   L.part_o = take(4 * pc * D.dh);
   L.part_ml = take(4 * pc * 2);
   const int64_t shapes[4][2] = {{3 * D.d, D.d}, {D.d, D.d}, {D.fw, D.d}, {D.d, D.f}};
-  for (const auto& sh : shapes) L.skp_bytes = std::max(L.skp_bytes, skinny_part_bytes(M, sh[0], sh[1]));
+  for (const auto& sh : shapes) L.skp_bytes = std::max(L.skp_bytes, skinny_fused_part_bytes(M, sh[0], sh[1]));
   L.skp = take(L.skp_bytes);
   L.total = o;
   return L;
@@ -1164,6 +1171,30 @@ int dec_proj(const void* A, int64_t lda, const void* g, float eps, const void* W
   if (e != hipSuccess) return fail(LD_E_HIP, "decode projection: %s", hipGetErrorString(e));
   const double wrows = act == kDecActSwiglu ? 2.0 * N : static_cast<double>(N);
   ps.end(2.0 * M * wrows * K, 2.0 * (M * K + wrows * K + M * N) + (R ? 2.0 * M * N : 0.0));
+  return LD_OK;
+}
+
+// Skinny GEMM (at most 64 rows) writing only its split-K partials, for a
+// fused reduction launched next; g and ks describe them.
+int skinny_part(const void* A, int64_t lda, const void* W, int64_t ldw, int64_t M, int64_t N, int64_t K,
+                float alpha, float* part, size_t part_bytes, hipStream_t s, SkinnyArgs& g, int& ks) {
+  g = SkinnyArgs{};
+  g.A = A;
+  g.lda = lda;
+  g.W = W;
+  g.ldw = ldw;
+  g.M = static_cast<int32_t>(M);
+  g.N = static_cast<int32_t>(N);
+  g.K = static_cast<int32_t>(K);
+  g.alpha = alpha;
+  g.part = part;
+  g.part_only = 1;
+  ks = skinny_ksplit(M, N, K);
+  if (static_cast<size_t>(ks) * M * N * 4 > part_bytes) return fail(LD_E_WORKSPACE, "skinny GEMM scratch too small");
+  ProfScope ps(M <= 32 ? "ld_gemm_bf16_skinny<1>" : "ld_gemm_bf16_skinny<2>", s);
+  const hipError_t e = launch_gemm_skinny(g, ks, s);
+  if (e != hipSuccess) return fail(LD_E_HIP, "skinny GEMM: %s", hipGetErrorString(e));
+  ps.end(2.0 * M * N * K, 2.0 * (M * K + N * K) + 4.0 * ks * M * N);
   return LD_OK;
 }
 
@@ -1483,6 +1514,11 @@ int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w,
   // projection is one fused launch that normalises its input rows and
   // applies the FFN activation itself.
   const bool fused = dec_gemm_ok(M, d, true) && dec_gemm_ok(M, D.f, false);
+  // 9 to 64 rows (verify steps): split-K skinny GEMMs whose partial sums are
+  // reduced together with what follows them: the residual and the next
+  // RMSNorm (output and down projections), or the FFN activation.
+  const bool part_fused = !fused && M <= kSkinnyMaxM;
+  bool h_ready = false;  // L.h holds RMSNorm(x) with this layer's gain
   const int act = D.kind == LD_BLOCK_SWIGLU ? kDecActSwiglu : kDecActRelu2;
   for (int32_t l = 0; l < n_layers; ++l) {
     if (active && !active[l]) continue;
@@ -1497,7 +1533,9 @@ int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w,
         return rc;
       kv_done = true;
     } else {
-      if (int rc = norm(x, wl.g_attn)) return rc;
+      if (!h_ready)
+        if (int rc = norm(x, wl.g_attn)) return rc;
+      h_ready = false;
       if (int rc = dec_gemm(P(L.h), d, wl.w_qkv, d, P(L.qkv), 3 * d, nullptr, 0, M, 3 * d, d, 1.f, skp,
                             L.skp_bytes, s, &ko, &kv_done))
         return rc;
@@ -1550,6 +1588,35 @@ int ld_stack_decode(const ld_config* cfg, int32_t n_layers, const ld_weights* w,
       if (int rc = dec_proj(P(L.s), D.f, nullptr, 0.f, wl.w_down, D.f, x, d, P(L.z), d, M, d, D.f, r,
                             kDecActNone, s))
         return rc;
+      continue;
+    }
+    if (part_fused) {
+      SkinnyArgs g{};
+      int ks = 1;
+      // z = x + r (att W_o^T) and h = RMSNorm(z)
+      if (int rc = skinny_part(P(L.att), d, wl.w_o, d, M, d, d, r, skp, L.skp_bytes, s, g, ks)) return rc;
+      g.C = P(L.z);
+      g.ldc = d;
+      g.R = x;
+      g.ldr = d;
+      if ((e = launch_skinny_reduce_norm(g, ks, wl.g_mlp, cfg->rms_eps, P(L.h), s)) != hipSuccess)
+        return fail(LD_E_HIP, "skinny reduce: %s", hipGetErrorString(e));
+      // s = act(h W_gate_up^T)
+      if (int rc = skinny_part(P(L.h), d, wl.w_gate_up, d, M, D.fw, d, 1.f, skp, L.skp_bytes, s, g, ks)) return rc;
+      if ((e = launch_skinny_reduce_act(g, ks, act, static_cast<int>(D.f), P(L.s), s)) != hipSuccess)
+        return fail(LD_E_HIP, "skinny reduce: %s", hipGetErrorString(e));
+      // x = z + r (s W_down^T), and the next active layer's h = RMSNorm(x)
+      if (int rc = skinny_part(P(L.s), D.f, wl.w_down, D.f, M, d, D.f, r, skp, L.skp_bytes, s, g, ks)) return rc;
+      g.C = x;
+      g.ldc = d;
+      g.R = P(L.z);
+      g.ldr = d;
+      int32_t next = l + 1;
+      while (next < n_layers && active && !active[next]) ++next;
+      const void* gain = next < n_layers ? w[next].g_attn : nullptr;
+      if ((e = launch_skinny_reduce_norm(g, ks, gain, cfg->rms_eps, P(L.h), s)) != hipSuccess)
+        return fail(LD_E_HIP, "skinny reduce: %s", hipGetErrorString(e));
+      h_ready = gain != nullptr;
       continue;
     }
     if (int rc = dec_gemm(P(L.att), d, wl.w_o, d, P(L.z), d, x, d, M, d, d, r, skp, L.skp_bytes, s))

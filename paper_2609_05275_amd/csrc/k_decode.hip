@@ -122,7 +122,7 @@ __global__ __launch_bounds__(256) void ld_gemm_bf16_skinny(SkinnyArgs g) {
     const int m = mb * 32 + 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
     const int n = n0 + (l & 31);
     if (m < g.M && n < g.N) {
-      if (gridDim.y > 1)
+      if (gridDim.y > 1 || g.part_only)
         g.part[(static_cast<int64_t>(blockIdx.y) * g.M + m) * g.N + n] = sum;
       else
         skinny_store(g, m, n, sum);
@@ -136,6 +136,83 @@ __global__ __launch_bounds__(256) void ld_skinny_reduce_k(SkinnyArgs g, int kspl
     float sum = g.part[i];
     for (int s = 1; s < ksplit; ++s) sum += g.part[s * total + i];
     skinny_store(g, static_cast<int>(i / g.N), static_cast<int>(i % g.N), sum);
+  }
+}
+
+__device__ __forceinline__ float bf16r(float x) { return static_cast<float>(static_cast<bf16>(x)); }
+
+// Split-K sums (split order) of one row of a skinny GEMM with alpha and the
+// residual, stored as C, then (when a gain is given) the RMSNorm of the
+// stored row (sum of squares over the workgroup in a fixed order):
+// h = bf16(C rstd gain).  One workgroup of 1024 threads per row.
+__global__ __launch_bounds__(1024) void ld_skinny_reduce_norm_k(SkinnyArgs g, int ksplit, const bf16* gain,
+                                                                 float eps, bf16* h) {
+  constexpr int kPer = 4;  // columns per thread and pass: one pass up to 4096 columns
+  __shared__ float wsum[16];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  const int64_t mn = static_cast<int64_t>(g.M) * g.N;
+  const float* prow = g.part + static_cast<int64_t>(m) * g.N;
+  bf16* C = static_cast<bf16*>(g.C) + static_cast<int64_t>(m) * g.ldc;
+  const bf16* R = g.R ? static_cast<const bf16*>(g.R) + static_cast<int64_t>(m) * g.ldr : nullptr;
+  float ss = 0.f;
+  for (int n0 = 0; n0 < g.N; n0 += 1024 * kPer) {
+    float sum[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) sum[i] = 0.f;
+    // the splits in order; every column's loads of a split are independent
+#pragma unroll 2
+    for (int sp = 0; sp < ksplit; ++sp)
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const int n = n0 + i * 1024 + tid;
+        if (n < g.N) sum[i] += prow[sp * mn + n];
+      }
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int n = n0 + i * 1024 + tid;
+      if (n < g.N) {
+        const bf16 o = static_cast<bf16>(g.alpha * sum[i] + (R ? static_cast<float>(R[n]) : 0.f));
+        C[n] = o;
+        const float of = static_cast<float>(o);
+        ss = __builtin_fmaf(of, of, ss);
+      }
+    }
+  }
+  if (!gain) return;  // no norm follows (workgroup-uniform)
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off, 64);
+  if ((tid & 63) == 0) wsum[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) tot += wsum[w];
+  const float rstd = rsqrtf(tot / static_cast<float>(g.N) + eps);
+  bf16* hr = h + static_cast<int64_t>(m) * g.N;
+  for (int n = tid; n < g.N; n += 1024)  // this thread's own stores, read back
+    hr[n] = static_cast<bf16>(static_cast<float>(C[n]) * rstd * static_cast<float>(gain[n]));
+}
+
+// The FFN activation from a skinny GEMM's partials: u (and v = column f + n
+// for SwiGLU) rounded to bf16 as stored outputs would be, s = act(u, v).
+__global__ __launch_bounds__(256) void ld_skinny_reduce_act_k(SkinnyArgs g, int ksplit, int act, int f, bf16* so) {
+  const int64_t mn = static_cast<int64_t>(g.M) * g.N, total = static_cast<int64_t>(g.M) * f;
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < total; i += gridDim.x * 256ll) {
+    const int64_t m = i / f, n = i % f, iu = m * g.N + n;
+    float su = g.part[iu];
+#pragma unroll 4
+    for (int sp = 1; sp < ksplit; ++sp) su += g.part[sp * mn + iu];
+    const float u = bf16r(g.alpha * su);
+    float out;
+    if (act == kDecActSwiglu) {
+      float sv = g.part[iu + f];
+#pragma unroll 4
+      for (int sp = 1; sp < ksplit; ++sp) sv += g.part[sp * mn + iu + f];
+      out = swiglu_fwd_f(u, bf16r(g.alpha * sv));
+    } else {
+      const float z = fmaxf(u, 0.f);
+      out = z * z;
+    }
+    so[m * f + n] = static_cast<bf16>(out);
   }
 }
 
@@ -165,8 +242,6 @@ constexpr int kDecU = 4;      // chunks per pass
 constexpr int kDecCus = 256;  // compute units
 
 __host__ __device__ inline int dec_pitch(int64_t K) { return static_cast<int>((K + 63) & ~63ll); }
-
-__device__ __forceinline__ float bf16r(float x) { return static_cast<float>(static_cast<bf16>(x)); }
 
 __device__ __forceinline__ float dot8(const bf16x8& w, const bf16x8& a, float c) {
 #pragma unroll
@@ -578,7 +653,7 @@ hipError_t launch_gemm_skinny(const SkinnyArgs& g, int ksplit, hipStream_t s) {
   else
     hipLaunchKernelGGL(ld_gemm_bf16_skinny<2>, grid, dim3(256), 0, s, g);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || ksplit == 1) return e;
+  if (e != hipSuccess || ksplit == 1 || g.part_only) return e;
   hipLaunchKernelGGL(ld_skinny_reduce_k, dim3(grid_for(static_cast<int64_t>(g.M) * g.N)), dim3(256), 0,
                      s, g, ksplit);
   return hipGetLastError();
@@ -617,6 +692,21 @@ hipError_t launch_gemm_dec(const SkinnyArgs& g, hipStream_t s) {
   if (g.act == kDecActRelu2)
     return tiles <= kDecCus ? gemm_dec_t<16, kDecActRelu2>(g, tiles, s) : gemm_dec_t<4, kDecActRelu2>(g, tiles, s);
   return tiles <= kDecCus ? gemm_dec_t<16, kDecActNone>(g, tiles, s) : gemm_dec_t<4, kDecActNone>(g, tiles, s);
+}
+
+hipError_t launch_skinny_reduce_norm(const SkinnyArgs& g, int ksplit, const void* gain, float eps, void* h,
+                                     hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  hipLaunchKernelGGL(ld_skinny_reduce_norm_k, dim3(g.M), dim3(1024), 0, s, g, ksplit, static_cast<const bf16*>(gain),
+                     eps, static_cast<bf16*>(h));
+  return hipGetLastError();
+}
+
+hipError_t launch_skinny_reduce_act(const SkinnyArgs& g, int ksplit, int act, int f, void* s_out, hipStream_t s) {
+  if (g.M <= 0 || f <= 0) return hipSuccess;
+  hipLaunchKernelGGL(ld_skinny_reduce_act_k, dim3(grid_for(static_cast<int64_t>(g.M) * f)), dim3(256), 0, s, g,
+                     ksplit, act, f, static_cast<bf16*>(s_out));
+  return hipGetLastError();
 }
 
 hipError_t launch_kv_store(const KvArgs& a, hipStream_t s) {

@@ -270,7 +270,8 @@ struct SkinnyArgs {
   int64_t lda, ldw, ldc, ldr;
   int32_t M, N, K;
   float alpha;
-  float* part;        // float32 [ksplit][M][N] when ksplit > 1
+  float* part;        // float32 [ksplit][M][N] when ksplit > 1 or part_only
+  int32_t part_only;  // write the partials even with ksplit == 1 (a fused reduction follows)
   // optional: columns kv_d.. of row m also go to the cache kv [*, s_max, 2 kv_d]
   // at position kv_pos + m % kv_n of sequence m / kv_n (the keys/values of a
   // qkv projection)
@@ -345,6 +346,13 @@ hipError_t launch_masks(const MaskArgs& a, hipStream_t s);
 hipError_t launch_zero_f32(const ZeroArgs& a, hipStream_t s);
 int skinny_ksplit(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_skinny(const SkinnyArgs& g, int ksplit, hipStream_t s);
+// Fused reductions of a skinny GEMM's partials (g.part_only launches):
+// C = bf16(alpha sum + R) and h = RMSNorm(C rows) with gain `gain`; or the
+// FFN activation s = act(bf16(alpha sum)) of f columns (SwiGLU pairs
+// columns n and f + n).
+hipError_t launch_skinny_reduce_norm(const SkinnyArgs& g, int ksplit, const void* gain, float eps, void* h,
+                                     hipStream_t s);
+hipError_t launch_skinny_reduce_act(const SkinnyArgs& g, int ksplit, int act, int f, void* s_out, hipStream_t s);
 hipError_t launch_kv_store(const KvArgs& a, hipStream_t s);
 hipError_t launch_attn_decode(const DecAttnArgs& a, hipStream_t s);
 hipError_t launch_gather(int dtype, const RowsArgs& a, hipStream_t s);
