@@ -264,6 +264,18 @@ def test_decode_draft_and_verify(sh):
     _decode_case(sh, steps, s_max=192)
 
 
+@pytest.mark.parametrize("sh", BF16_SHAPES, ids=BF16_IDS)
+def test_decode_draft_several_rows(sh):
+    """Draft steps of 2 and 3 rows per sequence (9 to 64 rows in all: the
+    reductions that carry the next active layer's RMSNorm skip the inactive
+    layers, and the last active layer's carries none)."""
+    L = sh.n_layers
+    draft = [1 if l % 2 == 0 else 0 for l in range(L)]
+    late = [0] * (L - 1) + [1]
+    steps = [(2, None), (2, draft), (3, draft), (3, late), (2, None)]
+    _decode_case(sh, steps, s_max=192)
+
+
 @pytest.mark.parametrize("sh", [SMALL_BF16, SMALL_P_128], ids=["small_bf16", "paper_small_dh128_h6"])
 def test_decode_across_key_chunks(sh):
     """Decoding steps of 8 from position 64 to past 256 (the attention's key
