@@ -180,7 +180,7 @@ def cpu_baseline(sh, target_s=15.0):
 
 
 # HBM-bound kernels of the step, with the algorithmic bytes each launch moves
-# (the library's profiling hook records them per launch; see DESIGN.md).
+# (the library's profiling hook records them per launch).
 HBM_KERNELS = ["ld_mask_compact", "ld_rmsnorm_fwd_k", "ld_rmsnorm_bwd_k", "ld_gather_rows_k",
                "ld_attn_delta", "ld_splitk_reduce"]
 
@@ -333,8 +333,8 @@ def main():
                          "variant is measured in a short pass and the slowest total is used)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU; this build has no multi-GPU path "
-              "(the data-parallel sharding is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (use --gpus 1)",
+              file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calib_mib > 0:

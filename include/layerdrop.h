@@ -52,7 +52,7 @@ typedef enum {
   LD_OK = 0,
   LD_E_INVALID = 1,     /* bad argument value (NULL pointer, p outside [0,1], NaN) */
   LD_E_SHAPE = 2,       /* inconsistent or unsupported shape                        */
-  LD_E_UNSUPPORTED = 3, /* valid request this build does not implement              */
+  LD_E_UNSUPPORTED = 3, /* valid request the library does not implement             */
   LD_E_WORKSPACE = 4,   /* workspace smaller than the matching *_bytes query       */
   LD_E_HIP = 5          /* a HIP runtime call failed                                */
 } ld_status;

@@ -7,7 +7,7 @@ Test infrastructure (see the package docstring).
 
 The paper being implemented says only that the layer mask is Bernoulli per
 sequence (Preliminary section, layer-dropout training equation); the generator
-is this build's reading: one Philox4x64-10 block per (sample, layer, step)
+is a reading of it: one Philox4x64-10 block per (sample, layer, step)
 counter under a (seed, 0) key, word 0 of the output used for the draw.
 
 One round maps (c0, c1, c2, c3) under key (k0, k1) to
