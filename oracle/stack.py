@@ -91,7 +91,7 @@ def layer_backward(ctx, G, cfg):
     """G = dL/dH^{l+1} [B, S, d] -> (dL/dH^l, grads summed over kept samples)."""
     G = np.asarray(G, dtype=np.float64)
     G_prev = G.copy()
-    grads = {k: np.zeros_like(v) for k, v in ctx["w"].items()}
+    grads = {k: np.zeros(v.shape) for k, v in ctx["w"].items()}
     for b in sorted(set(ctx["cache_a"]) | set(ctx["cache_f"])):
         g = G[b]
         if b in ctx["cache_f"]:
