@@ -125,12 +125,63 @@ def _check(status):
         raise LdError(status, last_error())
 
 
-def _ptr(t):
+def _ptr(t, name="tensor", inner=False):
+    """Device address of t.  A torch tensor must live on the GPU and be
+    contiguous (with inner=True, for calls that take a leading dimension,
+    only its last dimension must be); anything else -- a raw address (int) or
+    an object with data_ptr() -- is passed through for the library to check."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if isinstance(t, torch.Tensor):
+        if not t.is_cuda:
+            raise ValueError(f"{name}: a device tensor is required, got one on {t.device}")
+        if inner:
+            if t.dim() and t.stride(-1) != 1 and t.numel() > 1:
+                raise ValueError(f"{name}: the last dimension must be contiguous")
+        elif not t.is_contiguous():
+            raise ValueError(f"{name}: a contiguous tensor is required")
     return t.data_ptr()
+
+
+_TORCH_OF = {LD_F32: torch.float32, LD_BF16: torch.bfloat16}
+
+
+def _need(t, name, dtype=None, numel=None, min_bytes=None):
+    """Checks a torch tensor argument against what the call reads or writes
+    (dtype, element count, byte size) before anything is launched; other
+    objects pass through to the library's own checks."""
+    if not isinstance(t, torch.Tensor):
+        return
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name}: {t.numel()} elements, expected {numel}")
+    if min_bytes is not None and t.numel() * t.element_size() < min_bytes:
+        raise ValueError(f"{name}: {t.numel() * t.element_size()} bytes, at least {min_bytes} needed")
+
+
+def _n_masks(cfg):
+    return 2 if cfg.granularity & LD_GRAN_SUBLAYER_SEQ else 1
+
+
+def _weight_numel(cfg):
+    d, f = cfg.d_model, cfg.d_ff
+    return dict(g_attn=d, w_qkv=3 * d * d, w_o=d * d, g_mlp=d,
+                w_gate_up=(2 if cfg.block_kind == 0 else 1) * f * d, w_down=d * f)
+
+
+def _check_layer_tensors(cfg, w=None, dw=None, acts=()):
+    dt = _TORCH_OF.get(cfg.dtype)
+    n = _weight_numel(cfg)
+    for k in WEIGHT_KEYS:
+        if w is not None:
+            _need(w[k], k, dt, n[k])
+        if dw is not None:
+            _need(dw[k], "grad " + k, torch.float32, n[k])
+    for name, t in acts:
+        _need(t, name, dt, cfg.batch * cfg.seq * cfg.d_model)
 
 
 def _stream(stream):
@@ -157,11 +208,11 @@ def config(batch, seq, d_model, n_heads, d_ff, dtype=LD_BF16, rms_eps=1e-5, resc
 
 def weights(w):
     """ld_weights from a dict of device tensors keyed by WEIGHT_KEYS."""
-    return ld_weights(*[_ptr(w[k]) for k in WEIGHT_KEYS])
+    return ld_weights(*[_ptr(w[k], k) for k in WEIGHT_KEYS])
 
 
 def grads(g):
-    return ld_grads(*[_ptr(g[k]) for k in WEIGHT_KEYS])
+    return ld_grads(*[_ptr(g[k], "grad " + k) for k in WEIGHT_KEYS])
 
 
 # ------------------------------------------------------------------ entry points
@@ -175,25 +226,41 @@ def ld_schedule_p(dist, sched, p_max, layer, n_layers, t, n_steps):
 def ld_masks(p, seed, step, keep, idx, count, first_layer=0, stream=None):
     n = len(p)
     arr = (C.c_float * n)(*[float(v) for v in p])
-    _check(_lib.ld_masks(n, keep.shape[-1], arr, first_layer, seed, step, _ptr(keep), _ptr(idx),
-                         _ptr(count), _stream(stream)))
+    B = keep.shape[-1]
+    _need(keep, "keep", torch.uint8, n * B)
+    _need(idx, "idx", torch.int32, n * B)
+    _need(count, "count", torch.int32, n)
+    _check(_lib.ld_masks(n, B, arr, first_layer, seed, step, _ptr(keep, "keep"), _ptr(idx, "idx"),
+                         _ptr(count, "count"), _stream(stream)))
 
 
 def ld_masks_granular(granularity, p, seed, step, keep, idx, count, first_layer=0, stream=None):
     n = len(p)
     arr = (C.c_float * n)(*[float(v) for v in p])
-    _check(_lib.ld_masks_granular(granularity, n, keep.shape[-1], arr, first_layer, seed, step,
-                                  _ptr(keep), _ptr(idx), _ptr(count), _stream(stream)))
+    B = keep.shape[-1]
+    nm = 2 if granularity in (LD_GRAN_SUBLAYER_SEQ, LD_GRAN_SUBLAYER_BATCH) else 1
+    _need(keep, "keep", torch.uint8, n * nm * B)
+    _need(idx, "idx", torch.int32, n * nm * B)
+    _need(count, "count", torch.int32, n * nm)
+    _check(_lib.ld_masks_granular(granularity, n, B, arr, first_layer, seed, step,
+                                  _ptr(keep, "keep"), _ptr(idx, "idx"), _ptr(count, "count"),
+                                  _stream(stream)))
 
 
 def ld_gather_rows(cfg, idx, count, x, xk, stream=None):
-    _check(_lib.ld_gather_rows(C.byref(cfg), _ptr(idx), _ptr(count), _ptr(x), _ptr(xk),
-                               _stream(stream)))
+    _need(idx, "idx", torch.int32, cfg.batch)
+    _need(count, "count", torch.int32, 1)
+    _check_layer_tensors(cfg, acts=(("x", x), ("xk", xk)))
+    _check(_lib.ld_gather_rows(C.byref(cfg), _ptr(idx, "idx"), _ptr(count, "count"), _ptr(x, "x"),
+                               _ptr(xk, "xk"), _stream(stream)))
 
 
 def ld_scatter_add_rows(cfg, idx, count, r, yk, x, stream=None):
-    _check(_lib.ld_scatter_add_rows(C.byref(cfg), _ptr(idx), _ptr(count), r, _ptr(yk), _ptr(x),
-                                    _stream(stream)))
+    _need(idx, "idx", torch.int32, cfg.batch)
+    _need(count, "count", torch.int32, 1)
+    _check_layer_tensors(cfg, acts=(("yk", yk), ("x", x)))
+    _check(_lib.ld_scatter_add_rows(C.byref(cfg), _ptr(idx, "idx"), _ptr(count, "count"), r,
+                                    _ptr(yk, "yk"), _ptr(x, "x"), _stream(stream)))
 
 
 def ld_layer_ctx_bytes(cfg):
@@ -209,6 +276,9 @@ def ld_stack_ws_bytes(cfg, n_layers):
 
 
 def ld_layer_fwd(cfg, w, layer, p, seed, step, x, ctx, ws=None, keep_override=None, stream=None):
+    _check_layer_tensors(cfg, w=w, acts=(("x", x),))
+    _need(ctx, "ctx", min_bytes=ld_layer_ctx_bytes(cfg))
+    _need(keep_override, "keep_override", torch.uint8, _n_masks(cfg) * cfg.batch)
     wb = weights(w)
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(_lib.ld_layer_fwd(C.byref(cfg), C.byref(wb), layer, p, seed, step, _ptr(x), _ptr(ctx),
@@ -216,6 +286,8 @@ def ld_layer_fwd(cfg, w, layer, p, seed, step, x, ctx, ws=None, keep_override=No
 
 
 def ld_layer_bwd(cfg, w, ctx, dx, dw, ws, stream=None):
+    _check_layer_tensors(cfg, w=w, dw=dw, acts=(("dx", dx),))
+    _need(ctx, "ctx", min_bytes=ld_layer_ctx_bytes(cfg))
     wb, gb = weights(w), grads(dw)
     _check(_lib.ld_layer_bwd(C.byref(cfg), C.byref(wb), _ptr(ctx), _ptr(dx), C.byref(gb),
                              _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
@@ -224,6 +296,16 @@ def ld_layer_bwd(cfg, w, ctx, dx, dw, ws, stream=None):
 def ld_stack_step(cfg, ws_list, p, seed, step, x, dx, dw_list, ws, keep_override=None,
                   keep_out=None, idx_out=None, count_out=None, stream=None):
     L = len(ws_list)
+    if len(dw_list) != L or len(p) != L:
+        raise ValueError(f"{L} layers of weights, {len(dw_list)} of gradients, {len(p)} rates")
+    for l in range(L):
+        _check_layer_tensors(cfg, w=ws_list[l], dw=dw_list[l])
+    _check_layer_tensors(cfg, acts=(("x", x), ("dx", dx)))
+    nmb = L * _n_masks(cfg) * cfg.batch
+    _need(keep_override, "keep_override", torch.uint8, nmb)
+    _need(keep_out, "keep_out", torch.uint8, nmb)
+    _need(idx_out, "idx_out", torch.int32, nmb)
+    _need(count_out, "count_out", torch.int32, L * _n_masks(cfg))
     wa = (ld_weights * L)(*[weights(w) for w in ws_list])
     ga = (ld_grads * L)(*[grads(g) for g in dw_list])
     pa = (C.c_float * L)(*[float(v) for v in p])
@@ -286,10 +368,11 @@ def ld_gemm_skinny_ws_bytes(M, N, K):
 def ld_gemm_skinny(A, W, C_out, alpha=1.0, R=None, ws=None, stream=None):
     M, K = A.shape
     N = W.shape[0]
-    _check(_lib.ld_gemm_skinny(M, N, K, _ptr(A), A.stride(0), _ptr(W), W.stride(0), _ptr(C_out),
-                               C_out.stride(0), alpha, _ptr(R), 0 if R is None else R.stride(0),
-                               _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
-                               _stream(stream)))
+    _check(_lib.ld_gemm_skinny(M, N, K, _ptr(A, "A", inner=True), A.stride(0),
+                               _ptr(W, "W", inner=True), W.stride(0), _ptr(C_out, "C_out", inner=True),
+                               C_out.stride(0), alpha, _ptr(R, "R", inner=True),
+                               0 if R is None else R.stride(0), _ptr(ws, "ws"),
+                               0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 
 DEC_ACT_NONE, DEC_ACT_SWIGLU, DEC_ACT_RELU2 = 0, 1, 2
@@ -301,9 +384,10 @@ def ld_gemm_dec(A, W, C_out, g=None, eps=1e-5, alpha=1.0, R=None, act=DEC_ACT_NO
     the gate rows then the up rows and C has half as many columns."""
     M, K = A.shape
     N = C_out.shape[1]
-    _check(_lib.ld_gemm_dec(M, N, K, _ptr(A), A.stride(0), _ptr(g), eps, _ptr(W), W.stride(0), _ptr(C_out),
-                            C_out.stride(0), alpha, _ptr(R), 0 if R is None else R.stride(0), act,
-                            _stream(stream)))
+    _check(_lib.ld_gemm_dec(M, N, K, _ptr(A, "A", inner=True), A.stride(0), _ptr(g, "g"), eps,
+                            _ptr(W, "W", inner=True), W.stride(0), _ptr(C_out, "C_out", inner=True),
+                            C_out.stride(0), alpha, _ptr(R, "R", inner=True),
+                            0 if R is None else R.stride(0), act, _stream(stream)))
 
 
 def ld_kv_store(n_seq, n_new, d_model, pos, qkv, kv, s_max, stream=None):
@@ -370,9 +454,9 @@ def ld_gemm(a_kcontig, b_kcontig, M, N, K, A, lda, B, ldb, Cm, ldc, alpha=1.0, R
             c_f32=False, dtype=None, ws=None, stream=None):
     dt = _dtype_code(A) if dtype is None else dtype
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(_lib.ld_gemm(dt, int(a_kcontig), int(b_kcontig), M, N, K, _ptr(A), lda, _ptr(B), ldb,
-                        _ptr(Cm), ldc, int(c_f32), alpha, _ptr(R), ldr, _ptr(ws), ws_bytes,
-                        _stream(stream)))
+    _check(_lib.ld_gemm(dt, int(a_kcontig), int(b_kcontig), M, N, K, _ptr(A, "A", inner=True), lda,
+                        _ptr(B, "B", inner=True), ldb, _ptr(Cm, "C", inner=True), ldc, int(c_f32), alpha,
+                        _ptr(R, "R", inner=True), ldr, _ptr(ws, "ws"), ws_bytes, _stream(stream)))
 
 
 def ld_attn_fwd(n_seq, seq, n_heads, d_head, qkv, o, lse, stream=None, alibi=0):

@@ -185,3 +185,39 @@ def test_alibi_slope_host_function():
         got = [ld.ld_alibi_slope(i, h) for i in range(h)]
         assert np.allclose(got, block.alibi_slopes(h), rtol=1e-6, atol=0), h
     assert ld.ld_alibi_slope(-1, 8) == 0.0 and ld.ld_alibi_slope(8, 8) == 0.0
+
+
+def test_binding_rejects_host_noncontiguous_and_missized_tensors():
+    """The binding refuses, before any launch, torch tensors that are on the
+    host, not contiguous, of the wrong dtype or of the wrong size for the
+    configuration (runs without a GPU: every case fails in Python)."""
+    import torch
+    c = _cfg(batch=2, seq=64, d_model=128, n_heads=2, d_ff=256)
+    host = torch.zeros(2, 64, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device tensor"):
+        ld._ptr(host, "x")
+    meta = torch.empty(4, 8, dtype=torch.bfloat16, device="meta")
+    with pytest.raises(ValueError):
+        ld._ptr(meta, "x")
+    # dtype / size checks come before any pointer is taken
+    with pytest.raises(ValueError, match="dtype"):
+        ld._check_layer_tensors(c, acts=(("x", torch.zeros(2, 64, 128, dtype=torch.float32)),))
+    with pytest.raises(ValueError, match="elements"):
+        ld._check_layer_tensors(c, acts=(("x", torch.zeros(2, 63, 128, dtype=torch.bfloat16)),))
+    w = {k: torch.zeros(n, dtype=torch.bfloat16) for k, n in ld._weight_numel(c).items()}
+    ld._check_layer_tensors(c, w=w)
+    w["w_gate_up"] = torch.zeros(256 * 128, dtype=torch.bfloat16)   # W_up only: wrong for SwiGLU
+    with pytest.raises(ValueError, match="w_gate_up"):
+        ld._check_layer_tensors(c, w=w)
+    dw = {k: torch.zeros(n, dtype=torch.bfloat16) for k, n in ld._weight_numel(c).items()}
+    with pytest.raises(ValueError, match="grad"):
+        ld._check_layer_tensors(c, dw=dw)
+    with pytest.raises(ValueError, match="keep_override"):
+        ld.ld_layer_fwd(c, {k: 16 for k in ld.WEIGHT_KEYS}, 0, 0.1, 0, 0, 16, 16,
+                        keep_override=torch.zeros(3, dtype=torch.uint8), stream=0)
+    sub = _cfg(batch=2, seq=64, d_model=128, n_heads=2, d_ff=256, granularity=ld.LD_GRAN_SUBLAYER_SEQ)
+    with pytest.raises(ValueError, match="keep_override"):   # sub-layer masks: [n_masks = 2][B]
+        ld.ld_layer_fwd(sub, {k: 16 for k in ld.WEIGHT_KEYS}, 0, 0.1, 0, 0, 16, 16,
+                        keep_override=torch.zeros(2, dtype=torch.uint8), stream=0)
+    with pytest.raises(ValueError, match="layers"):
+        ld.ld_stack_step(c, [w, w], [0.1], 0, 0, 16, 16, [dw], torch.zeros(8, dtype=torch.uint8))
