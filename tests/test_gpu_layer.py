@@ -191,3 +191,66 @@ def test_layer_masks_match_stack_masks():
         ld.ld_layer_fwd(cfg, layer_weights_dev(sh, l)[0], l, float(ps[l]), 4, 9, xd, ctx)
         torch.cuda.synchronize()
         assert torch.equal(ctx[:sh.batch], keep[l])
+
+
+RESCALE_CASES = [(False, 1.0), (False, 1.7), (True, 0.5), (True, 1.7)]
+
+
+@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16], ids=["tiny_f32", "small_bf16"])
+@pytest.mark.parametrize("rescale,res_scale", RESCALE_CASES,
+                         ids=[f"rescale{int(a)}-c{b}" for a, b in RESCALE_CASES])
+def test_residual_scale_options_layer(sh, rescale, res_scale):
+    """r = res_scale / (1 - p) with rescaling, res_scale without (Dropout
+    Scale; the parameterisation table's branch multiplier): one layer
+    forward and backward against the oracle."""
+    cfg = _cfg(sh, rescale=rescale, res_scale=res_scale)
+    layer, p, seed, step = 1, np.float32(0.4), 3, 17
+    wd, w64 = layer_weights_dev(sh, layer, gain_jitter=True)
+    x, gy = inp.hidden(sh), inp.upstream_grad(sh)
+    keep = masks.keep_bits(p, seed, step, layer, sh.batch)
+    assert 0 < keep.sum() < sh.batch
+    xd, gd = x.to(DEV), gy.to(DEV)
+    ctx = _buf(ld.ld_layer_ctx_bytes(cfg))
+    ws = _buf(ld.ld_layer_ws_bytes(cfg))
+    ld.ld_layer_fwd(cfg, wd, layer, float(p), seed, step, xd, ctx, ws)
+    dw = zero_grads(sh)
+    ld.ld_layer_bwd(cfg, wd, ctx, gd, dw, ws)
+    torch.cuda.synchronize()
+    oc = _ocfg(sh, rescale=rescale, res_scale=res_scale)
+    X1, octx = stack.layer_forward(inp.f64(x), w64, keep, p, oc)
+    G0, grads = stack.layer_backward(octx, inp.f64(gy), oc)
+    t = tol(sh.dtype)
+    xo, go = f64(xd), f64(gd)
+    for b in range(sh.batch):
+        if keep[b]:
+            assert rel(xo[b], X1[b]) < t, b
+            assert rel(go[b], G0[b]) < t, b
+        else:
+            assert np.array_equal(xo[b], inp.f64(x)[b]) and np.array_equal(go[b], inp.f64(gy)[b])
+    _check_grads(dw, grads, t, (rescale, res_scale))
+
+
+@pytest.mark.parametrize("sh", [inp.SHAPES["tiny"], SMALL_BF16], ids=["tiny_f32", "small_bf16"])
+@pytest.mark.parametrize("rescale,res_scale", RESCALE_CASES,
+                         ids=[f"rescale{int(a)}-c{b}" for a, b in RESCALE_CASES])
+def test_residual_scale_options_stack(sh, rescale, res_scale):
+    cfg = _cfg(sh, rescale=rescale, res_scale=res_scale)
+    L = sh.n_layers
+    ps = schedule.rates(schedule.ILD, schedule.CONSTANT, 0.6, L, 0, 1)
+    seed, step = 2, 9
+    W = [layer_weights_dev(sh, l, gain_jitter=True) for l in range(L)]
+    x, gy = inp.hidden(sh), inp.upstream_grad(sh)
+    xd, gd = x.to(DEV), gy.to(DEV)
+    dws = [zero_grads(sh) for _ in range(L)]
+    ws = _buf(ld.ld_stack_ws_bytes(cfg, L))
+    cnt = torch.zeros(L, dtype=torch.int32, device=DEV)
+    ld.ld_stack_step(cfg, [w[0] for w in W], list(ps), seed, step, xd, gd, dws, ws, count_out=cnt)
+    torch.cuda.synchronize()
+    ref = stack.stack_step(inp.f64(x), [w[1] for w in W], ps, seed, step, inp.f64(gy),
+                           _ocfg(sh, rescale=rescale, res_scale=res_scale))
+    assert np.array_equal(cnt.cpu().numpy(), ref["count"])
+    t = tol(sh.dtype)
+    assert rel(f64(xd), ref["X_L"]) < t
+    assert rel(f64(gd), ref["G_0"]) < t
+    for l in range(L):
+        _check_grads(dws[l], ref["grads"][l], t, l)
