@@ -171,7 +171,10 @@ int ld_masks_granular(int32_t granularity, int32_t n_layers, int32_t batch, cons
                       int32_t* count, void* stream);
 
 /* Gather the rows of the kept sequences into a contiguous block:
- * xk[j*S + s, :] = x[idx[j]*S + s, :] for j < *count (bit copy).
+ * xk[j*S + s, :] = x[idx[j]*S + s, :] for j < *count (bit copy).  This is
+ * the first half of the efficient form of the layer-dropout training
+ * equation (Preliminary section, right after the per-sequence case form):
+ * f is executed on the kept sequences only, stacked contiguously.
  *   idx, count: device, as produced by ld_masks for one layer.
  *   x: device [B, S, d]; xk: device [B*S, d] (rows past count*S untouched). */
 int ld_gather_rows(const ld_config* cfg, const int32_t* idx, const int32_t* count, const void* x,
@@ -180,7 +183,11 @@ int ld_gather_rows(const ld_config* cfg, const int32_t* idx, const int32_t* coun
 /* Residual scatter-add of kept rows, in place:
  * x[idx[j]*S + s, c] = round(fmaf(r, yk[j*S + s, c], x[idx[j]*S + s, c]))
  * for j < *count, with one round-to-nearest-even to cfg->dtype.  Rows of
- * dropped sequences are not read or written.
+ * dropped sequences are not read or written.  This is the second half of
+ * the efficient form (Preliminary section): H^{l+1} = H^l + r M f(H^l)
+ * with the branch output of the kept sequences added back at their rows and
+ * the dropped rows left as they are (M = 0); r is r_train (Hyperparameters
+ * section, "Dropout Scale").
  *   yk: device [B*S, d] compacted branch output; x: device [B, S, d]. */
 int ld_scatter_add_rows(const ld_config* cfg, const int32_t* idx, const int32_t* count, float r,
                         const void* yk, void* x, void* stream);

@@ -77,8 +77,6 @@ def test_gemm_dec(M, N, K, mode):
     for N = 2048, 8 for the 11008-column SwiGLU, ragged column tiles for
     N = 130 and 704, a ragged k chunk for K = 200)."""
     norm = mode.startswith("norm")
-    if norm and K > 4096:
-        pytest.skip("the fused RMSNorm stages at most 4096 columns")
     act = ld.DEC_ACT_SWIGLU if "swiglu" in mode else ld.DEC_ACT_RELU2 if "relu2" in mode else ld.DEC_ACT_NONE
     rng = np.random.default_rng(M * 131 + N * 7 + K + len(mode))
     wrows = 2 * N if act == ld.DEC_ACT_SWIGLU else N
@@ -91,6 +89,15 @@ def test_gemm_dec(M, N, K, mode):
     Ad, Wd = A.to(DEV), W.to(DEV)
     Gd = None if G is None else G.to(DEV)
     Rd = None if R is None else R.to(DEV)
+    if norm and K > 4096:
+        # the fused RMSNorm stages at most 4096 columns: refused, nothing launched
+        C = torch.full((M, N), 3.0, dtype=torch.bfloat16, device=DEV)
+        with pytest.raises(ld.LdError) as e:
+            ld.ld_gemm_dec(Ad, Wd, C, g=Gd, eps=eps, alpha=alpha, R=Rd, act=act)
+        assert e.value.status == 3   # LD_E_UNSUPPORTED
+        torch.cuda.synchronize()
+        assert bool((C == 3.0).all())
+        return
     outs = []
     for _ in range(2):
         C = torch.full((M, N), 3.0, dtype=torch.bfloat16, device=DEV)
