@@ -175,7 +175,9 @@ constexpr size_t kAlign = 256;
 size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Saved activations of one layer, sized for the whole batch (kept rows are
-// stored compacted from row 0).
+// stored compacted from row 0).  xk (the layer input rows) and zk (Z, the
+// input of the FFN sub-block) are float32 in every configuration: they are
+// the residual stream inside the layer and the norm inputs of the backward.
 struct ActLayout {
   size_t xk, rstd1, h1, qkv, att, lse, zk, rstd2, h2, uv, s, total;
 };
@@ -189,13 +191,13 @@ ActLayout act_layout(const Dims& D) {
     return at;
   };
   const size_t es = D.es, T = D.T;
-  L.xk = take(es * T * D.d);
+  L.xk = take(4 * T * D.d);
   L.rstd1 = take(4 * T);
   L.h1 = take(es * T * D.d);
   L.qkv = take(es * T * 3 * D.d);
   L.att = take(es * T * D.d);
   L.lse = take(4 * T * D.H);
-  L.zk = take(es * T * D.d);
+  L.zk = take(4 * T * D.d);
   L.rstd2 = take(4 * T);
   L.h2 = take(es * T * D.d);
   L.uv = take(es * T * D.fw);
@@ -244,9 +246,12 @@ size_t splitk_bytes(const Dims& D) {
   return best;
 }
 
-// Backward scratch.
+// Backward scratch.  gz32: dL/dZ of the kept rows in float32 (the residual
+// gradient inside the layer); gz: the same rows in the configuration's type
+// (the operand of the output projection's backward GEMMs; unused in float32
+// configurations, where gz32 serves both).
 struct BwdLayout {
-  size_t gk, gs, guv, gh, gz, ga, gqkv, delta, dg_part, splitk, splitk_bytes, total;
+  size_t gk, gs, guv, gh, gz, gz32, ga, gqkv, delta, dg_part, splitk, splitk_bytes, total;
 };
 
 BwdLayout bwd_layout(const Dims& D) {
@@ -263,6 +268,7 @@ BwdLayout bwd_layout(const Dims& D) {
   L.guv = take(es * T * D.fw);
   L.gh = take(es * T * D.d);
   L.gz = take(es * T * D.d);
+  L.gz32 = take(4 * T * D.d);
   L.ga = take(es * T * D.d);
   L.gqkv = take(es * T * 3 * D.d);
   L.delta = take(4 * T * D.H);
@@ -292,6 +298,15 @@ struct LayerMasks {
   MaskView a, f;
   int host_a, host_f;
   int64_t hc_a, hc_f;
+};
+
+// A residual stream: x (forward) or dL/dx (backward) rows [B, S, d], float32
+// or the configuration's type.  ld_layer_fwd / ld_layer_bwd run on the
+// caller's tensors; ld_stack_step on float32 copies of them in its
+// workspace, so the stream is rounded to the caller's type only once.
+struct Stream {
+  void* p;
+  int f32;
 };
 
 struct ActPtrs {
@@ -347,7 +362,8 @@ int run_gemm(int dtype, int a_k, int b_k, GemmArgs g, int64_t max_m, int64_t hos
   const double es = dtype == LD_BF16 ? 2.0 : 4.0;
   const double M = static_cast<double>(host_m), N = g.N, K = static_cast<double>(host_k);
   const double out_es = g.c_f32 ? 4.0 : es;
-  ps.end(2.0 * M * N * K, es * (M * K + N * K) + out_es * M * N + (g.R ? out_es * M * N : 0.0));
+  const double r_es = g.r_f32 ? 4.0 : es;
+  ps.end(2.0 * M * N * K, es * (M * K + N * K) + out_es * M * N + (g.R ? r_es * M * N : 0.0));
   return LD_OK;
 }
 
@@ -411,7 +427,7 @@ int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmA
 // kv: null, or a cache [B, s_max, 2d] that receives the keys and values of
 // positions 0..S-1 (evaluation form only: every sequence processed).
 int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
-                      const ActPtrs& act, void* x, int64_t hc, bool scatter, hipStream_t s,
+                      const ActPtrs& act, Stream xs, int64_t hc, bool scatter, hipStream_t s,
                       void* kv = nullptr, int32_t s_max = 0) {
   const int dt = D.dtype;
   const int64_t T = D.T;
@@ -421,10 +437,11 @@ int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, 
   // gather kept rows of X + RMSNorm (attention input)
   {
     RmsFwdArgs a{};
-    a.x = x;
+    a.x = xs.p;
+    a.x_f32 = xs.f32;
     a.src = {mv.idx, static_cast<int32_t>(D.S)};
     a.g = w.g_attn;
-    a.xcopy = act.at(act.L.xk);
+    a.xcopy = act.at<float>(act.L.xk);
     a.y = act.at(act.L.h1);
     a.rstd = act.at<float>(act.L.rstd1);
     a.rc = {mv.count, static_cast<int32_t>(D.S), T};
@@ -432,7 +449,7 @@ int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, 
     a.eps = cfg->rms_eps;
     ProfScope ps("ld_rmsnorm_fwd_k", s);
     if ((e = launch_rmsnorm_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
-    ps.end(0, D.es * hm * D.d * 3.0 + 4.0 * hm);
+    ps.end(0, (xs.f32 ? 4.0 : D.es) * hm * D.d + 4.0 * hm * D.d + D.es * hm * D.d + 4.0 * hm);
   }
   // qkv = h1 W_qkv^T
   {
@@ -481,16 +498,18 @@ int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, 
     if ((e = launch_attn_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "attn_fwd: %s", hipGetErrorString(e));
     ps.end(2.0 * hc * D.d * D.S * (D.S + 1.0), D.es * hm * D.d * 4.0);
   }
-  // zk = xk + r * (att W_o^T), or x[kept rows] = the same
+  // zk = xk + r * (att W_o^T) (float32), or x[kept rows] = the same
   {
     GemmArgs g = gemm_args();
     g.A = act.at(act.L.att);
     g.lda = D.d;
     g.B = w.w_o;
     g.ldb = D.d;
-    g.C = scatter ? x : act.at(act.L.zk);
+    g.C = scatter ? xs.p : act.at(act.L.zk);
+    g.c_f32 = scatter ? xs.f32 : 1;
     g.ldc = D.d;
     g.R = act.at(act.L.xk);
+    g.r_f32 = 1;
     g.ldr = D.d;
     if (scatter) {
       g.r_mapped = 0;
@@ -512,7 +531,7 @@ int attn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, 
 // act (zk, left there by attn_forward_part for the same rows); gather = 1
 // reads the kept rows of x (which then holds Z) and saves them to zk.
 int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, const MaskView& mv,
-                     const ActPtrs& act, void* x, int64_t hc, bool gather, hipStream_t s) {
+                     const ActPtrs& act, Stream xs, int64_t hc, bool gather, hipStream_t s) {
   const int dt = D.dtype;
   const int64_t T = D.T;
   const int64_t hm = hc * D.S;
@@ -521,11 +540,13 @@ int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, c
   {
     RmsFwdArgs a{};
     if (gather) {
-      a.x = x;
+      a.x = xs.p;
+      a.x_f32 = xs.f32;
       a.src = {mv.idx, static_cast<int32_t>(D.S)};
-      a.xcopy = act.at(act.L.zk);
+      a.xcopy = act.at<float>(act.L.zk);
     } else {
       a.x = act.at(act.L.zk);
+      a.x_f32 = 1;
       a.src = {nullptr, 1};
     }
     a.g = w.g_mlp;
@@ -536,7 +557,7 @@ int ffn_forward_part(const ld_config* cfg, const Dims& D, const ld_weights& w, c
     a.eps = cfg->rms_eps;
     ProfScope ps("ld_rmsnorm_fwd_k", s);
     if ((e = launch_rmsnorm_fwd(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_fwd: %s", hipGetErrorString(e));
-    ps.end(0, D.es * hm * D.d * (gather ? 3.0 : 2.0) + 4.0 * hm);
+    ps.end(0, (gather ? (xs.f32 ? 4.0 : D.es) + 4.0 : 4.0) * hm * D.d + D.es * hm * D.d + 4.0 * hm);
   }
   // [u v] = h2 W_gate_up^T (SwiGLU), u = h2 W_up^T (squared ReLU)
   {
@@ -601,9 +622,11 @@ down_projection:
     g.lda = D.f;
     g.B = w.w_down;
     g.ldb = D.f;
-    g.C = x;
+    g.C = xs.p;
+    g.c_f32 = xs.f32;
     g.ldc = D.d;
     g.R = act.at(act.L.zk);
+    g.r_f32 = 1;
     g.ldr = D.d;
     g.r_mapped = 0;
     g.out_map = {mv.idx, static_cast<int32_t>(D.S)};
@@ -647,25 +670,26 @@ int zero_grads(const Dims& D, const ld_grads& dw, bool attn, bool ffn, hipStream
 // own rows, Z passed through x.  A sub-block the host knows to be dropped for
 // the whole batch launches nothing.
 int layer_forward(const ld_config* cfg, const Dims& D, const ld_weights& w, const LayerMasks& lm,
-                  const ActPtrs& act, void* x, hipStream_t s) {
+                  const ActPtrs& act, Stream xs, hipStream_t s) {
   if (!D.sub) {
     if (lm.host_a == 0) return LD_OK;
-    if (int rc = attn_forward_part(cfg, D, w, lm.a, act, x, lm.hc_a, false, s)) return rc;
-    return ffn_forward_part(cfg, D, w, lm.a, act, x, lm.hc_a, false, s);
+    if (int rc = attn_forward_part(cfg, D, w, lm.a, act, xs, lm.hc_a, false, s)) return rc;
+    return ffn_forward_part(cfg, D, w, lm.a, act, xs, lm.hc_a, false, s);
   }
   if (lm.host_a != 0)
-    if (int rc = attn_forward_part(cfg, D, w, lm.a, act, x, lm.hc_a, true, s)) return rc;
+    if (int rc = attn_forward_part(cfg, D, w, lm.a, act, xs, lm.hc_a, true, s)) return rc;
   if (lm.host_f != 0)
-    if (int rc = ffn_forward_part(cfg, D, w, lm.f, act, x, lm.hc_f, true, s)) return rc;
+    if (int rc = ffn_forward_part(cfg, D, w, lm.f, act, xs, lm.hc_f, true, s)) return rc;
   return LD_OK;
 }
 
 // Backward of ffn_forward_part on the rows mv keeps, given dL/dX^{l+1} in
-// dx.  scatter = 0 leaves dL/dZ of those rows compacted in the scratch (gz)
-// for the attention sub-block of the same rows; scatter = 1 writes it into
-// the kept rows of dx (sub-layer granularity).
+// the gradient stream ds.  scatter = 0 leaves dL/dZ of those rows compacted
+// in the scratch (gz32, and gz in bf16) for the attention sub-block of the
+// same rows; scatter = 1 writes it into the kept rows of the stream
+// (sub-layer granularity).
 int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, const ActPtrs& act,
-                      const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, int64_t hc,
+                      const BwdLayout& BL, char* ws, Stream ds, const ld_grads& dw, int64_t hc,
                       bool scatter, hipStream_t s) {
   const int dt = D.dtype;
   const int64_t T = D.T;
@@ -675,10 +699,12 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
   float* SK = BL.splitk_bytes ? reinterpret_cast<float*>(ws + BL.splitk) : nullptr;
   hipError_t e;
 
-  // gk = dL/dX^{l+1} on the kept rows
+  // gk = dL/dX^{l+1} on the kept rows, in the configuration's type (the
+  // operand of the down projection's backward GEMMs)
   {
     RowsArgs a{};
-    a.src = dx;
+    a.src = ds.p;
+    a.src_f32 = ds.f32;
     a.dst = W(BL.gk);
     a.src_map = {mv.idx, S};
     a.dst_map = {nullptr, 1};
@@ -686,7 +712,7 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     a.d = static_cast<int32_t>(D.d);
     ProfScope ps("ld_gather_rows_k", s);
     if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
-    ps.end(0, 2.0 * D.es * hm * D.d);
+    ps.end(0, ((ds.f32 ? 4.0 : D.es) + D.es) * hm * D.d);
   }
   // gs = r * gk W_down [M, f] and dW_down = r * gk^T s [d, f], one launch;
   // in the paired kernels the activation's backward is fused into the first
@@ -775,32 +801,48 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     g1.count_dim = 1;
     if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.fw, s, SK, BL.splitk_bytes)) return rc;
   }
-  // gz = gk + RMSNorm_bwd(zk, g_mlp, gh2); dg_mlp
+  // gz = dL/dX^{l+1} + RMSNorm_bwd(zk, g_mlp, gh2); dg_mlp.  The residual
+  // gradient is read from the stream itself; gz goes to gz32 (float32) and,
+  // in bf16 configurations, to gz (the operand of the next GEMMs) -- or,
+  // under sub-layer granularity, back into the stream.
   {
     RmsBwdArgs a{};
     a.x = act.at(act.L.zk);
+    a.x_f32 = 1;
     a.g = w.g_mlp;
     a.rstd = act.at<float>(act.L.rstd2);
     a.gy = W(BL.gh);
-    a.gres = W(BL.gk);
-    a.gx = scatter ? dx : W(BL.gz);
-    a.dst = scatter ? RowMap{mv.idx, S} : RowMap{nullptr, 1};
+    a.gres = ds.p;
+    a.gres_f32 = ds.f32;
+    a.res_map = {mv.idx, S};
+    if (scatter) {
+      a.gx = ds.p;
+      a.gx_f32 = ds.f32;
+      a.dst = {mv.idx, S};
+    } else {
+      a.gx = W(BL.gz32);
+      a.gx_f32 = 1;
+      a.dst = {nullptr, 1};
+      a.gx2 = dt == LD_BF16 ? W(BL.gz) : nullptr;
+    }
     a.dg_part = reinterpret_cast<float*>(ws + BL.dg_part);
     a.rc = {mv.count, S, T};
     a.d = static_cast<int32_t>(D.d);
     ProfScope ps("ld_rmsnorm_bwd_k", s);
     if ((e = launch_rmsnorm_bwd(dt, a, dw.g_mlp, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_bwd: %s", hipGetErrorString(e));
-    ps.end(0, D.es * hm * D.d * 4.0);
+    const double res_es = ds.f32 ? 4.0 : D.es;
+    const double out_es = scatter ? res_es : 4.0 + (a.gx2 ? D.es : 0.0);
+    ps.end(0, (4.0 + D.es + res_es + out_es) * hm * D.d);
   }
   return LD_OK;
 }
 
 // Backward of attn_forward_part on the rows mv keeps; dL/dX^l of those rows
-// is written into dx.  gather = 0 takes dL/dZ from the scratch (gz, left by
-// ffn_backward_part for the same rows); gather = 1 reads the kept rows of dx,
-// which then holds dL/dZ.
+// is written into the gradient stream ds.  gather = 0 takes dL/dZ from the
+// scratch (gz32 / gz, left by ffn_backward_part for the same rows); gather =
+// 1 reads the kept rows of the stream, which then holds dL/dZ.
 int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, const ActPtrs& act,
-                       const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, int64_t hc,
+                       const BwdLayout& BL, char* ws, Stream ds, const ld_grads& dw, int64_t hc,
                        bool gather, hipStream_t s) {
   const int dt = D.dtype;
   const int64_t T = D.T;
@@ -809,22 +851,27 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
   auto W = [&](size_t off) { return static_cast<void*>(ws + off); };
   float* SK = BL.splitk_bytes ? reinterpret_cast<float*>(ws + BL.splitk) : nullptr;
   hipError_t e;
+  // the operand of the output projection's backward GEMMs: gz (bf16) or
+  // gz32 (float32 configurations), gathered from the stream under sub-layer
+  // granularity
+  void* gz_op = dt == LD_BF16 ? W(BL.gz) : W(BL.gz32);
   if (gather) {
     RowsArgs a{};
-    a.src = dx;
-    a.dst = W(BL.gz);
+    a.src = ds.p;
+    a.src_f32 = ds.f32;
+    a.dst = gz_op;
     a.src_map = {mv.idx, S};
     a.dst_map = {nullptr, 1};
     a.rc = {mv.count, S, T};
     a.d = static_cast<int32_t>(D.d);
     ProfScope ps("ld_gather_rows_k", s);
     if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
-    ps.end(0, 2.0 * D.es * hm * D.d);
+    ps.end(0, ((ds.f32 ? 4.0 : D.es) + D.es) * hm * D.d);
   }
   // ga = r * gz W_o [M, d] and dW_o = r * gz^T att [d, d], one launch
   {
     GemmArgs g = gemm_args();
-    g.A = W(BL.gz);
+    g.A = gz_op;
     g.lda = D.d;
     g.B = w.w_o;
     g.ldb = D.d;
@@ -836,7 +883,7 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
     g.dev_count = mv.count;
     g.count_mult = S;
     GemmArgs g1 = gemm_args();
-    g1.A = W(BL.gz);
+    g1.A = gz_op;
     g1.lda = D.d;
     g1.B = act.at(act.L.att);
     g1.ldb = D.d;
@@ -906,22 +953,34 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
     g1.count_dim = 1;
     if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, 3 * D.d, s, SK, BL.splitk_bytes)) return rc;
   }
-  // dL/dX^l[kept rows] = gz + RMSNorm_bwd(xk, g_attn, gh1); dg_attn
+  // dL/dX^l[kept rows] = dL/dZ + RMSNorm_bwd(xk, g_attn, gh1); dg_attn.  dL/dZ
+  // is gz32 (float32), or the stream's rows under sub-layer granularity.
   {
     RmsBwdArgs a{};
     a.x = act.at(act.L.xk);
+    a.x_f32 = 1;
     a.g = w.g_attn;
     a.rstd = act.at<float>(act.L.rstd1);
     a.gy = W(BL.gh);
-    a.gres = W(BL.gz);
-    a.gx = dx;
+    if (gather) {
+      a.gres = ds.p;
+      a.gres_f32 = ds.f32;
+      a.res_map = {mv.idx, S};
+    } else {
+      a.gres = W(BL.gz32);
+      a.gres_f32 = 1;
+      a.res_map = {nullptr, 1};
+    }
+    a.gx = ds.p;
+    a.gx_f32 = ds.f32;
     a.dst = {mv.idx, S};
     a.dg_part = reinterpret_cast<float*>(ws + BL.dg_part);
     a.rc = {mv.count, S, T};
     a.d = static_cast<int32_t>(D.d);
     ProfScope ps("ld_rmsnorm_bwd_k", s);
     if ((e = launch_rmsnorm_bwd(dt, a, dw.g_attn, s)) != hipSuccess) return fail(LD_E_HIP, "rmsnorm_bwd: %s", hipGetErrorString(e));
-    ps.end(0, D.es * hm * D.d * 4.0);
+    const double st_es = ds.f32 ? 4.0 : D.es;
+    ps.end(0, (4.0 + D.es + (gather ? st_es : 4.0) + st_es) * hm * D.d);
   }
   return LD_OK;
 }
@@ -930,19 +989,19 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
 // A sub-block the host knows to be dropped for the whole batch launches only
 // the zero fill of its weight gradients.
 int layer_backward(const Dims& D, const ld_weights& w, const LayerMasks& lm, const ActPtrs& act,
-                   const BwdLayout& BL, char* ws, void* dx, const ld_grads& dw, hipStream_t s) {
+                   const BwdLayout& BL, char* ws, Stream ds, const ld_grads& dw, hipStream_t s) {
   if (!D.sub) {
     if (lm.host_a == 0) return zero_grads(D, dw, true, true, s);
-    if (int rc = ffn_backward_part(D, w, lm.a, act, BL, ws, dx, dw, lm.hc_a, false, s)) return rc;
-    return attn_backward_part(D, w, lm.a, act, BL, ws, dx, dw, lm.hc_a, false, s);
+    if (int rc = ffn_backward_part(D, w, lm.a, act, BL, ws, ds, dw, lm.hc_a, false, s)) return rc;
+    return attn_backward_part(D, w, lm.a, act, BL, ws, ds, dw, lm.hc_a, false, s);
   }
   if (lm.host_f == 0) {
     if (int rc = zero_grads(D, dw, false, true, s)) return rc;
-  } else if (int rc = ffn_backward_part(D, w, lm.f, act, BL, ws, dx, dw, lm.hc_f, true, s)) {
+  } else if (int rc = ffn_backward_part(D, w, lm.f, act, BL, ws, ds, dw, lm.hc_f, true, s)) {
     return rc;
   }
   if (lm.host_a == 0) return zero_grads(D, dw, true, false, s);
-  return attn_backward_part(D, w, lm.a, act, BL, ws, dx, dw, lm.hc_a, true, s);
+  return attn_backward_part(D, w, lm.a, act, BL, ws, ds, dw, lm.hc_a, true, s);
 }
 
 int check_weights(const ld_weights* w) {
@@ -1318,11 +1377,15 @@ size_t ld_layer_ws_bytes(const ld_config* cfg) {
   return bwd_layout(D).total;
 }
 
+// Bytes of the float32 copies of x and dx that ld_stack_step keeps in its
+// workspace (bf16 configurations; float32 ones run on the caller's tensors).
+size_t stream_bytes(const Dims& D) { return D.dtype == LD_BF16 ? up(4ull * D.T * D.d) : 0; }
+
 size_t ld_stack_ws_bytes(const ld_config* cfg, int32_t n_layers) {
   Dims D;
   if (check_cfg(cfg, &D) || n_layers < 1) return 0;
   return mask_layout(n_layers, D.B, D.nm).total + static_cast<size_t>(n_layers) * act_layout(D).total +
-         bwd_layout(D).total;
+         bwd_layout(D).total + 2 * stream_bytes(D);
 }
 
 int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float p, uint64_t seed,
@@ -1349,7 +1412,7 @@ int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float
   ActPtrs act{c + ml.total, act_layout(D)};
   const std::vector<int64_t> hc = host_counts_if_profiling(count, D.nm, s);
   const LayerMasks lm = layer_masks(D, ml, c, 0, layer, p, seed, step, keep_override, hc);
-  return layer_forward(cfg, D, *w, lm, act, x, s);
+  return layer_forward(cfg, D, *w, lm, act, Stream{x, D.dtype == LD_F32}, s);
 }
 
 int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, void* dx,
@@ -1371,7 +1434,7 @@ int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, voi
   // the ctx carries no p, seed or step: every decision is the device's
   LayerMasks lm = layer_masks(D, ml, c, 0, 0, 0.f, 0, 0, nullptr, hc);
   lm.host_a = lm.host_f = -1;
-  return layer_backward(D, *w, lm, act, BL, static_cast<char*>(ws), dx, *dw, s);
+  return layer_backward(D, *w, lm, act, BL, static_cast<char*>(ws), Stream{dx, D.dtype == LD_F32}, *dw, s);
 }
 
 int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, const float* p,
@@ -1402,6 +1465,11 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
   int32_t* count = reinterpret_cast<int32_t*>(base + ml.count);
   char* acts = base + ml.total;
   char* bws = acts + static_cast<size_t>(L) * al.total;
+  // bf16 configurations: the residual streams in float32 for the whole step
+  const bool cp = D.dtype == LD_BF16;
+  const Stream xs{cp ? bws + BL.total : x, 1};
+  const Stream dxs{cp ? bws + BL.total + stream_bytes(D) : dx, 1};
+  const int64_t n_elems = D.T * D.d;
 
   if (int rc = launch_mask_range(cfg, n_layers, static_cast<int32_t>(B), D.nm, D.per_batch, p, 0, seed,
                                  step, keep_override, keep, idx, count,
@@ -1411,14 +1479,29 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
   std::vector<LayerMasks> lms;
   lms.reserve(L);
   for (int64_t l = 0; l < L; ++l) lms.push_back(layer_masks(D, ml, base, l, l, p[l], seed, step, keep_override, hc));
+  auto convert = [&](const void* src, void* dst, int to_f32) {
+    ProfScope ps("ld_convert_k", s);
+    const hipError_t e = launch_convert(src, dst, n_elems, to_f32, s);
+    if (e != hipSuccess) return fail(LD_E_HIP, "convert: %s", hipGetErrorString(e));
+    ps.end(0, 6.0 * n_elems);
+    return static_cast<int>(LD_OK);
+  };
+  if (cp)
+    if (int rc = convert(x, xs.p, 1)) return rc;
   for (int64_t l = 0; l < L; ++l) {
     ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
-    if (int rc = layer_forward(cfg, D, w[l], lms[l], act, x, s)) return rc;
+    if (int rc = layer_forward(cfg, D, w[l], lms[l], act, xs, s)) return rc;
+  }
+  if (cp) {
+    if (int rc = convert(xs.p, x, 0)) return rc;
+    if (int rc = convert(dx, dxs.p, 1)) return rc;
   }
   for (int64_t l = L - 1; l >= 0; --l) {
     ActPtrs act{acts + static_cast<size_t>(l) * al.total, al};
-    if (int rc = layer_backward(D, w[l], lms[l], act, BL, bws, dx, dw[l], s)) return rc;
+    if (int rc = layer_backward(D, w[l], lms[l], act, BL, bws, dxs, dw[l], s)) return rc;
   }
+  if (cp)
+    if (int rc = convert(dxs.p, dx, 0)) return rc;
   if (keep_out) LD_HIP(hipMemcpyAsync(keep_out, keep, L * nm * B, hipMemcpyDeviceToDevice, s));
   if (idx_out) LD_HIP(hipMemcpyAsync(idx_out, idx, 4 * L * nm * B, hipMemcpyDeviceToDevice, s));
   if (count_out) LD_HIP(hipMemcpyAsync(count_out, count, 4 * L * nm, hipMemcpyDeviceToDevice, s));
@@ -1456,9 +1539,10 @@ int ld_stack_eval(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
   for (int32_t l = 0; l < n_layers; ++l) {
     if (active && !active[l]) continue;
     MaskView mv{nullptr, nullptr, nullptr, nullptr, r_eval ? r_eval[l] : 1.f};
-    if (int rc = attn_forward_part(cfg, D, w[l], mv, act, x, D.B, false, s, kv ? kv[l] : nullptr, s_max))
+    const Stream xs{x, D.dtype == LD_F32};
+    if (int rc = attn_forward_part(cfg, D, w[l], mv, act, xs, D.B, false, s, kv ? kv[l] : nullptr, s_max))
       return rc;
-    if (int rc = ffn_forward_part(cfg, D, w[l], mv, act, x, D.B, false, s)) return rc;
+    if (int rc = ffn_forward_part(cfg, D, w[l], mv, act, xs, D.B, false, s)) return rc;
   }
   return LD_OK;
 }
@@ -1955,26 +2039,17 @@ size_t ld_attn_bwd_ws_bytes(int32_t n_seq, int32_t seq, int32_t n_heads) {
   return 4ull * n_seq * seq * n_heads;
 }
 
-int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
-                int32_t alibi, const void* qkv, const void* o, const float* lse, const void* go,
-                void* gqkv, void* ws, size_t ws_bytes, void* stream) {
-  t_err.clear();
-  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
-  if (n_seq < 0 || seq < 1 || n_heads < 1) return fail(LD_E_SHAPE, "bad shape");
-  if (dtype == LD_BF16 ? (d_head != 64 && d_head != 128) || seq % 64
-                       : (d_head != 16 && d_head != 32 && d_head != 64))
-    return fail(LD_E_UNSUPPORTED, "unsupported d_head/seq");
-  if (alibi != 0 && alibi != 1) return fail(LD_E_INVALID, "alibi must be 0 or 1");
-  if (n_seq == 0) return LD_OK;
-  if (!qkv || !o || !lse || !go || !gqkv || !ws) return fail(LD_E_INVALID, "NULL pointer");
-  if (ws_bytes < ld_attn_bwd_ws_bytes(n_seq, seq, n_heads)) return fail(LD_E_WORKSPACE, "workspace too small");
+namespace {
+int attn_bwd_common(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head, int32_t alibi,
+                    const void* qkv, const void* o, const float* lse, const void* go, void* gqkv, float* delta,
+                    void* stream) {
   AttnArgs a{};
   a.qkv = qkv;
   a.o = o;
   a.go = go;
   a.out = gqkv;
   a.lse = const_cast<float*>(lse);
-  a.delta = static_cast<float*>(ws);
+  a.delta = delta;
   a.n_seq = n_seq;
   a.S = seq;
   a.H = n_heads;
@@ -1984,6 +2059,29 @@ int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int3
   hipError_t e = launch_attn_bwd(dtype, a, as_stream(stream));
   if (e != hipSuccess) return fail(LD_E_HIP, "attn_bwd: %s", hipGetErrorString(e));
   return LD_OK;
+}
+
+int check_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head, int32_t alibi) {
+  if (dtype != LD_F32 && dtype != LD_BF16) return fail(LD_E_INVALID, "unknown dtype");
+  if (n_seq < 0 || seq < 1 || n_heads < 1) return fail(LD_E_SHAPE, "bad shape");
+  if (dtype == LD_BF16 ? (d_head != 64 && d_head != 128) || seq % 64
+                       : (d_head != 16 && d_head != 32 && d_head != 64))
+    return fail(LD_E_UNSUPPORTED, "unsupported d_head/seq");
+  if (alibi != 0 && alibi != 1) return fail(LD_E_INVALID, "alibi must be 0 or 1");
+  return LD_OK;
+}
+}  // namespace
+
+int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
+                int32_t alibi, const void* qkv, const void* o, const float* lse, const void* go,
+                void* gqkv, void* ws, size_t ws_bytes, void* stream) {
+  t_err.clear();
+  if (int rc = check_attn_bwd(dtype, n_seq, seq, n_heads, d_head, alibi)) return rc;
+  if (n_seq == 0) return LD_OK;
+  if (!qkv || !o || !lse || !go || !gqkv || !ws) return fail(LD_E_INVALID, "NULL pointer");
+  if (ws_bytes < ld_attn_bwd_ws_bytes(n_seq, seq, n_heads)) return fail(LD_E_WORKSPACE, "workspace too small");
+  return attn_bwd_common(dtype, n_seq, seq, n_heads, d_head, alibi, qkv, o, lse, go, gqkv,
+                         static_cast<float*>(ws), stream);
 }
 
 // -------------------------------------------------------------- profiling

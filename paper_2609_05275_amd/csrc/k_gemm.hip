@@ -133,7 +133,7 @@ __device__ __forceinline__ void epilogue_store(const GemmArgs& g, float alpha, i
   const int64_t orow = map_row(g.out_map, row);
   if (g.R) {
     const int64_t rrow = g.r_mapped ? orow : row;
-    if (g.c_f32)
+    if (g.r_f32)
       val += static_cast<const float*>(g.R)[rrow * g.ldr + col];
     else
       val += static_cast<float>(static_cast<const bf16*>(g.R)[rrow * g.ldr + col]);
@@ -515,7 +515,26 @@ __device__ __forceinline__ void epilogue_rows_full(const GemmArgs& g, float* par
 #pragma unroll
     for (int it = 0; it < 16; ++it) orow[it] = r0 + 2 * it;
   }
-  if (g.R) {  // bf16 residual (a float32 one takes the edge path)
+  if (g.R && g.r_f32) {  // float32 residual (the residual streams)
+    const float* R = static_cast<const float*>(g.R);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {  // two halves of 8 rows: fewer registers live
+      float4 rv[8];
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        const int64_t rrow = g.r_mapped ? orow[8 * h + it] : r0 + 2 * (8 * h + it);
+        rv[it] = *reinterpret_cast<const float4*>(R + rrow * g.ldr + n);
+      }
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        float4& t = v[8 * h + it];
+        t.x += rv[it].x;
+        t.y += rv[it].y;
+        t.z += rv[it].z;
+        t.w += rv[it].w;
+      }
+    }
+  } else if (g.R) {  // bf16 residual
     uint2 rv[16];
     const bf16* R = static_cast<const bf16*>(g.R);
 #pragma unroll
@@ -547,8 +566,8 @@ __device__ __forceinline__ void epilogue_rows_full(const GemmArgs& g, float* par
   }
 }
 
-// Block row with rows past M or columns past N (or a float32 residual): one
-// row at a time, each checked.
+// Block row with rows past M or columns past N: one row at a time, each
+// checked.
 __device__ __forceinline__ void epilogue_rows_edge(const GemmArgs& g, float* part, const float* stage,
                                                    int r0, int half, int c, int n, int M) {
 #pragma unroll 1
@@ -563,7 +582,7 @@ __device__ __forceinline__ void epilogue_rows_edge(const GemmArgs& g, float* par
     const int64_t orow = map_row(g.out_map, m);
     if (g.R) {
       const int64_t rrow = g.r_mapped ? orow : m;
-      if (g.c_f32) {
+      if (g.r_f32) {
         const float4 r = *reinterpret_cast<const float4*>(static_cast<const float*>(g.R) + rrow * g.ldr + n);
         v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
       } else {
@@ -868,8 +887,8 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
   const int c = lm * 4;
   const int n = n0 + wn * 128 + c;
   // A block row takes the branch-free path when all its 32 rows and 128
-  // columns are in range (and the residual, if any, is bf16).
-  const bool full_cols = n0 + wn * 128 + 128 <= g.N && !(g.R && g.c_f32);
+  // columns are in range.
+  const bool full_cols = n0 + wn * 128 + 128 <= g.N;
   // Largest kept sequence index, for the row map (rows < M only).
   const int q_last = g.out_map.idx && M > 0 ? (M - 1) / g.out_map.S : 0;
   dma_barrier<0>();  // the loop's last loads (zeros) land before the ring is reused

@@ -1,6 +1,8 @@
 // Mask + compaction, row gather / scatter-add, RMSNorm and SwiGLU kernels.
 // All of these are HBM-bound: 16-byte vector accesses, one wave per row for
 // the normalisations, fp32 arithmetic on bf16 or fp32 storage.
+#include <type_traits>
+
 #include "ld_internal.h"
 
 namespace ld {
@@ -110,16 +112,53 @@ __global__ __launch_bounds__(256) void ld_zero_f32_k(ZeroArgs a) {
 
 // ------------------------------------------------------- gather / scatter
 
-template <typename T>
+// Chunks of VN consecutive elements (8 or 16, 16 or 32 bytes per lane).
+template <typename T, int VN>
+struct alignas(sizeof(T) * VN < 16 ? sizeof(T) * VN : 16) Chunk {
+  T v[VN];
+};
+template <typename T, int VN>
+__device__ __forceinline__ Chunk<T, VN> ldc(const T* p) {
+  return *reinterpret_cast<const Chunk<T, VN>*>(p);
+}
+template <typename T, int VN>
+__device__ __forceinline__ void stc(T* p, const Chunk<T, VN>& c) {
+  *reinterpret_cast<Chunk<T, VN>*>(p) = c;
+}
+
+// Row gather: dst rows (type TD) from src rows (type TS) through the row
+// maps; a bit copy when the types agree, one rounding to nearest even when
+// float32 rows go to bf16.
+template <typename TS, typename TD>
 __global__ __launch_bounds__(256) void ld_gather_rows_k(RowsArgs a) {
-  constexpr int VN = Pack<T>::N;
+  constexpr int VN = 16 / sizeof(TD);
   const int64_t chunks = a.d / VN;
   const int64_t total = row_count(a.rc) * chunks;
-  const T* src = static_cast<const T*>(a.src);
-  T* dst = static_cast<T*>(a.dst);
+  const TS* src = static_cast<const TS*>(a.src);
+  TD* dst = static_cast<TD*>(a.dst);
   for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < total; id += gridDim.x * 256ll) {
     const int64_t row = id / chunks, c = (id % chunks) * VN;
-    store16(dst + map_row(a.dst_map, row) * a.d + c, load16(src + map_row(a.src_map, row) * a.d + c));
+    const Chunk<TS, VN> v = ldc<TS, VN>(src + map_row(a.src_map, row) * a.d + c);
+    if constexpr (std::is_same<TS, TD>::value) {
+      stc<TD, VN>(dst + map_row(a.dst_map, row) * a.d + c, v);
+    } else {
+      Chunk<TD, VN> o;
+#pragma unroll
+      for (int i = 0; i < VN; ++i) o.v[i] = from_f<TD>(to_f(v.v[i]));
+      stc<TD, VN>(dst + map_row(a.dst_map, row) * a.d + c, o);
+    }
+  }
+}
+
+// bf16 <-> float32 over n elements (8 per thread and step).
+template <typename TS, typename TD>
+__global__ __launch_bounds__(256) void ld_convert_k(const TS* src, TD* dst, int64_t n8) {
+  for (int64_t id = blockIdx.x * 256ll + threadIdx.x; id < n8; id += gridDim.x * 256ll) {
+    const Chunk<TS, 8> v = ldc<TS, 8>(src + id * 8);
+    Chunk<TD, 8> o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o.v[i] = from_f<TD>(to_f(v.v[i]));
+    stc<TD, 8>(dst + id * 8, o);
   }
 }
 
@@ -142,23 +181,26 @@ __global__ __launch_bounds__(256) void ld_scatter_add_rows_k(RowsArgs a) {
 }
 
 // ---------------------------------------------------------------- RMSNorm
-// One wave per row, NCH 16-byte chunks per lane held in registers.
+// One wave per row; a lane holds NCH chunks of VN consecutive elements (VN =
+// 8 in bf16 configurations, 4 in float32 ones).  Each tensor has its own
+// element type (see RmsFwdArgs / RmsBwdArgs): the source rows of the forward
+// and the saved inputs, residual gradients and outputs of the backward may be
+// float32 (the residual streams) while the GEMM operands are bf16.
 
-template <typename T, int NCH>
+template <typename TS, typename TY, int VN, int NCH>
 __global__ __launch_bounds__(256) void ld_rmsnorm_fwd_k(RmsFwdArgs a) {
-  constexpr int VN = Pack<T>::N;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t row = blockIdx.x * 4ll + wave;
   if (row >= row_count(a.rc)) return;
-  const T* x = static_cast<const T*>(a.x) + map_row(a.src, row) * a.d;
-  const T* g = static_cast<const T*>(a.g);
-  Pack<T> v[NCH];
+  const TS* x = static_cast<const TS*>(a.x) + map_row(a.src, row) * a.d;
+  const TY* g = static_cast<const TY*>(a.g);
+  Chunk<TS, VN> v[NCH];
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     const int col = (c * 64 + lane) * VN;
     if (col < a.d) {
-      v[c] = load16(x + col);
+      v[c] = ldc<TS, VN>(x + col);
 #pragma unroll
       for (int i = 0; i < VN; ++i) {
         const float f = to_f(v[c].v[i]);
@@ -168,18 +210,23 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_fwd_k(RmsFwdArgs a) {
   }
   ss = wave_sum(ss);
   const float rstd = rsqrtf(ss / static_cast<float>(a.d) + a.eps);
-  T* y = static_cast<T*>(a.y) + row * a.d;
-  T* xc = a.xcopy ? static_cast<T*>(a.xcopy) + row * a.d : nullptr;
+  TY* y = static_cast<TY*>(a.y) + row * a.d;
+  float* xc = a.xcopy ? a.xcopy + row * a.d : nullptr;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     const int col = (c * 64 + lane) * VN;
     if (col < a.d) {
-      if (xc) store16(xc + col, v[c]);
-      const Pack<T> gv = load16(g + col);
-      Pack<T> o;
+      if (xc) {
+        Chunk<float, VN> cc;
 #pragma unroll
-      for (int i = 0; i < VN; ++i) o.v[i] = from_f<T>(to_f(v[c].v[i]) * rstd * to_f(gv.v[i]));
-      store16(y + col, o);
+        for (int i = 0; i < VN; ++i) cc.v[i] = to_f(v[c].v[i]);
+        stc<float, VN>(xc + col, cc);
+      }
+      const Chunk<TY, VN> gv = ldc<TY, VN>(g + col);
+      Chunk<TY, VN> o;
+#pragma unroll
+      for (int i = 0; i < VN; ++i) o.v[i] = from_f<TY>(to_f(v[c].v[i]) * rstd * to_f(gv.v[i]));
+      stc<TY, VN>(y + col, o);
     }
   }
   if (lane == 0) a.rstd[row] = rstd;
@@ -188,59 +235,62 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_fwd_k(RmsFwdArgs a) {
 constexpr int kBwdRowsPerWave = 8;
 constexpr int kBwdRowsPerBlock = 4 * kBwdRowsPerWave;
 
-template <typename T, int NCH>
+template <typename TX, typename TY, typename TR, int VN, int NCH>
 struct NormRow {
-  Pack<T> x[NCH], gy[NCH], res[NCH];
+  Chunk<TX, VN> x[NCH];
+  Chunk<TY, VN> gy[NCH];
+  Chunk<TR, VN> res[NCH];
   float rstd;
 };
 
-template <typename T, int NCH>
-__device__ __forceinline__ void norm_row_load(NormRow<T, NCH>& r, const RmsBwdArgs& a, int64_t row,
+template <typename TX, typename TY, typename TR, int VN, int NCH>
+__device__ __forceinline__ void norm_row_load(NormRow<TX, TY, TR, VN, NCH>& r, const RmsBwdArgs& a, int64_t row,
                                               int lane) {
-  const T* x = static_cast<const T*>(a.x) + row * a.d;
-  const T* gy = static_cast<const T*>(a.gy) + row * a.d;
-  const T* gres = a.gres ? static_cast<const T*>(a.gres) + row * a.d : nullptr;
+  const TX* x = static_cast<const TX*>(a.x) + row * a.d;
+  const TY* gy = static_cast<const TY*>(a.gy) + row * a.d;
+  const TR* gres = a.gres ? static_cast<const TR*>(a.gres) + map_row(a.res_map, row) * a.d : nullptr;
   r.rstd = a.rstd[row];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    const int col = (c * 64 + lane) * Pack<T>::N;
+    const int col = (c * 64 + lane) * VN;
     if (col < a.d) {
-      r.x[c] = load16(x + col);
-      r.gy[c] = load16(gy + col);
-      if (gres) r.res[c] = load16(gres + col);
+      r.x[c] = ldc<TX, VN>(x + col);
+      r.gy[c] = ldc<TY, VN>(gy + col);
+      if (gres) r.res[c] = ldc<TR, VN>(gres + col);
     }
   }
 }
 
-// gx = gres + rstd*(g*gy) - x*rstd^3*mean_d(x*g*gy); per-block dg partials
-// summed over the block's rows in a fixed order (rows in sequence inside a
-// wave, then waves 0..3 through LDS).  The next row's loads are issued
-// before the current row's reduction so a wave keeps two rows in flight.
-template <typename T, int NCH>
+// gx = gres + rstd*(g*gy) - x*rstd^3*mean_d(x*g*gy), written through the dst
+// map (type TO) and, when gx2 is set, as a compacted copy in the
+// configuration's type; per-block dg partials summed over the block's rows
+// in a fixed order (rows in sequence inside a wave, then waves 0..3 through
+// LDS).  Where a lane's rows fit in registers twice, the next row's loads are
+// issued before the current row's reduction (two rows in flight per wave).
+template <typename TX, typename TY, typename TR, typename TO, int VN, int NCH>
 __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
-  constexpr int VN = Pack<T>::N;
   extern __shared__ float dg_lds[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t rows = row_count(a.rc);
-  const T* gp = static_cast<const T*>(a.g);
-  float gf[NCH][VN], dga[NCH][VN];
+  const TY* gp = static_cast<const TY*>(a.g);
+  Chunk<TY, VN> graw[NCH];
+  float dga[NCH][VN];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
     const int col = (c * 64 + lane) * VN;
-    Pack<T> gv{};
-    if (col < a.d) gv = load16(gp + col);
+    if (col < a.d) graw[c] = ldc<TY, VN>(gp + col);
 #pragma unroll
     for (int i = 0; i < VN; ++i) {
-      gf[c][i] = to_f(gv.v[i]);
+      if (col >= a.d) graw[c].v[i] = from_f<TY>(0.f);
       dga[c][i] = 0.f;
     }
   }
   const float inv_d = 1.f / static_cast<float>(a.d);
   const int64_t r0 = blockIdx.x * static_cast<int64_t>(kBwdRowsPerBlock) + wave * kBwdRowsPerWave;
   const int64_t r1 = min(r0 + kBwdRowsPerWave, rows);
-  // two rows in flight when they fit in registers (up to 4 chunks per lane)
-  constexpr bool kPrefetch = NCH <= 4;
-  NormRow<T, NCH> cur, nxt;
+  constexpr int kRowBytes = NCH * VN * (sizeof(TX) + sizeof(TY) + sizeof(TR));
+  constexpr bool kPrefetch = kRowBytes <= 4 * 8 * 6;   // at most 48 registers a row
+  NormRow<TX, TY, TR, VN, NCH> cur, nxt;
   if (kPrefetch && r0 < r1) norm_row_load(cur, a, r0, lane);
   for (int64_t row = r0; row < r1; ++row) {
     if (kPrefetch) {
@@ -255,27 +305,31 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
       if (col < a.d) {
 #pragma unroll
         for (int i = 0; i < VN; ++i)
-          dot = __builtin_fmaf(to_f(cur.x[c].v[i]) * gf[c][i], to_f(cur.gy[c].v[i]), dot);
+          dot = __builtin_fmaf(to_f(cur.x[c].v[i]) * to_f(graw[c].v[i]), to_f(cur.gy[c].v[i]), dot);
       }
     }
     dot = wave_sum(dot);
     const float rstd = cur.rstd;
     const float coef = rstd * rstd * rstd * dot * inv_d;
-    T* gx = static_cast<T*>(a.gx) + map_row(a.dst, row) * a.d;
+    TO* gx = static_cast<TO*>(a.gx) + map_row(a.dst, row) * a.d;
+    TY* gx2 = a.gx2 ? static_cast<TY*>(a.gx2) + row * a.d : nullptr;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int col = (c * 64 + lane) * VN;
       if (col < a.d) {
-        Pack<T> o;
+        Chunk<TO, VN> o;
+        Chunk<TY, VN> o2;
 #pragma unroll
         for (int i = 0; i < VN; ++i) {
           const float xf = to_f(cur.x[c].v[i]), gyf = to_f(cur.gy[c].v[i]);
-          float val = rstd * gf[c][i] * gyf - xf * coef;
+          float val = rstd * to_f(graw[c].v[i]) * gyf - xf * coef;
           if (a.gres) val += to_f(cur.res[c].v[i]);
-          o.v[i] = from_f<T>(val);
+          o.v[i] = from_f<TO>(val);
+          o2.v[i] = from_f<TY>(val);
           dga[c][i] = __builtin_fmaf(gyf * xf, rstd, dga[c][i]);
         }
-        store16(gx + col, o);
+        stc<TO, VN>(gx + col, o);
+        if (gx2) stc<TY, VN>(gx2 + col, o2);
       }
     }
     if (kPrefetch) cur = nxt;
@@ -424,35 +478,35 @@ int elt_grid(int64_t total_chunks) {
   return static_cast<int>(g);
 }
 
-template <typename T>
-int nch_for(int d) {
-  const int per = 64 * Pack<T>::N;
-  return (d + per - 1) / per;
+template <int VN>
+int nch_bucket(int d) {
+  const int nch = (d + 64 * VN - 1) / (64 * VN);
+  return nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : 8;
 }
 
-template <typename T>
+template <typename TS, typename TY>
 hipError_t rms_fwd_t(const RmsFwdArgs& a, hipStream_t s) {
-  const int nch = nch_for<T>(a.d);
-  const int64_t max_rows = a.rc.dev_count ? a.rc.rows : a.rc.rows;
-  const dim3 grid(static_cast<unsigned>((max_rows + 3) / 4));
+  constexpr int VN = std::is_same<TY, bf16>::value ? 8 : 4;
+  const int64_t max_rows = a.rc.rows;
   if (max_rows == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((max_rows + 3) / 4));
 #define LD_RF(N) \
-  case N: hipLaunchKernelGGL((ld_rmsnorm_fwd_k<T, N>), grid, dim3(256), 0, s, a); break;
-  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : 8) {
+  case N: hipLaunchKernelGGL((ld_rmsnorm_fwd_k<TS, TY, VN, N>), grid, dim3(256), 0, s, a); break;
+  switch (nch_bucket<VN>(a.d)) {
     LD_RF(1) LD_RF(2) LD_RF(4) LD_RF(8)
   }
 #undef LD_RF
   return hipGetLastError();
 }
 
-template <typename T>
+template <typename TX, typename TY, typename TR, typename TO>
 hipError_t rms_bwd_t(const RmsBwdArgs& a, float* dg, hipStream_t s) {
-  const int nch = nch_for<T>(a.d);
+  constexpr int VN = std::is_same<TY, bf16>::value ? 8 : 4;
   const int64_t nblk = rmsnorm_bwd_blocks(a.rc.rows);
   const size_t lds = static_cast<size_t>(a.d) * sizeof(float);
 #define LD_RB(N) \
-  case N: hipLaunchKernelGGL((ld_rmsnorm_bwd_k<T, N>), dim3(nblk), dim3(256), lds, s, a); break;
-  switch (nch <= 1 ? 1 : nch <= 2 ? 2 : nch <= 4 ? 4 : 8) {
+  case N: hipLaunchKernelGGL((ld_rmsnorm_bwd_k<TX, TY, TR, TO, VN, N>), dim3(nblk), dim3(256), lds, s, a); break;
+  switch (nch_bucket<VN>(a.d)) {
     LD_RB(1) LD_RB(2) LD_RB(4) LD_RB(8)
   }
 #undef LD_RB
@@ -461,6 +515,16 @@ hipError_t rms_bwd_t(const RmsBwdArgs& a, float* dg, hipStream_t s) {
   hipLaunchKernelGGL(ld_dg_reduce_k, dim3((a.d + kDgCols - 1) / kDgCols), dim3(kDgCols * kDgGroups), 0, s, a.dg_part, nblk,
                      a.d, dg);
   return hipGetLastError();
+}
+
+// bf16 configuration: x, gres and gx each bf16 or float32
+template <typename TX, typename TR>
+hipError_t rms_bwd_bf16_o(const RmsBwdArgs& a, float* dg, hipStream_t s) {
+  return a.gx_f32 ? rms_bwd_t<TX, bf16, TR, float>(a, dg, s) : rms_bwd_t<TX, bf16, TR, bf16>(a, dg, s);
+}
+template <typename TX>
+hipError_t rms_bwd_bf16_r(const RmsBwdArgs& a, float* dg, hipStream_t s) {
+  return a.gres_f32 ? rms_bwd_bf16_o<TX, float>(a, dg, s) : rms_bwd_bf16_o<TX, bf16>(a, dg, s);
 }
 
 }  // namespace
@@ -488,10 +552,25 @@ hipError_t launch_zero_f32(const ZeroArgs& a, hipStream_t s) {
 hipError_t launch_gather(int dtype, const RowsArgs& a, hipStream_t s) {
   const int vn = dtype == LD_BF16 ? 8 : 4;
   const int grid = elt_grid(a.rc.rows * (a.d / vn));
-  if (dtype == LD_BF16)
-    hipLaunchKernelGGL(ld_gather_rows_k<bf16>, dim3(grid), dim3(256), 0, s, a);
+  if (dtype == LD_BF16 && a.src_f32)
+    hipLaunchKernelGGL((ld_gather_rows_k<float, bf16>), dim3(grid), dim3(256), 0, s, a);
+  else if (dtype == LD_BF16)
+    hipLaunchKernelGGL((ld_gather_rows_k<bf16, bf16>), dim3(grid), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(ld_gather_rows_k<float>, dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((ld_gather_rows_k<float, float>), dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert(const void* src, void* dst, int64_t n, int to_f32, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (n % 8) return hipErrorInvalidValue;
+  const int grid = elt_grid(n / 8);
+  if (to_f32)
+    hipLaunchKernelGGL((ld_convert_k<bf16, float>), dim3(grid), dim3(256), 0, s, static_cast<const bf16*>(src),
+                       static_cast<float*>(dst), n / 8);
+  else
+    hipLaunchKernelGGL((ld_convert_k<float, bf16>), dim3(grid), dim3(256), 0, s, static_cast<const float*>(src),
+                       static_cast<bf16*>(dst), n / 8);
   return hipGetLastError();
 }
 
@@ -506,11 +585,13 @@ hipError_t launch_scatter_add(int dtype, const RowsArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s) {
-  return dtype == LD_BF16 ? rms_fwd_t<bf16>(a, s) : rms_fwd_t<float>(a, s);
+  if (dtype != LD_BF16) return rms_fwd_t<float, float>(a, s);
+  return a.x_f32 ? rms_fwd_t<float, bf16>(a, s) : rms_fwd_t<bf16, bf16>(a, s);
 }
 
 hipError_t launch_rmsnorm_bwd(int dtype, const RmsBwdArgs& a, float* dg, hipStream_t s) {
-  return dtype == LD_BF16 ? rms_bwd_t<bf16>(a, dg, s) : rms_bwd_t<float>(a, dg, s);
+  if (dtype != LD_BF16) return rms_bwd_t<float, float, float, float>(a, dg, s);
+  return a.x_f32 ? rms_bwd_bf16_r<float>(a, dg, s) : rms_bwd_bf16_r<bf16>(a, dg, s);
 }
 
 hipError_t launch_relu2_fwd(int dtype, const EltArgs& a, hipStream_t s) {

@@ -160,11 +160,16 @@ struct ZeroArgs {
   int32_t count;
 };
 
+// Element types of the row kernels: g, y (forward) and gy, gx2 (backward)
+// have the configuration's type; the others say theirs (x_f32 etc.), so the
+// residual stream and the saved norm inputs can be float32 while the GEMM
+// operands are bf16.
 struct RmsFwdArgs {
   const void* x;      // source rows (through `src` map)
   RowMap src;
+  int32_t x_f32;      // x is float32 (else the configuration's type)
   const void* g;
-  void* xcopy;        // optional compacted copy of the source rows
+  float* xcopy;       // optional compacted float32 copy of the source rows
   void* y;            // compacted normalised rows
   float* rstd;        // compacted
   RowCount rc;
@@ -174,12 +179,17 @@ struct RmsFwdArgs {
 
 struct RmsBwdArgs {
   const void* x;      // compacted rows
+  int32_t x_f32;
   const void* g;
   const float* rstd;
   const void* gy;
-  const void* gres;   // optional compacted residual gradient
+  const void* gres;   // optional residual gradient rows (through `res_map`)
+  RowMap res_map;
+  int32_t gres_f32;
   void* gx;           // output rows through `dst` map
   RowMap dst;
+  int32_t gx_f32;
+  void* gx2;          // optional second, compacted copy of gx in the configuration's type
   float* dg_part;     // [n_blocks][d]
   RowCount rc;
   int32_t d;
@@ -200,6 +210,7 @@ struct RowsArgs {
   RowCount rc;
   int32_t d;
   float r;
+  int32_t src_f32;    // gather: src is float32 (converted to the dtype); else both have the dtype
 };
 
 // C[m, n] = (R ? R[m, n] : 0) + alpha * sum_k A(m, k) B(n, k), see ld_gemm.
@@ -215,6 +226,7 @@ struct GemmArgs {
   int32_t count_dim;
   RowMap out_map;            // output (and R) row remap; R uses it too when r_mapped
   int32_t r_mapped;
+  int32_t r_f32;             // R is float32 (else the configuration's type)
   float alpha;
   const float* alpha_dev;    // when set, alpha is multiplied by *alpha_dev
   int32_t c_f32;
@@ -356,6 +368,9 @@ hipError_t launch_skinny_reduce_act(const SkinnyArgs& g, int ksplit, int act, in
 hipError_t launch_kv_store(const KvArgs& a, hipStream_t s);
 hipError_t launch_attn_decode(const DecAttnArgs& a, hipStream_t s);
 hipError_t launch_gather(int dtype, const RowsArgs& a, hipStream_t s);
+// n elements between bf16 and float32 (to_f32: bf16 -> float32, else
+// float32 -> bf16 with round to nearest even); n % 8 == 0.
+hipError_t launch_convert(const void* src, void* dst, int64_t n, int to_f32, hipStream_t s);
 hipError_t launch_scatter_add(int dtype, const RowsArgs& a, hipStream_t s);
 hipError_t launch_rmsnorm_fwd(int dtype, const RmsFwdArgs& a, hipStream_t s);
 // Needs rmsnorm_bwd_blocks(max_rows) * d floats of dg_part.
