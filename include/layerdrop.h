@@ -415,6 +415,19 @@ int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int3
                 int32_t alibi, const void* qkv, const void* o, const float* lse, const void* go,
                 void* gqkv, void* ws, size_t ws_bytes, void* stream);
 
+/* ld_attn_bwd with no workspace argument and no allocation, for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc).  The delta rows live in a
+ * fixed scratch array built into the library: 8 MiB on each GPU it runs on,
+ * held until the process ends, so n_seq * n_heads * seq <= 2^21 (larger
+ * requests return LD_E_UNSUPPORTED before anything is launched).  Every call
+ * on a GPU shares that GPU's array, so calls that overlap on one GPU
+ * (other streams or threads) race.  The first call on a device looks up the
+ * array's address there.  Arguments and results as ld_attn_bwd. */
+int ld_attn_bwd_noalloc(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
+                        int32_t alibi, const void* qkv, const void* o, const float* lse, const void* go,
+                        void* gqkv, void* stream);
+
 /* ------------------------------------------------------------- profiling
  * Per-kernel timing with HIP events recorded on the launch stream around
  * every launch of the named kernel (its __global__ name, e.g.

@@ -84,6 +84,8 @@ _SIGS = {
     "ld_attn_bwd_ws_bytes": (_sz, [_i32, _i32, _i32]),
     "ld_attn_bwd": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                               _sz, _vp]),
+    "ld_attn_bwd_noalloc": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
+                                      _vp]),
     "ld_eval_ws_bytes": (_sz, [_PCFG]),
     "ld_stack_eval": (C.c_int, [_PCFG, _i32, C.POINTER(ld_weights), _vp, _vp, _vp, _vp, _i32, _vp,
                                 _sz, _vp]),
@@ -472,6 +474,12 @@ def ld_attn_bwd(n_seq, seq, n_heads, d_head, qkv, o, lse, go, gqkv, ws, stream=N
     _check(_lib.ld_attn_bwd(_dtype_code(qkv), n_seq, seq, n_heads, d_head, int(alibi), _ptr(qkv),
                             _ptr(o), _ptr(lse), _ptr(go), _ptr(gqkv), _ptr(ws),
                             ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ld_attn_bwd_noalloc(n_seq, seq, n_heads, d_head, qkv, o, lse, go, gqkv, stream=None, alibi=0):
+    _check(_lib.ld_attn_bwd_noalloc(_dtype_code(qkv), n_seq, seq, n_heads, d_head, int(alibi),
+                                    _ptr(qkv, "qkv"), _ptr(o, "o"), _ptr(lse, "lse"), _ptr(go, "go"),
+                                    _ptr(gqkv, "gqkv"), _stream(stream)))
 
 
 def ld_prof_start(kernel_name):

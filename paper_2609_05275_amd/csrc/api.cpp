@@ -2084,6 +2084,23 @@ int ld_attn_bwd(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int3
                          static_cast<float*>(ws), stream);
 }
 
+int ld_attn_bwd_noalloc(int32_t dtype, int32_t n_seq, int32_t seq, int32_t n_heads, int32_t d_head,
+                        int32_t alibi, const void* qkv, const void* o, const float* lse, const void* go,
+                        void* gqkv, void* stream) {
+  t_err.clear();
+  if (int rc = check_attn_bwd(dtype, n_seq, seq, n_heads, d_head, alibi)) return rc;
+  if (n_seq == 0) return LD_OK;
+  if (!qkv || !o || !lse || !go || !gqkv) return fail(LD_E_INVALID, "NULL pointer");
+  const size_t need = ld_attn_bwd_ws_bytes(n_seq, seq, n_heads);
+  if (need > kAttnScratchBytes)
+    return fail(LD_E_UNSUPPORTED, "n_seq * n_heads * seq = %lld exceeds the fixed scratch (%zu bytes, %zu rows)",
+                static_cast<long long>(need / 4), kAttnScratchBytes, kAttnScratchBytes / 4);
+  float* delta = nullptr;
+  hipError_t e = attn_scratch_ptr(&delta);
+  if (e != hipSuccess) return fail(LD_E_HIP, "scratch address: %s", hipGetErrorString(e));
+  return attn_bwd_common(dtype, n_seq, seq, n_heads, d_head, alibi, qkv, o, lse, go, gqkv, delta, stream);
+}
+
 // -------------------------------------------------------------- profiling
 
 int ld_prof_start(const char* kernel_name) {

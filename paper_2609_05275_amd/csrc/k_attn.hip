@@ -21,6 +21,7 @@
 //   diagonal.  Heavy causal tiles are scheduled first.
 // fp32 path: plain SIMT kernels, one thread per query (or key) row, used by
 // the fp32 configuration only.
+#include <mutex>
 #include <type_traits>
 
 #include "ld_internal.h"
@@ -1107,6 +1108,37 @@ hipError_t launch_attn_bwd_part(int dtype, int part, const AttnArgs& a, hipStrea
     case 64: return bwd_dh<64>(dtype, part, a, s);
   }
   return hipErrorInvalidValue;
+}
+
+// ----------------------------------------------- fixed scratch, no allocation
+// The backward's only scratch is delta = rowsum(dO * O).  The no-allocation
+// entry point keeps it in this array instead of a caller workspace; each GPU
+// holds its own copy until the process ends, and every call on a GPU shares
+// it (calls that overlap on one GPU race).  The delta kernel writes every
+// entry the other two kernels read, so nothing needs clearing.  On the host
+// the array's name is only a stand-in: kernels get the address
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) float scratch[kAttnScratchBytes / sizeof(float)];
+
+constexpr int kScratchMaxDevices = 64;
+
+hipError_t attn_scratch_ptr(float** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchMaxDevices) return hipErrorInvalidDevice;
+  static std::mutex mu;
+  static void* addr[kScratchMaxDevices] = {};
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = static_cast<float*>(addr[dev]);
+  return hipSuccess;
 }
 
 hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {

@@ -413,6 +413,12 @@ hipError_t launch_gemm_glu_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s);
 hipError_t launch_gemm_relu2_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s);
 hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmPlan& p, GemmArgs g,
                             int64_t max_m, hipStream_t s);
+// Fixed scratch of the no-allocation attention backward (the delta rows,
+// one float per (sequence, head, row)), a file-scope device array of this
+// many bytes in k_attn.hip.  attn_scratch_ptr gives its address on the
+// current device (looked up once per device; no allocation).
+constexpr size_t kAttnScratchBytes = size_t(8) << 20;
+hipError_t attn_scratch_ptr(float** out);
 hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
 // The three backward kernels one at a time: 0 delta, 1 dK/dV, 2 dQ.
