@@ -604,8 +604,6 @@ __device__ __forceinline__ void epilogue_rows_edge(const GemmArgs& g, float* par
 
 constexpr int kEpiPlain = 0, kEpiGluFwd = 1, kEpiGluBwd = 2, kEpiRelu2Fwd = 3, kEpiRelu2Bwd = 4;
 
-__device__ __forceinline__ float bf16r(float x) { return static_cast<float>(static_cast<bf16>(x)); }
-
 __device__ __forceinline__ uint2 pack4_bf16(float a, float b, float c, float d) {
   __attribute__((aligned(8))) bf16 o[4] = {static_cast<bf16>(a), static_cast<bf16>(b), static_cast<bf16>(c),
                                            static_cast<bf16>(d)};
@@ -669,15 +667,15 @@ __device__ __forceinline__ void glu_fwd_s_rows(const GemmArgs& g, const float* s
 }
 
 // Fused SwiGLU backward: the staged gs values (alpha applied; rows r0 + 2 it,
-// columns n..n+3 < N = f), rounded to bf16 as a stored gs would be, with u
-// and v read from aux, give gu and gv in C columns n and f + n.
+// columns n..n+3 < N = f), kept in float32 (gs is never stored), with u and
+// v read from aux, give gu and gv in C columns n and f + n.
 __device__ __forceinline__ void glu_bwd_one(const GemmArgs& g, float4 gs, uint2 ur, uint2 vr, int64_t m, int n) {
   const float4 u = unpack4_bf16(ur), v = unpack4_bf16(vr);
   float gu[4], gv[4];
-  swiglu_bwd_f(u.x, v.x, bf16r(gs.x), gu[0], gv[0]);
-  swiglu_bwd_f(u.y, v.y, bf16r(gs.y), gu[1], gv[1]);
-  swiglu_bwd_f(u.z, v.z, bf16r(gs.z), gu[2], gv[2]);
-  swiglu_bwd_f(u.w, v.w, bf16r(gs.w), gu[3], gv[3]);
+  swiglu_bwd_f(u.x, v.x, gs.x, gu[0], gv[0]);
+  swiglu_bwd_f(u.y, v.y, gs.y, gu[1], gv[1]);
+  swiglu_bwd_f(u.z, v.z, gs.z, gu[2], gv[2]);
+  swiglu_bwd_f(u.w, v.w, gs.w, gu[3], gv[3]);
   bf16* C = static_cast<bf16*>(g.C) + m * g.ldc;
   *reinterpret_cast<uint2*>(C + n) = pack4_bf16(gu[0], gu[1], gu[2], gu[3]);
   *reinterpret_cast<uint2*>(C + g.glu_f + n) = pack4_bf16(gv[0], gv[1], gv[2], gv[3]);
@@ -713,10 +711,10 @@ __device__ __forceinline__ void glu_bwd_rows(const GemmArgs& g, const float* sta
 }
 
 // Fused squared-ReLU forward: staged values (alpha applied) of rows r0 + 2 it,
-// columns n..n+3, go to C as u (bf16) and to aux as s = relu(u)^2 of the
-// bf16 u, as the elementwise kernel computes it from a stored u.
+// columns n..n+3, go to C as u (bf16, kept for the backward) and to aux as
+// s = relu(u)^2 of the float32 u (one rounding fewer than from a stored u).
 __device__ __forceinline__ void relu2_fwd_one(const GemmArgs& g, float4 v, int64_t m, int n) {
-  const float u[4] = {bf16r(v.x), bf16r(v.y), bf16r(v.z), bf16r(v.w)};
+  const float u[4] = {v.x, v.y, v.z, v.w};
   float q[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -745,13 +743,13 @@ __device__ __forceinline__ void relu2_fwd_rows(const GemmArgs& g, const float* s
   }
 }
 
-// Fused squared-ReLU backward: the staged gs values, rounded to bf16 as a
-// stored gs would be, with u read from aux, give gu = gs 2 relu(u) in C.
+// Fused squared-ReLU backward: the staged gs values, kept in float32 (gs is
+// never stored), with u read from aux, give gu = gs 2 relu(u) in C.
 __device__ __forceinline__ void relu2_bwd_one(const GemmArgs& g, float4 gs, uint2 ur, int64_t m, int n) {
   const float4 u = unpack4_bf16(ur);
   *reinterpret_cast<uint2*>(static_cast<bf16*>(g.C) + m * g.ldc + n) =
-      pack4_bf16(bf16r(gs.x) * 2.f * fmaxf(u.x, 0.f), bf16r(gs.y) * 2.f * fmaxf(u.y, 0.f),
-                 bf16r(gs.z) * 2.f * fmaxf(u.z, 0.f), bf16r(gs.w) * 2.f * fmaxf(u.w, 0.f));
+      pack4_bf16(gs.x * 2.f * fmaxf(u.x, 0.f), gs.y * 2.f * fmaxf(u.y, 0.f), gs.z * 2.f * fmaxf(u.z, 0.f),
+                 gs.w * 2.f * fmaxf(u.w, 0.f));
 }
 
 __device__ __forceinline__ void relu2_bwd_rows(const GemmArgs& g, const float* stage, int r0, int half, int c,
@@ -909,8 +907,10 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
       const int gc = tn * 128 + wn * 64 + (c & 63) + (c >= 64 ? g.glu_f : 0);
       glu_fwd_uv_rows(g, stage, mb + half, half, c, gc, M, mb + 32 <= M);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      // s = silu(u) v from the pairs of accumulators, staged over the gate
-      // columns and stored as 64-column rows
+      // s = silu(u) v from the pairs of float32 accumulators (the stored
+      // [u v] are bf16; rounding them first would add the largest single
+      // error of the block's forward), staged over the gate columns and
+      // stored as 64-column rows
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -918,7 +918,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
           float sv[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            sv[e] = swiglu_fwd_f(bf16r(alpha * acc[i][j][4 * q + e]), bf16r(alpha * acc[i][j + 2][4 * q + e]));
+            sv[e] = swiglu_fwd_f(alpha * acc[i][j][4 * q + e], alpha * acc[i][j + 2][4 * q + e]);
           *reinterpret_cast<float4*>(stage + lm * kStagePitch + j * 32 + 8 * q + 4 * half) =
               make_float4(sv[0], sv[1], sv[2], sv[3]);
         }

@@ -232,8 +232,7 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_fwd_k(RmsFwdArgs a) {
   if (lane == 0) a.rstd[row] = rstd;
 }
 
-constexpr int kBwdRowsPerWave = 8;
-constexpr int kBwdRowsPerBlock = 4 * kBwdRowsPerWave;
+constexpr int kBwdRowsPerBlock = 16;
 
 template <typename TX, typename TY, typename TR, int VN, int NCH>
 struct NormRow {
@@ -243,16 +242,17 @@ struct NormRow {
   float rstd;
 };
 
+// Column of chunk c of thread t: (c * 256 + t) * VN.
 template <typename TX, typename TY, typename TR, int VN, int NCH>
 __device__ __forceinline__ void norm_row_load(NormRow<TX, TY, TR, VN, NCH>& r, const RmsBwdArgs& a, int64_t row,
-                                              int lane) {
+                                              int tid) {
   const TX* x = static_cast<const TX*>(a.x) + row * a.d;
   const TY* gy = static_cast<const TY*>(a.gy) + row * a.d;
   const TR* gres = a.gres ? static_cast<const TR*>(a.gres) + map_row(a.res_map, row) * a.d : nullptr;
   r.rstd = a.rstd[row];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    const int col = (c * 64 + lane) * VN;
+    const int col = (c * 256 + tid) * VN;
     if (col < a.d) {
       r.x[c] = ldc<TX, VN>(x + col);
       r.gy[c] = ldc<TY, VN>(gy + col);
@@ -263,45 +263,44 @@ __device__ __forceinline__ void norm_row_load(NormRow<TX, TY, TR, VN, NCH>& r, c
 
 // gx = gres + rstd*(g*gy) - x*rstd^3*mean_d(x*g*gy), written through the dst
 // map (type TO) and, when gx2 is set, as a compacted copy in the
-// configuration's type; per-block dg partials summed over the block's rows
-// in a fixed order (rows in sequence inside a wave, then waves 0..3 through
-// LDS).  Where a lane's rows fit in registers twice, the next row's loads are
-// issued before the current row's reduction (two rows in flight per wave).
+// configuration's type.  A workgroup takes a strip of kBwdRowsPerBlock rows;
+// thread t owns the same columns of every row, so its dg = sum_rows gy*x*rstd
+// is summed in registers (rows in order) and written as the block's partial
+// with no cross-thread reduction.  A row's dot product is summed over the
+// wave (shuffles), then over the 4 waves in order through LDS (two slots by
+// row parity: one barrier per row).  The next row's loads are issued before
+// the current row's reduction.
 template <typename TX, typename TY, typename TR, typename TO, int VN, int NCH>
 __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
-  extern __shared__ float dg_lds[];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ float red[2][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t rows = row_count(a.rc);
+  const int64_t r0 = blockIdx.x * static_cast<int64_t>(kBwdRowsPerBlock);
+  const int64_t r1 = min(r0 + kBwdRowsPerBlock, rows);
   const TY* gp = static_cast<const TY*>(a.g);
   Chunk<TY, VN> graw[NCH];
   float dga[NCH][VN];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    const int col = (c * 64 + lane) * VN;
-    if (col < a.d) graw[c] = ldc<TY, VN>(gp + col);
+    const int col = (c * 256 + tid) * VN;
+    if (col < a.d) {
+      graw[c] = ldc<TY, VN>(gp + col);
+    } else {
 #pragma unroll
-    for (int i = 0; i < VN; ++i) {
-      if (col >= a.d) graw[c].v[i] = from_f<TY>(0.f);
-      dga[c][i] = 0.f;
+      for (int i = 0; i < VN; ++i) graw[c].v[i] = from_f<TY>(0.f);
     }
+#pragma unroll
+    for (int i = 0; i < VN; ++i) dga[c][i] = 0.f;
   }
   const float inv_d = 1.f / static_cast<float>(a.d);
-  const int64_t r0 = blockIdx.x * static_cast<int64_t>(kBwdRowsPerBlock) + wave * kBwdRowsPerWave;
-  const int64_t r1 = min(r0 + kBwdRowsPerWave, rows);
-  constexpr int kRowBytes = NCH * VN * (sizeof(TX) + sizeof(TY) + sizeof(TR));
-  constexpr bool kPrefetch = kRowBytes <= 4 * 8 * 6;   // at most 48 registers a row
   NormRow<TX, TY, TR, VN, NCH> cur, nxt;
-  if (kPrefetch && r0 < r1) norm_row_load(cur, a, r0, lane);
+  if (r0 < r1) norm_row_load(cur, a, r0, tid);
   for (int64_t row = r0; row < r1; ++row) {
-    if (kPrefetch) {
-      if (row + 1 < r1) norm_row_load(nxt, a, row + 1, lane);
-    } else {
-      norm_row_load(cur, a, row, lane);
-    }
+    if (row + 1 < r1) norm_row_load(nxt, a, row + 1, tid);
     float dot = 0.f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int col = (c * 64 + lane) * VN;
+      const int col = (c * 256 + tid) * VN;
       if (col < a.d) {
 #pragma unroll
         for (int i = 0; i < VN; ++i)
@@ -309,13 +308,17 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
       }
     }
     dot = wave_sum(dot);
+    const int slot = static_cast<int>(row - r0) & 1;
+    if (lane == 0) red[slot][wave] = dot;
+    __syncthreads();
+    dot = ((red[slot][0] + red[slot][1]) + red[slot][2]) + red[slot][3];
     const float rstd = cur.rstd;
     const float coef = rstd * rstd * rstd * dot * inv_d;
     TO* gx = static_cast<TO*>(a.gx) + map_row(a.dst, row) * a.d;
     TY* gx2 = a.gx2 ? static_cast<TY*>(a.gx2) + row * a.d : nullptr;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int col = (c * 64 + lane) * VN;
+      const int col = (c * 256 + tid) * VN;
       if (col < a.d) {
         Chunk<TO, VN> o;
         Chunk<TY, VN> o2;
@@ -332,23 +335,19 @@ __global__ __launch_bounds__(256) void ld_rmsnorm_bwd_k(RmsBwdArgs a) {
         if (gx2) stc<TY, VN>(gx2 + col, o2);
       }
     }
-    if (kPrefetch) cur = nxt;
-  }
-  for (int w = 0; w < 4; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        const int col = (c * 64 + lane) * VN;
-        if (col < a.d) {
-#pragma unroll
-          for (int i = 0; i < VN; ++i) dg_lds[col + i] = (w == 0 ? 0.f : dg_lds[col + i]) + dga[c][i];
-        }
-      }
-    }
-    __syncthreads();
+    cur = nxt;
   }
   float* part = a.dg_part + static_cast<int64_t>(blockIdx.x) * a.d;
-  for (int col = threadIdx.x; col < a.d; col += 256) part[col] = dg_lds[col];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int col = (c * 256 + tid) * VN;
+    if (col < a.d) {
+      Chunk<float, VN> o;
+#pragma unroll
+      for (int i = 0; i < VN; ++i) o.v[i] = dga[c][i];
+      stc<float, VN>(part + col, o);
+    }
+  }
 }
 
 // dg[c] = sum over blocks of part[b][c] in a fixed order: 32 row-strided
@@ -503,11 +502,12 @@ template <typename TX, typename TY, typename TR, typename TO>
 hipError_t rms_bwd_t(const RmsBwdArgs& a, float* dg, hipStream_t s) {
   constexpr int VN = std::is_same<TY, bf16>::value ? 8 : 4;
   const int64_t nblk = rmsnorm_bwd_blocks(a.rc.rows);
-  const size_t lds = static_cast<size_t>(a.d) * sizeof(float);
+  // chunks of VN columns per thread of the 256
+  const int nch = (a.d + 256 * VN - 1) / (256 * VN);
 #define LD_RB(N) \
-  case N: hipLaunchKernelGGL((ld_rmsnorm_bwd_k<TX, TY, TR, TO, VN, N>), dim3(nblk), dim3(256), lds, s, a); break;
-  switch (nch_bucket<VN>(a.d)) {
-    LD_RB(1) LD_RB(2) LD_RB(4) LD_RB(8)
+  case N: hipLaunchKernelGGL((ld_rmsnorm_bwd_k<TX, TY, TR, TO, VN, N>), dim3(nblk), dim3(256), 0, s, a); break;
+  switch (nch <= 1 ? 1 : 2) {
+    LD_RB(1) LD_RB(2)
   }
 #undef LD_RB
   hipError_t e = hipGetLastError();

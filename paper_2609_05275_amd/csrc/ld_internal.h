@@ -63,8 +63,9 @@ __device__ __forceinline__ void dma_barrier() {
 // SwiGLU on float inputs (the gate u and up v as stored): s = silu(u) v, and
 // the gradients gu = g v silu'(u), gv = g silu(u) with
 // silu'(u) = sigmoid(u) (1 + u (1 - sigmoid(u))).  One definition for the
-// elementwise kernels and the GEMM epilogues that fuse them, so both give
-// the same bits.
+// elementwise kernels and the GEMM epilogues that fuse them; the fused ones
+// apply it to float32 accumulator values where the elementwise kernels read
+// the stored bf16 tensors.
 __device__ __forceinline__ float swiglu_sigmoid(float u) { return 1.f / (1.f + expf(-u)); }
 __device__ __forceinline__ float swiglu_fwd_f(float u, float v) { return u * swiglu_sigmoid(u) * v; }
 __device__ __forceinline__ void swiglu_bwd_f(float u, float v, float g, float& gu, float& gv) {
