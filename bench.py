@@ -84,6 +84,29 @@ def traffic_record(kernel, workload):
     return rec
 
 
+def counters_record(workload):
+    """Per-kernel counter records (MFMA busy, clock, HBM bytes) of the
+    committed counter summary for this workload, keyed by kernel name without
+    template arguments; kernels whose sources changed since are left out."""
+    rec = profsum.read_counters(os.path.join(ROOT, "profiles", f"stack_step_{workload}_counters.md"))
+    if not rec:
+        return {}
+    out, hashes = {}, {}
+    for name, r in rec.items():
+        src = r.get("source")
+        if not src:
+            continue
+        if src not in hashes:
+            hashes[src] = profsum.source_hash(src, ROOT)
+        if hashes[src] != r.get("source_sha256"):
+            continue
+        base = name.split("<")[0]
+        prev = out.get(base)
+        if prev is None or r["calls"] > prev["calls"]:
+            out[base] = r
+    return out
+
+
 def copy_calibration(mib):
     """Elementwise y = 1 * x over float32 tensors of `mib` MiB, 3 times: the
     known-size reference the HBM traffic counters are scaled by."""
@@ -200,9 +223,11 @@ HBM_KERNELS = ["ld_mask_compact", "ld_rmsnorm_fwd_k", "ld_rmsnorm_bwd_k", "ld_ga
                "ld_attn_delta", "ld_splitk_reduce"]
 
 
-def hbm_kernels(st, ps, step):
+def hbm_kernels(st, ps, step, crec):
     """One profiled step per kernel: launches, average duration (HIP events on
-    the library's stream), algorithmic bytes and the rate they imply."""
+    the library's stream), algorithmic bytes and the rate they imply; with a
+    counter record for the kernel, also its counter-measured HBM bytes per
+    launch and the rate those imply at this run's duration."""
     out = {}
     for k in HBM_KERNELS:
         ld.ld_prof_start(k)
@@ -217,6 +242,11 @@ def hbm_kernels(st, ps, step):
                   "avg_us": round(r["ms"] * 1e3 / r["launches"], 2),
                   "bytes_per_launch": round(r["bytes"] / r["launches"]),
                   "gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        c = crec.get(k)
+        if c and "hbm_bytes" in c:
+            cg = c["hbm_bytes"] / max(r["ms"] * 1e-3 / r["launches"], 1e-12) / 1e9
+            out[k].update(counter_bytes_per_launch=c["hbm_bytes"], counter_gbs=round(cg, 1),
+                          counter_frac=round(cg / PEAK_HBM_GBS, 4))
     return out
 
 
@@ -414,7 +444,8 @@ def main():
     pr = ld.ld_prof_result()
     exec_tflops = exec_flops(kept) / (ms * 1e-3) / 1e12
     achieved = pr["flops"] / (pr["ms"] * 1e-3) / 1e12 if pr["ms"] > 0 else 0.0
-    hbm = hbm_kernels(st, ps, first)
+    crec = counters_record(args.workload)
+    hbm = hbm_kernels(st, ps, first, crec)
     print(f"# hbm kernels: {json.dumps(hbm)}", file=sys.stderr, flush=True)
     maskb = mask_microbench(dev)
     print(f"# mask microbench: {json.dumps(maskb)}", file=sys.stderr, flush=True)
@@ -496,7 +527,12 @@ def main():
                      "traffic_unit": "bytes per launch (HBM, counter-measured)",
                      "algorithmic_bytes": round(pr["bytes"] / max(pr["launches"], 1)),
                      "launches": pr["launches"],
-                     "avg_launch_us": round(pr["ms"] * 1e3 / max(pr["launches"], 1), 2)},
+                     "avg_launch_us": round(pr["ms"] * 1e3 / max(pr["launches"], 1), 2),
+                     "mfma_busy": crec.get(prof_kernel, {}).get("mfma_busy"),
+                     "clock_ghz": crec.get(prof_kernel, {}).get("clock_ghz")},
+        "mfma_kernels": {k: {kk: v[kk] for kk in ("avg_us", "clock_ghz", "mfma_busy", "mfma_tflops")
+                             if kk in v}
+                         for k, v in crec.items() if "mfma_busy" in v and v["mfma_busy"] > 0},
         "hbm_kernels": hbm,
         "mask_microbench": maskb,
         "cpu_baseline": cpu,

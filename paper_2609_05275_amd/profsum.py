@@ -140,12 +140,13 @@ def kernel_source(kernel: str) -> str | None:
 
 
 def _durations(db: str) -> dict[str, tuple[int, float]]:
+    """(calls, total microseconds) per kernel of a --kernel-trace --stats run."""
     con = sqlite3.connect(db)
     out: dict[str, tuple[int, float]] = {}
     for n, c, t in con.execute("select name, total_calls, total_duration from top_kernels"):
         k = short(n)
         c0, t0 = out.get(k, (0, 0.0))
-        out[k] = (c0 + int(c), t0 + float(t))   # total_duration in ns
+        out[k] = (c0 + int(c), t0 + float(t))   # top_kernels durations are in microseconds
     return out
 
 
@@ -174,10 +175,10 @@ def counters(trace_db: str, mfma_db: str, fetch_db: str, write_db: str, title: s
     write = _means(write_db, "WRITE_SIZE")
     recs = {}
     for k in sorted(dur, key=lambda k: -dur[k][1]):
-        calls, tot_ns = dur[k]
+        calls, tot_us = dur[k]
         if not k.startswith("ld_") or calls == 0:
             continue
-        avg_us = tot_ns / calls / 1e3
+        avg_us = tot_us / calls
         r = {"calls": calls, "avg_us": round(avg_us, 2)}
         if k in grbm and grbm[k][1] > 0:
             cyc = grbm[k][1] / N_XCD
