@@ -294,18 +294,24 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 // MFMA blocks, 256 fp32 accumulators per lane), k walked in tiles of 32.
 //
 // Operand tiles go from global memory straight into LDS: buffer loads with an
-// LDS destination, so no register staging and no LDS write instructions, in a
-// ring of four stages (32 KB each: the A and B tiles), so the loads of a tile
-// have three tile-times to land.  Such a load writes the 16 bytes of lane i
-// at LDS offset 16*i from a wave-uniform base, so the LDS layout is set by
-// which global chunk each lane fetches:
-//   k-contiguous operand: [256 rows][32 k], the 16-byte chunks of a row
-//     XOR-swizzled by the row; a fragment is one 16-byte read per lane.
-//   mn-contiguous operand: [32 k][256 mn] as in memory, chunks XOR-swizzled
-//     by k; a fragment is two transposing reads (ds_read_b64_tr_b16: in each
-//     group of 16 lanes, lane j receives element j%4 of the four-element rows
-//     read by lanes j/4, j/4+4, j/4+8 and j/4+12, so 16 lanes reading rows
-//     k..k+3 at mn offsets 0, 4, 8, 12 give lane j the values k..k+3 at mn j).
+// LDS destination, so no register staging and no LDS write instructions.
+// Such a load writes the 16 bytes of lane i at LDS offset 16*i from a
+// wave-uniform base, so the LDS layout is set by which global chunk each lane
+// fetches.  Each operand has a region of the ring:
+//   mn-contiguous operand: four stages of one k tile, [32 k][256 mn] as in
+//     memory, chunks XOR-swizzled by k; a load instruction fetches two whole
+//     512-byte k rows.  A fragment is two transposing reads
+//     (ds_read_b64_tr_b16: in each group of 16 lanes, lane j receives element
+//     j%4 of the four-element rows read by lanes j/4, j/4+4, j/4+8 and
+//     j/4+12, so 16 lanes reading rows k..k+3 at mn offsets 0, 4, 8, 12 give
+//     lane j the values k..k+3 at mn j).
+//   k-contiguous operand: slots of a PAIR of k tiles, [256 rows][64 k], so
+//     a load instruction fetches 8 rows as whole 128-byte lines (a single k
+//     tile is 64 bytes of a row: half lines, twice the cache requests for
+//     the same bytes).  Two slots, or three for A when both operands are
+//     k-contiguous (96 KB; the ring is then the whole 160 KB of LDS).  The
+//     16-byte chunks of a row are XOR-swizzled by the row; a fragment is one
+//     16-byte read per lane.
 // Rows past the operand's end, and k chunks past the split's end, are
 // fetched from an offset outside the buffer descriptor's range and land in
 // LDS as zeros.  The loads are issued as inline assembly (ld_internal.h),
@@ -315,9 +321,13 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 // Per k tile (two k-substeps of 16): one barrier at the top, where each wave
 // has waited until the next tile has landed; then the tile's 32 MFMAs run on
 // fragments read during the previous tile, next to the reads of all of the
-// next tile's fragments and the loads of the tile four ahead, which go into
-// the stage this tile was read from (its reads completed before the
-// barrier).  No MFMA waits on a recent LDS read.
+// next tile's fragments and the loads for later tiles: an mn-contiguous
+// stage is reloaded (tile kt+4) during the tile kt it holds, whose fragments
+// were read before the barrier; a k-contiguous slot is reloaded once both
+// of its tiles have been read: with two slots, pair kt+3, kt+4 during odd
+// tiles kt; A's third slot lets its pair kt+5, kt+6 load half during odd
+// tile kt and half during kt+1.  Every load has at least one tile-time,
+// most two or more, to land.  No MFMA waits on a recent LDS read.
 //
 // The MFMA is issued as B x A so each lane ends with 4 consecutive output
 // columns of one row.  Tiles are ordered XCD-aware: consecutive workgroup ids
@@ -325,26 +335,47 @@ constexpr size_t kGemmLds = 4 * kTileElems * sizeof(bf16);
 // range of tiles, walked in groups of 8 tile-rows for L2 reuse.  Split-K
 // (grid.y) writes fp32 partials that a second kernel sums in split order.
 
-constexpr int GB = 256, GK = 32, NSTAGE = 4;
-constexpr int kBigTile = GB * GK;      // elements per operand tile
-constexpr int kStage = 2 * kBigTile;   // A and B tiles of one stage
-constexpr int kLoads = 4;              // load instructions per wave per operand tile
-constexpr int kStagePitch = 132;       // floats per staged epilogue row (128 + 4 pad)
+constexpr int GB = 256, GK = 32;
+constexpr int kBigTile = GB * GK;       // elements of one operand's k tile
+constexpr int kLoadsMC = 4;             // load instructions per wave per mn-contiguous tile
+constexpr int kLoadsKC = 8;             // load instructions per wave per k-contiguous pair
+constexpr int kStagePitch = 132;        // floats per staged epilogue row (128 + 4 pad)
 constexpr uint32_t kOob = kDmaOob;
 constexpr int64_t kBigMaxSpan = kDmaMaxSpan;
-static_assert(NSTAGE * kStage * 2 >= 4 * 32 * kStagePitch * 4, "epilogue staging fits the stages");
+// Ring regions (elements): a k-contiguous A takes three pair slots when B
+// is k-contiguous too, every other operand four tile stages or two pair
+// slots (64 KB).
+template <bool AK, bool BKC>
+constexpr int slots_a() { return AK && BKC ? 3 : 2; }
+template <bool AK, bool BKC>
+constexpr int region_a() { return AK ? slots_a<AK, BKC>() * 2 * kBigTile : 4 * kBigTile; }
+template <bool AK, bool BKC>
+constexpr int ring_elems() { return region_a<AK, BKC>() + 4 * kBigTile; }
+static_assert(ring_elems<true, true>() * 2 <= 160 * 1024, "the ring fits the LDS");
+static_assert(ring_elems<false, false>() * 2 >= 4 * 32 * kStagePitch * 4, "epilogue staging fits the ring");
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef dma_rsrc v4i;
 #define LD_LDS(T, p) ((__attribute__((address_space(3))) T*)(p))
 
-// k-contiguous tile: element (row, k) of a [256][32] tile.  The chunk swizzle
-// depends on row bits 2-3 only: 16 lanes reading one chunk of 16 consecutive
-// rows hit 16 different 16-byte bank groups, and moving by a multiple of 32
-// rows is a plain offset.
-__device__ __forceinline__ int kc_swz(int row) { return (row >> 2) & 3; }
+// Element offset, in an operand's region, of the stage (mn-contiguous) or
+// pair slot (k-contiguous, NS slots) holding k tile kt.
+template <bool KC, int NS>
+__device__ __forceinline__ int tile_base(int kt) {
+  if constexpr (KC)
+    return ((kt >> 1) % NS) * (2 * kBigTile);
+  else
+    return (kt & 3) * kBigTile;
+}
+
+// k-contiguous pair slot: element (row, k) of a [256][64] slot.  The chunk
+// swizzle uses row bits 1-3: of 16 lanes reading one chunk of 16
+// consecutive rows, the two rows of each pair sit 128 bytes apart and the 8
+// pairs on 8 different chunks, so all 16 hit different 16-byte bank groups;
+// moving by a multiple of 16 rows is a plain offset.
+__device__ __forceinline__ int kc_swz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int swz_off(int row, int k) {
-  return row * GK + (((k >> 3) ^ kc_swz(row)) << 3) + (k & 7);
+  return row * (2 * GK) + ((((k >> 3) ^ kc_swz(row)) << 3) | (k & 7));
 }
 
 // mn-contiguous tile: element (k, m) of a [32][256] tile.  The swizzle puts
@@ -360,8 +391,8 @@ __device__ __forceinline__ int mc_off(int k, int m) {
 template <bool KC>
 struct OpLanes {
   uint32_t ld_off[2];  // byte offset of the lane's first 16-byte chunk (mn: per k-row parity)
-  int kchunk;          // k-contiguous: k offset of the lane's chunk in the tile
-  int frag[4];         // element offsets of fragment reads: per k-substep (KC) or block (MC)
+  int kchunk;          // k-contiguous: k offset of the lane's chunk in the pair
+  int frag[4];         // element offsets of fragment reads: per (k half, k-substep) (KC) or block (MC)
 };
 
 // `r`: the first of the wave's 128 fragment rows (0 or 128).
@@ -369,14 +400,16 @@ template <bool KC>
 __device__ __forceinline__ OpLanes<KC> op_lanes(int64_t ld, int lane, int wave, int r) {
   OpLanes<KC> o;
   if constexpr (KC) {
-    // load instruction p fills rows (4p + wave)*16 .. +15, lane -> row +
-    // lane/4, physical chunk lane%4; the swizzle is the same for every p
-    const int row = wave * 16 + (lane >> 2);
-    o.kchunk = ((lane & 3) ^ kc_swz(row)) << 3;
+    // load instruction p fills slot rows 8 (4p + wave) .. +7, lane -> row
+    // + lane/8, physical chunk lane%8; the swizzle is the same for every p
+    const int row = wave * 8 + (lane >> 3);
+    o.kchunk = ((lane & 7) ^ kc_swz(row)) << 3;
     o.ld_off[0] = o.ld_off[1] = static_cast<uint32_t>((static_cast<int64_t>(row) * ld + o.kchunk) * 2);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) o.frag[ks] = swz_off(r + (lane & 31), ks * 16 + (lane >> 5) * 8);
-    o.frag[2] = o.frag[3] = 0;
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        o.frag[2 * h + ks] = swz_off(r + (lane & 31), h * GK + ks * 16 + (lane >> 5) * 8);
   } else {
     // load instruction p fills k rows 8p + 2*wave + lane/32, physical chunk
     // lane%32; the swizzle depends on p only through its parity (k bit 3)
@@ -396,10 +429,11 @@ __device__ __forceinline__ OpLanes<KC> op_lanes(int64_t ld, int lane, int wave, 
   return o;
 }
 
-// Load instruction p (0-3) of the tile (rows r0.., k0..) of operand X into
-// `lds`: 16 bytes per lane; all 4 fill the tile.  k-contiguous: instruction p
-// fills 16 rows per wave; mn-contiguous: 2 k rows.  Columns past the end of a
-// valid row read real memory; they only reach outputs that are never stored,
+// Load instruction p of operand X's rows r0.. into `lds` (its stage or
+// slot), 16 bytes per lane.  mn-contiguous: instruction p (0-3) fills 2 k
+// rows per wave of the tile at k0.  k-contiguous: instruction p (0-7) fills
+// 8 rows per wave of the pair at k0 (64 k).  Columns past the end of a valid
+// row read real memory; they only reach outputs that are never stored,
 // except a k tail of a k-contiguous operand, which is fetched out of range
 // (zeros), as is everything of a tile that starts at or past K.
 template <bool KC>
@@ -407,7 +441,7 @@ __device__ __forceinline__ void tile_part(bf16* lds, const OpLanes<KC>& o, const
                                           int r0, int R, int k0, int K, int wave, int p) {
   if constexpr (KC) {
     const v4i rs = dma_make_rsrc(X + static_cast<int64_t>(r0) * ld, (static_cast<int64_t>(R) - r0) * ld * 2);
-    const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 64 * ld + k0) * 2);
+    const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p) * 32 * ld + k0) * 2);
     const uint32_t off = k0 + o.kchunk < K ? o.ld_off[0] + u : kOob;
     dma16(rs, lds + (p * 4 + wave) * 512, off);
   } else {
@@ -418,28 +452,33 @@ __device__ __forceinline__ void tile_part(bf16* lds, const OpLanes<KC>& o, const
   (void)R;
 }
 
-// B tile of the fused SwiGLU forward: load instruction p fills the tile's
-// 64-row block p with gate rows (p even) or up rows (p odd)
-// tn*128 + (p/2)*64 .. +63 of W_gate_up [2f, K], so the tile holds
-// [gate 0-63 | up 0-63 | gate 64-127 | up 64-127] of its 128 d_ff columns and
-// each wave's 128 rows pair every gate row with its up row 64 further on.
+// B slot of the fused SwiGLU forward: the slot's 64-row block b = p/2 holds
+// gate rows (b even) or up rows (b odd) tn*128 + (b/2)*64 .. +63 of
+// W_gate_up [2f, K], so the tile holds [gate 0-63 | up 0-63 | gate 64-127 |
+// up 64-127] of its 128 d_ff columns and each wave's 128 rows pair every
+// gate row with its up row 64 further on.  Instruction p (0-7) fills rows
+// 32 (p%2) + 8 wave .. +7 of block b.
 __device__ __forceinline__ void tile_part_glu(bf16* lds, const OpLanes<true>& o, const bf16* W, int64_t ld,
                                               int tn, int f, int k0, int K, int wave, int p) {
-  const int64_t rbase = ((p & 1) ? f : 0) + static_cast<int64_t>(tn) * 128 + (p >> 1) * 64;
+  const int b = p >> 1;
+  const int64_t rbase = ((b & 1) ? f : 0) + static_cast<int64_t>(tn) * 128 + (b >> 1) * 64;
   const v4i rs = dma_make_rsrc(W + rbase * ld, 64 * ld * 2);
-  const uint32_t off = k0 + o.kchunk < K ? o.ld_off[0] + static_cast<uint32_t>(k0 * 2) : kOob;
+  const uint32_t u = static_cast<uint32_t>((static_cast<int64_t>(p & 1) * 32 * ld + k0) * 2);
+  const uint32_t off = k0 + o.kchunk < K ? o.ld_off[0] + u : kOob;
   dma16(rs, lds + (p * 4 + wave) * 512, off);
 }
 
-// Fragment of block i of the wave's 128 rows for k-substep ks: the lane's
-// MFMA row is r + 32 i + lane % 32 (r as given to op_lanes), its 8 k values
-// start at ks*16 + (lane/32)*8.  Only the per-lane offset is a register; the
-// rest is a constant offset of the LDS instruction.
+// Fragment of block i of the wave's 128 rows for k-substep ks of the tile
+// whose stage or slot starts at t (h: the tile's half of a k-contiguous
+// pair): the lane's MFMA row is r + 32 i + lane % 32 (r as given to
+// op_lanes), its 8 k values start at ks*16 + (lane/32)*8.  Only the per-lane
+// offset is a register; the rest is a constant offset of the LDS instruction.
 template <bool KC>
-__device__ __forceinline__ bf16x8 frag(const bf16* t, const OpLanes<KC>& o, int i, int ks) {
+__device__ __forceinline__ bf16x8 frag(const bf16* t, const OpLanes<KC>& o, int i, int h, int ks) {
   if constexpr (KC) {
-    return *reinterpret_cast<const bf16x8*>(t + 32 * i * GK + o.frag[ks]);
+    return *reinterpret_cast<const bf16x8*>(t + 32 * i * (2 * GK) + o.frag[2 * h + ks]);
   } else {
+    (void)h;
     const bf16* p = t + o.frag[i] + ks * 16 * GB;
     const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LD_LDS(v4s, p));
     const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LD_LDS(v4s, p + 4 * GB));
@@ -810,23 +849,44 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
 
   const OpLanes<AK> oa = op_lanes<AK>(g.lda, lane, wave, wm * 128);
   const OpLanes<BKC> ob = op_lanes<BKC>(g.ldb, lane, wave, wn * 128);
-  // load instruction q (0-7) of tile kt into stage st: A's 4, then B's 4
-  auto load_part = [&](int st, int kt, int q) {
-    bf16* sa = ring + st * kStage;
-    const int k0 = (kt0 + kt) * GK;
-    if (q < kLoads)
-      tile_part<AK>(sa, oa, A, g.lda, m0, M, k0, kend, wave, q);
-    else if constexpr (EPI == kEpiGluFwd)
-      tile_part_glu(sa + kBigTile, ob, B, g.ldb, tn, g.glu_f, k0, kend, wave, q - kLoads);
-    else
-      tile_part<BKC>(sa + kBigTile, ob, B, g.ldb, n0, g.N, k0, kend, wave, q - kLoads);
+  constexpr int NSA = slots_a<AK, BKC>(), NSB = 2;  // pair slots of a k-contiguous A, B
+  bf16* const ra = ring;                            // A's region
+  bf16* const rb = ring + region_a<AK, BKC>();      // B's region
+  // Load instruction q of A or B into the stage of tile kt (mn-contiguous,
+  // q 0-3) or the slot of the pair starting at tile kt (k-contiguous, q 0-7).
+  auto load_a = [&](int kt, int q) {
+    tile_part<AK>(ra + tile_base<AK, NSA>(kt), oa, A, g.lda, m0, M, (kt0 + kt) * GK, kend, wave, q);
   };
-  // The ring starts full: tiles 0-3 (zeros past the split's end).
+  auto load_b = [&](int kt, int q) {
+    if constexpr (EPI == kEpiGluFwd)
+      tile_part_glu(rb + tile_base<true, NSB>(kt), ob, B, g.ldb, tn, g.glu_f, (kt0 + kt) * GK, kend, wave, q);
+    else
+      tile_part<BKC>(rb + tile_base<BKC, NSB>(kt), ob, B, g.ldb, n0, g.N, (kt0 + kt) * GK, kend, wave, q);
+  };
+  // The ring starts full: per k tile t = 0..3, A's then B's loads of that
+  // tile (a k-contiguous operand loads its pair at even t), then, with three
+  // A slots, the first half of A's pair at tiles 4, 5; zeros past the
+  // split's end.
 #pragma unroll
-  for (int st = 0; st < NSTAGE; ++st)
+  for (int t = 0; t < 4; ++t) {
 #pragma unroll
-    for (int q = 0; q < 2 * kLoads; ++q) load_part(st, st, q);
-  dma_barrier<(NSTAGE - 1) * 2 * kLoads>();  // tile 0 has landed
+    for (int q = 0; q < (AK ? kLoadsKC : kLoadsMC); ++q)
+      if (!AK || t % 2 == 0) load_a(t, q);
+#pragma unroll
+    for (int q = 0; q < (BKC ? kLoadsKC : kLoadsMC); ++q)
+      if (!BKC || t % 2 == 0) load_b(t, q);
+  }
+  if constexpr (NSA == 3) {
+#pragma unroll
+    for (int q = 0; q < kLoadsKC / 2; ++q) load_a(4, q);
+  }
+  // Loads that may still be in flight at the barriers (counted over the issue
+  // order of the first fill and of the tiles, below): at the first barrier,
+  // and at the top of even and odd tiles.
+  constexpr int kWaitFirst = NSA == 3 ? 20 : AK && BKC ? 16 : AK || BKC ? 20 : 24;
+  constexpr int kWaitEven = 16;
+  constexpr int kWaitOdd = NSA == 3 ? 4 : AK && BKC ? 0 : BKC ? 4 : AK ? 8 : 16;
+  dma_barrier<kWaitFirst>();  // tile 0 has landed
   // Fragments are read one whole tile ahead: fa/fb[set][ks][block], the
   // set alternating with the tile's parity.
   bf16x8 fa[2][2][4], fb[2][2][4];
@@ -834,18 +894,22 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
   for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      fa[0][ks][i] = frag<AK>(ring, oa, i, ks);
-      fb[0][ks][i] = frag<BKC>(ring + kBigTile, ob, i, ks);
+      fa[0][ks][i] = frag<AK>(ra + tile_base<AK, NSA>(0), oa, i, 0, ks);
+      fb[0][ks][i] = frag<BKC>(rb + tile_base<BKC, NSB>(0), ob, i, 0, ks);
     }
-  // Tile kt: one barrier at the top (tile kt+1 has landed; tile kt's stage,
-  // read during the previous tile, is free), then 32 MFMAs on fragments in
-  // hand; next to the first 16 the 16 fragment reads of tile kt+1, and one
-  // load instruction of tile kt+4 (into tile kt's stage) per 4 MFMAs.
+  // Tile kt: one barrier at the top, then 32 MFMAs on fragments in hand;
+  // next to the first 16 the 16 fragment reads of tile kt+1, and the loads,
+  // A's before B's: a k-contiguous A with three slots loads half of its pair
+  // kt+5, kt+6 (odd kt) or the other half of pair kt+4, kt+5 (even kt), with
+  // two slots its pair kt+3, kt+4 (odd kt); a k-contiguous B its pair kt+3,
+  // kt+4 (odd kt); an mn-contiguous operand its tile kt+4.  At the barrier
+  // tile kt+1 must have landed; only loads issued after its last one may
+  // still be in flight.
   auto tile = [&](auto parity, int kt) {
-    constexpr int P = decltype(parity)::value;
-    const int st = kt & (NSTAGE - 1);
-    const bf16* na = ring + ((kt + 1) & (NSTAGE - 1)) * kStage;
-    dma_barrier<(NSTAGE - 2) * 2 * kLoads>();
+    constexpr int P = decltype(parity)::value;  // kt % 2
+    const bf16* na = ra + tile_base<AK, NSA>(kt + 1);
+    const bf16* nb = rb + tile_base<BKC, NSB>(kt + 1);
+    dma_barrier<P == 0 ? kWaitEven : kWaitOdd>();
 #pragma unroll
     for (int q = 0; q < 32; ++q) {
       const int ks = q >> 4, i = (q >> 2) & 3, j = q & 3;
@@ -853,11 +917,23 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
       if (q < 16) {  // read order per k-substep: B0 A0 B1 B2 B3 A1 A2 A3
         const int rk = q >> 3, r = q & 7;
         if (r == 0 || r == 2 || r == 3 || r == 4)
-          fb[P ^ 1][rk][r == 0 ? 0 : r - 1] = frag<BKC>(na + kBigTile, ob, r == 0 ? 0 : r - 1, rk);
+          fb[P ^ 1][rk][r == 0 ? 0 : r - 1] = frag<BKC>(nb, ob, r == 0 ? 0 : r - 1, P ^ 1, rk);
         else
-          fa[P ^ 1][rk][r == 1 ? 0 : r - 4] = frag<AK>(na, oa, r == 1 ? 0 : r - 4, rk);
+          fa[P ^ 1][rk][r == 1 ? 0 : r - 4] = frag<AK>(na, oa, r == 1 ? 0 : r - 4, P ^ 1, rk);
       }
-      if ((q & 3) == 3) load_part(st, kt + NSTAGE, q >> 2);
+      if constexpr (NSA == 3) {
+        if (q < 8 && (q & 1) == 0) load_a(P == 1 ? kt + 5 : kt + 4, (P == 1 ? 0 : 4) + (q >> 1));
+      } else if constexpr (AK) {
+        if (P == 1 && q < 16 && (q & 1)) load_a(kt + 3, q >> 1);
+      } else {
+        if (q < 16 && (q & 3) == 3) load_a(kt + 4, q >> 2);
+      }
+      if constexpr (BKC) {
+        constexpr int q0 = AK ? 8 : 16;  // after A's loads
+        if (P == 1 && q >= q0 && q < q0 + kLoadsKC) load_b(kt + 3, q - q0);
+      } else {
+        if (q >= 16 && (q & 3) == 3) load_b(kt + 4, (q - 16) >> 2);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -943,7 +1019,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
 #define LD_BIG_ATTRS __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 #define LD_BIG_KERNEL(name, ak, bk)                                                    \
   LD_BIG_ATTRS void name(GemmArgs g) {                                                 \
-    __shared__ __align__(16) bf16 ring[NSTAGE * kStage];                               \
+    __shared__ __align__(16) bf16 ring[ring_elems<ak, bk>()];                          \
     gemm_big_body<ak, bk>(g, ring, blockIdx.x, gridDim.x, blockIdx.y, gridDim.y);      \
   }
 LD_BIG_KERNEL(ld_gemm_bf16_nt_256, true, true)
@@ -953,13 +1029,13 @@ LD_BIG_KERNEL(ld_gemm_bf16_tt_256, false, true)
 
 // C = [u v] rows and aux = silu(u) v rows of the SwiGLU projection (see GemmArgs).
 LD_BIG_ATTRS void ld_gemm_bf16_nt_glu_256(GemmArgs g) {
-  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
+  __shared__ __align__(16) bf16 ring[ring_elems<true, true>()];
   gemm_big_body<true, true, kEpiGluFwd>(g, ring, blockIdx.x, gridDim.x, 0, 1);
 }
 
 // C = u rows and aux = relu(u)^2 rows of the squared-ReLU projection (see GemmArgs).
 LD_BIG_ATTRS void ld_gemm_bf16_nt_relu2_256(GemmArgs g) {
-  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
+  __shared__ __align__(16) bf16 ring[ring_elems<true, true>()];
   gemm_big_body<true, true, kEpiRelu2Fwd>(g, ring, blockIdx.x, gridDim.x, 0, 1);
 }
 
@@ -972,7 +1048,7 @@ LD_BIG_ATTRS void ld_gemm_bf16_nt_relu2_256(GemmArgs g) {
 template <int EPI2>
 __device__ __forceinline__ void gemm_pair_body(const GemmArgs& g1, const GemmArgs& g2, int tiles1, int splits1,
                                                int tiles2, int g2_first) {
-  __shared__ __align__(16) bf16 ring[NSTAGE * kStage];
+  __shared__ __align__(16) bf16 ring[ring_elems<true, false>()];
   const int n1 = tiles1 * splits1;
   int id = blockIdx.x;
   bool first = true;
