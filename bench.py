@@ -62,6 +62,7 @@ T_RAMP = 1001               # steps 0..1000 of the p_max ramp
 # the configurations' p_max values, then the hero-run values (0.8, 0.99),
 # which take the realised keep fraction down to ~0.5 for the step-time fit
 SWEEP_P_MAX = (0.0, 0.1, 0.2, 0.5, 0.8, 0.99)
+SWEEP_P_UNIFORM = (0.25, 0.5, 0.75, 0.9)
 
 
 # Kernel -> source file it is built from (for the traffic record's hash check).
@@ -247,6 +248,11 @@ def hbm_kernels(st, ps, step, crec):
             cg = c["hbm_bytes"] / max(r["ms"] * 1e-3 / r["launches"], 1e-12) / 1e9
             out[k].update(counter_bytes_per_launch=c["hbm_bytes"], counter_gbs=round(cg, 1),
                           counter_frac=round(cg / PEAK_HBM_GBS, 4))
+        if c and c.get("avg_us"):
+            # the kernel's own duration (rocprofv3 kernel trace): the events
+            # above also hold the gap between launches
+            tg = (r["bytes"] / r["launches"]) / (c["avg_us"] * 1e-6) / 1e9
+            out[k].update(trace_avg_us=c["avg_us"], trace_gbs=round(tg, 1), trace_frac=round(tg / PEAK_HBM_GBS, 4))
     return out
 
 
@@ -272,6 +278,31 @@ def mask_microbench(dev, layers=128, batch=1 << 17, iters=5):
     # 20 64x64->128-bit products (~360 vector instructions in the kernel)
     return {"draws": layers * batch, "ms": round(ms, 3), "draws_per_s": round(layers * batch / (ms * 1e-3), 1),
             "bound": "alu", "gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def hbm_ceiling(dev, mib=1024, iters=5):
+    """What plain streaming kernels (torch's own) reach on this GPU: a float32
+    copy (read + write), a sum (read) and a fill (write) over `mib` MiB,
+    timed with events: the practical ceiling beside the 8 TB/s peak."""
+    n = mib * 2**20 // 4
+    x = torch.ones(n, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    out = {}
+    for name, fn, nbytes in (("copy", lambda: y.copy_(x), 2 * 4 * n),
+                             ("read", lambda: torch.sum(x), 4 * n),
+                             ("write", lambda: y.fill_(2.0), 4 * n)):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        gbs = nbytes / (e0.elapsed_time(e1) / iters * 1e-3) / 1e9
+        out[name] = {"gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    del x, y
+    return out
 
 
 def _timed(fn, steps, warmup):
@@ -449,6 +480,8 @@ def main():
     print(f"# hbm kernels: {json.dumps(hbm)}", file=sys.stderr, flush=True)
     maskb = mask_microbench(dev)
     print(f"# mask microbench: {json.dumps(maskb)}", file=sys.stderr, flush=True)
+    ceil = hbm_ceiling(dev)
+    print(f"# hbm ceiling: {json.dumps(ceil)}", file=sys.stderr, flush=True)
     trec = traffic_record(prof_kernel, args.workload)
 
     sweep = []
@@ -462,6 +495,15 @@ def main():
                                   tokens_per_s=round(tokens / (sms * 1e-3), 1),
                                   exec_tflops=round(exec_flops(skept) / (sms * 1e-3) / 1e12, 1)))
                 print(f"# sweep {sweep[-1]}", file=sys.stderr, flush=True)
+        # the same drop rate at every layer, down to a keep fraction of ~0.1:
+        # the step's fixed cost is measured, not extrapolated
+        for p_u in SWEEP_P_UNIFORM:
+            pp = [p_u] * sh.n_layers
+            sms, skept = time_steps(st, pp, 20_000, 5, 1)
+            sweep.append(dict(p_uniform=p_u, ms=round(sms, 3), drop_frac=round(drop_frac(skept), 4),
+                              tokens_per_s=round(tokens / (sms * 1e-3), 1),
+                              exec_tflops=round(exec_flops(skept) / (sms * 1e-3) / 1e12, 1)))
+            print(f"# sweep {sweep[-1]}", file=sys.stderr, flush=True)
     fit = None
     if len(sweep) >= 3:
         keep_frac = np.array([1 - s["drop_frac"] for s in sweep])
@@ -535,6 +577,7 @@ def main():
                          for k, v in crec.items() if "mfma_busy" in v and v["mfma_busy"] > 0},
         "hbm_kernels": hbm,
         "mask_microbench": maskb,
+        "hbm_ceiling": ceil,
         "cpu_baseline": cpu,
         "sweep": sweep,
         "sweep_fit": fit,

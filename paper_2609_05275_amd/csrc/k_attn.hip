@@ -60,7 +60,9 @@ constexpr int kFwdRowsPerWave = 32;  // forward: query rows per wave (8 waves)
 
 // --------------------------------------------------------------- backward
 
-// delta[seq, head, q] = sum_d dO * O (float32).  One wave per token row of
+// delta[seq, head, q] = -sum_d dO * O (float32, stored negated so that it can
+// start the dP accumulation: dP - rowsum(dO * O) comes out of the MFMAs).
+// One wave per token row of
 // H*DH values: each pass reads 16 contiguous bytes per lane of O and dO (the
 // row in 64*16-byte pieces), the DH/VN lanes of a head sum their products
 // with butterfly shuffles, and the first lane of each head writes it.
@@ -89,7 +91,7 @@ __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
     }
 #pragma unroll
     for (int off = G / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-    if (e < W && lane % G == 0) a.delta[(seq * a.H + e / DH) * a.S + q] = s;
+    if (e < W && lane % G == 0) a.delta[(seq * a.H + e / DH) * a.S + q] = -s;
   }
 }
 
@@ -239,7 +241,7 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   // 2ks + hf) for step A, transposing reads (rows tr_r and tr_r + 8) for
   // step C, and the log-sum-exp of the lane's first query for step B.  The
   // dO block, the half, the 16-row groups and delta are immediates.
-  uint32_t aq[DH / 16], at0[DH / 32], at1[DH / 32], al;
+  uint32_t aq[DH / 16], at0[DH / 32], at1[DH / 32], al, ad;
   {
     const uint32_t r0 = lds_addr(ring);
     const int sw_c = qd_swz<DH>(cl);
@@ -255,17 +257,33 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
       at1[db] = r0 + 2u * ((tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7));
     }
     al = r0 + 4u * BQ * DH + 16u * hf;
+    ad = al;
   }
   constexpr uint32_t kOb = 2u * BQ * DH;  // dO block after the Q block (bytes)
   constexpr uint32_t kDl = 4u * BQ;       // delta after the log-sum-exp (bytes)
   // moving a set from the stage of block b to that of block b + 1
   auto adv = [](int b) { return (b & 3) == 3 ? static_cast<uint32_t>(-3 * SB) : static_cast<uint32_t>(SB); };
 
-  // A: scores S = Q K^T and dP = dO V^T of half qh of the block aq points at.
+  // The negated delta of the lane's 16 queries of half qh of the block `ad`
+  // points at, in accumulator order: dP starts from it, so the MFMAs give
+  // dP - delta directly.
+  auto neg_delta = [&](int qh) {
+    floatx16 z;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const floatx4 t = lds_f4(ad + kDl + 4u * (qh * 32 + 8 * g));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) z[4 * g + e] = t[e];
+    }
+    return z;
+  };
+  // A: scores S = Q K^T and dP - delta = dO V^T - delta of half qh of the
+  // block aq (and ad) point at.
   auto step_a = [&](int qh, floatx16& sc, floatx16& dp) {
     const uint32_t hq = 2u * qh * 32 * DH;
+    const floatx16 nd = neg_delta(qh);
     sc = mfma(lds_frag(aq[0] + hq), kf[0], floatx16{});
-    dp = mfma(lds_frag(aq[0] + hq + kOb), vf[0], floatx16{});
+    dp = mfma(lds_frag(aq[0] + hq + kOb), vf[0], nd);
 #pragma unroll
     for (int ks = 1; ks < DH / 16; ++ks) {
       sc = mfma(lds_frag(aq[ks] + hq), kf[ks], sc);
@@ -273,15 +291,14 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     }
   };
   // B: P and dS of half qh of query block qb (the block al points at), as
-  // bf16 MFMA operands.
-  auto step_b = [&](const floatx16& sc, const floatx16& dp, int qb, int qh, bf16x8 (&pb)[2],
+  // bf16 MFMA operands.  The causal mask is needed only in the blocks that
+  // hold queries before some of the workgroup's keys (MASK).
+  auto step_b = [&](auto mask, const floatx16& sc, const floatx16& dp, int qb, int qh, bf16x8 (&pb)[2],
                     bf16x8 (&dsb)[2]) {
-    floatx4 l4[4], d4[4];
+    constexpr bool MASK = decltype(mask)::value;
+    floatx4 l4[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      l4[g] = lds_f4(al + 4u * (qh * 32 + 8 * g));
-      d4[g] = lds_f4(al + kDl + 4u * (qh * 32 + 8 * g));
-    }
+    for (int g = 0; g < 4; ++g) l4[g] = lds_f4(al + 4u * (qh * 32 + 8 * g));
     const int t = key - (qb + qh * 32 + 4 * hf);  // key minus the lane's first query
     const float ab = al2 * static_cast<float>(t);  // ALiBi bias at that query
 #pragma unroll
@@ -290,9 +307,9 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
       float x = fmaf(sc[v], sl2, -l4[v >> 2][v & 3] * kLog2e);
       if constexpr (AL) x += fmaf(-al2, static_cast<float>(c), ab);
       float p = __builtin_amdgcn_exp2f(x);
-      p = t > c ? 0.f : p;  // causal: keys after the query
+      if constexpr (MASK) p = t > c ? 0.f : p;  // causal: keys after the query
       pb[v >> 3][v & 7] = static_cast<bf16>(p);
-      dsb[v >> 3][v & 7] = static_cast<bf16>(p * (dp[v] - d4[v >> 2][v & 3]));
+      dsb[v >> 3][v & 7] = static_cast<bf16>(p * dp[v]);
     }
   };
   // C: dV^T += dO^T P, dK^T += Q^T dS for half qh of the block at0/at1 point at.
@@ -318,9 +335,10 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   // apart and none waits on the one before it.  The softmax elements of B
   // go between the MFMAs, the fragments of iteration i+2 are read during
   // iteration i, and scheduling barriers keep the compiler to this order.
-  auto half_step = [&](const bf16x8 (&pbc)[2], const bf16x8 (&dsbc)[2], int qh_c, int qh_a, floatx16& sc,
-                       floatx16& dp, const floatx16& scb, const floatx16& dpb, int qb_b, int qh_b,
+  auto half_step = [&](auto mask, const bf16x8 (&pbc)[2], const bf16x8 (&dsbc)[2], int qh_c, int qh_a,
+                       floatx16& sc, floatx16& dp, const floatx16& scb, const floatx16& dpb, int qb_b, int qh_b,
                        bf16x8 (&pbo)[2], bf16x8 (&dsbo)[2]) {
+    constexpr bool MASK = decltype(mask)::value;
     constexpr int N = DH / 16, NDB = DH / 32, EPI = 16 / N;  // softmax elements per iteration
     const uint32_t hq = 2u * qh_a * 32 * DH;
     struct Frags {
@@ -340,12 +358,10 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     Frags fr[3];
     load(fr[0], 0);
     load(fr[1], 1);
-    floatx4 l4[4], d4[4];
+    const floatx16 nd = neg_delta(qh_a);
+    floatx4 l4[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      l4[g] = lds_f4(al + 4u * (qh_b * 32 + 8 * g));
-      d4[g] = lds_f4(al + kDl + 4u * (qh_b * 32 + 8 * g));
-    }
+    for (int g = 0; g < 4; ++g) l4[g] = lds_f4(al + 4u * (qh_b * 32 + 8 * g));
     const int t = key - (qb_b + qh_b * 32 + 4 * hf);  // key minus the lane's first query
     const float ab = al2 * static_cast<float>(t);      // ALiBi bias at that query
     auto softmax = [&](int v) {
@@ -353,9 +369,9 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
       float x = fmaf(scb[v], sl2, -l4[v >> 2][v & 3] * kLog2e);
       if constexpr (AL) x += fmaf(-al2, static_cast<float>(c), ab);
       float p = __builtin_amdgcn_exp2f(x);
-      p = t > c ? 0.f : p;  // causal: keys after the query
+      if constexpr (MASK) p = t > c ? 0.f : p;  // causal: keys after the query
       pbo[v >> 3][v & 7] = static_cast<bf16>(p);
-      dsbo[v >> 3][v & 7] = static_cast<bf16>(p * (dpb[v] - d4[v >> 2][v & 3]));
+      dsbo[v >> 3][v & 7] = static_cast<bf16>(p * dpb[v]);
     };
 #pragma unroll
     for (int i = 0; i < N; ++i) {
@@ -368,7 +384,7 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
       for (int e = 0; e < EPI / 2; ++e) softmax(EPI * i + e);
       dv[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(f.ol, f.oh, 0, 1, 2, 3, 4, 5, 6, 7)), pbc[c], dv[db]);
       __builtin_amdgcn_sched_barrier(0);
-      dp = mfma(f.of, vf[i], i == 0 ? floatx16{} : dp);
+      dp = mfma(f.of, vf[i], i == 0 ? nd : dp);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int e = EPI / 2; e < EPI; ++e) softmax(EPI * i + e);
@@ -394,26 +410,36 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   dma_barrier<2 * NL>();  // block 0 has landed
   step_a(0, scx, dpx);
   step_a(1, scy, dpy);
-  step_b(scx, dpx, q_first, 0, pbx, dsbx);
+  const std::integral_constant<bool, true> masked;
+  const std::integral_constant<bool, false> unmasked;
+  step_b(masked, scx, dpx, q_first, 0, pbx, dsbx);
   dma_barrier<NL>();  // block 1 has landed; block 3 goes to the fourth stage
   load_block(3, q_first + 3 * BQ);
   move(aq, adv(0));
-  half_step(pbx, dsbx, 0, 0, scx, dpx, scy, dpy, q_first, 1, pby, dsby);
+  ad += adv(0);
+  half_step(masked, pbx, dsbx, 0, 0, scx, dpx, scy, dpy, q_first, 1, pby, dsby);
   al += adv(0);
   // Block j: C(2j-1) (block j-1) and A(2j+1) next to B(2j); barrier (block
   // j+1 has landed, block j+3 goes to the stage block j-1 left); C(2j) and
   // A(2j+2) (block j+1) next to B(2j+1).
-  for (int j = 1; j < nqb; ++j) {
+  auto block = [&](auto mask, int j) {
     const int qb = q_first + j * BQ;
-    half_step(pby, dsby, 1, 1, scy, dpy, scx, dpx, qb, 0, pbx, dsbx);
+    half_step(mask, pby, dsby, 1, 1, scy, dpy, scx, dpx, qb, 0, pbx, dsbx);
     dma_barrier<NL>();
     load_block((j + 3) & 3, qb + 3 * BQ);
     move(aq, adv(j));
+    ad += adv(j);
     move(at0, adv(j - 1));
     move(at1, adv(j - 1));
-    half_step(pbx, dsbx, 0, 0, scx, dpx, scy, dpy, qb, 1, pby, dsby);
+    half_step(mask, pbx, dsbx, 0, 0, scx, dpx, scy, dpy, qb, 1, pby, dsby);
     al += adv(j);
-  }
+  };
+  // Only the blocks that start before the workgroup's last key hold queries
+  // that some of its keys come after.
+  constexpr int kMaskBlocks = BKEYS / BQ;
+  int j = 1;
+  for (; j < nqb && j < kMaskBlocks; ++j) block(masked, j);
+  for (; j < nqb; ++j) block(unmasked, j);
   step_c(pby, dsby, 1);  // C of the last half
   dma_barrier<0>();  // no load may still write LDS when the workgroup ends
   if (active && key < S) {
@@ -806,7 +832,7 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
             if (8 * (v >> 2) + (v & 3) > t) pv[v] = 0.f;
         }
 #pragma unroll
-        for (int v = 0; v < 16; ++v) dsb[v >> 3][v & 7] = static_cast<bf16>(pv[v] * (dpt[v] - dl));
+        for (int v = 0; v < 16; ++v) dsb[v >> 3][v & 7] = static_cast<bf16>(pv[v] * (dpt[v] + dl));
         // dQ^T += K^T dS^T, the d blocks innermost (consecutive MFMAs use
         // different accumulators)
 #pragma unroll
@@ -937,7 +963,7 @@ __global__ __launch_bounds__(64) void ld_attn_bwd_dq_f32(AttnArgs a) {
         dp = __builtin_fmaf(dov[i], Vs[j][i], dp);
       }
       const float p = expf(s * a.scale - al * static_cast<float>(q - key) - lse);
-      const float ds = p * (dp - dl);
+      const float ds = p * (dp + dl);
       for (int i = 0; i < DH; ++i) dq[i] = __builtin_fmaf(ds, Ks[j][i], dq[i]);
     }
     __syncthreads();
@@ -991,7 +1017,7 @@ __global__ __launch_bounds__(64) void ld_attn_bwd_dkdv_f32(AttnArgs a) {
           dp = __builtin_fmaf(Os[j][i], vv[i], dp);
         }
         const float p = expf(s * a.scale - al * static_cast<float>(q - key) - ls[j]);
-        const float ds = p * (dp - dls[j]);
+        const float ds = p * (dp + dls[j]);
         for (int i = 0; i < DH; ++i) {
           dv[i] = __builtin_fmaf(p, Os[j][i], dv[i]);
           dk[i] = __builtin_fmaf(ds, Qs[j][i], dk[i]);
