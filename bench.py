@@ -282,14 +282,13 @@ def mask_microbench(dev, layers=128, batch=1 << 17, iters=5):
 
 def hbm_ceiling(dev, mib=1024, iters=5):
     """What plain streaming kernels (torch's own) reach on this GPU: a float32
-    copy (read + write), a sum (read) and a fill (write) over `mib` MiB,
-    timed with events: the practical ceiling beside the 8 TB/s peak."""
+    copy (read + write) and a fill (write) over `mib` MiB, timed with events:
+    the practical ceiling beside the 8 TB/s peak."""
     n = mib * 2**20 // 4
     x = torch.ones(n, dtype=torch.float32, device=dev)
     y = torch.empty_like(x)
     out = {}
     for name, fn, nbytes in (("copy", lambda: y.copy_(x), 2 * 4 * n),
-                             ("read", lambda: torch.sum(x), 4 * n),
                              ("write", lambda: y.fill_(2.0), 4 * n)):
         fn()
         torch.cuda.synchronize()
