@@ -387,8 +387,11 @@ int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmA
     if (int rc = run_gemm(dtype, 1, 0, g2, max_m2, host_m2, host_k2, s)) return rc;
     return run_gemm(dtype, 0, 0, g1, g1.M, g1.M, host_k1, s, part, part_bytes, max_k1);
   }
-  // at most the split count the standalone plan (and the scratch) allows
-  const PairPlan pp = plan_gemm_pair(g1.M, g1.N, max_k1, max_m2, g2.N, g2.K, p1.splits);
+  // at most the split count the standalone plan (and the scratch) allows,
+  // planned for the kept rows when the host knows them (the grid still
+  // covers max_m2 rows; the device counts decide which work)
+  const int64_t plan_k1 = host_k1 >= 0 ? host_k1 : max_k1, plan_m2 = host_m2 >= 0 ? host_m2 : max_m2;
+  const PairPlan pp = plan_gemm_pair(g1.M, g1.N, plan_k1, plan_m2, g2.N, g2.K, p1.splits);
   if (pp.splits1 > 1) {
     GemmPlan q = p1;
     q.splits = pp.splits1;
@@ -1062,10 +1065,28 @@ int host_mask_state(const Dims& D, float p, int64_t layer, uint64_t seed, uint64
   return mask_draw(0, static_cast<uint64_t>(layer), step, seed, 1, m) < thr ? 0 : 1;
 }
 
+// Kept count of mask m of `layer`, from the mask kernel's own draws taken
+// again on the host (B Philox blocks), or -1 when an override decides.
+int64_t host_kept_count(const Dims& D, float p, int64_t layer, uint64_t seed, uint64_t step, const uint8_t* ovr,
+                        int m) {
+  if (ovr) return -1;
+  uint64_t thr;
+  uint8_t drop_all;
+  threshold(p, &thr, &drop_all);
+  if (drop_all) return 0;
+  int64_t kept = 0;
+  for (int64_t b = 0; b < D.B; ++b)
+    kept += mask_draw(static_cast<uint64_t>(b), static_cast<uint64_t>(layer), step, seed, D.per_batch, m) < thr ? 0 : 1;
+  return kept;
+}
+
 // The masks of layer l of a block laid out by mask_layout (layer-major).
+// draws: p, seed and step are the ones the mask kernel draws with, so the
+// host knows the kept counts (the device still decides every row; the
+// counts only plan launches and skip a sub-block no sample keeps).
 LayerMasks layer_masks(const Dims& D, const MaskLayout& ml, char* base, int64_t l, int64_t layer_id,
                        float p, uint64_t seed, uint64_t step, const uint8_t* ovr,
-                       const std::vector<int64_t>& hc) {
+                       const std::vector<int64_t>& hc, bool draws = true) {
   uint8_t* keep = reinterpret_cast<uint8_t*>(base + ml.keep);
   int32_t* idx = reinterpret_cast<int32_t*>(base + ml.idx);
   int32_t* count = reinterpret_cast<int32_t*>(base + ml.count);
@@ -1081,6 +1102,12 @@ LayerMasks layer_masks(const Dims& D, const MaskLayout& ml, char* base, int64_t 
   lm.host_f = host_mask_state(D, p, layer_id, seed, step, ovr, D.nm - 1);
   lm.hc_a = hc[l * D.nm];
   lm.hc_f = hc[l * D.nm + D.nm - 1];
+  if (draws && !ovr) {
+    lm.hc_a = host_kept_count(D, p, layer_id, seed, step, ovr, 0);
+    lm.hc_f = D.nm > 1 ? host_kept_count(D, p, layer_id, seed, step, ovr, D.nm - 1) : lm.hc_a;
+    if (lm.hc_a == 0) lm.host_a = 0;
+    if (lm.hc_f == 0) lm.host_f = 0;
+  }
   return lm;
 }
 
@@ -1432,7 +1459,7 @@ int ld_layer_bwd(const ld_config* cfg, const ld_weights* w, const void* ctx, voi
   const std::vector<int64_t> hc =
       host_counts_if_profiling(reinterpret_cast<int32_t*>(c + ml.count), D.nm, s);
   // the ctx carries no p, seed or step: every decision is the device's
-  LayerMasks lm = layer_masks(D, ml, c, 0, 0, 0.f, 0, 0, nullptr, hc);
+  LayerMasks lm = layer_masks(D, ml, c, 0, 0, 0.f, 0, 0, nullptr, hc, false);
   lm.host_a = lm.host_f = -1;
   return layer_backward(D, *w, lm, act, BL, static_cast<char*>(ws), Stream{dx, D.dtype == LD_F32}, *dw, s);
 }
