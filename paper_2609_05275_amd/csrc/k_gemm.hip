@@ -340,6 +340,7 @@ constexpr int kBigTile = GB * GK;       // elements of one operand's k tile
 constexpr int kLoadsMC = 4;             // load instructions per wave per mn-contiguous tile
 constexpr int kLoadsKC = 8;             // load instructions per wave per k-contiguous pair
 constexpr int kStagePitch = 132;        // floats per staged epilogue row (128 + 4 pad)
+constexpr int kStagePitch16 = 132;      // bf16 per staged row of a bf16 epilogue (264 bytes)
 constexpr uint32_t kOob = kDmaOob;
 constexpr int64_t kBigMaxSpan = kDmaMaxSpan;
 // Ring regions (elements): a k-contiguous A takes three pair slots when B
@@ -816,6 +817,22 @@ __device__ __forceinline__ void relu2_bwd_rows(const GemmArgs& g, const float* s
 // One workgroup's tile of a GEMM: `pid` in [0, n_tiles) picks the tile
 // (n_tiles covers every row the grid was sized for), `sp` of `splits` the
 // k range; `ring` is the workgroup's LDS.
+// Plain bf16 output of a 32-row block row that crosses M: straight from the
+// accumulators, each row checked (lane: row lm, columns j*32 + 8q + 4 half).
+__device__ __forceinline__ void epilogue_plain_edge_bf16(const GemmArgs& g, const floatx16 (&acc)[4], float alpha,
+                                                         int mb, int nb, int lm, int half, int M) {
+  if (mb + lm >= M) return;
+  bf16* C = static_cast<bf16*>(g.C) + static_cast<int64_t>(mb + lm) * g.ldc + nb;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const floatx16& a = acc[j];
+      *reinterpret_cast<uint2*>(C + j * 32 + 8 * q + 4 * half) =
+          pack4_bf16(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
+    }
+}
+
 template <bool AK, bool BKC, int EPI = kEpiPlain>
 __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int pid, int n_tiles, int sp,
                                               int splits) {
@@ -966,6 +983,49 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
   // Largest kept sequence index, for the row map (rows < M only).
   const int q_last = g.out_map.idx && M > 0 ? (M - 1) / g.out_map.S : 0;
   dma_barrier<0>();  // the loop's last loads (zeros) land before the ring is reused
+  // A plain bf16 output (no residual, row map or partials) is rounded as it
+  // is staged: half the LDS traffic, and 16-byte stores that cover a row's
+  // 128 columns with 16 lanes (four rows per instruction).  The same single
+  // rounding of alpha * acc as the float32 staging gives.  Block rows that
+  // cross M store straight from the accumulators, row by row.
+  if constexpr (EPI == kEpiPlain) {
+    if (!part && !g.R && !g.c_f32 && !g.out_map.idx && full_cols) {
+      bf16* st16 = reinterpret_cast<bf16*>(stage);
+      const int rr = lane >> 4, cc = (lane & 15) * 8;  // read: row rr of each 4, columns cc..cc+7
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int mb = m0 + wm * 128 + i * 32;
+        if (mb + 32 > M) {
+          if (mb < M) epilogue_plain_edge_bf16(g, acc[i], alpha, mb, n0 + wn * 128, lm, half, M);
+          continue;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const floatx16& a = acc[i][j];
+            *reinterpret_cast<uint2*>(st16 + lm * kStagePitch16 + j * 32 + 8 * q + 4 * half) =
+                pack4_bf16(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
+          }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        // rows are 264 bytes apart (8-byte aligned, no bank conflicts for the
+        // 8-byte stage writes), so each 16 bytes are read as two 8-byte halves
+        uint4 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const bf16* src = st16 + (4 * k + rr) * kStagePitch16 + cc;
+          const uint2 lo = *reinterpret_cast<const uint2*>(src), hi = *reinterpret_cast<const uint2*>(src + 4);
+          v[k] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+        bf16* C = static_cast<bf16*>(g.C);
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          *reinterpret_cast<uint4*>(C + static_cast<int64_t>(mb + 4 * k + rr) * g.ldc + n0 + wn * 128 + cc) = v[k];
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // reads done before the block is rewritten
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
