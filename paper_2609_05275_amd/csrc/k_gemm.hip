@@ -656,56 +656,6 @@ __device__ __forceinline__ float4 unpack4_bf16(uint2 r) {
                      static_cast<float>(b[3]));
 }
 
-// Fused SwiGLU forward, [u v] part: the staged block row (lane rows
-// r0 + 2 it, 4 columns at stage column c) goes to C column gc.  `full`: all
-// 32 rows are below M (loads of the block issued before any store).
-__device__ __forceinline__ void glu_fwd_uv_rows(const GemmArgs& g, const float* stage, int r0, int half, int c,
-                                                int gc, int M, bool full) {
-  bf16* C = static_cast<bf16*>(g.C);
-  if (full) {
-    float4 v[16];
-#pragma unroll
-    for (int it = 0; it < 16; ++it) v[it] = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
-#pragma unroll
-    for (int it = 0; it < 16; ++it)
-      *reinterpret_cast<uint2*>(C + static_cast<int64_t>(r0 + 2 * it) * g.ldc + gc) =
-          pack4_bf16(v[it].x, v[it].y, v[it].z, v[it].w);
-  } else {
-#pragma unroll 1
-    for (int it = 0; it < 16; ++it) {
-      if (r0 + 2 * it >= M) break;
-      const float4 v = *reinterpret_cast<const float4*>(stage + (2 * it + half) * kStagePitch + c);
-      *reinterpret_cast<uint2*>(C + static_cast<int64_t>(r0 + 2 * it) * g.ldc + gc) = pack4_bf16(v.x, v.y, v.z, v.w);
-    }
-  }
-}
-
-// Fused SwiGLU forward, s part: 32 staged rows of 64 columns (stage columns
-// 0-63) to aux columns sc0..sc0+63; lane: row 4 it + lane/16, 4 columns at
-// 4 (lane % 16).
-__device__ __forceinline__ void glu_fwd_s_rows(const GemmArgs& g, const float* stage, int mb, int lane, int sc0,
-                                               int M, bool full) {
-  bf16* Sp = static_cast<bf16*>(g.aux);
-  const int rl = lane >> 4, cc = (lane & 15) * 4;
-  if (full) {
-    float4 v[8];
-#pragma unroll
-    for (int it = 0; it < 8; ++it) v[it] = *reinterpret_cast<const float4*>(stage + (4 * it + rl) * kStagePitch + cc);
-#pragma unroll
-    for (int it = 0; it < 8; ++it)
-      *reinterpret_cast<uint2*>(Sp + static_cast<int64_t>(mb + 4 * it + rl) * g.glu_f + sc0 + cc) =
-          pack4_bf16(v[it].x, v[it].y, v[it].z, v[it].w);
-  } else {
-#pragma unroll 1
-    for (int it = 0; it < 8; ++it) {
-      const int m = mb + 4 * it + rl;
-      if (m >= M) continue;
-      const float4 v = *reinterpret_cast<const float4*>(stage + (4 * it + rl) * kStagePitch + cc);
-      *reinterpret_cast<uint2*>(Sp + static_cast<int64_t>(m) * g.glu_f + sc0 + cc) = pack4_bf16(v.x, v.y, v.z, v.w);
-    }
-  }
-}
-
 // Fused SwiGLU backward: the staged gs values (alpha applied; rows r0 + 2 it,
 // columns n..n+3 < N = f), kept in float32 (gs is never stored), with u and
 // v read from aux, give gu and gv in C columns n and f + n.
@@ -988,6 +938,66 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
   // 128 columns with 16 lanes (four rows per instruction).  The same single
   // rounding of alpha * acc as the float32 staging gives.  Block rows that
   // cross M store straight from the accumulators, row by row.
+  if constexpr (EPI == kEpiGluFwd) {
+    // [u v] and s are bf16 outputs too, staged as bf16 the same way; rows
+    // past M are not stored
+    {
+      bf16* st16 = reinterpret_cast<bf16*>(stage);
+      const int rr = lane >> 4, cc = (lane & 15) * 8;  // [u v]: row rr of each 4, columns cc..cc+7
+      const int rs = lane >> 3, cs = (lane & 7) * 8;   // s: row rs of each 8, columns cs..cs+7
+      const int f0 = tn * 128 + wn * 64;               // the wave's first d_ff column
+      bf16* C = static_cast<bf16*>(g.C);
+      bf16* Sp = static_cast<bf16*>(g.aux);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int mb = m0 + wm * 128 + i * 32;
+        if (mb >= M) break;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const floatx16& a = acc[i][j];
+            *reinterpret_cast<uint2*>(st16 + lm * kStagePitch16 + j * 32 + 8 * q + 4 * half) =
+                pack4_bf16(alpha * a[4 * q], alpha * a[4 * q + 1], alpha * a[4 * q + 2], alpha * a[4 * q + 3]);
+          }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        // staged columns 0-63 are gate (u) columns, 64-127 up (v) columns
+        const int gcol = cc < 64 ? f0 + cc : g.glu_f + f0 + cc - 64;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const bf16* src = st16 + (4 * k + rr) * kStagePitch16 + cc;
+          const uint2 lo = *reinterpret_cast<const uint2*>(src), hi = *reinterpret_cast<const uint2*>(src + 4);
+          if (mb + 4 * k + rr < M)
+            *reinterpret_cast<uint4*>(C + static_cast<int64_t>(mb + 4 * k + rr) * g.ldc + gcol) =
+                make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        // s = silu(u) v from the float32 accumulators (see below)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float sv[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              sv[e] = swiglu_fwd_f(alpha * acc[i][j][4 * q + e], alpha * acc[i][j + 2][4 * q + e]);
+            *reinterpret_cast<uint2*>(st16 + lm * kStagePitch16 + j * 32 + 8 * q + 4 * half) =
+                pack4_bf16(sv[0], sv[1], sv[2], sv[3]);
+          }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const bf16* src = st16 + (8 * k + rs) * kStagePitch16 + cs;
+          const uint2 lo = *reinterpret_cast<const uint2*>(src), hi = *reinterpret_cast<const uint2*>(src + 4);
+          if (mb + 8 * k + rs < M)
+            *reinterpret_cast<uint4*>(Sp + static_cast<int64_t>(mb + 8 * k + rs) * g.glu_f + f0 + cs) =
+                make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // reads done before the block is rewritten
+      }
+      return;
+    }
+  }
   if constexpr (EPI == kEpiPlain) {
     if (!part && !g.R && !g.c_f32 && !g.out_map.idx && full_cols) {
       bf16* st16 = reinterpret_cast<bf16*>(stage);
@@ -1038,29 +1048,7 @@ __device__ __forceinline__ void gemm_big_body(const GemmArgs& g, bf16* ring, int
       }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // staged values visible to the wave
     const int mb = m0 + wm * 128 + i * 32;             // first row of the block row
-    if constexpr (EPI == kEpiGluFwd) {
-      // [u v] rows: the wave's columns c < 64 are gate columns, the rest up
-      const int gc = tn * 128 + wn * 64 + (c & 63) + (c >= 64 ? g.glu_f : 0);
-      glu_fwd_uv_rows(g, stage, mb + half, half, c, gc, M, mb + 32 <= M);
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      // s = silu(u) v from the pairs of float32 accumulators (the stored
-      // [u v] are bf16; rounding them first would add the largest single
-      // error of the block's forward), staged over the gate columns and
-      // stored as 64-column rows
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float sv[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            sv[e] = swiglu_fwd_f(alpha * acc[i][j][4 * q + e], alpha * acc[i][j + 2][4 * q + e]);
-          *reinterpret_cast<float4*>(stage + lm * kStagePitch + j * 32 + 8 * q + 4 * half) =
-              make_float4(sv[0], sv[1], sv[2], sv[3]);
-        }
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      glu_fwd_s_rows(g, stage, mb, lane, tn * 128 + wn * 64, M, mb + 32 <= M);
-    } else if constexpr (EPI == kEpiGluBwd) {
+    if constexpr (EPI == kEpiGluBwd) {
       glu_bwd_rows(g, stage, mb + half, half, c, n, M, n0 + wn * 128 + 128 <= g.N && mb + 32 <= M);
     } else if constexpr (EPI == kEpiRelu2Fwd) {
       relu2_fwd_rows(g, stage, mb + half, half, c, n, M, n0 + wn * 128 + 128 <= g.N && mb + 32 <= M);
