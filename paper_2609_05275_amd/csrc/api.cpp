@@ -1111,6 +1111,17 @@ LayerMasks layer_masks(const Dims& D, const MaskLayout& ml, char* base, int64_t 
   return lm;
 }
 
+// When the device counts were read back (profiling), the host's own counts
+// must equal them: they plan the launches and skip sub-blocks.
+int check_host_counts(const Dims& D, const LayerMasks& lm, const std::vector<int64_t>& hc, int64_t l) {
+  const int64_t da = hc[l * D.nm], df = hc[l * D.nm + D.nm - 1];
+  if ((da >= 0 && lm.hc_a >= 0 && da != lm.hc_a) || (df >= 0 && lm.hc_f >= 0 && df != lm.hc_f))
+    return fail(LD_E_HIP, "layer %lld: device kept counts %lld/%lld, host %lld/%lld", static_cast<long long>(l),
+                static_cast<long long>(da), static_cast<long long>(df), static_cast<long long>(lm.hc_a),
+                static_cast<long long>(lm.hc_f));
+  return LD_OK;
+}
+
 // ------------------------------------------------------ decoding helpers
 
 // Scratch of ld_stack_decode for n_new rows per sequence and caches of s_max
@@ -1439,6 +1450,7 @@ int ld_layer_fwd(const ld_config* cfg, const ld_weights* w, int32_t layer, float
   ActPtrs act{c + ml.total, act_layout(D)};
   const std::vector<int64_t> hc = host_counts_if_profiling(count, D.nm, s);
   const LayerMasks lm = layer_masks(D, ml, c, 0, layer, p, seed, step, keep_override, hc);
+  if (int rc = check_host_counts(D, lm, hc, 0)) return rc;
   return layer_forward(cfg, D, *w, lm, act, Stream{x, D.dtype == LD_F32}, s);
 }
 
@@ -1506,6 +1518,8 @@ int ld_stack_step(const ld_config* cfg, int32_t n_layers, const ld_weights* w, c
   std::vector<LayerMasks> lms;
   lms.reserve(L);
   for (int64_t l = 0; l < L; ++l) lms.push_back(layer_masks(D, ml, base, l, l, p[l], seed, step, keep_override, hc));
+  for (int64_t l = 0; l < L; ++l)
+    if (int rc = check_host_counts(D, lms[l], hc, l)) return rc;
   auto convert = [&](const void* src, void* dst, int to_f32) {
     ProfScope ps("ld_convert_k", s);
     const hipError_t e = launch_convert(src, dst, n_elems, to_f32, s);

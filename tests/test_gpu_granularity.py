@@ -197,3 +197,27 @@ def test_per_batch_layer_fwd_skips_and_bwd_zero_grads():
     assert not ctx[:sh.batch].cpu().numpy().any()
     for k in ld.WEIGHT_KEYS:
         assert not dw[k].any(), k
+
+
+@pytest.mark.parametrize("gran", GRANS, ids=GRAN_IDS)
+@pytest.mark.parametrize("p", [0.0, 0.7, 0.95])
+def test_host_counts_plan_only(gran, p):
+    """The host takes the mask draws again to know each layer's kept counts
+    (they plan split counts and skip sub-blocks no sample keeps).  Under
+    profiling the device counts are read back and must agree (the step fails
+    otherwise), the counts are the oracle's, and the results are bitwise
+    those of the unprofiled step."""
+    sh = SMALL_BF16
+    ps = [p] * sh.n_layers
+    a = _stack_case(sh, gran, ps, 11, 40)
+    ld.ld_prof_start("ld_mask_compact")
+    try:
+        b = _stack_case(sh, gran, ps, 11, 40)
+    finally:
+        ld.ld_prof_stop()
+    _, _, c = masks.masks_granular(ps, 11, 40, sh.batch, gran)
+    assert np.array_equal(a["cnt"], c) and np.array_equal(b["cnt"], c)
+    assert torch.equal(a["xd"], b["xd"]) and torch.equal(a["gd"], b["gd"])
+    for da, db in zip(a["dws"], b["dws"]):
+        for k in da:
+            assert torch.equal(da[k], db[k]), k
