@@ -221,7 +221,7 @@ def cpu_model():
 # HBM-bound kernels of the step, with the algorithmic bytes each launch moves
 # (the library's profiling hook records them per launch).
 HBM_KERNELS = ["ld_mask_compact", "ld_rmsnorm_fwd_k", "ld_rmsnorm_bwd_k", "ld_gather_rows_k",
-               "ld_attn_delta", "ld_splitk_reduce"]
+               "ld_splitk_reduce"]
 
 
 def hbm_kernels(st, ps, step, crec):

@@ -918,14 +918,18 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
     a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(D.dh)));
     a.alibi = D.kind == LD_BLOCK_ALIBI_RELU2;
     // algorithmic FLOPs of the backward (2x the forward), split over the two
-    // MFMA kernels in proportion to the products each forms (4 and 3)
+    // MFMA kernels in proportion to the products each forms (dK/dV 4, dQ 3);
+    // bytes: the delta kernel reads O and dO, the MFMA kernels five tensors
+    // (the bf16 dQ kernel, which forms delta, also O)
     const double fl_bwd = 4.0 * hc * D.d * D.S * (D.S + 1.0);
-    const double parts_fl[3] = {0.0, fl_bwd * 4.0 / 7.0, fl_bwd * 3.0 / 7.0};
-    for (int part = 0; part < 3; ++part) {
-      ProfScope ps(attn_bwd_kernel_name(dt, part), s);
+    for (int part = 0; part < attn_bwd_parts(dt); ++part) {
+      const char* name = attn_bwd_kernel_name(dt, part);
+      const bool dkdv = std::strstr(name, "dkdv") != nullptr, dq = std::strstr(name, "_dq_") != nullptr;
+      ProfScope ps(name, s);
       if ((e = launch_attn_bwd_part(dt, part, a, s)) != hipSuccess)
         return fail(LD_E_HIP, "attn_bwd: %s", hipGetErrorString(e));
-      ps.end(parts_fl[part], D.es * hm * D.d * (part == 0 ? 2.0 : 5.0));
+      ps.end(dkdv ? fl_bwd * 4.0 / 7.0 : dq ? fl_bwd * 3.0 / 7.0 : 0.0,
+             D.es * hm * D.d * (dkdv ? 5.0 : dq ? (dt == LD_BF16 ? 6.0 : 5.0) : 2.0));
     }
   }
   // gh1 = gqkv W_qkv [M, d] and dW_qkv = gqkv^T h1 [3d, d], one launch

@@ -14,11 +14,12 @@
 //   Forward: one workgroup per (256-row query tile, head, kept sequence),
 //   eight waves of 32 query rows; online softmax in base 2 with lazy
 //   rescaling, O normalised at the end and the natural log-sum-exp saved.
-//   Backward (no float atomics): delta = rowsum(dO * O); a dK/dV kernel per
-//   (128-key tile, head, sequence) walks the query blocks at and after the
-//   diagonal recomputing P from the saved log-sum-exp; a dQ kernel per
-//   (256-row query tile, head, sequence) walks the key blocks up to the
-//   diagonal.  Heavy causal tiles are scheduled first.
+//   Backward (no float atomics): a dQ kernel per (256-row query tile, head,
+//   sequence) forms delta = rowsum(dO * O) of its rows first (stored negated
+//   for the next kernel) and walks the key blocks up to the diagonal; then a
+//   dK/dV kernel per (128-key tile, head, sequence) walks the query blocks at
+//   and after the diagonal recomputing P from the saved log-sum-exp.  Heavy
+//   causal tiles are scheduled first.
 // fp32 path: plain SIMT kernels, one thread per query (or key) row, used by
 // the fp32 configuration only.
 #include <mutex>
@@ -737,13 +738,25 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   const bool qok = qrow < S;
   const int64_t srow = (static_cast<int64_t>(seq) * H + head) * S + (qok ? qrow : 0);
   const float lse2 = qok ? a.lse[srow] * kLog2e : 0.f;
-  const float dl = qok ? a.delta[srow] : 0.f;
   bf16x8 qf[DH / 16], of[DH / 16];
+  const bf16* Orow = static_cast<const bf16*>(a.o) + static_cast<int64_t>(seq) * S * ldo + head * DH +
+                     static_cast<int64_t>(qok ? qrow : 0) * ldo;
+  float dsum = 0.f;
 #pragma unroll
   for (int ks = 0; ks < DH / 16; ++ks) {
     qf[ks] = qok ? load8(Qp + static_cast<int64_t>(qrow) * ldq + ks * 16 + hf * 8) : zero8();
     of[ks] = qok ? load8(dOp + static_cast<int64_t>(qrow) * ldo + ks * 16 + hf * 8) : zero8();
+    const bf16x8 ov = qok ? load8(Orow + ks * 16 + hf * 8) : zero8();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dsum = fmaf(static_cast<float>(of[ks][e]), static_cast<float>(ov[e]), dsum);
   }
+  // delta of the row (the two half-waves hold its two halves of d), stored
+  // negated for the dK/dV kernel, which runs after this one
+  const float dl = -(dsum + __shfl_xor(dsum, 32, 64));
+  if (qok && hf == 0) a.delta[srow] = dl;
+  // the store has completed before the first LDS load is issued: those are
+  // counted by the waits below, which know of no other memory operation
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   // The fragments must have arrived before the first LDS load is issued
   // (the compiler does not see those loads).
 #pragma unroll
@@ -1057,22 +1070,22 @@ hipError_t fwd_dh(int dtype, const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// bf16: part 0 is the dQ kernel (it also forms and stores delta), part 1
+// the dK/dV kernel; float32: delta, dK/dV, dQ.
 template <int DH>
 hipError_t bwd_dh(int dtype, int part, const AttnArgs& a, hipStream_t s) {
   const int64_t tokens = static_cast<int64_t>(a.n_seq) * a.S;  // one wave per token
   const dim3 dgrid(static_cast<unsigned>((tokens + 3) / 4));
   if constexpr (DH >= 64) {
     if (dtype == LD_BF16) {
-      if (part == 0)
-        hipLaunchKernelGGL((ld_attn_delta<bf16, DH>), dgrid, dim3(256), 0, s, a);
-      else if (part == 1) {
+      if (part == 1) {
         constexpr int nw = dkdv_waves<DH>();
         const dim3 grid(a.H, a.n_seq, (a.S + 32 * nw - 1) / (32 * nw));
         if (a.alibi)
           hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw, true>), grid, dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
         else
           hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw, false>), grid, dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
-      } else {
+      } else if (part == 0) {
         const dim3 grid(a.H, a.n_seq, (a.S + DQ_ROWS - 1) / DQ_ROWS);
         if (a.alibi)
           hipLaunchKernelGGL((ld_attn_bwd_dq_bf16<DH, true>), grid, dim3(512), dq_lds_bytes<DH>(), s, a);
@@ -1115,9 +1128,11 @@ hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+int attn_bwd_parts(int dtype) { return dtype == LD_BF16 ? 2 : 3; }
+
 const char* attn_bwd_kernel_name(int dtype, int part) {
   static const char* names[2][3] = {{"ld_attn_delta", "ld_attn_bwd_dkdv_f32", "ld_attn_bwd_dq_f32"},
-                                    {"ld_attn_delta", "ld_attn_bwd_dkdv_bf16", "ld_attn_bwd_dq_bf16"}};
+                                    {"ld_attn_bwd_dq_bf16", "ld_attn_bwd_dkdv_bf16", ""}};
   return names[dtype == LD_BF16 ? 1 : 0][part];
 }
 
@@ -1140,8 +1155,9 @@ hipError_t launch_attn_bwd_part(int dtype, int part, const AttnArgs& a, hipStrea
 // The backward's only scratch is delta = rowsum(dO * O).  The no-allocation
 // entry point keeps it in this array instead of a caller workspace; each GPU
 // holds its own copy until the process ends, and every call on a GPU shares
-// it (calls that overlap on one GPU race).  The delta kernel writes every
-// entry the other two kernels read, so nothing needs clearing.  On the host
+// it (calls that overlap on one GPU race).  The kernel that forms delta (dQ
+// in bf16, a delta kernel in float32) writes every entry the dK/dV kernel
+// reads before it runs, so nothing needs clearing.  On the host
 // the array's name is only a stand-in: kernels get the address
 // hipGetSymbolAddress returns for the current device.
 static __device__ __align__(256) float scratch[kAttnScratchBytes / sizeof(float)];
@@ -1168,7 +1184,7 @@ hipError_t attn_scratch_ptr(float** out) {
 }
 
 hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
-  for (int part = 0; part < 3; ++part) {
+  for (int part = 0; part < attn_bwd_parts(dtype); ++part) {
     const hipError_t e = launch_attn_bwd_part(dtype, part, a, s);
     if (e != hipSuccess) return e;
   }

@@ -422,7 +422,9 @@ constexpr size_t kAttnScratchBytes = size_t(8) << 20;
 hipError_t attn_scratch_ptr(float** out);
 hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
-// The three backward kernels one at a time: 0 delta, 1 dK/dV, 2 dQ.
+// The backward kernels one at a time, attn_bwd_parts of them: bf16 0 dQ
+// (which also forms delta), 1 dK/dV; float32 0 delta, 1 dK/dV, 2 dQ.
+int attn_bwd_parts(int dtype);
 hipError_t launch_attn_bwd_part(int dtype, int part, const AttnArgs& a, hipStream_t s);
 const char* attn_bwd_kernel_name(int dtype, int part);
 const char* attn_fwd_kernel_name(int dtype);
