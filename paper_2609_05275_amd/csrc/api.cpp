@@ -367,33 +367,65 @@ int run_gemm(int dtype, int a_k, int b_k, GemmArgs g, int64_t max_m, int64_t hos
   return LD_OK;
 }
 
-// A weight-gradient GEMM (g1: both operands mn-contiguous, float32 out, its
-// reduction length the kept rows) and the input-gradient GEMM that reads the
-// same upstream gradient (g2: A k-contiguous, B mn-contiguous) in one launch
-// when both take the 256x256 kernel; otherwise one after the other.
-bool gemm_pair_ok(int dtype, const GemmArgs& g1, int64_t max_k1, const GemmArgs& g2, int64_t max_m2) {
-  return dtype == LD_BF16 && plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, true).big &&
+// Weight-gradient GEMMs (g1, and g3 when given: both operands mn-contiguous,
+// float32 out, their reduction length the kept rows) and an input-gradient
+// GEMM (g2: A k-contiguous, B mn-contiguous) in one launch when all take the
+// 256x256 kernel; otherwise one after the other.  g1.M = 0: no g1.
+bool gemm_pair_ok(int dtype, const GemmArgs& g1, int64_t max_k1, const GemmArgs& g2, int64_t max_m2,
+                  const GemmArgs* g3 = nullptr) {
+  return dtype == LD_BF16 && (g1.M == 0 || plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, true).big) &&
+         (!g3 || plan_gemm(dtype, 0, 0, *g3, g3->M, max_k1, false).big) &&
          plan_gemm(dtype, 1, 0, g2, max_m2, 0, false).big;
+}
+
+// The plan run_gemm_pair takes for these GEMMs (the 256x256 kernels).
+PairPlan pair_plan(int dtype, const GemmArgs& g1, int64_t host_k1, int64_t max_k1, const GemmArgs& g2,
+                   int64_t max_m2, int64_t host_m2, bool can_split, const GemmArgs* g3 = nullptr) {
+  const bool has1 = g1.M > 0;
+  const int max_splits = has1 ? plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, can_split).splits : 1;
+  const int64_t plan_k1 = host_k1 >= 0 ? host_k1 : max_k1, plan_m2 = host_m2 >= 0 ? host_m2 : max_m2;
+  return plan_gemm_pair(has1 ? g1.M : 0, g1.N, plan_k1, g3 ? g3->M : 0, g3 ? g3->N : 0, plan_m2, g2.N, g2.K,
+                        max_splits);
+}
+
+// Whether the backward of a sub-block runs its input-gradient GEMM gA alone
+// and puts its weight gradient wA into the launch of (wB, gB) -- three
+// GEMMs in one launch -- rather than the two pairs (wA, gA) and (wB, gB):
+// when all take the 256x256 kernels and the launches' estimated times say
+// so for these kept rows.
+bool group_weight_grads(int dtype, const GemmArgs& wA, const GemmArgs& gA, const GemmArgs& wB, const GemmArgs& gB,
+                        int64_t host_k, int64_t T, bool can_split) {
+  const GemmArgs none = gemm_args();
+  if (host_k < 0 || !gemm_pair_ok(dtype, wA, T, gA, T) || !gemm_pair_ok(dtype, none, T, gA, T) ||
+      !gemm_pair_ok(dtype, wB, T, gB, T, &wA))
+    return false;
+  const double pairs = pair_plan(dtype, wA, host_k, T, gA, T, host_k, can_split).est +
+                       pair_plan(dtype, wB, host_k, T, gB, T, host_k, can_split).est;
+  const double grouped = pair_plan(dtype, none, host_k, T, gA, T, host_k, can_split).est +
+                         pair_plan(dtype, wB, host_k, T, gB, T, host_k, can_split, &wA).est;
+  return grouped < pairs;
 }
 
 // g2.glu_f > 0 (only when gemm_pair_ok): the SwiGLU backward is fused into
 // g2's epilogue (see GemmArgs).
 int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmArgs g2, int64_t max_m2,
-                  int64_t host_m2, int64_t host_k2, hipStream_t s, float* part, size_t part_bytes) {
-  const GemmPlan p1 = plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, part != nullptr);
-  const GemmPlan p2 = plan_gemm(dtype, 1, 0, g2, max_m2, 0, false);
-  if (dtype != LD_BF16 || !p1.big || !p2.big) {
+                  int64_t host_m2, int64_t host_k2, hipStream_t s, float* part, size_t part_bytes,
+                  const GemmArgs* g3 = nullptr) {
+  const bool has1 = g1.M > 0;
+  if (!gemm_pair_ok(dtype, g1, max_k1, g2, max_m2, g3)) {
     if (g2.glu_f > 0 || g2.relu2) return fail(LD_E_INVALID, "a fused activation backward needs the paired 256x256 kernels");
     if (int rc = run_gemm(dtype, 1, 0, g2, max_m2, host_m2, host_k2, s)) return rc;
-    return run_gemm(dtype, 0, 0, g1, g1.M, g1.M, host_k1, s, part, part_bytes, max_k1);
+    if (has1)
+      if (int rc = run_gemm(dtype, 0, 0, g1, g1.M, g1.M, host_k1, s, part, part_bytes, max_k1)) return rc;
+    if (g3) return run_gemm(dtype, 0, 0, *g3, g3->M, g3->M, host_k1, s, part, part_bytes, max_k1);
+    return LD_OK;
   }
   // at most the split count the standalone plan (and the scratch) allows,
   // planned for the kept rows when the host knows them (the grid still
   // covers max_m2 rows; the device counts decide which work)
-  const int64_t plan_k1 = host_k1 >= 0 ? host_k1 : max_k1, plan_m2 = host_m2 >= 0 ? host_m2 : max_m2;
-  const PairPlan pp = plan_gemm_pair(g1.M, g1.N, plan_k1, plan_m2, g2.N, g2.K, p1.splits);
+  const PairPlan pp = pair_plan(dtype, g1, host_k1, max_k1, g2, max_m2, host_m2, part != nullptr, g3);
   if (pp.splits1 > 1) {
-    GemmPlan q = p1;
+    GemmPlan q = plan_gemm(dtype, 0, 0, g1, g1.M, max_k1, true);
     q.splits = pp.splits1;
     if (gemm_part_bytes(q, g1.M, g1.N) > part_bytes) return fail(LD_E_WORKSPACE, "split-K scratch too small");
     g1.part = part;
@@ -401,15 +433,17 @@ int run_gemm_pair(int dtype, GemmArgs g1, int64_t host_k1, int64_t max_k1, GemmA
   const char* name = g2.relu2 ? "ld_gemm_bf16_tn_nn_relu2_256"
                     : g2.glu_f > 0 ? "ld_gemm_bf16_tn_nn_glu_256" : "ld_gemm_bf16_tn_nn_256";
   ProfScope ps(name, s);
-  const hipError_t e = launch_gemm_pair(g1, pp, g2, max_m2, s);
+  const hipError_t e = launch_gemm_pair(g1, g3, pp, g2, max_m2, s);
   if (e != hipSuccess) return fail(LD_E_HIP, "%s launch: %s", name, hipGetErrorString(e));
-  const double M1 = g1.M, N1 = g1.N, K1 = static_cast<double>(host_k1);
+  const double K1 = static_cast<double>(host_k1);
   const double M2 = static_cast<double>(host_m2), N2 = g2.N, K2 = static_cast<double>(host_k2);
+  const double mn1 = has1 ? static_cast<double>(g1.M) * g1.N : 0.0, mn3 = g3 ? static_cast<double>(g3->M) * g3->N : 0.0;
+  const double mk1 = has1 ? static_cast<double>(g1.M + g1.N) : 0.0, mk3 = g3 ? static_cast<double>(g3->M + g3->N) : 0.0;
   // a fused epilogue reads [u v] and writes [gu gv] (u and gu with squared
   // ReLU) instead of writing gs
   const double out2 = g2.relu2 ? 2.0 * M2 * N2 : g2.glu_f > 0 ? 4.0 * M2 * N2 : 1.0 * M2 * N2;
-  ps.end(2.0 * (M1 * N1 * K1 + M2 * N2 * K2),
-         2.0 * (M1 * K1 + N1 * K1) + 4.0 * M1 * N1 * pp.splits1 + 2.0 * (M2 * K2 + N2 * K2 + out2));
+  ps.end(2.0 * ((mn1 + mn3) * K1 + M2 * N2 * K2),
+         2.0 * (mk1 + mk3) * K1 + 4.0 * (mn1 * pp.splits1 + mn3) + 2.0 * (M2 * K2 + N2 * K2 + out2));
   if (pp.splits1 > 1) {
     const int64_t mn = static_cast<int64_t>(g1.M) * g1.N;
     ProfScope pr("ld_splitk_reduce", s);
@@ -717,47 +751,72 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
     if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
     ps.end(0, ((ds.f32 ? 4.0 : D.es) + D.es) * hm * D.d);
   }
-  // gs = r * gk W_down [M, f] and dW_down = r * gk^T s [d, f], one launch;
-  // in the paired kernels the activation's backward is fused into the first
-  // product's epilogue (guv from gs without storing gs)
-  bool act_fused = false;
-  {
-    GemmArgs g = gemm_args();
-    g.A = W(BL.gk);
-    g.lda = D.d;
-    g.B = w.w_down;
-    g.ldb = D.f;
-    g.C = W(BL.gs);
-    g.ldc = D.f;
-    g.alpha_dev = mv.r;
-    g.N = static_cast<int32_t>(D.f);
-    g.K = static_cast<int32_t>(D.d);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    GemmArgs g1 = gemm_args();
-    g1.A = W(BL.gk);
-    g1.lda = D.d;
-    g1.B = act.at(act.L.s);
-    g1.ldb = D.f;
-    g1.C = dw.w_down;
-    g1.ldc = D.f;
-    g1.c_f32 = 1;
-    g1.alpha_dev = mv.r;
-    g1.M = static_cast<int32_t>(D.d);
-    g1.N = static_cast<int32_t>(D.f);
-    g1.dev_count = mv.count;
-    g1.count_mult = S;
-    g1.count_dim = 1;
-    if (gemm_pair_ok(dt, g1, T, g, T)) {
-      act_fused = true;
-      g.C = W(BL.guv);
-      g.ldc = D.fw;
-      g.aux = act.at(act.L.uv);
-      g.glu_f = static_cast<int32_t>(D.f);
-      g.relu2 = D.kind == LD_BLOCK_ALIBI_RELU2;
-    }
-    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
+  // gs = r * gk W_down [M, f] and dW_down = r * gk^T s [d, f]; gh2 = guv
+  // W_gate_up [M, d] and dW_gate_up = guv^T h2 [fw, d].  With the 256x256
+  // kernels the activation's backward is fused into gs's epilogue (guv from
+  // gs without storing gs), and dW_down waits for the gate/up launch, which
+  // then holds both weight gradients (mostly without split-K).
+  GemmArgs g_gs = gemm_args();
+  g_gs.A = W(BL.gk);
+  g_gs.lda = D.d;
+  g_gs.B = w.w_down;
+  g_gs.ldb = D.f;
+  g_gs.C = W(BL.gs);
+  g_gs.ldc = D.f;
+  g_gs.alpha_dev = mv.r;
+  g_gs.N = static_cast<int32_t>(D.f);
+  g_gs.K = static_cast<int32_t>(D.d);
+  g_gs.dev_count = mv.count;
+  g_gs.count_mult = S;
+  GemmArgs g_wd = gemm_args();
+  g_wd.A = W(BL.gk);
+  g_wd.lda = D.d;
+  g_wd.B = act.at(act.L.s);
+  g_wd.ldb = D.f;
+  g_wd.C = dw.w_down;
+  g_wd.ldc = D.f;
+  g_wd.c_f32 = 1;
+  g_wd.alpha_dev = mv.r;
+  g_wd.M = static_cast<int32_t>(D.d);
+  g_wd.N = static_cast<int32_t>(D.f);
+  g_wd.dev_count = mv.count;
+  g_wd.count_mult = S;
+  g_wd.count_dim = 1;
+  GemmArgs g_gh2 = gemm_args();
+  g_gh2.A = W(BL.guv);
+  g_gh2.lda = D.fw;
+  g_gh2.B = w.w_gate_up;
+  g_gh2.ldb = D.d;
+  g_gh2.C = W(BL.gh);
+  g_gh2.ldc = D.d;
+  g_gh2.N = static_cast<int32_t>(D.d);
+  g_gh2.K = static_cast<int32_t>(D.fw);
+  g_gh2.dev_count = mv.count;
+  g_gh2.count_mult = S;
+  GemmArgs g_wgu = gemm_args();
+  g_wgu.A = W(BL.guv);
+  g_wgu.lda = D.fw;
+  g_wgu.B = act.at(act.L.h2);
+  g_wgu.ldb = D.d;
+  g_wgu.C = dw.w_gate_up;
+  g_wgu.ldc = D.d;
+  g_wgu.c_f32 = 1;
+  g_wgu.M = static_cast<int32_t>(D.fw);
+  g_wgu.N = static_cast<int32_t>(D.d);
+  g_wgu.dev_count = mv.count;
+  g_wgu.count_mult = S;
+  g_wgu.count_dim = 1;
+  const GemmArgs none = gemm_args();  // M = 0: no weight gradient in the launch
+  const bool act_fused = gemm_pair_ok(dt, g_wd, T, g_gs, T);
+  const bool grouped = act_fused && group_weight_grads(dt, g_wd, g_gs, g_wgu, g_gh2, hm, T, SK != nullptr);
+  if (act_fused) {
+    g_gs.C = W(BL.guv);
+    g_gs.ldc = D.fw;
+    g_gs.aux = act.at(act.L.uv);
+    g_gs.glu_f = static_cast<int32_t>(D.f);
+    g_gs.relu2 = D.kind == LD_BLOCK_ALIBI_RELU2;
   }
+  if (int rc = run_gemm_pair(dt, grouped ? none : g_wd, hm, T, g_gs, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
   // guv = SwiGLU backward, or gu = squared-ReLU backward
   if (!act_fused) {
     EltArgs a{};
@@ -776,34 +835,8 @@ int ffn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, co
       ps.end(0, D.es * hm * D.f * 3.0);
     }
   }
-  // gh2 = guv W_gate_up [M, d] and dW_gate_up = guv^T h2 [fw, d], one launch
-  {
-    GemmArgs g = gemm_args();
-    g.A = W(BL.guv);
-    g.lda = D.fw;
-    g.B = w.w_gate_up;
-    g.ldb = D.d;
-    g.C = W(BL.gh);
-    g.ldc = D.d;
-    g.N = static_cast<int32_t>(D.d);
-    g.K = static_cast<int32_t>(D.fw);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    GemmArgs g1 = gemm_args();
-    g1.A = W(BL.guv);
-    g1.lda = D.fw;
-    g1.B = act.at(act.L.h2);
-    g1.ldb = D.d;
-    g1.C = dw.w_gate_up;
-    g1.ldc = D.d;
-    g1.c_f32 = 1;
-    g1.M = static_cast<int32_t>(D.fw);
-    g1.N = static_cast<int32_t>(D.d);
-    g1.dev_count = mv.count;
-    g1.count_mult = S;
-    g1.count_dim = 1;
-    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.fw, s, SK, BL.splitk_bytes)) return rc;
-  }
+  if (int rc = run_gemm_pair(dt, g_wgu, hm, T, g_gh2, T, hm, D.fw, s, SK, BL.splitk_bytes, grouped ? &g_wd : nullptr))
+    return rc;
   // gz = dL/dX^{l+1} + RMSNorm_bwd(zk, g_mlp, gh2); dg_mlp.  The residual
   // gradient is read from the stream itself; gz goes to gz32 (float32) and,
   // in bf16 configurations, to gz (the operand of the next GEMMs) -- or,
@@ -871,36 +904,64 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
     if ((e = launch_gather(dt, a, s)) != hipSuccess) return fail(LD_E_HIP, "gather: %s", hipGetErrorString(e));
     ps.end(0, ((ds.f32 ? 4.0 : D.es) + D.es) * hm * D.d);
   }
-  // ga = r * gz W_o [M, d] and dW_o = r * gz^T att [d, d], one launch
-  {
-    GemmArgs g = gemm_args();
-    g.A = gz_op;
-    g.lda = D.d;
-    g.B = w.w_o;
-    g.ldb = D.d;
-    g.C = W(BL.ga);
-    g.ldc = D.d;
-    g.alpha_dev = mv.r;
-    g.N = static_cast<int32_t>(D.d);
-    g.K = static_cast<int32_t>(D.d);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    GemmArgs g1 = gemm_args();
-    g1.A = gz_op;
-    g1.lda = D.d;
-    g1.B = act.at(act.L.att);
-    g1.ldb = D.d;
-    g1.C = dw.w_o;
-    g1.ldc = D.d;
-    g1.c_f32 = 1;
-    g1.alpha_dev = mv.r;
-    g1.M = static_cast<int32_t>(D.d);
-    g1.N = static_cast<int32_t>(D.d);
-    g1.dev_count = mv.count;
-    g1.count_mult = S;
-    g1.count_dim = 1;
-    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
-  }
+  // ga = r * gz W_o [M, d] and dW_o = r * gz^T att [d, d]; gh1 = gqkv W_qkv
+  // [M, d] and dW_qkv = gqkv^T h1 [3d, d].  With the 256x256 kernels dW_o
+  // waits for the QKV launch, which then holds both weight gradients: ga
+  // runs alone, and the two weight gradients (long workgroups) and gh1
+  // (short ones) fill one launch, mostly without split-K.
+  GemmArgs g_ga = gemm_args();
+  g_ga.A = gz_op;
+  g_ga.lda = D.d;
+  g_ga.B = w.w_o;
+  g_ga.ldb = D.d;
+  g_ga.C = W(BL.ga);
+  g_ga.ldc = D.d;
+  g_ga.alpha_dev = mv.r;
+  g_ga.N = static_cast<int32_t>(D.d);
+  g_ga.K = static_cast<int32_t>(D.d);
+  g_ga.dev_count = mv.count;
+  g_ga.count_mult = S;
+  GemmArgs g_wo = gemm_args();
+  g_wo.A = gz_op;
+  g_wo.lda = D.d;
+  g_wo.B = act.at(act.L.att);
+  g_wo.ldb = D.d;
+  g_wo.C = dw.w_o;
+  g_wo.ldc = D.d;
+  g_wo.c_f32 = 1;
+  g_wo.alpha_dev = mv.r;
+  g_wo.M = static_cast<int32_t>(D.d);
+  g_wo.N = static_cast<int32_t>(D.d);
+  g_wo.dev_count = mv.count;
+  g_wo.count_mult = S;
+  g_wo.count_dim = 1;
+  GemmArgs g_gh1 = gemm_args();
+  g_gh1.A = W(BL.gqkv);
+  g_gh1.lda = 3 * D.d;
+  g_gh1.B = w.w_qkv;
+  g_gh1.ldb = D.d;
+  g_gh1.C = W(BL.gh);
+  g_gh1.ldc = D.d;
+  g_gh1.N = static_cast<int32_t>(D.d);
+  g_gh1.K = static_cast<int32_t>(3 * D.d);
+  g_gh1.dev_count = mv.count;
+  g_gh1.count_mult = S;
+  GemmArgs g_wqkv = gemm_args();
+  g_wqkv.A = W(BL.gqkv);
+  g_wqkv.lda = 3 * D.d;
+  g_wqkv.B = act.at(act.L.h1);
+  g_wqkv.ldb = D.d;
+  g_wqkv.C = dw.w_qkv;
+  g_wqkv.ldc = D.d;
+  g_wqkv.c_f32 = 1;
+  g_wqkv.M = static_cast<int32_t>(3 * D.d);
+  g_wqkv.N = static_cast<int32_t>(D.d);
+  g_wqkv.dev_count = mv.count;
+  g_wqkv.count_mult = S;
+  g_wqkv.count_dim = 1;
+  const GemmArgs none = gemm_args();  // M = 0: no weight gradient in the launch
+  const bool grouped = group_weight_grads(dt, g_wo, g_ga, g_wqkv, g_gh1, hm, T, SK != nullptr);
+  if (int rc = run_gemm_pair(dt, grouped ? none : g_wo, hm, T, g_ga, T, hm, D.d, s, SK, BL.splitk_bytes)) return rc;
   // attention backward -> gqkv
   {
     AttnArgs a{};
@@ -932,34 +993,9 @@ int attn_backward_part(const Dims& D, const ld_weights& w, const MaskView& mv, c
              D.es * hm * D.d * (dkdv ? 5.0 : dq ? (dt == LD_BF16 ? 6.0 : 5.0) : 2.0));
     }
   }
-  // gh1 = gqkv W_qkv [M, d] and dW_qkv = gqkv^T h1 [3d, d], one launch
-  {
-    GemmArgs g = gemm_args();
-    g.A = W(BL.gqkv);
-    g.lda = 3 * D.d;
-    g.B = w.w_qkv;
-    g.ldb = D.d;
-    g.C = W(BL.gh);
-    g.ldc = D.d;
-    g.N = static_cast<int32_t>(D.d);
-    g.K = static_cast<int32_t>(3 * D.d);
-    g.dev_count = mv.count;
-    g.count_mult = S;
-    GemmArgs g1 = gemm_args();
-    g1.A = W(BL.gqkv);
-    g1.lda = 3 * D.d;
-    g1.B = act.at(act.L.h1);
-    g1.ldb = D.d;
-    g1.C = dw.w_qkv;
-    g1.ldc = D.d;
-    g1.c_f32 = 1;
-    g1.M = static_cast<int32_t>(3 * D.d);
-    g1.N = static_cast<int32_t>(D.d);
-    g1.dev_count = mv.count;
-    g1.count_mult = S;
-    g1.count_dim = 1;
-    if (int rc = run_gemm_pair(dt, g1, hm, T, g, T, hm, 3 * D.d, s, SK, BL.splitk_bytes)) return rc;
-  }
+  if (int rc = run_gemm_pair(dt, g_wqkv, hm, T, g_gh1, T, hm, 3 * D.d, s, SK, BL.splitk_bytes,
+                             grouped ? &g_wo : nullptr))
+    return rc;
   // dL/dX^l[kept rows] = dL/dZ + RMSNorm_bwd(xk, g_attn, gh1); dg_attn.  dL/dZ
   // is gz32 (float32), or the stream's rows under sub-layer granularity.
   {

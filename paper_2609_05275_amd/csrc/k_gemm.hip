@@ -18,7 +18,9 @@
 // configuration only.
 #include <algorithm>
 #include <functional>
+#include <initializer_list>
 #include <queue>
+#include <utility>
 #include <type_traits>
 #include <vector>
 
@@ -1087,44 +1089,47 @@ LD_BIG_ATTRS void ld_gemm_bf16_nt_relu2_256(GemmArgs g) {
   gemm_big_body<true, true, kEpiRelu2Fwd>(g, ring, blockIdx.x, gridDim.x, 0, 1);
 }
 
-// Two GEMMs in one launch: a weight-gradient GEMM g1 (both operands
-// mn-contiguous, tiles1 tiles, each split into splits1 k ranges) and an
-// input-gradient GEMM g2 (A k-contiguous, B mn-contiguous, tiles2 tiles) that
-// read the same upstream gradient.  The workgroups of one GEMM come first
-// (g2's when g2_first); the other's then fill the CUs the first leaves idle,
-// so neither GEMM's last partial round of tiles runs on a part-empty chip.
+// Up to three GEMMs in one launch: weight-gradient GEMMs g1 (tiles1 tiles,
+// each split into splits1 k ranges) and g3 (tiles3 tiles, never split; both
+// with both operands mn-contiguous) and an input-gradient GEMM g2 (A
+// k-contiguous, B mn-contiguous, tiles2 tiles).  The workgroups go in the
+// order g3, g1, g2, or g2 first (g2_first); the later GEMMs' workgroups
+// fill the CUs the earlier ones leave idle, so no GEMM's last partial round
+// runs on a part-empty chip.  tiles1 = tiles3 = 0 leaves g2 alone.
 template <int EPI2>
-__device__ __forceinline__ void gemm_pair_body(const GemmArgs& g1, const GemmArgs& g2, int tiles1, int splits1,
-                                               int tiles2, int g2_first) {
+__device__ __forceinline__ void gemm_pair_body(const GemmArgs& g1, const GemmArgs& g3, const GemmArgs& g2, int tiles1,
+                                               int splits1, int tiles3, int tiles2, int g2_first) {
   __shared__ __align__(16) bf16 ring[ring_elems<true, false>()];
   const int n1 = tiles1 * splits1;
   int id = blockIdx.x;
-  bool first = true;
   if (g2_first) {
-    first = id >= tiles2;
-    id = first ? id - tiles2 : id;
-  } else if (id >= n1) {
-    first = false;
-    id -= n1;
+    if (id < tiles2) {
+      gemm_big_body<true, false, EPI2>(g2, ring, id, tiles2, 0, 1);
+      return;
+    }
+    id -= tiles2;
+  } else if (id >= tiles3 + n1) {
+    gemm_big_body<true, false, EPI2>(g2, ring, id - tiles3 - n1, tiles2, 0, 1);
+    return;
   }
-  if (first)
-    gemm_big_body<false, false>(g1, ring, id % tiles1, tiles1, id / tiles1, splits1);
+  if (id < tiles3)
+    gemm_big_body<false, false>(g3, ring, id, tiles3, 0, 1);
   else
-    gemm_big_body<true, false, EPI2>(g2, ring, id, tiles2, 0, 1);
+    gemm_big_body<false, false>(g1, ring, (id - tiles3) % tiles1, tiles1, (id - tiles3) / tiles1, splits1);
 }
-LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
-                                         int g2_first) {
-  gemm_pair_body<kEpiPlain>(g1, g2, tiles1, splits1, tiles2, g2_first);
+LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_256(GemmArgs g1, GemmArgs g3, GemmArgs g2, int tiles1, int splits1, int tiles3,
+                                         int tiles2, int g2_first) {
+  gemm_pair_body<kEpiPlain>(g1, g3, g2, tiles1, splits1, tiles3, tiles2, g2_first);
 }
 // The same with the SwiGLU backward fused into g2's epilogue (see GemmArgs).
-LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_glu_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
-                                             int g2_first) {
-  gemm_pair_body<kEpiGluBwd>(g1, g2, tiles1, splits1, tiles2, g2_first);
+LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_glu_256(GemmArgs g1, GemmArgs g3, GemmArgs g2, int tiles1, int splits1,
+                                             int tiles3, int tiles2, int g2_first) {
+  gemm_pair_body<kEpiGluBwd>(g1, g3, g2, tiles1, splits1, tiles3, tiles2, g2_first);
 }
 // The same with the squared-ReLU backward fused into g2's epilogue.
-LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_relu2_256(GemmArgs g1, GemmArgs g2, int tiles1, int splits1, int tiles2,
-                                               int g2_first) {
-  gemm_pair_body<kEpiRelu2Bwd>(g1, g2, tiles1, splits1, tiles2, g2_first);
+LD_BIG_ATTRS void ld_gemm_bf16_tn_nn_relu2_256(GemmArgs g1, GemmArgs g3, GemmArgs g2, int tiles1, int splits1,
+                                               int tiles3, int tiles2, int g2_first) {
+  gemm_pair_body<kEpiRelu2Bwd>(g1, g3, g2, tiles1, splits1, tiles3, tiles2, g2_first);
 }
 
 // C[i] = sum over splits of part[s][i], float32, in split order.  Every
@@ -1252,60 +1257,65 @@ hipError_t launch_gemm_plan(int dtype, int a_kcontig, int b_kcontig, const GemmP
 }
 
 // Estimated finish time, in k tiles of 32 (~1 us each at these shapes), of
-// n1 workgroups of cost c1 followed by n2 of cost c2 dealt in launch order to
-// n_cu CUs, one workgroup per CU, each CU taking the next when it frees.
-static double list_schedule(int64_t n1, double c1, int64_t n2, double c2, int n_cu) {
+// classes of workgroups (count, cost each) dealt in launch order to n_cu
+// CUs, one workgroup per CU, each CU taking the next when it frees.
+static double list_schedule(std::initializer_list<std::pair<int64_t, double>> classes, int n_cu) {
   std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
   for (int i = 0; i < n_cu; ++i) cu.push(0.0);
   double end = 0.0;
-  for (int64_t w = 0; w < n1 + n2; ++w) {
-    const double t = cu.top() + (w < n1 ? c1 : c2);
-    cu.pop();
-    cu.push(t);
-    end = std::max(end, t);
-  }
+  for (const auto& c : classes)
+    for (int64_t w = 0; w < c.first; ++w) {
+      const double t = cu.top() + c.second;
+      cu.pop();
+      cu.push(t);
+      end = std::max(end, t);
+    }
   return end;
 }
 
-PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m2, int64_t n2, int64_t k2,
-                         int max_splits) {
+PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m3, int64_t n3, int64_t m2, int64_t n2,
+                        int64_t k2, int max_splits) {
   int dev = 0, n_cu = 256;
   if (hipGetDevice(&dev) == hipSuccess)
     (void)hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
   if (n_cu <= 0) n_cu = 256;
   struct Entry {
-    int64_t key[7];
+    int64_t key[9];
     PairPlan plan;
   };
-  thread_local Entry cache[8];
+  constexpr int kEntries = 64;  // the kept counts of a step give a few dozen shapes
+  thread_local Entry cache[kEntries];
   thread_local int next = 0;
-  const int64_t key[7] = {m1, n1, k1, m2, n2, k2, max_splits * 4096ll + n_cu};
+  const int64_t key[9] = {m1, n1, k1, m3, n3, m2, n2, k2, max_splits * 4096ll + n_cu};
   for (const Entry& e : cache)
-    if (std::equal(key, key + 7, e.key)) return e.plan;
+    if (std::equal(key, key + 9, e.key)) return e.plan;
   constexpr double kEpi = 8.0;       // epilogue of one tile, in k-tile times
   constexpr double kLaunch = 4.0;    // a second (reduction) launch
   constexpr double kTileUs = 0.95;   // one k tile of 32 on one CU
-  const int64_t tiles1 = ((m1 + GB - 1) / GB) * ((n1 + GB - 1) / GB);
-  const int64_t tiles2 = ((m2 + GB - 1) / GB) * ((n2 + GB - 1) / GB);
+  auto tiles = [](int64_t m, int64_t n) { return ((m + GB - 1) / GB) * ((n + GB - 1) / GB); };
+  const int64_t tiles1 = m1 > 0 ? tiles(m1, n1) : 0, tiles3 = m3 > 0 ? tiles(m3, n3) : 0;
+  const int64_t tiles2 = tiles(m2, n2);
+  const int64_t nkt1 = (k1 + GK - 1) / GK;
   const double c2 = static_cast<double>((k2 + GK - 1) / GK) + kEpi;
-  PairPlan best{1, 0};
+  const double c3 = static_cast<double>(nkt1) + kEpi;
+  PairPlan best{1, 0, 0.0};
   double best_t = 0.0;
-  for (int sp = 1; sp <= max_splits; ++sp) {
-    const double c1 = static_cast<double>(((k1 + GK - 1) / GK + sp - 1) / sp) + kEpi;
+  for (int sp = 1; sp <= (tiles1 > 0 ? max_splits : 1); ++sp) {
+    const double c1 = static_cast<double>((nkt1 + sp - 1) / sp) + kEpi;
     for (int order = 0; order < 2; ++order) {
-      double t = order ? list_schedule(tiles2, c2, tiles1 * sp, c1, n_cu)
-                       : list_schedule(tiles1 * sp, c1, tiles2, c2, n_cu);
+      double t = order ? list_schedule({{tiles2, c2}, {tiles3, c3}, {tiles1 * sp, c1}}, n_cu)
+                       : list_schedule({{tiles3, c3}, {tiles1 * sp, c1}, {tiles2, c2}}, n_cu);
       if (sp > 1)  // partials written and read back at ~5 TB/s, plus a launch
         t += kLaunch + (sp + 1.0) * 4.0 * m1 * n1 / 5e12 / (kTileUs * 1e-6);
       if ((sp == 1 && order == 0) || t < best_t - 1e-9) {
         best_t = t;
-        best = PairPlan{sp, order};
+        best = PairPlan{sp, order, t};
       }
     }
   }
   Entry& e = cache[next];
-  next = (next + 1) % 8;
-  std::copy(key, key + 7, e.key);
+  next = (next + 1) % kEntries;
+  std::copy(key, key + 9, e.key);
   e.plan = best;
   return best;
 }
@@ -1324,26 +1334,34 @@ hipError_t launch_gemm_relu2_fwd(const GemmArgs& g, int64_t max_m, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s) {
+hipError_t launch_gemm_pair(GemmArgs g1, const GemmArgs* g3, const PairPlan& p, const GemmArgs& g2, int64_t max_m2,
+                            hipStream_t s) {
   const int splits1 = p.splits1;
-  const int64_t tiles1 = ((static_cast<int64_t>(g1.M) + GB - 1) / GB) * ((g1.N + GB - 1) / GB);
+  const int64_t tiles1 =
+      g1.M > 0 ? ((static_cast<int64_t>(g1.M) + GB - 1) / GB) * ((g1.N + GB - 1) / GB) : 0;
+  const int64_t tiles3 =
+      g3 ? ((static_cast<int64_t>(g3->M) + GB - 1) / GB) * ((g3->N + GB - 1) / GB) : 0;
   const int64_t tiles2 = ((max_m2 + GB - 1) / GB) * ((g2.N + GB - 1) / GB);
   if (splits1 > 1) {
     if (!g1.part) return hipErrorInvalidValue;
   } else {
     g1.part = nullptr;
   }
-  const int64_t wg = tiles1 * splits1 + tiles2;
+  const GemmArgs g3v = g3 ? *g3 : g1;
+  const int64_t wg = tiles1 * splits1 + tiles3 + tiles2;
   if (wg <= 0) return hipSuccess;
   if (g2.relu2)
-    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_relu2_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
-                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
+    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_relu2_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g3v, g2,
+                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles3), static_cast<int>(tiles2),
+                       p.g2_first);
   else if (g2.glu_f > 0)
-    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_glu_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
-                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
+    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_glu_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g3v, g2,
+                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles3), static_cast<int>(tiles2),
+                       p.g2_first);
   else
-    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g2,
-                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles2), p.g2_first);
+    hipLaunchKernelGGL(ld_gemm_bf16_tn_nn_256, dim3(static_cast<unsigned>(wg)), dim3(256), 0, s, g1, g3v, g2,
+                       static_cast<int>(tiles1), splits1, static_cast<int>(tiles3), static_cast<int>(tiles2),
+                       p.g2_first);
   return hipGetLastError();
 }
 

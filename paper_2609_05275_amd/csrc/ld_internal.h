@@ -389,21 +389,24 @@ const char* gemm_kernel_name(int dtype, int a_kcontig, int b_kcontig);
 GemmPlan plan_gemm(int dtype, int a_kcontig, int b_kcontig, const GemmArgs& g, int64_t max_m,
                    int64_t max_k, bool allow_split);
 size_t gemm_part_bytes(const GemmPlan& p, int64_t M, int64_t N);
-// A weight-gradient GEMM g1 (both operands mn-contiguous, float32 out) and an
+// Weight-gradient GEMMs g1 and g3 (both operands mn-contiguous, float32
+// out; g3 optional and never split, g1 absent when g1.M = 0) and an
 // input-gradient GEMM g2 (A k-contiguous, B mn-contiguous) in one launch,
-// both of whose plans are the 256x256 kernel.  plan_gemm_pair picks g1's
-// split count (at most max_splits) and which GEMM's workgroups go first from
-// an estimate of the pair's finish time; g1.part must hold
-// splits1 * M1 * N1 floats when splits1 > 1.
+// all of whose plans are the 256x256 kernel.  plan_gemm_pair picks g1's
+// split count (at most max_splits) and whether g2's workgroups go first
+// from an estimate of the launch's finish time (m3 = 0: no g3); g1.part
+// must hold splits1 * M1 * N1 floats when splits1 > 1.
 struct PairPlan {
   int splits1;
   int g2_first;
+  double est;  // estimated launch time (k-tile times of one CU), reduction included
 };
-PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m2, int64_t n2, int64_t k2,
-                        int max_splits);
-// Launches the pair kernel only; with p.splits1 > 1 the caller then sums the
+PairPlan plan_gemm_pair(int64_t m1, int64_t n1, int64_t k1, int64_t m3, int64_t n3, int64_t m2, int64_t n2,
+                        int64_t k2, int max_splits);
+// Launches the kernel only; with p.splits1 > 1 the caller then sums g1's
 // partials with launch_splitk_reduce.
-hipError_t launch_gemm_pair(GemmArgs g1, const PairPlan& p, const GemmArgs& g2, int64_t max_m2, hipStream_t s);
+hipError_t launch_gemm_pair(GemmArgs g1, const GemmArgs* g3, const PairPlan& p, const GemmArgs& g2, int64_t max_m2,
+                            hipStream_t s);
 // C[i] = sum over splits of part[s * mn + i] (float32, split order).
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t mn, float* C, hipStream_t s);
 // The SwiGLU projection with its activation fused (GemmArgs glu_f, aux):
