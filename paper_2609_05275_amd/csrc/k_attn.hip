@@ -99,9 +99,8 @@ __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
 constexpr int BQ = 64;       // query rows per step of the dK/dV kernel
 constexpr int DK_NST = 4;    // dK/dV ring stages (query blocks in LDS)
 
-// Waves per dK/dV workgroup: four, one per SIMD.
-template <int DH>
-constexpr int dkdv_waves() { return 4; }
+// Key groups of 32 per dK/dV workgroup: four, each served by a pair of waves.
+constexpr int DK_GROUPS = 4;
 
 // Q and dO blocks in the dK/dV ring are [64 q][DH] without padding, the
 // 16-byte chunks of a row XOR-swizzled by row bits 0-3: 16 lanes reading one
@@ -122,10 +121,14 @@ __device__ __forceinline__ int qd_off(int r, int d) {
 // One ring stage: the Q block, the dO block, then log-sum-exp and delta.
 template <int DH>
 constexpr int dk_stage_bytes() { return 4 * BQ * DH + 8 * BQ; }
-// Loads per wave per stage: Q and dO in 1 KB pieces split over the waves,
-// plus the log-sum-exp and delta rows (every wave loads both: same bytes).
+// Loads per loading wave per stage: Q and dO in 1 KB pieces split over NW
+// waves, plus the log-sum-exp and delta rows (every loading wave loads both:
+// same bytes).
 template <int DH, int NW>
 constexpr int dk_loads() { return 2 * (BQ * DH * 2 / 1024) / NW + 2; }
+// P exchange area after the ring: the key groups x 4 KB (64 lanes x 16
+// floats).
+constexpr int kDkPBytes = DK_GROUPS * 4096;
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 
@@ -134,9 +137,13 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8_t;
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) const floatx4 lds_float4_t;
+typedef __attribute__((address_space(3))) floatx4 lds_float4_w_t;
 typedef __attribute__((address_space(3))) v4s lds_v4s_t;
 __device__ __forceinline__ bf16x8 lds_frag(uint32_t addr) {
   return *reinterpret_cast<lds_bf16x8_t*>(static_cast<uintptr_t>(addr));
+}
+__device__ __forceinline__ void lds_put(uint32_t addr, const floatx4& v) {
+  *reinterpret_cast<lds_float4_w_t*>(static_cast<uintptr_t>(addr)) = v;
 }
 __device__ __forceinline__ floatx4 lds_f4(uint32_t addr) {
   return *reinterpret_cast<lds_float4_t*>(static_cast<uintptr_t>(addr));
@@ -144,34 +151,46 @@ __device__ __forceinline__ floatx4 lds_f4(uint32_t addr) {
 __device__ __forceinline__ v4s lds_tr(uint32_t addr) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4s_t*>(static_cast<uintptr_t>(addr)));
 }
+__device__ __forceinline__ bf16x8 tr_pair(const v4s& lo, const v4s& hi) {
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
 
-// dK, dV.  A workgroup of NW waves owns 32 NW keys (32 per wave, K and V
-// fragments in registers) and walks the 64-row query blocks from the diagonal
-// to the end.  Q, dO, log-sum-exp and delta of each block go from global
-// memory straight into a four-stage LDS ring (buffer loads with an LDS
-// destination, see ld_internal.h), so a block's loads have two block-times to
-// land.  P = 2^(s*scale*log2e - lse*log2e) is recomputed, dS = P (dP - delta);
-// dV^T += dO^T P and dK^T += Q^T dS take P and dS straight from the score
-// accumulators (their rows are a fixed permutation of the MFMA k index), and
-// dO^T, Q^T come from the same [q][d] blocks through transposing reads
-// (ds_read_b64_tr_b16) in that permutation.
+// Waits for this wave's LDS accesses, then meets the workgroup.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// dK, dV.  A workgroup owns 128 keys in four groups of 32 and walks the
+// 64-row query blocks from the diagonal to the end, in 32-query halves.  Each
+// key group has two waves with different work, meant to share a SIMD (waves
+// g and g + 4): wave A holds K and forms the scores S = Q K^T, P =
+// 2^(s*scale*log2e - lse*log2e) (bf16) and dV^T += dO^T P; wave B holds V and
+// forms dP - delta = dO V^T - delta, dS = P (dP - delta) and dK^T += Q^T dS.
+// P (float32) goes from A to B through LDS, one half behind: in half u, A
+// computes S(u) and P(u) and the dV product of half u-1, B computes dS(u-1),
+// its dK product and dP(u).  Two workgroup barriers per half guard the one
+// P slot per key group: B reads P(u-1) before the first, A writes P(u) after
+// it, and the second ends the half.  A's vector work (the
+// exponentials) follows its MFMAs while B's (dS) precedes them, so the two
+// waves of a SIMD keep its matrix pipe busy in turn; with at most 256
+// registers each, two waves fit on a SIMD.  dV^T and dK^T take P and dS
+// straight from the score layout (their rows are a fixed permutation of the
+// MFMA k index), dO^T and Q^T come from the same [q][d] blocks through
+// transposing reads (ds_read_b64_tr_b16) in that permutation.
 //
-// Work goes in 32-row halves of a block, three steps each: A (scores S and
-// dP, 16 MFMAs), B (softmax, vector ALU only) and C (dV and dK, 16 MFMAs).
-// They are software-pipelined: while B of half u runs, the MFMAs of A(u+1)
-// and C(u-1) run beside it, so the softmax hides under matrix work instead
-// of stalling it.  Each block is one loop iteration of two half-steps with
-// the ring's barrier between them.  Fragment addresses are per-lane offsets
-// moved by one stage per block; the loop has no branch around its MFMAs
-// (query rows before a wave's keys are computed and masked to P = 0, a
-// phantom block past the end multiplies zeros, and waves past the end
-// compute on zero K/V and store nothing).
-template <int DH, int NW, bool AL>
-__global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
-  constexpr int BKEYS = 32 * NW, SB = dk_stage_bytes<DH>(), NL = dk_loads<DH, NW>();
+// Q, dO, log-sum-exp and delta of each block go from global memory straight
+// into a four-stage LDS ring (buffer loads with an LDS destination, issued by
+// the B waves, see ld_internal.h), so a block's loads have two block-times to
+// land.  Fragment addresses are per-lane offsets moved by one stage per
+// block; the loop has no branch around its MFMAs (query rows before a wave's
+// keys are computed and masked to P = 0, blocks past the end read zeros, and
+// waves past the end compute on zero K/V and store nothing).
+template <int DH, int NG, bool AL>
+__global__ __launch_bounds__(128 * NG) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
+  constexpr int BKEYS = 32 * NG, SB = dk_stage_bytes<DH>(), NL = dk_loads<DH, NG>();
   constexpr int RPI = 512 / DH, LPR = 64 / RPI;   // rows per 1 KB load, lanes per row
-  constexpr int NPW = (BQ * DH * 2 / 1024) / NW;  // 1 KB loads per wave per tile
+  constexpr int NPW = (BQ * DH * 2 / 1024) / NG;  // 1 KB loads per loading wave per tensor
+  constexpr int N = DH / 16, NDB = DH / 32;       // k steps of the score products, d blocks
   static_assert(DK_NST == 4, "stage arithmetic assumes a ring of four");
+  static_assert(NG == DK_GROUPS, "the P area is sized for DK_GROUPS key groups");
   extern __shared__ __align__(16) char ring[];
   const int S = a.S, H = a.H;
   // grid (head, sequence, tile), tile slowest: early key tiles see the most
@@ -181,55 +200,59 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   if (seq >= seq_count(a)) return;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool role_b = wave >= NG;  // wave-uniform
+  const int grp = wave & (NG - 1);
   const int hf = lane >> 5, cl = lane & 31;
-  const int k0 = kt * BKEYS, kw = k0 + wave * 32, key = kw + cl;
+  const int k0 = kt * BKEYS, kw = k0 + grp * 32, key = kw + cl;
   if (k0 >= S) return;  // the whole workgroup is past the end
   const bool active = kw < S;
   const int64_t ldq = 3ll * H * DH, ldo = static_cast<int64_t>(H) * DH;
   const bf16* base = static_cast<const bf16*>(a.qkv) + static_cast<int64_t>(seq) * S * ldq;
   const bf16* Qp = base + head * DH;
-  const bf16* Kp = base + static_cast<int64_t>(H) * DH + head * DH;
-  const bf16* Vp = base + 2ll * H * DH + head * DH;
+  // wave A holds K, wave B holds V: the same fragment slots
+  const bf16* KVp = base + (role_b ? 2ll : 1ll) * H * DH + head * DH;
   const bf16* dOp = static_cast<const bf16*>(a.go) + static_cast<int64_t>(seq) * S * ldo + head * DH;
   const float* lse = a.lse + (static_cast<int64_t>(seq) * H + head) * S;
   const float* del = a.delta + (static_cast<int64_t>(seq) * H + head) * S;
   const float sl2 = a.scale * kLog2e;
   const float al2 = AL ? alibi_slope(head, H) * kLog2e : 0.f;
 
-  bf16x8 kf[DH / 16], vf[DH / 16];
+  // K or V fragments of the wave's keys, loaded after the first ring block
+  // was requested (one wait covers both).  They must have arrived before the
+  // next ring loads are issued: the compiler does not see those loads, so a
+  // wait of its own for these inside the loop would wait for all of them.
+  bf16x8 kv[N];
+  auto load_kv = [&]() {
 #pragma unroll
-  for (int ks = 0; ks < DH / 16; ++ks) {
-    kf[ks] = key < S ? load8(Kp + static_cast<int64_t>(key) * ldq + ks * 16 + hf * 8) : zero8();
-    vf[ks] = key < S ? load8(Vp + static_cast<int64_t>(key) * ldq + ks * 16 + hf * 8) : zero8();
-  }
-  // The fragments must have arrived before the first LDS load is issued:
-  // the compiler does not see those loads, so a wait of its own for these
-  // inside the loop would wait for all of them, every iteration.
+    for (int ks = 0; ks < N; ++ks)
+      kv[ks] = key < S ? load8(KVp + static_cast<int64_t>(key) * ldq + ks * 16 + hf * 8) : zero8();
 #pragma unroll
-  for (int ks = 0; ks < DH / 16; ++ks) asm volatile("" ::"v"(kf[ks]), "v"(vf[ks]));
-  floatx16 dv[DH / 32], dk[DH / 32];
+    for (int ks = 0; ks < N; ++ks) asm volatile("" ::"v"(kv[ks]));
+  };
+  floatx16 acc[NDB];  // dV^T (wave A) or dK^T (wave B)
 #pragma unroll
-  for (int db = 0; db < DH / 32; ++db)
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) dv[db][v] = dk[db][v] = 0.f;
+    for (int v = 0; v < 16; ++v) acc[db][v] = 0.f;
 
-  // Loads of query block qb into stage st.  Blocks past the end (qb >= S)
-  // read zeros; every wave issues NL loads per stage.
+  // Loads of query block qb into stage st, by the B waves.  Blocks past the
+  // end (qb >= S) read zeros.
   const dma_rsrc rq = dma_make_rsrc(Qp, static_cast<int64_t>(S) * ldq * 2);
   const dma_rsrc ro = dma_make_rsrc(dOp, static_cast<int64_t>(S) * ldo * 2);
   const dma_rsrc rl = dma_make_rsrc(lse, static_cast<int64_t>(S) * 4);
   const dma_rsrc rd = dma_make_rsrc(del, static_cast<int64_t>(S) * 4);
-  const int lrow = wave * RPI + lane / LPR;                           // row of load 0
+  const int lrow = grp * RPI + lane / LPR;                            // row of load 0
   const int lchk = ((lane % LPR) ^ qd_swz<DH>(lrow)) << 3;            // its logical column
   const uint32_t lq = static_cast<uint32_t>((lrow * ldq + lchk) * 2);
   const uint32_t lo = static_cast<uint32_t>((lrow * ldo + lchk) * 2);
   auto load_block = [&](int st, int qb) {
+    if (!role_b) return;
     char* sb = ring + st * SB;
     const bool in = qb < S;
 #pragma unroll
     for (int i = 0; i < NPW; ++i) {
-      const int p = wave + NW * i;
-      const int64_t r = qb + static_cast<int64_t>(NW) * i * RPI;
+      const int p = grp + NG * i;
+      const int64_t r = qb + static_cast<int64_t>(NG) * i * RPI;
       dma16(rq, sb + p * 1024, in ? lq + static_cast<uint32_t>(r * ldq * 2) : kDmaOob);
       dma16(ro, sb + BQ * DH * 2 + p * 1024, in ? lo + static_cast<uint32_t>(r * ldo * 2) : kDmaOob);
     }
@@ -237,228 +260,257 @@ __global__ __launch_bounds__(64 * NW) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     dma4(rd, sb + 4 * BQ * DH + 4 * BQ, in ? static_cast<uint32_t>((qb + lane) * 4) : kDmaOob);
   };
 
-  // Per-lane LDS byte addresses of the fragments, each set pointing into the
-  // stage of the block it serves: plain reads of Q (row cl, 16-byte chunk
-  // 2ks + hf) for step A, transposing reads (rows tr_r and tr_r + 8) for
-  // step C, and the log-sum-exp of the lane's first query for step B.  The
-  // dO block, the half, the 16-row groups and delta are immediates.
-  uint32_t aq[DH / 16], at0[DH / 32], at1[DH / 32], al, ad;
+  // Per-lane LDS byte addresses, each set pointing into the stage of the
+  // block it serves: plain reads (row cl, 16-byte chunk 2ks + hf) of Q
+  // (wave A) or dO (wave B) for the score products, transposing reads (rows
+  // tr_r and tr_r + 8) of dO (wave A) or Q (wave B) for the dV/dK products,
+  // and the log-sum-exp (wave A) or delta (wave B) of the lane's first query.
+  // The half, the 16-row groups and d blocks are immediates.
+  uint32_t aq[N], at0[NDB], at1[NDB], al;
   {
     const uint32_t r0 = lds_addr(ring);
+    const uint32_t plain = role_b ? 2u * BQ * DH : 0u, trans = role_b ? 0u : 2u * BQ * DH;
     const int sw_c = qd_swz<DH>(cl);
 #pragma unroll
-    for (int ks = 0; ks < DH / 16; ++ks) aq[ks] = r0 + 2u * (cl * DH + (((2 * ks + hf) ^ sw_c) << 3));
+    for (int ks = 0; ks < N; ++ks) aq[ks] = r0 + plain + 2u * (cl * DH + (((2 * ks + hf) ^ sw_c) << 3));
     const int tr_r = 4 * hf + ((lane & 15) >> 2);
     const int tr_d = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
     const int sw0 = qd_swz<DH>(tr_r), sw1 = qd_swz<DH>(tr_r + 8);
 #pragma unroll
-    for (int db = 0; db < DH / 32; ++db) {
+    for (int db = 0; db < NDB; ++db) {
       const int d0 = db * 32 + tr_d;
-      at0[db] = r0 + 2u * (tr_r * DH + (((d0 >> 3) ^ sw0) << 3) + (d0 & 7));
-      at1[db] = r0 + 2u * ((tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7));
+      at0[db] = r0 + trans + 2u * (tr_r * DH + (((d0 >> 3) ^ sw0) << 3) + (d0 & 7));
+      at1[db] = r0 + trans + 2u * ((tr_r + 8) * DH + (((d0 >> 3) ^ sw1) << 3) + (d0 & 7));
     }
-    al = r0 + 4u * BQ * DH + 16u * hf;
-    ad = al;
+    al = r0 + 4u * BQ * DH + (role_b ? 4u * BQ : 0u) + 16u * hf;
   }
-  constexpr uint32_t kOb = 2u * BQ * DH;  // dO block after the Q block (bytes)
-  constexpr uint32_t kDl = 4u * BQ;       // delta after the log-sum-exp (bytes)
+  // the lane's 16-byte slots of the P exchange (floats 4c .. 4c+3 of its 16
+  // at + 1024 c)
+  const uint32_t pslot = lds_addr(ring) + DK_NST * SB + grp * 4096 + 16u * lane;
   // moving a set from the stage of block b to that of block b + 1
   auto adv = [](int b) { return (b & 3) == 3 ? static_cast<uint32_t>(-3 * SB) : static_cast<uint32_t>(SB); };
-
-  // The negated delta of the lane's 16 queries of half qh of the block `ad`
-  // points at, in accumulator order: dP starts from it, so the MFMAs give
-  // dP - delta directly.
-  auto neg_delta = [&](int qh) {
-    floatx16 z;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const floatx4 t = lds_f4(ad + kDl + 4u * (qh * 32 + 8 * g));
-#pragma unroll
-      for (int e = 0; e < 4; ++e) z[4 * g + e] = t[e];
-    }
-    return z;
-  };
-  // A: scores S = Q K^T and dP - delta = dO V^T - delta of half qh of the
-  // block aq (and ad) point at.
-  auto step_a = [&](int qh, floatx16& sc, floatx16& dp) {
-    const uint32_t hq = 2u * qh * 32 * DH;
-    const floatx16 nd = neg_delta(qh);
-    sc = mfma(lds_frag(aq[0] + hq), kf[0], floatx16{});
-    dp = mfma(lds_frag(aq[0] + hq + kOb), vf[0], nd);
-#pragma unroll
-    for (int ks = 1; ks < DH / 16; ++ks) {
-      sc = mfma(lds_frag(aq[ks] + hq), kf[ks], sc);
-      dp = mfma(lds_frag(aq[ks] + hq + kOb), vf[ks], dp);
-    }
-  };
-  // B: P and dS of half qh of query block qb (the block al points at), as
-  // bf16 MFMA operands.  The causal mask is needed only in the blocks that
-  // hold queries before some of the workgroup's keys (MASK).
-  auto step_b = [&](auto mask, const floatx16& sc, const floatx16& dp, int qb, int qh, bf16x8 (&pb)[2],
-                    bf16x8 (&dsb)[2]) {
-    constexpr bool MASK = decltype(mask)::value;
-    floatx4 l4[4];
-#pragma unroll
-    for (int g = 0; g < 4; ++g) l4[g] = lds_f4(al + 4u * (qh * 32 + 8 * g));
-    const int t = key - (qb + qh * 32 + 4 * hf);  // key minus the lane's first query
-    const float ab = al2 * static_cast<float>(t);  // ALiBi bias at that query
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int c = 8 * (v >> 2) + (v & 3);  // the element's query after the first
-      float x = fmaf(sc[v], sl2, -l4[v >> 2][v & 3] * kLog2e);
-      if constexpr (AL) x += fmaf(-al2, static_cast<float>(c), ab);
-      float p = __builtin_amdgcn_exp2f(x);
-      if constexpr (MASK) p = t > c ? 0.f : p;  // causal: keys after the query
-      pb[v >> 3][v & 7] = static_cast<bf16>(p);
-      dsb[v >> 3][v & 7] = static_cast<bf16>(p * dp[v]);
-    }
-  };
-  // C: dV^T += dO^T P, dK^T += Q^T dS for half qh of the block at0/at1 point at.
-  auto step_c = [&](const bf16x8 (&pb)[2], const bf16x8 (&dsb)[2], int qh) {
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-#pragma unroll
-      for (int db = 0; db < DH / 32; ++db) {
-        const uint32_t rr = 2u * (qh * 32 + 16 * c) * DH;
-        const v4s ol = lds_tr(at0[db] + rr + kOb), oh = lds_tr(at1[db] + rr + kOb);
-        const v4s ql_ = lds_tr(at0[db] + rr), qh_ = lds_tr(at1[db] + rr);
-        dv[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ol, oh, 0, 1, 2, 3, 4, 5, 6, 7)), pb[c], dv[db]);
-        dk[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(ql_, qh_, 0, 1, 2, 3, 4, 5, 6, 7)), dsb[c], dk[db]);
-      }
-    }
-  };
-  // One half-step of the pipeline, ordered by hand: C of half qh_c (the
-  // block at0/at1 point at), A of half qh_a (the block aq points at) and B of
-  // the half whose scores are scb/dpb.  Iteration i issues, in this order,
-  // the S MFMA of k step i, the dV MFMA of C pair i, the dP MFMA and the dK
-  // MFMA ((db, c) = (i % (DH/32), i / (DH/32)); both steps have DH/16
-  // iterations), so an accumulator's consecutive MFMAs are at least four
-  // apart and none waits on the one before it.  The softmax elements of B
-  // go between the MFMAs, the fragments of iteration i+2 are read during
-  // iteration i, and scheduling barriers keep the compiler to this order.
-  auto half_step = [&](auto mask, const bf16x8 (&pbc)[2], const bf16x8 (&dsbc)[2], int qh_c, int qh_a,
-                       floatx16& sc, floatx16& dp, const floatx16& scb, const floatx16& dpb, int qb_b, int qh_b,
-                       bf16x8 (&pbo)[2], bf16x8 (&dsbo)[2]) {
-    constexpr bool MASK = decltype(mask)::value;
-    constexpr int N = DH / 16, NDB = DH / 32, EPI = 16 / N;  // softmax elements per iteration
-    const uint32_t hq = 2u * qh_a * 32 * DH;
-    struct Frags {
-      v4s ol, oh, ql, qh;
-      bf16x8 qf, of;
-    };
-    auto load = [&](Frags& f, int i) {
-      const int db = i % NDB, c = i / NDB;
-      const uint32_t rr = 2u * (qh_c * 32 + 16 * c) * DH;
-      f.ol = lds_tr(at0[db] + rr + kOb);
-      f.oh = lds_tr(at1[db] + rr + kOb);
-      f.ql = lds_tr(at0[db] + rr);
-      f.qh = lds_tr(at1[db] + rr);
-      f.qf = lds_frag(aq[i] + hq);
-      f.of = lds_frag(aq[i] + hq + kOb);
-    };
-    Frags fr[3];
-    load(fr[0], 0);
-    load(fr[1], 1);
-    const floatx16 nd = neg_delta(qh_a);
-    floatx4 l4[4];
-#pragma unroll
-    for (int g = 0; g < 4; ++g) l4[g] = lds_f4(al + 4u * (qh_b * 32 + 8 * g));
-    const int t = key - (qb_b + qh_b * 32 + 4 * hf);  // key minus the lane's first query
-    const float ab = al2 * static_cast<float>(t);      // ALiBi bias at that query
-    auto softmax = [&](int v) {
-      const int c = 8 * (v >> 2) + (v & 3);  // the element's query after the first
-      float x = fmaf(scb[v], sl2, -l4[v >> 2][v & 3] * kLog2e);
-      if constexpr (AL) x += fmaf(-al2, static_cast<float>(c), ab);
-      float p = __builtin_amdgcn_exp2f(x);
-      if constexpr (MASK) p = t > c ? 0.f : p;  // causal: keys after the query
-      pbo[v >> 3][v & 7] = static_cast<bf16>(p);
-      dsbo[v >> 3][v & 7] = static_cast<bf16>(p * dpb[v]);
-    };
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      if (i + 2 < N) load(fr[(i + 2) % 3], i + 2);
-      const Frags& f = fr[i % 3];
-      const int db = i % NDB, c = i / NDB;
-      sc = mfma(f.qf, kf[i], i == 0 ? floatx16{} : sc);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int e = 0; e < EPI / 2; ++e) softmax(EPI * i + e);
-      dv[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(f.ol, f.oh, 0, 1, 2, 3, 4, 5, 6, 7)), pbc[c], dv[db]);
-      __builtin_amdgcn_sched_barrier(0);
-      dp = mfma(f.of, vf[i], i == 0 ? nd : dp);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int e = EPI / 2; e < EPI; ++e) softmax(EPI * i + e);
-      dk[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(f.ql, f.qh, 0, 1, 2, 3, 4, 5, 6, 7)), dsbc[c], dk[db]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
   auto move = [](auto& set, uint32_t d) {
 #pragma unroll
     for (auto& x : set) x += d;
   };
 
-  const int q_first = k0;  // the first query that can see key k0
-  const int nqb = (S - q_first) / BQ;
-  floatx16 scx, dpx, scy, dpy;  // scores of two halves in flight
-  bf16x8 pbx[2], dsbx[2], pby[2], dsby[2];
-
-  // Block 0: A(0); then A(1) next to B(0); the ring's barrier; then C(0)
-  // and A(2) (block 1) next to B(1).
-  load_block(0, q_first);
-  load_block(1, q_first + BQ);
-  load_block(2, q_first + 2 * BQ);
-  dma_barrier<2 * NL>();  // block 0 has landed
-  step_a(0, scx, dpx);
-  step_a(1, scy, dpy);
-  const std::integral_constant<bool, true> masked;
-  const std::integral_constant<bool, false> unmasked;
-  step_b(masked, scx, dpx, q_first, 0, pbx, dsbx);
-  dma_barrier<NL>();  // block 1 has landed; block 3 goes to the fourth stage
-  load_block(3, q_first + 3 * BQ);
-  move(aq, adv(0));
-  ad += adv(0);
-  half_step(masked, pbx, dsbx, 0, 0, scx, dpx, scy, dpy, q_first, 1, pby, dsby);
-  al += adv(0);
-  // Block j: C(2j-1) (block j-1) and A(2j+1) next to B(2j); barrier (block
-  // j+1 has landed, block j+3 goes to the stage block j-1 left); C(2j) and
-  // A(2j+2) (block j+1) next to B(2j+1).
-  auto block = [&](auto mask, int j) {
-    const int qb = q_first + j * BQ;
-    half_step(mask, pby, dsby, 1, 1, scy, dpy, scx, dpx, qb, 0, pbx, dsbx);
-    dma_barrier<NL>();
-    load_block((j + 3) & 3, qb + 3 * BQ);
-    move(aq, adv(j));
-    ad += adv(j);
-    move(at0, adv(j - 1));
-    move(at1, adv(j - 1));
-    half_step(mask, pbx, dsbx, 0, 0, scx, dpx, scy, dpy, qb, 1, pby, dsby);
-    al += adv(j);
-  };
-  // Only the blocks that start before the workgroup's last key hold queries
-  // that some of its keys come after.
-  constexpr int kMaskBlocks = BKEYS / BQ;
-  int j = 1;
-  for (; j < nqb && j < kMaskBlocks; ++j) block(masked, j);
-  for (; j < nqb; ++j) block(unmasked, j);
-  step_c(pby, dsby, 1);  // C of the last half
-  dma_barrier<0>();  // no load may still write LDS when the workgroup ends
-  if (active && key < S) {
-    bf16* G = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + key) * ldq + head * DH;
-    bf16* Gk = G + static_cast<int64_t>(H) * DH;
-    bf16* Gv = G + 2ll * H * DH;
+  // Wave A, one half: S of half hs of the block aq points at, then the dV
+  // product of half hv of the block at0/at1 point at (P of that half in pin)
+  // with P of half hs (query block qb, for the mask and ALiBi) formed
+  // between its MFMAs into pout; the middle barrier; P into the exchange.
+  auto half_a = [&](auto mask, auto do_s, auto do_v, int hs, int hv, int qb, const bf16x8 (&pin)[2],
+                    bf16x8 (&pout)[2]) {
+    constexpr bool MASK = decltype(mask)::value, DS = decltype(do_s)::value, DV = decltype(do_v)::value;
+    const uint32_t hq = 2u * hs * 32 * DH;
+    floatx16 sc;
+    struct Fr {
+      bf16x8 q;
+    };
+    auto load = [&](Fr& f, int i) {
+      if constexpr (DS) f.q = lds_frag(aq[i] + hq);
+    };
+    Fr fr[3];
+    load(fr[0], 0);
+    load(fr[1], 1);
+    floatx4 l4[4];
+    if constexpr (DS) {
 #pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
+      for (int g = 0; g < 4; ++g) l4[g] = lds_f4(al + 4u * (hs * 32 + 8 * g));
+    }
+    // S first (its fragments two steps ahead), the dV fragments meanwhile
+    bf16x8 trf[N];
+    auto load_tr = [&](int i) {
+      if constexpr (DV) {
+        const int db = i % NDB, c = i / NDB;
+        const uint32_t rr = 2u * (hv * 32 + 16 * c) * DH;
+        trf[i] = tr_pair(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr));
+      }
+    };
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if (i + 2 < N) load(fr[(i + 2) % 3], i + 2);
+      load_tr(i);
+      if constexpr (DS) sc = mfma(fr[i % 3].q, kv[i], i == 0 ? floatx16{} : sc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const int t = key - (qb + hs * 32 + 4 * hf);  // key minus the lane's first query
+    const float ab = al2 * static_cast<float>(t);  // ALiBi bias at that query
+    floatx4 pf[4];  // P in float32 for B's dS
+    auto softmax = [&](int v) {
+      const int c = 8 * (v >> 2) + (v & 3);  // the element's query after the first
+      float x = fmaf(sc[v], sl2, -l4[v >> 2][v & 3] * kLog2e);
+      if constexpr (AL) x += fmaf(-al2, static_cast<float>(c), ab);
+      float p = __builtin_amdgcn_exp2f(x);
+      if constexpr (MASK) p = t > c ? 0.f : p;  // causal: keys after the query
+      pout[v >> 3][v & 7] = static_cast<bf16>(p);
+      pf[v >> 2][v & 3] = p;
+    };
+    // then the dV products with the softmax of S between them
+    constexpr int EPI = 16 / N;  // softmax elements per dV MFMA
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if constexpr (DV) acc[i % NDB] = mfma(trf[i], pin[i / NDB], acc[i % NDB]);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (DS) {
+#pragma unroll
+        for (int e = 0; e < EPI; ++e) softmax(EPI * i + e);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    lds_barrier();  // B has read the previous P
+    if constexpr (DS) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) lds_put(pslot + 1024u * g, pf[g]);
+    }
+  };
+  // Wave B, one half: dP - delta of half hs of the block aq/al point at
+  // into dpout, with dS of the previous half (P from the exchange, dP - delta
+  // in dpin) formed between its MFMAs; the dK product of half hk of the
+  // block at0/at1 point at; the middle barrier.
+  auto half_b = [&](auto do_k, auto do_p, int hs, int hk, const floatx16& dpin, floatx16& dpout) {
+    constexpr bool DK = decltype(do_k)::value, DP = decltype(do_p)::value;
+    const uint32_t hq = 2u * hs * 32 * DH;
+    floatx4 pf[4];
+    bf16x8 dsb[2];
+    if constexpr (DK) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) pf[g] = lds_f4(pslot + 1024u * g);
+    }
+    floatx16 nd;
+    if constexpr (DP) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        __attribute__((aligned(8))) bf16 tk[4], tv[4];
+        const floatx4 t = lds_f4(al + 4u * (hs * 32 + 8 * g));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          tk[i] = static_cast<bf16>(dk[db][4 * g + i] * a.scale);
-          tv[i] = static_cast<bf16>(dv[db][4 * g + i]);
-        }
-        *reinterpret_cast<uint2*>(Gk + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(tk);
-        *reinterpret_cast<uint2*>(Gv + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(tv);
+        for (int e = 0; e < 4; ++e) nd[4 * g + e] = t[e];
+      }
+    }
+    bf16x8 of[3], trf[N];
+    auto load = [&](int i) {
+      if constexpr (DP) of[i % 3] = lds_frag(aq[i] + hq);
+    };
+    auto load_tr = [&](int i) {
+      if constexpr (DK) {
+        const int db = i % NDB, c = i / NDB;
+        const uint32_t rr = 2u * (hk * 32 + 16 * c) * DH;
+        trf[i] = tr_pair(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr));
+      }
+    };
+    auto ds = [&](int v) { dsb[v >> 3][v & 7] = static_cast<bf16>(pf[v >> 2][v & 3] * dpin[v]); };
+    load(0);
+    load(1);
+    // dP (its fragments two steps ahead, the dK fragments meanwhile) with
+    // dS of the previous half between its MFMAs; then the dK products
+    constexpr int EPI = 16 / N;  // dS elements per dP MFMA
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if (i + 2 < N) load(i + 2);
+      load_tr(i);
+      if constexpr (DP) dpout = mfma(of[i % 3], kv[i], i == 0 ? nd : dpout);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (DK) {
+#pragma unroll
+        for (int e = 0; e < EPI; ++e) ds(EPI * i + e);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (DK) {
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        acc[i % NDB] = mfma(trf[i], dsb[i / NDB], acc[i % NDB]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    lds_barrier();  // P read: A may write the next
+  };
+
+  const std::integral_constant<bool, true> yes;
+  const std::integral_constant<bool, false> no;
+  const int q_first = k0;  // the first query that can see key k0
+  const int nqb = (S - q_first) / BQ;
+  // The whole walk for one role, so that the other role's state is not live
+  // in it.
+  auto walk = [&](auto is_b) {
+    constexpr bool RB = decltype(is_b)::value;
+    bf16x8 pbx[2], pby[2];  // wave A: P of the two halves of a block
+    floatx16 dpx, dpy;      // wave B: dP - delta of the two halves of a block
+    // one half: S/P or dP of half hs, the dV or dK product of half hv
+    auto half = [&](auto mask, auto first, auto second, int hs, int hv, int qb, bool odd) {
+      if constexpr (!RB) {
+        if (odd)
+          half_a(mask, first, second, hs, hv, qb, pbx, pby);
+        else
+          half_a(mask, first, second, hs, hv, qb, pby, pbx);
+      } else {
+        // B: first = the dK product (of the previous half), second = dP
+        if (odd)
+          half_b(first, second, hs, hv, dpx, dpy);
+        else
+          half_b(first, second, hs, hv, dpy, dpx);
+      }
+    };
+    // Block 0 into the ring and the K/V fragments (1, 2 in flight), then
+    // its first half.
+    load_block(0, q_first);
+    load_kv();
+    load_block(1, q_first + BQ);
+    load_block(2, q_first + 2 * BQ);
+    dma_barrier<2 * NL>();  // block 0 has landed
+    if constexpr (!RB)
+      half(yes, yes, no, 0, 0, q_first, false);
+    else
+      half(yes, no, yes, 0, 0, q_first, false);
+    lds_barrier();
+    load_block(3, q_first + 3 * BQ);
+    // its second half, with the products of the first
+    half(yes, yes, yes, 1, 0, q_first, true);
+    dma_barrier<2 * NL>();  // block 1 has landed
+    move(aq, adv(0));
+    al += adv(0);
+    // Block j: first half (with the products of block j-1's second half);
+    // barrier; block j+3 goes to the stage block j-1 left; second half (with
+    // the products of the first); barrier (block j+1 has landed).
+    auto block = [&](auto mask, int j) {
+      const int qb = q_first + j * BQ;
+      half(mask, yes, yes, 0, 1, qb, false);
+      lds_barrier();
+      load_block((j + 3) & 3, qb + 3 * BQ);
+      move(at0, adv(j - 1));
+      move(at1, adv(j - 1));
+      half(mask, yes, yes, 1, 0, qb, true);
+      dma_barrier<2 * NL>();
+      move(aq, adv(j));
+      al += adv(j);
+    };
+    // Only the blocks that start before the workgroup's last key hold
+    // queries that some of its keys come after.
+    constexpr int kMaskBlocks = BKEYS / BQ;
+    int j = 1;
+    for (; j < nqb && j < kMaskBlocks; ++j) block(yes, j);
+    for (; j < nqb; ++j) block(no, j);
+    // the products of the last half
+    if constexpr (!RB)
+      half(no, no, yes, 0, 1, 0, false);
+    else
+      half(no, yes, no, 0, 1, 0, false);
+  };
+  if (role_b)
+    walk(yes);
+  else
+    walk(no);
+  dma_barrier<0>();  // no load may still write LDS when the workgroup ends
+  if (active && key < S) {
+    bf16* G = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + key) * ldq + head * DH +
+              (role_b ? 1ll : 2ll) * H * DH;
+    const float f = role_b ? a.scale : 1.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        __attribute__((aligned(8))) bf16 t[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) t[i] = static_cast<bf16>(acc[db][4 * g + i] * f);
+        *reinterpret_cast<uint2*>(G + db * 32 + 8 * g + 4 * hf) = *reinterpret_cast<uint2*>(t);
       }
   }
 }
@@ -689,8 +741,9 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
 
 template <int DH>
 constexpr size_t dkdv_lds_bytes() {
-  return static_cast<size_t>(DK_NST) * dk_stage_bytes<DH>();
+  return static_cast<size_t>(DK_NST) * dk_stage_bytes<DH>() + kDkPBytes;
 }
+static_assert(dkdv_lds_bytes<128>() <= 160 * 1024, "the dK/dV ring and P area fit the LDS");
 
 constexpr int DQ_ROWS = 256;  // query rows per dQ workgroup (8 waves x 32)
 
@@ -1079,12 +1132,12 @@ hipError_t bwd_dh(int dtype, int part, const AttnArgs& a, hipStream_t s) {
   if constexpr (DH >= 64) {
     if (dtype == LD_BF16) {
       if (part == 1) {
-        constexpr int nw = dkdv_waves<DH>();
-        const dim3 grid(a.H, a.n_seq, (a.S + 32 * nw - 1) / (32 * nw));
+        constexpr int ng = DK_GROUPS;
+        const dim3 grid(a.H, a.n_seq, (a.S + 32 * ng - 1) / (32 * ng));
         if (a.alibi)
-          hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw, true>), grid, dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
+          hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, ng, true>), grid, dim3(128 * ng), dkdv_lds_bytes<DH>(), s, a);
         else
-          hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, nw, false>), grid, dim3(64 * nw), dkdv_lds_bytes<DH>(), s, a);
+          hipLaunchKernelGGL((ld_attn_bwd_dkdv_bf16<DH, ng, false>), grid, dim3(128 * ng), dkdv_lds_bytes<DH>(), s, a);
       } else if (part == 0) {
         const dim3 grid(a.H, a.n_seq, (a.S + DQ_ROWS - 1) / DQ_ROWS);
         if (a.alibi)
