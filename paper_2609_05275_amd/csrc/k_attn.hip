@@ -628,30 +628,49 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
     load_block((kb + 3) & (FWD_NST - 1), k0 + 3 * FKV);
     if (qw < S && k0 <= qw + RPW - 1) {
       const bool diag = k0 + FKV - 1 > qw;  // some key of the block is past some row
-      // scores of every 32-row block: each K fragment feeds NSB MFMA chains
+      // scores of every 32-row block: each K fragment feeds NSB MFMA chains;
+      // fragments read two steps ahead (step i: ks = i / 2, kh = i % 2)
+      constexpr int NS = 2 * (DH / 16), NP = 4 * (DH / 32);
       floatx16 sc[NSB][2];
+      bf16x8 kfr[3];
+      auto ldk = [&](int i) { kfr[i % 3] = lds_frag(ak[i / 2] + 2u * (i % 2) * 32 * DH); };
+      ldk(0);
+      ldk(1);
 #pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks)
+      for (int i = 0; i < NS; ++i) {
+        if (i + 2 < NS) ldk(i + 2);
+        const int ks = i / 2, kh = i % 2;
 #pragma unroll
-        for (int kh = 0; kh < 2; ++kh) {
-          const bf16x8 kf = lds_frag(ak[ks] + 2u * kh * 32 * DH);
-#pragma unroll
-          for (int sb = 0; sb < NSB; ++sb) sc[sb][kh] = mfma(kf, qf[sb][ks], ks == 0 ? floatx16{} : sc[sb][kh]);
-        }
+        for (int sb = 0; sb < NSB; ++sb) sc[sb][kh] = mfma(kfr[i % 3], qf[sb][ks], ks == 0 ? floatx16{} : sc[sb][kh]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // the first V^T fragments land during the softmax (step i: kh = i /
+      // (2 NDB), c = i / NDB % 2, db = i % NDB)
+      bf16x8 vfr[3];
+      auto ldv = [&](int i) {
+        const int kh = i / (2 * (DH / 32)), c = (i / (DH / 32)) % 2, db = i % (DH / 32);
+        const uint32_t rr = 2u * (kh * 32 + 16 * c) * DH;
+        vfr[i % 3] = __builtin_bit_cast(
+            bf16x8, __builtin_shufflevector(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr), 0, 1, 2, 3, 4, 5, 6, 7));
+      };
+      ldv(0);
+      ldv(1);
       bf16x8 pb[NSB][2][2];
 #pragma unroll
       for (int sb = 0; sb < NSB; ++sb) {
         const int qrow = qw + sb * 32 + cl;
         const float ab = al2 * static_cast<float>(k0 + 4 * hf - qrow);  // bias of the lane's first key
         float mx = -INFINITY;
+        // With ALiBi the scores are scaled and biased here; without, they
+        // stay raw until the exponent (scale > 0, so the maximum of the raw
+        // scores times the scale is the maximum of the scaled ones).
+        if constexpr (AL) {
 #pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
+          for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float x = sc[sb][kh][v] * sl2;
-            if constexpr (AL) x += fmaf(al2, static_cast<float>(kh * 32 + 8 * (v >> 2) + (v & 3)), ab);
-            sc[sb][kh][v] = x;
-          }
+            for (int v = 0; v < 16; ++v)
+              sc[sb][kh][v] = fmaf(sc[sb][kh][v], sl2, fmaf(al2, static_cast<float>(kh * 32 + 8 * (v >> 2) + (v & 3)), ab));
+        }
         if (diag) {  // causal mask, only on blocks that reach past a row (wave-uniform)
           const int t = qrow - k0 - 4 * hf;  // the row minus the lane's first key
 #pragma unroll
@@ -665,6 +684,7 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
 #pragma unroll
           for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[sb][kh][v]);
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        if constexpr (!AL) mx *= sl2;
         // Lazy rescaling: the running maximum only moves (and O, l are only
         // rescaled) when a row's maximum grows by more than 8 in log2 units;
         // otherwise p = 2^(s - m) stays below 2^8, exact enough in bf16 and
@@ -685,7 +705,7 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const float p = __builtin_amdgcn_exp2f(sc[sb][kh][v] - m[sb]);
+            const float p = __builtin_amdgcn_exp2f(AL ? sc[sb][kh][v] - m[sb] : fmaf(sc[sb][kh][v], sl2, -m[sb]));
             ls += p;
             pb[sb][kh][v >> 3][v & 7] = static_cast<bf16>(p);
           }
@@ -694,18 +714,13 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
       // O^T += V^T P^T; consecutive MFMAs go to different accumulators (the
       // d blocks innermost), so none waits on the one before it
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
+      for (int i = 0; i < NP; ++i) {
+        if (i + 2 < NP) ldv(i + 2);
+        const int kh = i / (2 * (DH / 32)), c = (i / (DH / 32)) % 2, db = i % (DH / 32);
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const uint32_t rr = 2u * (kh * 32 + 16 * c) * DH;
-#pragma unroll
-          for (int db = 0; db < DH / 32; ++db) {
-            const v4s lo = lds_tr(at0[db] + rr), hi = lds_tr(at1[db] + rr);
-            const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-            for (int sb = 0; sb < NSB; ++sb) o[sb][db] = mfma(vf, pb[sb][kh][c], o[sb][db]);
-          }
-        }
+        for (int sb = 0; sb < NSB; ++sb) o[sb][db] = mfma(vfr[i % 3], pb[sb][kh][c], o[sb][db]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     // next block: one stage on (wrapping around the ring)
     const uint32_t adv = st == FWD_NST - 1 ? static_cast<uint32_t>(-(FWD_NST - 1) * SB) : static_cast<uint32_t>(SB);
@@ -820,6 +835,11 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) dq[db][v] = 0.f;
+  // dP accumulations start from the row's negated delta: the MFMAs give dP -
+  // delta
+  floatx16 dls;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) dls[v] = dl;
 
   // Loads of key block k0 into stage st; blocks at or past the end read zeros.
   const dma_rsrc rk = dma_make_rsrc(Kp, static_cast<int64_t>(S) * ldq * 2);
@@ -874,14 +894,34 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
       const bool diag = k0 + FKV - 1 > qw;  // some key of the block is past some row
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
+        constexpr int N = DH / 16, NC = 2 * (DH / 32);
         const uint32_t hk = 2u * kh * 32 * DH;
-        floatx16 st_ = mfma(lds_frag(ak[0] + hk), qf[0], floatx16{});
-        floatx16 dpt = mfma(lds_frag(ak[0] + hk + kVb), of[0], floatx16{});
+        // S^T and dP^T - delta, the K and V fragments read two steps ahead
+        bf16x8 kfr[3], vfr[3];
+        auto ld = [&](int ks) {
+          kfr[ks % 3] = lds_frag(ak[ks] + hk);
+          vfr[ks % 3] = lds_frag(ak[ks] + hk + kVb);
+        };
+        ld(0);
+        ld(1);
+        floatx16 st_, dpt;
 #pragma unroll
-        for (int ks = 1; ks < DH / 16; ++ks) {
-          st_ = mfma(lds_frag(ak[ks] + hk), qf[ks], st_);
-          dpt = mfma(lds_frag(ak[ks] + hk + kVb), of[ks], dpt);
+        for (int ks = 0; ks < N; ++ks) {
+          if (ks + 2 < N) ld(ks + 2);
+          st_ = mfma(kfr[ks % 3], qf[ks], ks == 0 ? floatx16{} : st_);
+          dpt = mfma(vfr[ks % 3], of[ks], ks == 0 ? dls : dpt);
+          __builtin_amdgcn_sched_barrier(0);
         }
+        // the first K^T fragments of the dQ product land during the softmax
+        bf16x8 tf[3];
+        auto ldt = [&](int i) {
+          const int db = i % (DH / 32), c = i / (DH / 32);
+          const uint32_t rr = hk + 2u * 16 * c * DH;
+          tf[i % 3] = __builtin_bit_cast(
+              bf16x8, __builtin_shufflevector(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr), 0, 1, 2, 3, 4, 5, 6, 7));
+        };
+        ldt(0);
+        ldt(1);
         bf16x8 dsb[2];
         const float ab = al2 * static_cast<float>(k0 + kh * 32 + 4 * hf - qrow);  // bias of the lane's first key
         float pv[16];
@@ -898,17 +938,14 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
             if (8 * (v >> 2) + (v & 3) > t) pv[v] = 0.f;
         }
 #pragma unroll
-        for (int v = 0; v < 16; ++v) dsb[v >> 3][v & 7] = static_cast<bf16>(pv[v] * (dpt[v] + dl));
+        for (int v = 0; v < 16; ++v) dsb[v >> 3][v & 7] = static_cast<bf16>(pv[v] * dpt[v]);
         // dQ^T += K^T dS^T, the d blocks innermost (consecutive MFMAs use
-        // different accumulators)
+        // different accumulators), fragments two steps ahead
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const uint32_t rr = hk + 2u * 16 * c * DH;
-#pragma unroll
-          for (int db = 0; db < DH / 32; ++db) {
-            const v4s lo = lds_tr(at0[db] + rr), hi = lds_tr(at1[db] + rr);
-            dq[db] = mfma(__builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7)), dsb[c], dq[db]);
-          }
+        for (int i = 0; i < NC; ++i) {
+          if (i + 2 < NC) ldt(i + 2);
+          dq[i % (DH / 32)] = mfma(tf[i % 3], dsb[i / (DH / 32)], dq[i % (DH / 32)]);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
