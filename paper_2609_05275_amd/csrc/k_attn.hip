@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void ld_attn_delta(AttnArgs a) {
 }
 
 constexpr int BQ = 64;       // query rows per step of the dK/dV kernel
-constexpr int DK_NST = 4;    // dK/dV ring stages (query blocks in LDS)
+constexpr int DK_NST = 3;    // dK/dV ring stages (query blocks in LDS)
 
 // Key groups of 32 per dK/dV workgroup: four, each served by a pair of waves.
 constexpr int DK_GROUPS = 4;
@@ -126,9 +126,10 @@ constexpr int dk_stage_bytes() { return 4 * BQ * DH + 8 * BQ; }
 // same bytes).
 template <int DH, int NW>
 constexpr int dk_loads() { return 2 * (BQ * DH * 2 / 1024) / NW + 2; }
-// P exchange area after the ring: the key groups x 4 KB (64 lanes x 16
-// floats).
-constexpr int kDkPBytes = DK_GROUPS * 4096;
+// P exchange area after the ring: two slots (by half parity) x the key
+// groups x 4 KB (64 lanes x 16 floats).
+constexpr int kDkPSlot = DK_GROUPS * 4096;
+constexpr int kDkPBytes = 2 * kDkPSlot;
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 
@@ -166,30 +167,31 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 // forms dP - delta = dO V^T - delta, dS = P (dP - delta) and dK^T += Q^T dS.
 // P (float32) goes from A to B through LDS, one half behind: in half u, A
 // computes S(u) and P(u) and the dV product of half u-1, B computes dS(u-1),
-// its dK product and dP(u).  Two workgroup barriers per half guard the one
-// P slot per key group: B reads P(u-1) before the first, A writes P(u) after
-// it, and the second ends the half.  A's vector work (the
-// exponentials) follows its MFMAs while B's (dS) precedes them, so the two
-// waves of a SIMD keep its matrix pipe busy in turn; with at most 256
-// registers each, two waves fit on a SIMD.  dV^T and dK^T take P and dS
+// its dK product and dP(u).  A workgroup barrier ends every half; P has two
+// slots per key group, by half parity, so A writes P(u) while B reads
+// P(u-1).  Each wave spreads its vector work over its own MFMAs (A: the
+// exponentials between its dV products, B: dS between its dP products),
+// and with at most 256 registers each the two waves of a group share a
+// SIMD, one's MFMAs filling the other's waits.  dV^T and dK^T take P and dS
 // straight from the score layout (their rows are a fixed permutation of the
 // MFMA k index), dO^T and Q^T come from the same [q][d] blocks through
 // transposing reads (ds_read_b64_tr_b16) in that permutation.
 //
 // Q, dO, log-sum-exp and delta of each block go from global memory straight
-// into a four-stage LDS ring (buffer loads with an LDS destination, issued by
-// the B waves, see ld_internal.h), so a block's loads have two block-times to
-// land.  Fragment addresses are per-lane offsets moved by one stage per
-// block; the loop has no branch around its MFMAs (query rows before a wave's
-// keys are computed and masked to P = 0, blocks past the end read zeros, and
-// waves past the end compute on zero K/V and store nothing).
+// into a three-stage LDS ring (buffer loads with an LDS destination, issued
+// by the B waves, see ld_internal.h): block j+2 is requested once block j-1
+// is done, half a block into block j.  Fragment addresses are per-lane
+// offsets moved by one stage per block; the loop has no branch around its
+// MFMAs (query rows before a wave's keys are computed and masked to P = 0,
+// blocks past the end read zeros, and waves past the end compute on zero
+// K/V and store nothing).
 template <int DH, int NG, bool AL>
 __global__ __launch_bounds__(128 * NG) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   constexpr int BKEYS = 32 * NG, SB = dk_stage_bytes<DH>(), NL = dk_loads<DH, NG>();
   constexpr int RPI = 512 / DH, LPR = 64 / RPI;   // rows per 1 KB load, lanes per row
   constexpr int NPW = (BQ * DH * 2 / 1024) / NG;  // 1 KB loads per loading wave per tensor
   constexpr int N = DH / 16, NDB = DH / 32;       // k steps of the score products, d blocks
-  static_assert(DK_NST == 4, "stage arithmetic assumes a ring of four");
+  static_assert(DK_NST == 3, "stage arithmetic assumes a ring of three");
   static_assert(NG == DK_GROUPS, "the P area is sized for DK_GROUPS key groups");
   extern __shared__ __align__(16) char ring[];
   const int S = a.S, H = a.H;
@@ -285,10 +287,10 @@ __global__ __launch_bounds__(128 * NG) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     al = r0 + 4u * BQ * DH + (role_b ? 4u * BQ : 0u) + 16u * hf;
   }
   // the lane's 16-byte slots of the P exchange (floats 4c .. 4c+3 of its 16
-  // at + 1024 c)
+  // at + 1024 c; parity 1 at + kDkPSlot)
   const uint32_t pslot = lds_addr(ring) + DK_NST * SB + grp * 4096 + 16u * lane;
   // moving a set from the stage of block b to that of block b + 1
-  auto adv = [](int b) { return (b & 3) == 3 ? static_cast<uint32_t>(-3 * SB) : static_cast<uint32_t>(SB); };
+  auto adv = [](int b) { return b % DK_NST == DK_NST - 1 ? static_cast<uint32_t>(-(DK_NST - 1) * SB) : static_cast<uint32_t>(SB); };
   auto move = [](auto& set, uint32_t d) {
 #pragma unroll
     for (auto& x : set) x += d;
@@ -297,8 +299,8 @@ __global__ __launch_bounds__(128 * NG) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
   // Wave A, one half: S of half hs of the block aq points at, then the dV
   // product of half hv of the block at0/at1 point at (P of that half in pin)
   // with P of half hs (query block qb, for the mask and ALiBi) formed
-  // between its MFMAs into pout; the middle barrier; P into the exchange.
-  auto half_a = [&](auto mask, auto do_s, auto do_v, int hs, int hv, int qb, const bf16x8 (&pin)[2],
+  // between its MFMAs into pout and the exchange slot of parity par.
+  auto half_a = [&](auto mask, auto do_s, auto do_v, int hs, int hv, int qb, int par, const bf16x8 (&pin)[2],
                     bf16x8 (&pout)[2]) {
     constexpr bool MASK = decltype(mask)::value, DS = decltype(do_s)::value, DV = decltype(do_v)::value;
     const uint32_t hq = 2u * hs * 32 * DH;
@@ -357,24 +359,23 @@ __global__ __launch_bounds__(128 * NG) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    lds_barrier();  // B has read the previous P
     if constexpr (DS) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) lds_put(pslot + 1024u * g, pf[g]);
+      for (int g = 0; g < 4; ++g) lds_put(pslot + par * kDkPSlot + 1024u * g, pf[g]);
     }
   };
   // Wave B, one half: dP - delta of half hs of the block aq/al point at
-  // into dpout, with dS of the previous half (P from the exchange, dP - delta
-  // in dpin) formed between its MFMAs; the dK product of half hk of the
-  // block at0/at1 point at; the middle barrier.
-  auto half_b = [&](auto do_k, auto do_p, int hs, int hk, const floatx16& dpin, floatx16& dpout) {
+  // into dpout, with dS of the previous half (P from the exchange slot of
+  // parity par, dP - delta in dpin) formed between its MFMAs; then the dK
+  // product of half hk of the block at0/at1 point at.
+  auto half_b = [&](auto do_k, auto do_p, int hs, int hk, int par, const floatx16& dpin, floatx16& dpout) {
     constexpr bool DK = decltype(do_k)::value, DP = decltype(do_p)::value;
     const uint32_t hq = 2u * hs * 32 * DH;
     floatx4 pf[4];
     bf16x8 dsb[2];
     if constexpr (DK) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) pf[g] = lds_f4(pslot + 1024u * g);
+      for (int g = 0; g < 4; ++g) pf[g] = lds_f4(pslot + par * kDkPSlot + 1024u * g);
     }
     floatx16 nd;
     if constexpr (DP) {
@@ -421,7 +422,6 @@ __global__ __launch_bounds__(128 * NG) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    lds_barrier();  // P read: A may write the next
   };
 
   const std::integral_constant<bool, true> yes;
@@ -435,50 +435,51 @@ __global__ __launch_bounds__(128 * NG) void ld_attn_bwd_dkdv_bf16(AttnArgs a) {
     bf16x8 pbx[2], pby[2];  // wave A: P of the two halves of a block
     floatx16 dpx, dpy;      // wave B: dP - delta of the two halves of a block
     // one half: S/P or dP of half hs, the dV or dK product of half hv
+    // (odd: the second half of a block; A writes the P slot of its parity,
+    // B reads the other)
     auto half = [&](auto mask, auto first, auto second, int hs, int hv, int qb, bool odd) {
       if constexpr (!RB) {
         if (odd)
-          half_a(mask, first, second, hs, hv, qb, pbx, pby);
+          half_a(mask, first, second, hs, hv, qb, 1, pbx, pby);
         else
-          half_a(mask, first, second, hs, hv, qb, pby, pbx);
+          half_a(mask, first, second, hs, hv, qb, 0, pby, pbx);
       } else {
         // B: first = the dK product (of the previous half), second = dP
         if (odd)
-          half_b(first, second, hs, hv, dpx, dpy);
+          half_b(first, second, hs, hv, 0, dpx, dpy);
         else
-          half_b(first, second, hs, hv, dpy, dpx);
+          half_b(first, second, hs, hv, 1, dpy, dpx);
       }
     };
-    // Block 0 into the ring and the K/V fragments (1, 2 in flight), then
-    // its first half.
+    // Block 0 into the ring and the K/V fragments (1 in flight), then its
+    // first half.
     load_block(0, q_first);
     load_kv();
     load_block(1, q_first + BQ);
-    load_block(2, q_first + 2 * BQ);
-    dma_barrier<2 * NL>();  // block 0 has landed
+    dma_barrier<NL>();  // block 0 has landed
     if constexpr (!RB)
       half(yes, yes, no, 0, 0, q_first, false);
     else
       half(yes, no, yes, 0, 0, q_first, false);
     lds_barrier();
-    load_block(3, q_first + 3 * BQ);
+    load_block(2, q_first + 2 * BQ);
     // its second half, with the products of the first
     half(yes, yes, yes, 1, 0, q_first, true);
-    dma_barrier<2 * NL>();  // block 1 has landed
+    dma_barrier<NL>();  // block 1 has landed
     move(aq, adv(0));
     al += adv(0);
     // Block j: first half (with the products of block j-1's second half);
-    // barrier; block j+3 goes to the stage block j-1 left; second half (with
+    // barrier; block j+2 goes to the stage block j-1 left; second half (with
     // the products of the first); barrier (block j+1 has landed).
     auto block = [&](auto mask, int j) {
       const int qb = q_first + j * BQ;
       half(mask, yes, yes, 0, 1, qb, false);
       lds_barrier();
-      load_block((j + 3) & 3, qb + 3 * BQ);
+      load_block((j + 2) % DK_NST, qb + 2 * BQ);
       move(at0, adv(j - 1));
       move(at1, adv(j - 1));
       half(mask, yes, yes, 1, 0, qb, true);
-      dma_barrier<2 * NL>();
+      dma_barrier<NL>();
       move(aq, adv(j));
       al += adv(j);
     };
@@ -650,8 +651,7 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
       auto ldv = [&](int i) {
         const int kh = i / (2 * (DH / 32)), c = (i / (DH / 32)) % 2, db = i % (DH / 32);
         const uint32_t rr = 2u * (kh * 32 + 16 * c) * DH;
-        vfr[i % 3] = __builtin_bit_cast(
-            bf16x8, __builtin_shufflevector(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr), 0, 1, 2, 3, 4, 5, 6, 7));
+        vfr[i % 3] = tr_pair(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr));
       };
       ldv(0);
       ldv(1);
@@ -917,8 +917,7 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
         auto ldt = [&](int i) {
           const int db = i % (DH / 32), c = i / (DH / 32);
           const uint32_t rr = hk + 2u * 16 * c * DH;
-          tf[i % 3] = __builtin_bit_cast(
-              bf16x8, __builtin_shufflevector(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr), 0, 1, 2, 3, 4, 5, 6, 7));
+          tf[i % 3] = tr_pair(lds_tr(at0[db] + rr), lds_tr(at1[db] + rr));
         };
         ldt(0);
         ldt(1);
