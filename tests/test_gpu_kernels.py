@@ -241,7 +241,7 @@ def _attn_ref(qkv, n, S, H, dh, alibi=0):
 
 
 @pytest.mark.parametrize("alibi", [0, 1])
-@pytest.mark.parametrize("dt,n,S,H,dh", [("bf16", 2, 192, 2, 64), ("bf16", 2, 256, 2, 128),
+@pytest.mark.parametrize("dt,n,S,H,dh", [("bf16", 2, 64, 2, 128), ("bf16", 2, 192, 2, 64), ("bf16", 2, 256, 2, 128),
                                          ("bf16", 1, 1024, 1, 128), ("bf16", 1, 512, 6, 128),
                                          ("f32", 3, 32, 4, 16), ("f32", 2, 100, 2, 64)])
 def test_attention_fwd_bwd(dt, n, S, H, dh, alibi):
@@ -279,3 +279,28 @@ def test_attention_fwd_bwd(dt, n, S, H, dh, alibi):
             m = s.max(axis=1)
             want = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
             assert np.max(np.abs(lsef[b, h] - want)) < (2e-2 if dt == "bf16" else 1e-4)
+
+
+@pytest.mark.parametrize("dh", [64, 128])
+def test_attention_bwd_bf16_repeatable(dh):
+    """The bf16 backward passes P between waves through LDS under barriers;
+    repeated runs on the same inputs must give the same bits (a missing
+    wait would show up as run-to-run differences)."""
+    n, S, H = 3, 1024, 2
+    d = H * dh
+    g = torch.Generator().manual_seed(11)
+    qd = torch.randn(n * S, 3 * d, generator=g).to(torch.bfloat16).to(DEV)
+    god = torch.randn(n * S, d, generator=g).to(torch.bfloat16).to(DEV)
+    o = torch.empty(n * S, d, dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty(n, H, S, dtype=torch.float32, device=DEV)
+    ld.ld_attn_fwd(n, S, H, dh, qd, o, lse)
+    ws = torch.empty(ld.ld_attn_bwd_ws_bytes(n, S, H), dtype=torch.uint8, device=DEV)
+    outs = []
+    for _ in range(4):
+        gq = torch.full((n * S, 3 * d), float("nan"), dtype=torch.bfloat16, device=DEV)
+        ld.ld_attn_bwd(n, S, H, dh, qd, o, lse, god, gq, ws)
+        torch.cuda.synchronize()
+        outs.append(gq.view(torch.int16).cpu())
+    assert not torch.isnan(gq.float()).any()
+    for x in outs[1:]:
+        assert torch.equal(x, outs[0])
