@@ -46,6 +46,19 @@ __device__ __forceinline__ floatx16 mfma(const bf16x8& a, const bf16x8& b, const
 
 __device__ __forceinline__ bf16x8 load8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
+// The value of the lane 32 apart, as two halves of a wave: gfx950's
+// v_permlane32_swap with x as both operands leaves the lower half's x in
+// every lane of one result and the upper half's in the other, without an
+// LDS round trip.
+__device__ __forceinline__ float half_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ bf16x8 zero8() {
   bf16x8 z;
 #pragma unroll
@@ -683,7 +696,7 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
           for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[sb][kh][v]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        mx = half_max(mx);
         if constexpr (!AL) mx *= sl2;
         // Lazy rescaling: the running maximum only moves (and O, l are only
         // rescaled) when a row's maximum grows by more than 8 in log2 units;
@@ -736,7 +749,7 @@ __global__ __launch_bounds__(64 * (FWQ / RPW)) void ld_attn_fwd_bf16(AttnArgs a)
 #pragma unroll
   for (int sb = 0; sb < NSB; ++sb) {
     const int qrow = qw + sb * 32 + cl;
-    const float lt = l[sb] + __shfl_xor(l[sb], 32, 64);
+    const float lt = half_sum(l[sb]);
     if (qrow < S) {
       const float inv = 1.f / lt;
       bf16* Op = static_cast<bf16*>(a.out) + (static_cast<int64_t>(seq) * S + qrow) * (static_cast<int64_t>(H) * DH) + head * DH;
@@ -820,7 +833,7 @@ __global__ __launch_bounds__(512) void ld_attn_bwd_dq_bf16(AttnArgs a) {
   }
   // delta of the row (the two half-waves hold its two halves of d), stored
   // negated for the dK/dV kernel, which runs after this one
-  const float dl = -(dsum + __shfl_xor(dsum, 32, 64));
+  const float dl = -half_sum(dsum);
   if (qok && hf == 0) a.delta[srow] = dl;
   // the store has completed before the first LDS load is issued: those are
   // counted by the waits below, which know of no other memory operation
