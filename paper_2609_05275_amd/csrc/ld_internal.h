@@ -66,7 +66,14 @@ __device__ __forceinline__ void dma_barrier() {
 // elementwise kernels and the GEMM epilogues that fuse them; the fused ones
 // apply it to float32 accumulator values where the elementwise kernels read
 // the stored bf16 tensors.
-__device__ __forceinline__ float swiglu_sigmoid(float u) { return 1.f / (1.f + expf(-u)); }
+// sigmoid(u) = 1 / (1 + 2^(-u log2 e)) with the hardware base-2 exponential
+// and reciprocal (v_exp_f32, v_rcp_f32, about 1 ulp each): two instructions
+// where expf and a correctly rounded division take a range reduction and a
+// division sequence; far below the bf16 rounding the outputs take.  u = -inf
+// gives 0, u = +inf gives 1.
+__device__ __forceinline__ float swiglu_sigmoid(float u) {
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(u * -1.4426950408889634f));
+}
 __device__ __forceinline__ float swiglu_fwd_f(float u, float v) { return u * swiglu_sigmoid(u) * v; }
 __device__ __forceinline__ void swiglu_bwd_f(float u, float v, float g, float& gu, float& gv) {
   const float sg = swiglu_sigmoid(u);
